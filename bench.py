@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Benchmark: 1080p frames/s, encode + decode, on one MI355X, fp16 and int16 paths.
+
+One step = one frame of the 1920x1088 P-frame sequence (C = 256 at 1/8
+scale, 8 + 8 DC blocks) encoded by one context and decoded by another; all
+frames are resident in HBM before the timed region starts.  ``value`` is the
+fp16 path's frames/s (encode + decode of each frame); the int16 path is
+measured in the same run and reported under ``"int16"``.
+
+After the timed region an instrumented pass over the same frames records
+HIP events around every kernel on the codec's stream; the dominant kernel's
+average duration gives ``roofline.achieved``.  The CPU oracle is timed on a
+bounded spatial sample of the same workload for ``cpu_baseline``.
+
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "1080p frames/sec encode and decode on 1 MI355X (fp16 and int path)"
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+MFMA_I8_PEAK_TOPS = 5000.0
+
+
+def workload_model(H, W, C, ne, nd):
+    """Algorithmic flops and HBM bytes per launch of each kernel kind (weights excluded)."""
+    P8 = (H // 8) * (W // 8)
+    P16 = P8 // 4
+    fmap = P8 * C * 2
+    lat = P16 * C * 2
+    frame = 3 * H * W * 2
+    k = {
+        "embed": (2 * P8 * C * 192, frame + fmap),
+        "fuse": (2 * P8 * C * 2 * C, 3 * fmap),
+        "dcblock": (P8 * (8 * C * C + 18 * C), 2 * fmap),
+        "down": (2 * P16 * C * 4 * C, fmap + lat),
+        "prior_enc": (2 * P16 * 2 * C * C, 4 * lat),
+        "prior_dec": (2 * P16 * C * C, 3 * lat),
+        "up": (2 * P16 * 4 * C * C, lat + fmap),
+        "recon": (2 * P8 * 192 * C, fmap + frame),
+    }
+    enc = ["embed", "fuse"] + ["dcblock"] * ne + ["down", "prior_enc", "up", "fuse"] + ["dcblock"] * nd
+    dec = ["prior_dec", "up", "fuse"] + ["dcblock"] * nd + ["recon"]
+    return k, enc, dec
+
+
+def roofline_seconds(kinds, names, flop_peak):
+    t = 0.0
+    for n in names:
+        fl, by = kinds[n]
+        t += max(fl / flop_peak, by / (HBM_PEAK_GBS * 1e9))
+    return t
+
+
+def macs_per_frame(H, W, C, ne, nd):
+    kinds, enc, dec = workload_model(H, W, C, ne, nd)
+    return sum(kinds[n][0] for n in enc) / 2, sum(kinds[n][0] for n in dec) / 2
+
+
+def cpu_baseline(pre, weights, strip_rows):
+    """Oracle (float64 NumPy) encode + decode of a horizontal strip of the first frame."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from oracle import codec_float as cf
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=os.cpu_count())
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    p = oracle.unpack(weights, pre.channels, pre.n_enc, pre.n_dec)
+    x = next(synth.frame_sequence(pre, 1))[:, :strip_rows, :]
+    st = cf.zero_state(p, strip_rows, pre.width)
+    t0 = time.perf_counter()
+    r = cf.encode_frame(p, x, st)
+    cf.decode_frame(p, r.q, st)
+    dt = time.perf_counter() - t0
+    frac = strip_rows / pre.height
+    return {"value": frac / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp16-path oracle (float64 NumPy) encode + decode of the top {strip_rows} of {pre.height} rows "
+                      f"of 1080p frame 0 ({dt:.1f} s), scaled by {frac:.3f}; host cpu_count={os.cpu_count()}"}
+
+
+def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
+    H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
+    enc = Codec(H, W, C, ne, nd, path, weights)
+    dec = Codec(H, W, C, ne, nd, path, weights)
+    stream = torch.cuda.current_stream()
+    odt = torch.int16 if path == "int16" else torch.float16
+    qbuf = [torch.empty(enc.q_shape, dtype=torch.int16, device="cuda") for _ in range(steps)]
+    bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
+    xout = torch.empty(enc.frame_shape, dtype=odt, device="cuda")
+    nfr = len(gframes)
+    for i in range(warmup):
+        q, _ = enc.encode(gframes[i % nfr])
+        dec.decode(q, out=xout)
+    torch.cuda.synchronize()
+
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e2 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for k in range(steps):
+        enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
+    e1.record(stream)
+    for k in range(steps):
+        dec.decode(qbuf[k], out=xout)
+    e2.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    enc_ms, dec_ms = e0.elapsed_time(e1), e1.elapsed_time(e2)
+
+    # instrumented pass: events around every kernel, same frames
+    enc.reset()
+    dec.reset()
+    enc.timing(True)
+    dec.timing(True)
+    for k in range(steps):
+        enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
+        dec.decode(qbuf[k], out=xout)
+    te, td = enc.timing_read(), dec.timing_read()
+    kern = {}
+    for src in (te, td):
+        for kind, (n, ms) in src.items():
+            a = kern.setdefault(kind, [0, 0.0])
+            a[0] += n
+            a[1] += ms
+    return {
+        "enc_ms": enc_ms, "dec_ms": dec_ms, "wall_s": wall,
+        "bits_per_frame": float(bits.mean().item()),
+        "kernels": {k: {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms} for k, (n, ms) in kern.items()},
+        "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)],
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--paths", default="fp16,int16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-strip-rows", type=int, default=272)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the per-frame transform runs on a single MI355X "
+              "(frames of one stream are sequential); --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2502_20762_amd.ncodec import Codec
+
+    pre = synth.PRESETS["hd1080"]
+    H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
+    weights = synth.make_weights(C, ne, nd)
+    nfr = min(args.steps + args.warmup, pre.n_frames)
+    frames = list(synth.frame_sequence(pre, nfr))
+    gframes = [torch.from_numpy(f).to("cuda") for f in frames]
+    torch.cuda.synchronize()
+
+    kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd)
+    res = {}
+    for path in args.paths.split(","):
+        res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
+
+    def summary(path, r, peak_tflops, op_scale, unit):
+        K = args.steps
+        fl, by = kinds["dcblock"]
+        kd = r["kernels"]["dcblock"]
+        achieved = op_scale * fl / (kd["avg_us"] * 1e-6) / 1e12
+        t_roof = roofline_seconds(kinds, enc_list + dec_list, peak_tflops * 1e12 / op_scale)
+        step_ms = (r["enc_ms"] + r["dec_ms"]) / K
+        return {
+            "value": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3),
+            "ms_per_step": step_ms,
+            "encode_fps": K / (r["enc_ms"] * 1e-3),
+            "decode_fps": K / (r["dec_ms"] * 1e-3),
+            "roofline": {"kernel": "dcblock", "bound": "mfma", "achieved": achieved, "peak": peak_tflops,
+                         "unit": unit, "frac": achieved / peak_tflops, "traffic": None,
+                         "per_launch": {"algorithmic_ops": op_scale * fl, "algorithmic_bytes": by,
+                                        "avg_us": kd["avg_us"], "launches": kd["launches"]}},
+            "frame_roofline_fps": 1.0 / t_roof,
+            "frac_of_frame_roofline": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3) * t_roof,
+            "kernels_us": {k: round(v["avg_us"], 2) for k, v in r["kernels"].items()},
+            "kernels_per_frame": r["kernels_per_frame"],
+            "bits_per_frame": r["bits_per_frame"],
+        }
+
+    out = {"metric": METRIC}
+    main_path = "fp16" if "fp16" in res else next(iter(res))
+    s_main = summary(main_path, res[main_path], *(
+        (MFMA_F16_PEAK_TFLOPS, 1, "TFLOP/s") if main_path == "fp16" else (MFMA_I8_PEAK_TOPS, 4, "TOP/s")))
+    out.update({
+        "value": s_main["value"], "unit": "frames/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": s_main["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16" if main_path == "fp16" else "int16", "data": "synthetic",
+        "config": {"workload": "1080p P-frame sequence, 1920x1088 (padded), C=256 at 1/8 scale (240x136), "
+                               "8+8 DC blocks, latent 120x68x256; one step = encode + decode of one frame",
+                   "height": H, "width": W, "channels": C, "n_enc_blocks": ne, "n_dec_blocks": nd,
+                   "path": main_path},
+        "encode_fps": s_main["encode_fps"], "decode_fps": s_main["decode_fps"],
+        "roofline": s_main["roofline"],
+        "frame_roofline_fps": s_main["frame_roofline_fps"],
+        "frac_of_frame_roofline": s_main["frac_of_frame_roofline"],
+        "kernels_us": s_main["kernels_us"], "kernels_per_frame": s_main["kernels_per_frame"],
+    })
+    if "int16" in res and main_path != "int16":
+        out["int16"] = summary("int16", res["int16"], MFMA_I8_PEAK_TOPS, 4, "TOP/s")
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(pre, weights, args.cpu_strip_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

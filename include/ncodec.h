@@ -1,0 +1,169 @@
+/*
+ * ncodec -- C ABI of the MI355X (gfx950) implementation of the per-frame
+ * transform of DCVC-RT (Jia et al., "Towards Practical Real-Time Neural Video
+ * Compression", CVPR 2025).
+ *
+ * Problem statement followed (Sec. 4.1, Fig. 4; Sec. 5.1 "Test Details"):
+ * low-delay P-frame coding.  The encoder codes frame x_t conditioned on the
+ * temporal context it shares with the decoder (the previous decoded 1/8-scale
+ * feature f_{t-1}, Sec. 4.3) and on the previous quantised latent; the
+ * decoder, holding the same state, reproduces the frame from the symbols.
+ * Encoder and decoder are separate contexts, each carrying its own state.
+ *
+ * Transform (one frame, C channels, h = H/8, w = W/8):
+ *   patch embed     e  = W_pe * unshuffle8(x) + b_pe            (Sec. 4.2)
+ *   temporal fuse   z  = W_fe * [e ; f_{t-1}] + b_fe            (Sec. 4.3)
+ *   N_e DC blocks   z += W2 * LReLU_0.1(W1 * dw3x3(z) + b1) + b2 (Supp. B.1)
+ *   downsample      y  = conv2x2/s2(z)                          (1/16 latent)
+ *   prior           [mu ; s] = W_h * yhat_{t-1} + b_h
+ *   quantise        q  = round(y - mu), yhat = q + mu           (Fig. 4 "Q")
+ *   rate            bits = sum -log2 L(q; sigma), sigma = max(softplus(s), 0.11)
+ *   decoder         d  = shuffle2(W_u * yhat + b_u); z' = W_fd * [d ; f_{t-1}] + b_fd;
+ *                   N_d DC blocks -> f_t (the next frame's context, taken
+ *                   before reconstruction, Supp. B.3)
+ *   reconstruction  xhat = clamp(shuffle8(W_r * f_t + b_r), 0, 1)  (decode only)
+ *
+ * Integerised path (Sec. 4.5, Eq. 3; Supp. B.4, Alg. 1): features are int16
+ * at K1 = 512 (1.0 -> 512), weights and biases int16 at K2 = 8192, every conv
+ * accumulates conv(x_i, w_i) + 512 b_i in int32 and returns
+ * clip(round_half_even(a / 8192), int16).  Results are bit-exact and
+ * identical on every device.
+ *
+ * Conventions
+ *  - Every device pointer is caller-owned device memory (e.g. a torch tensor's
+ *    data_ptr()).  The library never allocates device memory: all persistent
+ *    state and weights live in the caller's workspace.
+ *  - Every call enqueues work on the context's HIP stream and returns without
+ *    synchronising; results are valid once the stream has been synchronised.
+ *  - Arguments are validated on the host before anything is enqueued.  A
+ *    negative ncodec_status is returned on error; nothing is thrown across the
+ *    ABI.  ncodec_last_error() gives a message.  A context is not thread-safe.
+ *  - Public tensors are planar (NCHW with N = 1).  Internal layouts are
+ *    private.
+ */
+#ifndef NCODEC_H
+#define NCODEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ncodec_ctx ncodec_ctx;
+
+typedef enum {
+  NCODEC_OK = 0,
+  NCODEC_EINVAL = -1,     /* null pointer, bad enum, bad weight value        */
+  NCODEC_ESHAPE = -2,     /* H, W not multiples of 16, bad C or block count   */
+  NCODEC_EHIP = -3,       /* a HIP runtime call failed                        */
+  NCODEC_ESTATE = -4,     /* call does not match the context's configuration  */
+  NCODEC_EOVERFLOW = -5,  /* reserved: int32 accumulator overflow detected    */
+  NCODEC_ENOMEM = -6      /* workspace smaller than ncodec_workspace_bytes()  */
+} ncodec_status;
+
+typedef enum { NCODEC_PATH_FP16 = 0, NCODEC_PATH_INT16 = 1 } ncodec_path;
+
+typedef struct {
+  int32_t height;        /* H, multiple of 16, 16..8192 (caller pads 1080 -> 1088) */
+  int32_t width;         /* W, multiple of 16, 16..8192                             */
+  int32_t channels;      /* C in {64, 128, 256}                                     */
+  int32_t n_enc_blocks;  /* N_e, 0..32                                              */
+  int32_t n_dec_blocks;  /* N_d, 0..32                                              */
+  int32_t path;          /* ncodec_path                                             */
+} ncodec_config;
+
+/* Number of float32 values in the canonical parameter list for cfg, or 0 if
+ * cfg is invalid.  Canonical order (each weight row-major, followed by its
+ * bias): pe W(C,192) b(C); fuse_enc W(C,2C) b(C) with input channels
+ * [e ; f_prev]; N_e blocks of {dw W(C,3,3) b(C); pw1 W(2C,C) b(2C);
+ * pw2 W(C,2C) b(C)}; down W(C,C,2,2) b(C); head W(2C,C) b(2C) with rows
+ * [mu ; s]; up W(4C,C) b(4C), row 4c+2i+j -> pixel-shuffle position (c,i,j);
+ * fuse_dec W(C,2C) b(C) with input channels [d ; f_prev]; N_d blocks;
+ * rec W(192,C) b(192), row 64c+8i+j -> colour c at pixel (8y+i, 8x+j).
+ * Pure host function. */
+size_t ncodec_weight_count(const ncodec_config* cfg);
+
+/* Bytes of device workspace a context needs (weights in kernel-ready form,
+ * state, intermediates), or 0 if cfg is invalid.  Pure host function. */
+size_t ncodec_workspace_bytes(const ncodec_config* cfg);
+
+/* Create a context.  host_weights: n_weights float32 values in canonical
+ * order (host memory, copied; the fp16 path rounds them to fp16, the int
+ * path converts them to round(8192 w) and rejects any weight of the
+ * pointwise / 2x2 convolutions whose integer value exceeds 32639 in magnitude
+ * with NCODEC_EINVAL).  d_workspace: caller-owned device buffer of at least
+ * ncodec_workspace_bytes(cfg) bytes, 256-byte aligned, that must outlive the
+ * context.  hip_stream: a hipStream_t (NULL = default stream).  The weight
+ * upload is synchronous on that stream.  State starts as an I-frame (zero).
+ * Errors: EINVAL (null pointer, wrong n_weights, weight out of range),
+ * ESHAPE (bad cfg), ENOMEM (workspace too small or misaligned), EHIP. */
+ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights, size_t n_weights,
+                            void* d_workspace, size_t ws_bytes, void* hip_stream, ncodec_ctx** out);
+
+/* Make the next frame an I-frame: zero f_{t-1} and yhat_{t-1} (enqueued). */
+ncodec_status ncodec_reset(ncodec_ctx* ctx);
+
+/* Encode one frame (Sec. 4.1, Fig. 4 encoder side, Supp. B.3 encoding).
+ *  d_frame: 3 x H x W planar fp16 (IEEE binary16), values in [0, 1]; the int
+ *           path converts it with x_i = round(512 x) (Alg. 1).
+ *  d_q:     C x H/16 x W/16 planar int16 output symbols q.
+ *  d_bits:  device double receiving the frame's estimated bits, or NULL.
+ * Updates the context state to (f_t, yhat_t).  d_frame must not alias d_q. */
+ncodec_status ncodec_encode_frame(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits);
+
+/* Decode one frame from its symbols (Fig. 4 decoder side, Supp. B.3).
+ *  d_q:         C x H/16 x W/16 planar int16 symbols from ncodec_encode_frame.
+ *  d_frame_out: 3 x H x W planar; fp16 in [0,1] (fp16 path) or int16 in
+ *               [0, 512] (int path).
+ * Updates the context state to (f_t, yhat_t). */
+ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_out);
+
+/* Rate of n symbols under zero-mean Gaussians (Supp. B.2; likelihood
+ * L = Phi((|q|+1/2)/sigma) - Phi((|q|-1/2)/sigma), bits = sum -log2 max(L, 1e-9)).
+ *  d_q: n int16 symbols; d_sigma: n float32 scales (> 0); d_bits: device
+ *  double output.  The sum is formed in a fixed order (deterministic).
+ * n must be in [0, 2^31); n = 0 writes 0. */
+ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const float* d_sigma,
+                                   int64_t n, double* d_bits);
+
+/* Copy the state out of / into the context (enqueued).  d_feat: C x H/8 x W/8
+ * planar, d_yhat: C x H/16 x W/16 planar; fp16 (fp16 path) or int16 (int
+ * path).  Either pointer may be NULL to skip that tensor. */
+ncodec_status ncodec_get_state(ncodec_ctx* ctx, void* d_feat, void* d_yhat);
+ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* d_yhat);
+
+/* Kernel launches one ncodec_encode_frame / ncodec_decode_frame enqueues. */
+int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
+
+/* Optional per-kernel timing.  While enabled, each kernel the context
+ * enqueues is bracketed by a pair of HIP events recorded on the context's
+ * stream.  ncodec_timing_read() synchronises the stream, aggregates the
+ * recorded pairs per kernel kind (launch count and summed milliseconds),
+ * writes at most max_kinds records to out, sets *n_kinds, and clears the
+ * log.  Kinds: "embed", "fuse", "dcblock", "down", "prior", "reduce", "up",
+ * "recon".  Meant for measurement runs; off by default. */
+typedef struct {
+  char kind[16];
+  int32_t launches;
+  double total_ms;
+} ncodec_kernel_timing;
+
+ncodec_status ncodec_timing_enable(ncodec_ctx* ctx, int32_t enable);
+ncodec_status ncodec_timing_read(ncodec_ctx* ctx, ncodec_kernel_timing* out, int32_t max_kinds, int32_t* n_kinds);
+
+/* Message for the last error on ctx (or the last create failure if ctx is NULL). */
+const char* ncodec_last_error(const ncodec_ctx* ctx);
+
+/* Static description of a status code. */
+const char* ncodec_status_string(ncodec_status st);
+
+/* Release host resources of the context (the workspace stays caller-owned).
+ * Synchronises the context's stream first.  NULL is ignored. */
+void ncodec_destroy(ncodec_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NCODEC_H */

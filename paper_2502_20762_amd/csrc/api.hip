@@ -1,0 +1,664 @@
+// C ABI, weight preparation and the per-frame kernel schedule.
+//
+// The schedule follows the paper's encoding / decoding pipeline (Supp. B.3):
+// encoding runs patch embed -> temporal fuse -> encoder blocks -> downsample ->
+// prior/quantiser/bits -> decoder (upsample -> fuse -> blocks) and keeps the
+// decoder output f_t as the next context without reconstructing the frame;
+// decoding runs prior -> decoder -> reconstruction.
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ncodec.h"
+#include "common.hpp"
+#include "internal.hpp"
+
+using namespace nc;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool cfg_valid(const ncodec_config* c, std::string* why) {
+  if (!c) { if (why) *why = "cfg is NULL"; return false; }
+  if (c->height < 16 || c->width < 16 || c->height > 8192 || c->width > 8192 || c->height % 16 || c->width % 16) {
+    if (why) *why = "height and width must be multiples of 16 in [16, 8192]";
+    return false;
+  }
+  if (c->channels != 64 && c->channels != 128 && c->channels != 256) {
+    if (why) *why = "channels must be 64, 128 or 256";
+    return false;
+  }
+  if (c->n_enc_blocks < 0 || c->n_enc_blocks > 32 || c->n_dec_blocks < 0 || c->n_dec_blocks > 32) {
+    if (why) *why = "block counts must be in [0, 32]";
+    return false;
+  }
+  if (c->path != NCODEC_PATH_FP16 && c->path != NCODEC_PATH_INT16) {
+    if (why) *why = "path must be NCODEC_PATH_FP16 or NCODEC_PATH_INT16";
+    return false;
+  }
+  return true;
+}
+
+size_t weight_count(const ncodec_config& c) {
+  const size_t C = (size_t)c.channels;
+  const size_t blk = C * 9 + C + 2 * C * C + 2 * C + 2 * C * C + C;
+  return C * 192 + C + 2 * C * C + C + c.n_enc_blocks * blk + 4 * C * C + C + 2 * C * C + 2 * C + 4 * C * C + 4 * C +
+         2 * C * C + C + c.n_dec_blocks * blk + 192 * C + 192;
+}
+
+// ---------------------------------------------------------------- weight image
+struct ConvDev {
+  size_t w = 0, wlo = 0, bias = 0;
+};
+struct BlockDev {
+  size_t dww = 0, dwb = 0;
+  ConvDev pw1, pw2;
+};
+
+struct Image {
+  std::vector<uint8_t> bytes;
+  size_t add(size_t n) {
+    const size_t off = align_up(bytes.size());
+    bytes.resize(off + n);
+    return off;
+  }
+  template <class T> T* at(size_t off) { return (T*)(bytes.data() + off); }
+};
+
+int16_t q16(float w) {  // round(8192 w) with round-half-even, saturated (Alg. 1)
+  double v = std::nearbyint((double)w * 8192.0);
+  v = std::fmin(std::fmax(v, -32768.0), 32767.0);
+  return (int16_t)v;
+}
+
+struct Packer {
+  const ncodec_config& cfg;
+  Image& img;
+  bool is_int;
+  std::string* err;
+  bool ok = true;
+
+  // Pointwise-type conv, W is N x K row-major (source row stride ldw); row(n') and col(k')
+  // give the source indices of packed row n' and packed contraction index k'.
+  template <class RowMap, class ColMap>
+  ConvDev gemm(const float* W, const float* b, int N, int K, int ldw, RowMap row, ColMap col) {
+    ConvDev d;
+    if (!is_int) {
+      d.w = img.add((size_t)N * K * 2);
+      d.bias = img.add((size_t)N * 4);
+      f16* wp = img.at<f16>(d.w);
+      float* bp = img.at<float>(d.bias);
+      const int ks = K / 16;
+      for (int mt = 0; mt < N / 32; ++mt)
+        for (int s = 0; s < ks; ++s)
+          for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 8; ++e) {
+              const int n = 32 * mt + (l & 31), k = 16 * s + 8 * (l >> 5) + e;
+              wp[(((size_t)mt * ks + s) * 64 + l) * 8 + e] = (f16)W[(size_t)row(n) * ldw + col(k)];
+            }
+      for (int n = 0; n < N; ++n) bp[n] = (float)(f16)b[row(n)];
+      return d;
+    }
+    d.w = img.add((size_t)N * K);
+    d.wlo = img.add((size_t)N * K);
+    d.bias = img.add((size_t)N * 4);
+    int8_t* hp = img.at<int8_t>(d.w);
+    int8_t* lp = img.at<int8_t>(d.wlo);
+    int32_t* cp = img.at<int32_t>(d.bias);
+    const int ks = K / 32;
+    for (int mt = 0; mt < N / 32; ++mt)
+      for (int s = 0; s < ks; ++s)
+        for (int l = 0; l < 64; ++l)
+          for (int e = 0; e < 16; ++e) {
+            const int n = 32 * mt + (l & 31), k = 16 * (l >> 5) + 32 * s + e;
+            const int wi = q16(W[(size_t)row(n) * ldw + col(k)]);
+            if (wi > 32639) {
+              if (ok && err) *err = "integer weight above 32639 (|w| >= 3.984) cannot be split into int8 digits";
+              ok = false;
+            }
+            const int lo = ((wi + 128) & 255) - 128;
+            const int hi = (wi - lo) / 256;
+            const size_t at = (((size_t)mt * ks + s) * 64 + l) * 16 + e;
+            hp[at] = (int8_t)hi;
+            lp[at] = (int8_t)lo;
+          }
+    for (int n = 0; n < N; ++n) {
+      int64_t sum = 0;
+      for (int k = 0; k < K; ++k) sum += q16(W[(size_t)row(n) * ldw + col(k)]);
+      const int64_t corr = 512 * (int64_t)q16(b[row(n)]) + 128 * sum;
+      cp[n] = (int32_t)(uint32_t)(uint64_t)corr;  // wraps like the int32 accumulator
+    }
+    return d;
+  }
+
+  ConvDev plain(const float* W, const float* b, int N, int K) {
+    return gemm(W, b, N, K, K, [](int n) { return n; }, [](int k) { return k; });
+  }
+
+  BlockDev block(const float*& cur) {
+    const int C = cfg.channels;
+    BlockDev d;
+    const float* dw = cur; cur += (size_t)C * 9;
+    const float* dwb = cur; cur += C;
+    const float* w1 = cur; cur += (size_t)2 * C * C;
+    const float* b1 = cur; cur += 2 * C;
+    const float* w2 = cur; cur += (size_t)2 * C * C;
+    const float* b2 = cur; cur += C;
+    d.dww = img.add((size_t)9 * C * 2);
+    d.dwb = img.add((size_t)C * 4);
+    if (!is_int) {
+      f16* wp = img.at<f16>(d.dww);
+      float* bp = img.at<float>(d.dwb);
+      for (int t = 0; t < 9; ++t)
+        for (int c = 0; c < C; ++c) wp[t * C + c] = (f16)dw[c * 9 + t];
+      for (int c = 0; c < C; ++c) bp[c] = (float)(f16)dwb[c];
+    } else {
+      int16_t* wp = img.at<int16_t>(d.dww);
+      int32_t* bp = img.at<int32_t>(d.dwb);
+      for (int t = 0; t < 9; ++t)
+        for (int c = 0; c < C; ++c) wp[t * C + c] = q16(dw[c * 9 + t]);
+      for (int c = 0; c < C; ++c) bp[c] = 512 * (int32_t)q16(dwb[c]);
+    }
+    d.pw1 = plain(w1, b1, 2 * C, C);
+    // Second conv: its contraction index is permuted inside each 32-channel
+    // hidden chunk so that the first conv's accumulator registers can be used
+    // directly as this conv's operand.
+    if (!is_int)
+      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
+        return 32 * (k / 32) + 16 * ((k / 16) % 2) + 8 * ((k % 8) / 4) + 4 * ((k / 8) % 2) + (k % 4);
+      });
+    else
+      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
+        return 32 * (k / 32) + 8 * ((k % 16) / 4) + 4 * ((k / 16) % 2) + (k % 4);
+      });
+    return d;
+  }
+};
+
+struct Layout {
+  ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
+  std::vector<BlockDev> enc, dec;
+  size_t sigma_tab = 0;
+  size_t image_bytes = 0;
+  // state and intermediates (offsets from the workspace base)
+  size_t feat[2], yhat[2], ed, zA, zB, y, partials;
+  int n_partials;
+  size_t total;
+};
+
+bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err) {
+  const int C = cfg.channels;
+  const bool is_int = cfg.path == NCODEC_PATH_INT16;
+  std::vector<float> zeros;
+  if (!w) {
+    zeros.assign(weight_count(cfg), 0.f);
+    w = zeros.data();
+  }
+  Packer pk{cfg, img, is_int, err};
+  const float* cur = w;
+  auto take = [&](size_t n) { const float* p = cur; cur += n; return p; };
+  const float* pe_w = take((size_t)C * 192); const float* pe_b = take(C);
+  L.pe = pk.plain(pe_w, pe_b, C, 192);
+  const float* fe_w = take((size_t)2 * C * C); const float* fe_b = take(C);
+  L.fuse_enc = pk.plain(fe_w, fe_b, C, 2 * C);
+  for (int k = 0; k < cfg.n_enc_blocks; ++k) L.enc.push_back(pk.block(cur));
+  const float* dn_w = take((size_t)4 * C * C); const float* dn_b = take(C);
+  // packed k' = (2i + j) * C + c  <-  source column c * 4 + 2i + j
+  L.down = pk.gemm(dn_w, dn_b, C, 4 * C, 4 * C, [](int n) { return n; }, [C](int k) { return (k % C) * 4 + k / C; });
+  const float* hd_w = take((size_t)2 * C * C); const float* hd_b = take(2 * C);
+  L.head = pk.plain(hd_w, hd_b, 2 * C, C);
+  const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
+  // packed row n' = sp * C + c  <-  source row 4c + sp
+  L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });
+  const float* fd_w = take((size_t)2 * C * C); const float* fd_b = take(C);
+  L.fuse_dec = pk.plain(fd_w, fd_b, C, 2 * C);
+  for (int k = 0; k < cfg.n_dec_blocks; ++k) L.dec.push_back(pk.block(cur));
+  const float* rc_w = take((size_t)192 * C); const float* rc_b = take(192);
+  L.rec = pk.plain(rc_w, rc_b, 192, C);
+  if ((size_t)(cur - w) != weight_count(cfg)) {
+    if (err) *err = "internal: parameter walk mismatch";
+    return false;
+  }
+  if (is_int) {
+    L.sigma_tab = img.add(65536 * 4);
+    float* tab = img.at<float>(L.sigma_tab);
+    for (int i = 0; i < 65536; ++i) {
+      const double s = (double)(i - 32768) / 512.0;
+      const double sp = s > 30.0 ? s : std::log1p(std::exp(s));
+      tab[i] = (float)std::fmax(sp, 0.11);
+    }
+  }
+  L.image_bytes = align_up(img.bytes.size());
+
+  const size_t P8 = (size_t)(cfg.height / 8) * (cfg.width / 8);
+  const size_t P16 = P8 / 4;
+  const size_t fb = P8 * C * 2, lb = P16 * C * 2;
+  size_t off = L.image_bytes;
+  auto alloc = [&](size_t n) { const size_t o = off; off = align_up(off + n); return o; };
+  L.feat[0] = alloc(fb); L.feat[1] = alloc(fb);
+  L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
+  L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
+  L.y = alloc(lb);
+  const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
+  L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
+  L.partials = alloc((size_t)L.n_partials * 8);
+  L.total = off;
+  return pk.ok;
+}
+
+}  // namespace
+
+struct ncodec_ctx {
+  ncodec_config cfg;
+  int device;
+  hipStream_t stream;
+  char* ws;
+  Layout L;
+  int cur = 0;
+  std::string err;
+  struct TimedLaunch {
+    const char* kind;
+    hipEvent_t start, stop;
+  };
+  bool timing = false;
+  std::vector<TimedLaunch> log;
+  bool is_int() const { return cfg.path == NCODEC_PATH_INT16; }
+  template <class T = void> T* p(size_t off) const { return (T*)(ws + off); }
+};
+
+namespace {
+
+ncodec_status fail(ncodec_ctx* ctx, ncodec_status st, const std::string& msg) {
+  if (ctx) ctx->err = msg; else g_create_error = msg;
+  return st;
+}
+
+ncodec_status hip_fail(ncodec_ctx* ctx, hipError_t e, const char* where) {
+  return fail(ctx, NCODEC_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define NC_HIP(ctx, expr, where)                          \
+  do {                                                    \
+    hipError_t _e = (expr);                               \
+    if (_e != hipSuccess) return hip_fail(ctx, _e, where); \
+  } while (0)
+
+// Runs one launch; in timing mode brackets it with events on the context stream.
+template <class F>
+hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch) {
+  if (!ctx->timing) return launch();
+  ncodec_ctx::TimedLaunch t{kind, nullptr, nullptr};
+  hipError_t e = hipEventCreate(&t.start);
+  if (e == hipSuccess) e = hipEventCreate(&t.stop);
+  if (e == hipSuccess) e = hipEventRecord(t.start, ctx->stream);
+  if (e == hipSuccess) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(t.stop, ctx->stream);
+  ctx->log.push_back(t);
+  return e;
+}
+
+ncodec_status enter(ncodec_ctx* ctx) {
+  if (!ctx) return fail(nullptr, NCODEC_EINVAL, "ctx is NULL");
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  e = hipGetLastError();  // surfaces an earlier asynchronous failure
+  if (e != hipSuccess) return hip_fail(ctx, e, "earlier launch");
+  return NCODEC_OK;
+}
+
+hipError_t pw(ncodec_ctx* ctx, const char* kind, int loader, int epi, const PwArgs& a) {
+  return timed(ctx, kind, [&] {
+    return ctx->is_int() ? launch_pw_i16(loader, epi, a, ctx->stream) : launch_pw_f16(loader, epi, a, ctx->stream);
+  });
+}
+
+hipError_t dcblock(ncodec_ctx* ctx, const BlockArgs& ba) {
+  const int C = ctx->cfg.channels;
+  return timed(ctx, "dcblock", [&] {
+    return ctx->is_int() ? launch_dcblock_i16(C, ba, ctx->stream) : launch_dcblock_f16(C, ba, ctx->stream);
+  });
+}
+
+hipError_t prior(ncodec_ctx* ctx, const PriorArgs& pa, int* np) {
+  return timed(ctx, "prior", [&] {
+    return ctx->is_int() ? launch_prior_i16(pa, ctx->stream, np) : launch_prior_f16(pa, ctx->stream, np);
+  });
+}
+
+PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
+  PwArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.wfrag = ctx->p(c.w);
+  a.wfrag_lo = ctx->is_int() ? ctx->p(c.wlo) : nullptr;
+  a.bias = ctx->p(c.bias);
+  a.K = K;
+  a.N = N;
+  a.P = P;
+  a.w8 = ctx->cfg.width / 8;
+  a.H = ctx->cfg.height;
+  a.W = ctx->cfg.width;
+  return a;
+}
+
+// Runs the decoder-side transform from yhat_new (already written) into feat[nxt].
+ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int h8 = c.height / 8, w8 = c.width / 8;
+  const int P8 = h8 * w8, P16 = P8 / 4;
+  const Layout& L = ctx->L;
+  void* f_prev = ctx->p(L.feat[1 - nxt]);
+  void* f_new = ctx->p(L.feat[nxt]);
+
+  PwArgs a = conv_args(ctx, L.up, C, 4 * C, P16);
+  a.src0 = ctx->p(L.yhat[nxt]);
+  a.C0 = C;
+  a.dst = ctx->p(L.ed);
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "up", LD_NHWC, EP_UP, a), "upsample");
+
+  void* z = c.n_dec_blocks == 0 ? f_new : ctx->p(L.zA);
+  a = conv_args(ctx, L.fuse_dec, 2 * C, C, P8);
+  a.src0 = ctx->p(L.ed);
+  a.C0 = C;
+  a.src1 = f_prev;
+  a.C1 = C;
+  a.dst = z;
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_dec");
+
+  for (int k = 0; k < c.n_dec_blocks; ++k) {
+    void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
+    const BlockDev& b = L.dec[k];
+    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
+                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
+                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8};
+    NC_HIP(ctx, dcblock(ctx, ba), "decoder block");
+    z = dst;
+  }
+  return NCODEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ncodec_weight_count(const ncodec_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  return weight_count(*cfg);
+}
+
+size_t ncodec_workspace_bytes(const ncodec_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  Image img;
+  Layout L;
+  build_layout(*cfg, nullptr, img, L, nullptr);
+  return L.total;
+}
+
+ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights, size_t n_weights, void* d_workspace,
+                            size_t ws_bytes, void* hip_stream, ncodec_ctx** out) {
+  std::string why;
+  if (!out) return fail(nullptr, NCODEC_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(nullptr, NCODEC_EINVAL, "cfg is NULL");
+  if (!cfg_valid(cfg, &why)) return fail(nullptr, NCODEC_ESHAPE, why);
+  if (!host_weights) return fail(nullptr, NCODEC_EINVAL, "host_weights is NULL");
+  if (n_weights != weight_count(*cfg))
+    return fail(nullptr, NCODEC_EINVAL,
+                "n_weights is " + std::to_string(n_weights) + ", expected " + std::to_string(weight_count(*cfg)));
+  if (!d_workspace) return fail(nullptr, NCODEC_EINVAL, "d_workspace is NULL");
+  if ((uintptr_t)d_workspace % kAlign) return fail(nullptr, NCODEC_ENOMEM, "d_workspace must be 256-byte aligned");
+  for (size_t i = 0; i < n_weights; ++i)
+    if (!std::isfinite(host_weights[i])) return fail(nullptr, NCODEC_EINVAL, "non-finite weight");
+
+  Image img;
+  Layout L;
+  if (!build_layout(*cfg, host_weights, img, L, &why)) return fail(nullptr, NCODEC_EINVAL, why);
+  if (ws_bytes < L.total)
+    return fail(nullptr, NCODEC_ENOMEM,
+                "workspace has " + std::to_string(ws_bytes) + " bytes, needs " + std::to_string(L.total));
+
+  ncodec_ctx* ctx = new ncodec_ctx();
+  ctx->cfg = *cfg;
+  ctx->stream = (hipStream_t)hip_stream;
+  ctx->ws = (char*)d_workspace;
+  ctx->L = std::move(L);
+  hipError_t e = hipGetDevice(&ctx->device);
+  if (e == hipSuccess) e = hipMemcpyAsync(ctx->ws, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, ctx->stream);
+  if (e == hipSuccess) e = launch_fill_zero(ctx->ws + ctx->L.image_bytes, ctx->L.total - ctx->L.image_bytes, ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) {
+    g_create_error = std::string("create: ") + hipGetErrorString(e);
+    delete ctx;
+    return NCODEC_EHIP;
+  }
+  *out = ctx;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_reset(ncodec_ctx* ctx) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  const int C = ctx->cfg.channels;
+  const size_t P8 = (size_t)(ctx->cfg.height / 8) * (ctx->cfg.width / 8);
+  NC_HIP(ctx, launch_fill_zero(ctx->p(ctx->L.feat[ctx->cur]), P8 * C * 2, ctx->stream), "reset");
+  NC_HIP(ctx, launch_fill_zero(ctx->p(ctx->L.yhat[ctx->cur]), P8 / 4 * C * 2, ctx->stream), "reset");
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_encode_frame(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_frame || !d_q) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be non-NULL");
+  if ((uintptr_t)d_frame % 16 || (uintptr_t)d_q % 16) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be 16-byte aligned");
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int h8 = c.height / 8, w8 = c.width / 8;
+  const int P8 = h8 * w8, P16 = P8 / 4;
+  const Layout& L = ctx->L;
+  const int cur = ctx->cur, nxt = 1 - cur;
+
+  PwArgs a = conv_args(ctx, L.pe, 192, C, P8);
+  a.src0 = d_frame;
+  a.dst = ctx->p(L.ed);
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "embed", LD_FRAME, EP_NHWC, a), "patch embed");
+
+  void* z = ctx->p(L.zA);
+  a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
+  a.src0 = ctx->p(L.ed);
+  a.C0 = C;
+  a.src1 = ctx->p(L.feat[cur]);
+  a.C1 = C;
+  a.dst = z;
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_enc");
+
+  for (int k = 0; k < c.n_enc_blocks; ++k) {
+    void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
+    const BlockDev& b = L.enc[k];
+    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
+                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
+                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8};
+    NC_HIP(ctx, dcblock(ctx, ba), "encoder block");
+    z = dst;
+  }
+
+  a = conv_args(ctx, L.down, 4 * C, C, P16);
+  a.src0 = z;
+  a.Csrc = C;
+  a.dst = ctx->p(L.y);
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
+
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.head.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+  pa.bias = ctx->p(L.head.bias);
+  pa.yhat_prev = ctx->p(L.yhat[cur]);
+  pa.y = ctx->p(L.y);
+  pa.q_out = d_q;
+  pa.yhat_new = ctx->p(L.yhat[nxt]);
+  pa.partials = ctx->p<double>(L.partials);
+  pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
+  pa.C = C;
+  pa.P = P16;
+  pa.decode = 0;
+  int np = 0;
+  NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
+  if (d_bits)
+    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(pa.partials, np, d_bits, ctx->stream); }), "bits reduce");
+
+  st = run_decoder(ctx, nxt);
+  if (st) return st;
+  ctx->cur = nxt;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_out) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_q || !d_frame_out) return fail(ctx, NCODEC_EINVAL, "d_q and d_frame_out must be non-NULL");
+  if ((uintptr_t)d_frame_out % 16 || (uintptr_t)d_q % 16)
+    return fail(ctx, NCODEC_EINVAL, "d_q and d_frame_out must be 16-byte aligned");
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int P8 = (c.height / 8) * (c.width / 8), P16 = P8 / 4;
+  const Layout& L = ctx->L;
+  const int cur = ctx->cur, nxt = 1 - cur;
+
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.head.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+  pa.bias = ctx->p(L.head.bias);
+  pa.yhat_prev = ctx->p(L.yhat[cur]);
+  pa.q_in = d_q;
+  pa.yhat_new = ctx->p(L.yhat[nxt]);
+  pa.C = C;
+  pa.P = P16;
+  pa.decode = 1;
+  NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
+  st = run_decoder(ctx, nxt);
+  if (st) return st;
+
+  PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
+  a.src0 = ctx->p(L.feat[nxt]);
+  a.C0 = C;
+  a.dst = d_frame_out;
+  NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
+  ctx->cur = nxt;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const float* d_sigma, int64_t n,
+                                   double* d_bits) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_bits) return fail(ctx, NCODEC_EINVAL, "d_bits is NULL");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(ctx, NCODEC_EINVAL, "n out of range");
+  if (n > 0 && (!d_q || !d_sigma)) return fail(ctx, NCODEC_EINVAL, "d_q and d_sigma must be non-NULL");
+  NC_HIP(ctx, launch_estimate_bits(d_q, d_sigma, n, ctx->p<double>(ctx->L.partials), d_bits, ctx->stream),
+         "estimate_bits");
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_get_state(ncodec_ctx* ctx, void* d_feat, void* d_yhat) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  const int C = ctx->cfg.channels;
+  const int P8 = (ctx->cfg.height / 8) * (ctx->cfg.width / 8);
+  if (d_feat) NC_HIP(ctx, launch_nhwc_to_planar(ctx->p(ctx->L.feat[ctx->cur]), d_feat, C, P8, ctx->stream), "get_state");
+  if (d_yhat) NC_HIP(ctx, launch_nhwc_to_planar(ctx->p(ctx->L.yhat[ctx->cur]), d_yhat, C, P8 / 4, ctx->stream), "get_state");
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* d_yhat) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  const int C = ctx->cfg.channels;
+  const int P8 = (ctx->cfg.height / 8) * (ctx->cfg.width / 8);
+  if (d_feat) NC_HIP(ctx, launch_planar_to_nhwc(d_feat, ctx->p(ctx->L.feat[ctx->cur]), C, P8, ctx->stream), "set_state");
+  if (d_yhat) NC_HIP(ctx, launch_planar_to_nhwc(d_yhat, ctx->p(ctx->L.yhat[ctx->cur]), C, P8 / 4, ctx->stream), "set_state");
+  return NCODEC_OK;
+}
+
+int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
+  if (!ctx) return 0;
+  if (decode) return 4 + ctx->cfg.n_dec_blocks;
+  return 7 + ctx->cfg.n_enc_blocks + ctx->cfg.n_dec_blocks;
+}
+
+ncodec_status ncodec_timing_enable(ncodec_ctx* ctx, int32_t enable) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  ctx->timing = enable != 0;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_timing_read(ncodec_ctx* ctx, ncodec_kernel_timing* out, int32_t max_kinds, int32_t* n_kinds) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!n_kinds || (max_kinds > 0 && !out)) return fail(ctx, NCODEC_EINVAL, "out / n_kinds is NULL");
+  NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "timing_read");
+  std::vector<ncodec_kernel_timing> agg;
+  hipError_t err = hipSuccess;
+  for (auto& t : ctx->log) {
+    float ms = 0.f;
+    if (err == hipSuccess && t.start && t.stop) err = hipEventElapsedTime(&ms, t.start, t.stop);
+    size_t i = 0;
+    while (i < agg.size() && std::strcmp(agg[i].kind, t.kind) != 0) ++i;
+    if (i == agg.size()) {
+      ncodec_kernel_timing k;
+      std::memset(&k, 0, sizeof(k));
+      std::strncpy(k.kind, t.kind, sizeof(k.kind) - 1);
+      agg.push_back(k);
+    }
+    agg[i].launches += 1;
+    agg[i].total_ms += ms;
+    if (t.start) (void)hipEventDestroy(t.start);
+    if (t.stop) (void)hipEventDestroy(t.stop);
+  }
+  ctx->log.clear();
+  if (err != hipSuccess) return hip_fail(ctx, err, "hipEventElapsedTime");
+  *n_kinds = (int32_t)agg.size();
+  for (int32_t i = 0; i < max_kinds && i < (int32_t)agg.size(); ++i) out[i] = agg[i];
+  return NCODEC_OK;
+}
+
+const char* ncodec_last_error(const ncodec_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+const char* ncodec_status_string(ncodec_status st) {
+  switch (st) {
+    case NCODEC_OK: return "ok";
+    case NCODEC_EINVAL: return "invalid argument";
+    case NCODEC_ESHAPE: return "invalid shape or configuration";
+    case NCODEC_EHIP: return "HIP runtime error";
+    case NCODEC_ESTATE: return "call does not match the context";
+    case NCODEC_EOVERFLOW: return "int32 accumulator overflow";
+    case NCODEC_ENOMEM: return "workspace too small or misaligned";
+  }
+  return "unknown status";
+}
+
+void ncodec_destroy(ncodec_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipSetDevice(ctx->device);
+  (void)hipStreamSynchronize(ctx->stream);
+  for (auto& t : ctx->log) {
+    if (t.start) (void)hipEventDestroy(t.start);
+    if (t.stop) (void)hipEventDestroy(t.stop);
+  }
+  delete ctx;
+}
+
+}  // extern "C"

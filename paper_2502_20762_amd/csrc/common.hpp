@@ -1,0 +1,111 @@
+// Shared device helpers for the gfx950 kernels of ncodec.
+//
+// Every GEMM-shaped step is computed "transposed": out^T[rows = output
+// channels][cols = pixels] = W[rows][K] * act^T[K][pixels].  The weights are
+// the MFMA A operand (pre-packed in fragment order, one coalesced 1 KiB load
+// per wave per fragment), the activations are the B operand (8 or 16
+// consecutive channels of one pixel per lane, a 16/32-byte load from the
+// channels-last feature map), and in the 32x32 accumulator layout each lane
+// owns one pixel column, so chained contractions can feed one MFMA's result
+// straight into the next as its B operand without a trip through LDS.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef _Float16 f16;
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef int intx4 __attribute__((ext_vector_type(4)));
+typedef int intx16 __attribute__((ext_vector_type(16)));
+typedef short shortx8 __attribute__((ext_vector_type(8)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
+namespace nc {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerWG = 4;
+constexpr int kPxPerWave = 32;
+constexpr int kPxPerWG = kWave * kWavesPerWG / 2;  // 128 pixels per workgroup
+constexpr int kNumXCD = 8;
+
+// v_mfma_f32_32x32x16_f16: A lane l = row l%32, k 8*(l/32)+e; B lane l = k 8*(l/32)+e, col l%32.
+__device__ __forceinline__ floatx16 mfma_f16(half8 a, half8 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+// v_mfma_i32_32x32x32_i8: A lane l = row l%32, k 16*(l/32)+e (bytes); int32 accumulate wraps.
+__device__ __forceinline__ intx16 mfma_i8(intx4 a, intx4 b, intx16 c) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// Row of accumulator register r for lane half h in the 32x32 output layout.
+__host__ __device__ constexpr int drow(int r, int h) { return 8 * (r / 4) + 4 * h + (r % 4); }
+
+// Workgroup -> tile mapping that gives each XCD a contiguous range of tiles
+// (workgroups are dispatched round-robin over the 8 XCDs), so neighbouring
+// tiles that share halo rows hit the same L2.  The grid is a multiple of 8.
+__device__ __forceinline__ int xcd_tile(int bid, int nblk) {
+  const int per = nblk / kNumXCD;
+  return (bid % kNumXCD) * per + bid / kNumXCD;
+}
+
+// round-half-to-even of a / 2^s (1 <= s <= 30), from floor and remainder.
+__device__ __forceinline__ int rhe_shift(int a, int s) {
+  const int fl = a >> s;                       // arithmetic shift = floor
+  const int r = a & ((1 << s) - 1);            // a - fl * 2^s, in [0, 2^s)
+  const int half = 1 << (s - 1);
+  return fl + (int)((r > half) | ((r == half) & (fl & 1)));
+}
+__device__ __forceinline__ int clip16(int v) { return min(max(v, -32768), 32767); }
+
+// Combine the three partial products of an int16 x int16 contraction done as
+// int8 digits (x = 256 xh + xl' + 128, w = 256 wh + wl) in wrapping int32.
+__device__ __forceinline__ int combine_i16(int hh, int mid, int ll, int corr) {
+  const uint32_t v = ((uint32_t)hh << 16) + ((uint32_t)mid << 8) + (uint32_t)ll + (uint32_t)corr;
+  return (int)v;
+}
+
+// Split 4 int16 values (two dwords) into their high bytes (signed) and their
+// low bytes offset by -128 (xl' = (x & 255) - 128, i.e. the low byte ^ 0x80).
+__device__ __forceinline__ void split4(uint32_t d0, uint32_t d1, uint32_t& hi, uint32_t& lo) {
+  hi = ((d0 >> 8) & 0xFFu) | ((d0 >> 24) << 8) | (((d1 >> 8) & 0xFFu) << 16) | ((d1 >> 24) << 24);
+  lo = ((d0 & 0xFFu) | (((d0 >> 16) & 0xFFu) << 8) | ((d1 & 0xFFu) << 16) | (((d1 >> 16) & 0xFFu) << 24)) ^
+       0x80808080u;
+}
+
+// Split 16 int16 values (8 dwords) into hi / lo int8 fragments.
+__device__ __forceinline__ void split16(const uint32_t* d, intx4& hi, intx4& lo) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t h, l;
+    split4(d[2 * i], d[2 * i + 1], h, l);
+    hi[i] = (int)h;
+    lo[i] = (int)l;
+  }
+}
+
+__device__ __forceinline__ float leaky(float v) { return v >= 0.f ? v : 0.1f * v; }
+
+// Gaussian rate of one symbol, -log2(max(L, 1e-9)),
+// L = 1/2 [erfc((|q| - 1/2) / (sigma sqrt2)) - erfc((|q| + 1/2) / (sigma sqrt2))].
+__device__ __forceinline__ float symbol_bits(float q, float sigma) {
+  const float a = fabsf(q);
+  const float inv = 0.70710678118654752f / sigma;
+  const float L = 0.5f * (erfcf((a - 0.5f) * inv) - erfcf((a + 0.5f) * inv));
+  return -log2f(fmaxf(L, 1e-9f));
+}
+
+__device__ __forceinline__ float softplus_sigma(float s) {
+  const float sp = s > 20.f ? s : log1pf(expf(s));
+  return fmaxf(sp, 0.11f);
+}
+
+// Deterministic (fixed-order) wave reduction of a double.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+}  // namespace nc

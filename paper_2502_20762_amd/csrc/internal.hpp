@@ -1,0 +1,92 @@
+// Host-visible launch interface between the scheduler (api.hip) and the
+// kernel translation units.  Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace nc {
+
+// How a pointwise kernel gathers its activation operand (K index -> memory).
+enum Loader : int {
+  LD_NHWC = 0,   // k < C0: src0[p*C0 + k], else src1[p*C1 + k - C0]   (concat on channels)
+  LD_FRAME = 1,  // planar 3xHxW frame, pixel-unshuffle x8 on load: k = 64c + 8i + j
+  LD_DOWN = 2,   // 2x2 stride-2 gather: k = (2i+j)*Csrc + c from pixel (2Y+i, 2X+j)
+};
+// Where a pointwise kernel writes its result.
+enum Epi : int {
+  EP_NHWC = 0,  // dst[p*Cdst + n]
+  EP_UP = 1,    // rows ordered (sub-position, channel): pixel-shuffle x2 into the 1/8 grid
+  EP_REC = 2,   // rows 64c+8i+j: pixel-shuffle x8 into a planar 3xHxW frame, clamped
+};
+
+struct PwArgs {
+  const void* wfrag;     // fp16: half8 [N/32][K/16][64]; int: int8x16 hi plane [N/32][K/32][64]
+  const void* wfrag_lo;  // int: lo plane, same shape
+  const void* bias;      // fp16 path: float[N]; int path: int32 correction[N]
+  int K;
+  int N;
+  int P;                 // output pixels
+  const void* src0;
+  const void* src1;
+  int C0, C1;
+  int w8;                // width of the 1/8-scale grid
+  int H, W;              // frame size
+  int Csrc;              // channels of the LD_DOWN source
+  void* dst;
+  int Cdst;
+};
+
+struct BlockArgs {
+  const void* w1;
+  const void* w1lo;
+  const void* b1;
+  const void* w2;
+  const void* w2lo;
+  const void* b2;
+  const void* dww;  // [9][C]
+  const void* dwb;  // [C]
+  const void* src;  // z (NHWC)
+  void* dst;        // z' (NHWC), must not alias src
+  int h, w;
+};
+
+struct PriorArgs {
+  const void* wfrag;
+  const void* wfrag_lo;
+  const void* bias;       // [2C] (rows mu then s)
+  const void* yhat_prev;  // NHWC latent
+  const void* y;          // NHWC latent (encode)
+  const int16_t* q_in;    // planar (decode)
+  int16_t* q_out;         // planar (encode)
+  void* yhat_new;         // NHWC latent
+  double* partials;       // one per (tile, channel slice) (encode)
+  const float* sigma_tab; // int path: sigma for s_i + 32768
+  int C;
+  int P;
+  int decode;
+};
+
+hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
+hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
+hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st);
+hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st);
+hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials);
+hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials);
+int prior_partials_f16(int C, int P);
+int prior_partials_i16(int C, int P);
+
+hipError_t launch_reduce(const double* partials, int n, double* out, hipStream_t st);
+constexpr int kBitsBlocks = 1024;
+hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n, double* partials,
+                                double* out, hipStream_t st);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
+hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);
+
+inline int grid_tiles(int P) {
+  const int t = (P + 127) / 128;
+  return (t + 7) / 8 * 8;
+}
+
+}  // namespace nc

@@ -1,0 +1,402 @@
+// Integerised path kernels (Sec. 4.5; Supp. B.4, Alg. 1) for gfx950.
+//
+// CDNA4 has no int16 matrix instruction, so every int16 x int16 -> int32
+// contraction is done exactly on the int8 MFMA: activations split as
+// x = 256 xh + xl' + 128 (xh = x >> 8, xl' = (x & 255) - 128) and weights as
+// balanced digits w = 256 wh + wl, giving
+//   sum x w = 65536 sum xh wh + 256 (sum xh wl + sum xl' wh) + sum xl' wl + 128 sum w.
+// Each partial sum fits int32 for K <= 1024; the final combination wraps
+// modulo 2^32 exactly like an int32 accumulator, so the result equals the
+// exact sum whenever that sum fits int32 (the paper's accumulator contract).
+// The 128 sum w term and the bias term 512 b_i are pre-added per output
+// channel ("corr").  Every conv then rescales with round-half-to-even of
+// a / 8192 and saturates to int16.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace nc {
+
+__device__ __forceinline__ int rescale13(int a) { return clip16(rhe_shift(a, 13)); }
+
+__device__ __forceinline__ uint32_t pack2(int lo, int hi) {
+  return ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
+}
+
+// 16 consecutive int16 activations of pixel p starting at channel k0 -> hi/lo fragments.
+template <int LOADER>
+__device__ __forceinline__ void load_b_i16(const PwArgs& a, int p, int k0, intx4& bh, intx4& bl) {
+  uint32_t d[8];
+  if constexpr (LOADER == LD_FRAME) {
+    const int py = p / a.w8, px = p - py * a.w8;
+    const int c = k0 >> 6, i = (k0 >> 3) & 7;  // rows i and i + 1, 8 pixels each
+    const f16* base = (const f16*)a.src0 + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px;
+    const half8 r0 = *(const half8*)base;
+    const half8 r1 = *(const half8*)(base + a.W);
+    int v[16];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] = clip16((int)rintf((float)r0[e] * 512.f));
+      v[8 + e] = clip16((int)rintf((float)r1[e] * 512.f));
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = pack2(v[2 * e], v[2 * e + 1]);
+  } else {
+    const int16_t* ptr;
+    if constexpr (LOADER == LD_NHWC) {
+      ptr = (k0 < a.C0) ? (const int16_t*)a.src0 + (size_t)p * a.C0 + k0
+                        : (const int16_t*)a.src1 + (size_t)p * a.C1 + (k0 - a.C0);
+    } else {
+      const int w16 = a.w8 >> 1;
+      const int Y = p / w16, X = p - Y * w16;
+      const int tap = k0 / a.Csrc, c = k0 - tap * a.Csrc;
+      const int pix = (2 * Y + (tap >> 1)) * a.w8 + 2 * X + (tap & 1);
+      ptr = (const int16_t*)a.src0 + (size_t)pix * a.Csrc + c;
+    }
+    const intx4 q0 = *(const intx4*)ptr;
+    const intx4 q1 = *(const intx4*)(ptr + 8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
+  }
+  split16(d, bh, bl);
+}
+
+template <int NT, int LOADER, int EPI>
+__global__ __launch_bounds__(256) void k_pw_i16(PwArgs a) {
+  constexpr int MT = NT / 32;
+  const int ntile = (a.P + 127) / 128;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= ntile) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
+  const int p = tile * 128 + wave * 32 + (lane & 31);
+  const bool valid = p < a.P;
+  const int mt0 = blockIdx.y * MT;
+  const int ks = a.K / 32;
+  const intx4* wh = (const intx4*)a.wfrag;
+  const intx4* wl = (const intx4*)a.wfrag_lo;
+
+  intx16 ahh[MT], amid[MT], all[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) { ahh[t] = intx16{}; amid[t] = intx16{}; all[t] = intx16{}; }
+
+  for (int s = 0; s < ks; ++s) {
+    intx4 bh = {}, bl = {};
+    if (valid) load_b_i16<LOADER>(a, p, 32 * s + 16 * h, bh, bl);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const size_t idx = ((size_t)(mt0 + t) * ks + s) * 64 + lane;
+      const intx4 ah = wh[idx], al = wl[idx];
+      ahh[t] = mfma_i8(ah, bh, ahh[t]);
+      amid[t] = mfma_i8(ah, bl, amid[t]);
+      amid[t] = mfma_i8(al, bh, amid[t]);
+      all[t] = mfma_i8(al, bl, all[t]);
+    }
+  }
+  if (!valid) return;
+
+  const int* corr = (const int*)a.bias;
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = 32 * (mt0 + t) + 8 * g + 4 * h;
+      const intx4 cv = *(const intx4*)(corr + n);
+      int v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g + e;
+        v[e] = rescale13(combine_i16(ahh[t][r], amid[t][r], all[t][r], cv[e]));
+      }
+      if constexpr (EPI == EP_REC) {
+        shortx4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (short)min(max(v[e], 0), 512);
+        const int c = n >> 6, i = (n >> 3) & 7, j0 = n & 7;
+        const int py = p / a.w8, px = p - py * a.w8;
+        *(shortx4*)((int16_t*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px + j0) = o;
+      } else {
+        shortx4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (short)v[e];
+        if constexpr (EPI == EP_NHWC) {
+          *(shortx4*)((int16_t*)a.dst + (size_t)p * a.Cdst + n) = o;
+        } else {
+          const int C = a.Cdst;
+          const int sp = n / C, c = n - sp * C;
+          const int w16 = a.w8 >> 1;
+          const int Y = p / w16, X = p - Y * w16;
+          const int pix = (2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1);
+          *(shortx4*)((int16_t*)a.dst + (size_t)pix * C + c) = o;
+        }
+      }
+    }
+  }
+}
+
+// Whole DC block on the integer path.  The hidden activations g (2C per
+// pixel) are kept in registers as int8 digit fragments, then the second
+// pointwise conv runs one output tile at a time with three accumulators.
+template <int C>
+__global__ __launch_bounds__(256) void k_dcblock_i16(BlockArgs a) {
+  constexpr int KS = C / 32;       // k-steps (32 channels) over C
+  constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 = k-steps of the second conv
+  constexpr int MT = C / 32;
+  const int P = a.h * a.w;
+  const int ntile = (P + 127) / 128;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= ntile) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
+  const int p = tile * 128 + wave * 32 + (lane & 31);
+  const bool valid = p < P;
+  const int y = valid ? p / a.w : 0, x = valid ? p - y * a.w : 0;
+  const int16_t* z = (const int16_t*)a.src;
+
+  intx4 ah[KS], al[KS];
+  {
+    const int16_t* dww = (const int16_t*)a.dww;
+    const int* dwb = (const int*)a.dwb;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int c0 = 32 * s + 16 * h;
+      int acc[16];
+#pragma unroll
+      for (int e = 0; e < 16; e += 4) {
+        const intx4 bv = *(const intx4*)(dwb + c0 + e);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[e + u] = bv[u];
+      }
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const int yy = y + ky - 1;
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const int xx = x + kx - 1;
+          if (valid && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w) {
+            const shortx8* vp = (const shortx8*)(z + (size_t)(yy * a.w + xx) * C + c0);
+            const shortx8* wp = (const shortx8*)(dww + (ky * 3 + kx) * C + c0);
+            const shortx8 v0 = vp[0], v1 = vp[1], w0 = wp[0], w1 = wp[1];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              acc[e] += (int)w0[e] * (int)v0[e];
+              acc[8 + e] += (int)w1[e] * (int)v1[e];
+            }
+          }
+        }
+      }
+      uint32_t d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = pack2(rescale13(acc[2 * e]), rescale13(acc[2 * e + 1]));
+      split16(d, ah[s], al[s]);
+    }
+  }
+
+  const intx4* w1h = (const intx4*)a.w1;
+  const intx4* w1l = (const intx4*)a.w1lo;
+  const int* c1 = (const int*)a.b1;
+  intx4 gh[NCH], gl[NCH];
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) {
+    intx16 hh = {}, mid = {}, ll = {};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const size_t idx = ((size_t)j * KS + s) * 64 + lane;
+      const intx4 wa = w1h[idx], wb = w1l[idx];
+      hh = mfma_i8(wa, ah[s], hh);
+      mid = mfma_i8(wa, al[s], mid);
+      mid = mfma_i8(wb, ah[s], mid);
+      ll = mfma_i8(wb, al[s], ll);
+    }
+    int gv[16];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const intx4 cv = *(const intx4*)(c1 + 32 * j + 8 * g + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g + e;
+        const int hv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
+        gv[r] = hv >= 0 ? hv : rhe_shift(819 * hv, 13);
+      }
+    }
+    uint32_t d[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = pack2(gv[2 * e], gv[2 * e + 1]);
+    split16(d, gh[j], gl[j]);
+  }
+
+  const intx4* w2h = (const intx4*)a.w2;
+  const intx4* w2l = (const intx4*)a.w2lo;
+  const int* c2 = (const int*)a.b2;
+  int16_t* dst = (int16_t*)a.dst;
+#pragma unroll 1
+  for (int t = 0; t < MT; ++t) {
+    intx16 hh = {}, mid = {}, ll = {};
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      const size_t idx = ((size_t)t * NCH + j) * 64 + lane;
+      const intx4 wa = w2h[idx], wb = w2l[idx];
+      hh = mfma_i8(wa, gh[j], hh);
+      mid = mfma_i8(wa, gl[j], mid);
+      mid = mfma_i8(wb, gh[j], mid);
+      ll = mfma_i8(wb, gl[j], ll);
+    }
+    if (valid) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 32 * t + 8 * g + 4 * h;
+        const intx4 cv = *(const intx4*)(c2 + c);
+        const shortx4 zv = *(const shortx4*)(z + (size_t)p * C + c);
+        shortx4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          const int pv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
+          o[e] = (short)clip16((int)zv[e] + pv);
+        }
+        *(shortx4*)(dst + (size_t)p * C + c) = o;
+      }
+    }
+  }
+}
+
+// Integer prior head, quantiser q = round((y_i - mu_i) / 512), yhat = clip(512 q + mu_i)
+// and bits with sigma looked up from the 65536-entry table indexed by s_i.
+template <int CH, bool DECODE>
+__global__ __launch_bounds__(256) void k_prior_i16(PriorArgs a) {
+  constexpr int MT = CH / 32;
+  const int ntile = (a.P + 127) / 128;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= ntile) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
+  const int p = tile * 128 + wave * 32 + (lane & 31);
+  const bool valid = p < a.P;
+  const int C = a.C;
+  const int ct0 = blockIdx.y * MT;
+  const int ks = C / 32;
+  const intx4* wh = (const intx4*)a.wfrag;
+  const intx4* wl = (const intx4*)a.wfrag_lo;
+  const int16_t* yp = (const int16_t*)a.yhat_prev;
+
+  intx16 mhh[MT], mmid[MT], mll[MT], shh[MT], smid[MT], sll[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    mhh[t] = intx16{}; mmid[t] = intx16{}; mll[t] = intx16{};
+    shh[t] = intx16{}; smid[t] = intx16{}; sll[t] = intx16{};
+  }
+  for (int s = 0; s < ks; ++s) {
+    intx4 bh = {}, bl = {};
+    if (valid) {
+      const int16_t* ptr = yp + (size_t)p * C + 32 * s + 16 * h;
+      const intx4 q0 = *(const intx4*)ptr, q1 = *(const intx4*)(ptr + 8);
+      uint32_t d[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
+      split16(d, bh, bl);
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      size_t idx = ((size_t)(ct0 + t) * ks + s) * 64 + lane;
+      intx4 xa = wh[idx], xb = wl[idx];
+      mhh[t] = mfma_i8(xa, bh, mhh[t]);
+      mmid[t] = mfma_i8(xa, bl, mmid[t]);
+      mmid[t] = mfma_i8(xb, bh, mmid[t]);
+      mll[t] = mfma_i8(xb, bl, mll[t]);
+      if constexpr (!DECODE) {
+        idx = ((size_t)(C / 32 + ct0 + t) * ks + s) * 64 + lane;
+        xa = wh[idx];
+        xb = wl[idx];
+        shh[t] = mfma_i8(xa, bh, shh[t]);
+        smid[t] = mfma_i8(xa, bl, smid[t]);
+        smid[t] = mfma_i8(xb, bh, smid[t]);
+        sll[t] = mfma_i8(xb, bl, sll[t]);
+      }
+    }
+  }
+
+  const int* corr = (const int*)a.bias;
+  double bsum = 0.0;
+  if (valid) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 32 * (ct0 + t) + 8 * g + 4 * h;
+        const intx4 cm = *(const intx4*)(corr + c);
+        shortx4 yh;
+        if constexpr (DECODE) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e;
+            const int mu = rescale13(combine_i16(mhh[t][r], mmid[t][r], mll[t][r], cm[e]));
+            const int q = a.q_in[(size_t)(c + e) * a.P + p];
+            yh[e] = (short)clip16(512 * q + mu);
+          }
+        } else {
+          const intx4 cs = *(const intx4*)(corr + C + c);
+          const shortx4 yv = *(const shortx4*)((const int16_t*)a.y + (size_t)p * C + c);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e;
+            const int mu = rescale13(combine_i16(mhh[t][r], mmid[t][r], mll[t][r], cm[e]));
+            const int sv = rescale13(combine_i16(shh[t][r], smid[t][r], sll[t][r], cs[e]));
+            const int q = rhe_shift((int)yv[e] - mu, 9);
+            a.q_out[(size_t)(c + e) * a.P + p] = (int16_t)q;
+            yh[e] = (short)clip16(512 * q + mu);
+            bsum += (double)symbol_bits((float)q, a.sigma_tab[sv + 32768]);
+          }
+        }
+        *(shortx4*)((int16_t*)a.yhat_new + (size_t)p * C + c) = yh;
+      }
+    }
+  }
+  if constexpr (DECODE) return;
+  __shared__ double red[4];
+  bsum = wave_sum(bsum);
+  if (lane == 0) red[wave] = bsum;
+  __syncthreads();
+  if (threadIdx.x == 0) a.partials[(size_t)tile * gridDim.y + blockIdx.y] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+template <int NT>
+static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
+  dim3 grid(grid_tiles(a.P), a.N / NT), block(256);
+#define NC_PW(L, E)                                                            \
+  if (loader == L && epi == E) {                                               \
+    hipLaunchKernelGGL((k_pw_i16<NT, L, E>), grid, block, 0, st, a);           \
+    return hipGetLastError();                                                  \
+  }
+  NC_PW(LD_NHWC, EP_NHWC)
+  NC_PW(LD_FRAME, EP_NHWC)
+  NC_PW(LD_DOWN, EP_NHWC)
+  NC_PW(LD_NHWC, EP_UP)
+  NC_PW(LD_NHWC, EP_REC)
+#undef NC_PW
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
+  if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
+  if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
+  dim3 grid(grid_tiles(a.h * a.w)), block(256);
+  switch (C) {
+    case 64: hipLaunchKernelGGL((k_dcblock_i16<64>), grid, block, 0, st, a); break;
+    case 128: hipLaunchKernelGGL((k_dcblock_i16<128>), grid, block, 0, st, a); break;
+    case 256: hipLaunchKernelGGL((k_dcblock_i16<256>), grid, block, 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int prior_partials_i16(int C, int P) { return grid_tiles(P) * (C / 64); }
+
+hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials) {
+  dim3 grid(grid_tiles(a.P), a.C / 64), block(256);
+  if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / 64);
+  if (a.decode) hipLaunchKernelGGL((k_prior_i16<64, true>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((k_prior_i16<64, false>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace nc

@@ -1,0 +1,95 @@
+// Small kernels: deterministic bit reduction, the standalone rate estimate,
+// zero fill, and state layout conversion (channels-last <-> planar).
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace nc {
+
+// One workgroup; thread t sums partials t, t+256, ... in order, then a fixed
+// LDS tree.  The result does not depend on timing.
+__global__ __launch_bounds__(256) void k_reduce(const double* part, int n, double* out) {
+  __shared__ double sh[256];
+  double v = 0.0;
+  for (int i = threadIdx.x; i < n; i += 256) v += part[i];
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = sh[0];
+}
+
+// Block b owns elements [b*chunk, min(n, (b+1)*chunk)); chunk depends only on n.
+__global__ __launch_bounds__(256) void k_bits(const int16_t* q, const float* sigma, int64_t n, int64_t chunk,
+                                              double* part) {
+  const int64_t lo = (int64_t)blockIdx.x * chunk;
+  const int64_t hi = min(n, lo + chunk);
+  double v = 0.0;
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) v += (double)symbol_bits((float)q[i], sigma[i]);
+  __shared__ double red[4];
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+__global__ void k_fill_zero(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+// planar[c*P + p] = nhwc[p*C + c] (2-byte elements)
+__global__ void k_nhwc_to_planar(const uint16_t* src, uint16_t* dst, int C, int P) {
+  const size_t n = (size_t)C * P;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t c = i / P, p = i - c * P;
+    dst[i] = src[p * C + c];
+  }
+}
+
+__global__ void k_planar_to_nhwc(const uint16_t* src, uint16_t* dst, int C, int P) {
+  const size_t n = (size_t)C * P;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t p = i / C, c = i - p * C;
+    dst[i] = src[c * P + p];
+  }
+}
+
+hipError_t launch_reduce(const double* partials, int n, double* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_reduce, dim3(1), dim3(256), 0, st, partials, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n, double* partials, double* out,
+                                hipStream_t st) {
+  const int64_t chunk = n > 0 ? (n + kBitsBlocks - 1) / kBitsBlocks : 1;
+  hipLaunchKernelGGL(k_bits, dim3(kBitsBlocks), dim3(256), 0, st, q, sigma, n, chunk, partials);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_reduce(partials, kBitsBlocks, out, st);
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_fill_zero, dim3(blocks), dim3(256), 0, st, (uint32_t*)p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st) {
+  const size_t n = (size_t)C * P;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_nhwc_to_planar, dim3(blocks), dim3(256), 0, st, (const uint16_t*)src, (uint16_t*)dst, C, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st) {
+  const size_t n = (size_t)C * P;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_planar_to_nhwc, dim3(blocks), dim3(256), 0, st, (const uint16_t*)src, (uint16_t*)dst, C, P);
+  return hipGetLastError();
+}
+
+}  // namespace nc

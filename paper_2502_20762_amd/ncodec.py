@@ -1,0 +1,262 @@
+"""ctypes binding of libncodec.so (the C ABI declared in include/ncodec.h).
+
+The ``ncodec_*`` functions mirror the C entry points one to one and only
+marshal arguments: device buffers are passed as integer addresses, host
+weights as a float32 NumPy array.  :class:`Codec` is a thin convenience layer
+that uses PyTorch for device memory and the stream; every step of the
+transform runs in the HIP kernels of the library.  There is no fallback: if
+the library is not built, importing the binding raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libncodec.so")
+
+NCODEC_OK = 0
+NCODEC_EINVAL = -1
+NCODEC_ESHAPE = -2
+NCODEC_EHIP = -3
+NCODEC_ESTATE = -4
+NCODEC_EOVERFLOW = -5
+NCODEC_ENOMEM = -6
+NCODEC_PATH_FP16 = 0
+NCODEC_PATH_INT16 = 1
+
+PATHS = {"fp16": NCODEC_PATH_FP16, "int16": NCODEC_PATH_INT16}
+
+
+class ncodec_config(ctypes.Structure):
+    _fields_ = [
+        ("height", ctypes.c_int32),
+        ("width", ctypes.c_int32),
+        ("channels", ctypes.c_int32),
+        ("n_enc_blocks", ctypes.c_int32),
+        ("n_dec_blocks", ctypes.c_int32),
+        ("path", ctypes.c_int32),
+    ]
+
+
+class ncodec_kernel_timing(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_char * 16), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+class NcodecError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"ncodec status {status}: {message}")
+        self.status = status
+
+
+_P = ctypes.c_void_p
+_SIGNATURES = {
+    "ncodec_weight_count": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
+    "ncodec_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
+    "ncodec_create": (ctypes.c_int, [ctypes.POINTER(ncodec_config), _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P,
+                                     ctypes.POINTER(_P)]),
+    "ncodec_reset": (ctypes.c_int, [_P]),
+    "ncodec_encode_frame": (ctypes.c_int, [_P, _P, _P, _P]),
+    "ncodec_decode_frame": (ctypes.c_int, [_P, _P, _P]),
+    "ncodec_estimate_bits": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P]),
+    "ncodec_get_state": (ctypes.c_int, [_P, _P, _P]),
+    "ncodec_set_state": (ctypes.c_int, [_P, _P, _P]),
+    "ncodec_kernels_per_frame": (ctypes.c_int32, [_P, ctypes.c_int32]),
+    "ncodec_timing_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "ncodec_timing_read": (ctypes.c_int, [_P, ctypes.POINTER(ncodec_kernel_timing), ctypes.c_int32,
+                                          ctypes.POINTER(ctypes.c_int32)]),
+    "ncodec_last_error": (ctypes.c_char_p, [_P]),
+    "ncodec_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "ncodec_destroy": (None, [_P]),
+}
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2502_20762_amd.build` "
+                          "(there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path) -> ncodec_config:
+    if isinstance(path, str):
+        path = PATHS[path]
+    return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path)
+
+
+def _check(st: int, ctx=None) -> None:
+    if st != NCODEC_OK:
+        msg = load_library().ncodec_last_error(ctx)
+        raise NcodecError(st, (msg or b"").decode() or load_library().ncodec_status_string(st).decode())
+
+
+# ---------------------------------------------------------------- C entry points
+def ncodec_weight_count(cfg: ncodec_config) -> int:
+    return int(load_library().ncodec_weight_count(ctypes.byref(cfg)))
+
+
+def ncodec_workspace_bytes(cfg: ncodec_config) -> int:
+    return int(load_library().ncodec_workspace_bytes(ctypes.byref(cfg)))
+
+
+def ncodec_create(cfg: ncodec_config, host_weights: np.ndarray, d_workspace: int, ws_bytes: int,
+                  hip_stream: int = 0):
+    w = np.ascontiguousarray(host_weights, dtype=np.float32)
+    out = _P()
+    st = load_library().ncodec_create(ctypes.byref(cfg), w.ctypes.data, w.size, d_workspace, ws_bytes,
+                                      hip_stream or None, ctypes.byref(out))
+    _check(st, None)
+    return out
+
+
+def ncodec_reset(ctx) -> None:
+    _check(load_library().ncodec_reset(ctx), ctx)
+
+
+def ncodec_encode_frame(ctx, d_frame: int, d_q: int, d_bits: int = 0) -> None:
+    _check(load_library().ncodec_encode_frame(ctx, d_frame, d_q, d_bits or None), ctx)
+
+
+def ncodec_decode_frame(ctx, d_q: int, d_frame_out: int) -> None:
+    _check(load_library().ncodec_decode_frame(ctx, d_q, d_frame_out), ctx)
+
+
+def ncodec_estimate_bits(ctx, d_q: int, d_sigma: int, n: int, d_bits: int) -> None:
+    _check(load_library().ncodec_estimate_bits(ctx, d_q or None, d_sigma or None, n, d_bits), ctx)
+
+
+def ncodec_get_state(ctx, d_feat: int, d_yhat: int) -> None:
+    _check(load_library().ncodec_get_state(ctx, d_feat or None, d_yhat or None), ctx)
+
+
+def ncodec_set_state(ctx, d_feat: int, d_yhat: int) -> None:
+    _check(load_library().ncodec_set_state(ctx, d_feat or None, d_yhat or None), ctx)
+
+
+def ncodec_kernels_per_frame(ctx, decode: bool) -> int:
+    return int(load_library().ncodec_kernels_per_frame(ctx, 1 if decode else 0))
+
+
+def ncodec_timing_enable(ctx, enable: bool) -> None:
+    _check(load_library().ncodec_timing_enable(ctx, 1 if enable else 0), ctx)
+
+
+def ncodec_timing_read(ctx) -> dict:
+    """{kind: (launches, total_ms)} for the kernels enqueued since timing was enabled."""
+    buf = (ncodec_kernel_timing * 32)()
+    n = ctypes.c_int32(0)
+    _check(load_library().ncodec_timing_read(ctx, buf, 32, ctypes.byref(n)), ctx)
+    return {buf[i].kind.decode(): (int(buf[i].launches), float(buf[i].total_ms)) for i in range(min(n.value, 32))}
+
+
+def ncodec_last_error(ctx=None) -> str:
+    return (load_library().ncodec_last_error(ctx) or b"").decode()
+
+
+def ncodec_status_string(st: int) -> str:
+    return load_library().ncodec_status_string(st).decode()
+
+
+def ncodec_destroy(ctx) -> None:
+    load_library().ncodec_destroy(ctx)
+
+
+# ---------------------------------------------------------------- convenience
+class Codec:
+    """One encoder or decoder context with a torch-allocated workspace.
+
+    Frames are (3, H, W) fp16 CUDA tensors; symbols are (C, H/16, W/16) int16.
+    """
+
+    def __init__(self, height, width, channels, n_enc_blocks, n_dec_blocks, path, weights,
+                 device="cuda:0", stream=None):
+        import torch
+
+        self.torch = torch
+        self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path)
+        self.device = torch.device(device)
+        self.path = self.cfg.path
+        nbytes = ncodec_workspace_bytes(self.cfg)
+        if nbytes == 0:
+            raise NcodecError(NCODEC_ESHAPE, "invalid configuration")
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            self.ctx = ncodec_create(self.cfg, weights, self.workspace.data_ptr(), nbytes, self.stream.cuda_stream)
+        H, W, C = height, width, channels
+        self.frame_shape = (3, H, W)
+        self.q_shape = (C, H // 16, W // 16)
+        self.feat_shape = (C, H // 8, W // 8)
+        self.state_dtype = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float16
+
+    def _empty(self, shape, dtype):
+        return self.torch.empty(shape, dtype=dtype, device=self.device)
+
+    def encode(self, frame, q_out=None, bits_out=None, want_bits=True):
+        torch = self.torch
+        assert frame.dtype == torch.float16 and tuple(frame.shape) == self.frame_shape and frame.is_contiguous()
+        q = q_out if q_out is not None else self._empty(self.q_shape, torch.int16)
+        bits = bits_out if bits_out is not None else (self._empty((), torch.float64) if want_bits else None)
+        ncodec_encode_frame(self.ctx, frame.data_ptr(), q.data_ptr(), bits.data_ptr() if bits is not None else 0)
+        return q, bits
+
+    def decode(self, q, out=None):
+        torch = self.torch
+        assert q.dtype == torch.int16 and tuple(q.shape) == self.q_shape and q.is_contiguous()
+        odt = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float16
+        x = out if out is not None else self._empty(self.frame_shape, odt)
+        ncodec_decode_frame(self.ctx, q.data_ptr(), x.data_ptr())
+        return x
+
+    def estimate_bits(self, q, sigma, bits_out=None):
+        torch = self.torch
+        assert q.dtype == torch.int16 and sigma.dtype == torch.float32 and q.numel() == sigma.numel()
+        bits = bits_out if bits_out is not None else self._empty((), torch.float64)
+        ncodec_estimate_bits(self.ctx, q.data_ptr(), sigma.data_ptr(), q.numel(), bits.data_ptr())
+        return bits
+
+    def get_state(self):
+        feat = self._empty(self.feat_shape, self.state_dtype)
+        yhat = self._empty(self.q_shape, self.state_dtype)
+        ncodec_get_state(self.ctx, feat.data_ptr(), yhat.data_ptr())
+        return feat, yhat
+
+    def set_state(self, feat, yhat):
+        assert feat.dtype == self.state_dtype and yhat.dtype == self.state_dtype
+        assert feat.is_contiguous() and yhat.is_contiguous()
+        ncodec_set_state(self.ctx, feat.data_ptr(), yhat.data_ptr())
+
+    def reset(self):
+        ncodec_reset(self.ctx)
+
+    def kernels_per_frame(self, decode=False):
+        return ncodec_kernels_per_frame(self.ctx, decode)
+
+    def timing(self, enable: bool):
+        ncodec_timing_enable(self.ctx, enable)
+
+    def timing_read(self) -> dict:
+        return ncodec_timing_read(self.ctx)
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            ncodec_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

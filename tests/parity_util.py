@@ -1,0 +1,68 @@
+"""Helpers shared by the GPU parity tests (comparison rules and crops)."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+import synth
+from oracle import codec_float as cf
+from oracle import codec_int as ci
+
+FP16_TOL = 2e-2  # |gpu - ref| <= 2e-2 * max(1, |ref|) on the fp16 path
+
+
+def assert_close_fp16(got, ref, what, tol=FP16_TOL):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    err = np.abs(got - ref)
+    lim = tol * np.maximum(1.0, np.abs(ref))
+    bad = err > lim
+    assert not bad.any(), (f"{what}: {int(bad.sum())} of {bad.size} elements out of tolerance, "
+                           f"max err {err.max():.4g} (at ref {ref.flat[int(np.argmax(err))]:.4g})")
+    return float(err.max())
+
+
+def q_band(y, mu, tol=FP16_TOL):
+    """Elements whose rounding y - mu is ambiguous within the fp16 error band."""
+    d = np.asarray(y, np.float64) - np.asarray(mu, np.float64)
+    frac = d - np.floor(d)
+    return np.abs(frac - 0.5) <= tol * np.maximum(1.0, np.abs(np.asarray(y, np.float64)))
+
+
+def params_for(C, ne, nd):
+    flat = synth.make_weights(C, ne, nd)
+    p = oracle.unpack(flat, C, ne, nd)
+    return flat, p
+
+
+def check_fp16_encode(p, x, feat_prev, yhat_prev, q_gpu, bits_gpu, feat_new, yhat_new, what="",
+                      valid=None):
+    """Teacher-forced fp16 comparison of one encoded frame.
+
+    The oracle starts from the GPU's state; q must agree outside the rounding
+    band; bits, yhat and f_t are compared using the GPU's q.  ``valid`` is an
+    optional (latent-grid slice, 1/8-grid slice) pair restricting the
+    comparison to a region (crops)."""
+    y = cf.analysis(p, x, feat_prev)
+    mu, s = cf.prior(p, yhat_prev)
+    q = np.asarray(q_gpu, np.float64)
+    band = q_band(y, mu)
+    q_ref = np.rint(y - mu)
+    sl16, sl8 = valid if valid is not None else (np.s_[:, :, :], np.s_[:, :, :])
+    mism = (q != q_ref) & ~band
+    assert not mism[sl16].any(), f"{what}: q differs outside the rounding band at {int(mism[sl16].sum())} elements"
+    agree = float(np.mean((q == q_ref)[sl16]))
+    assert agree > 0.99, f"{what}: q agreement {agree}"
+    yhat_ref = q + mu
+    assert_close_fp16(np.asarray(yhat_new)[sl16], yhat_ref[sl16], what + " yhat")
+    f_ref = cf.decoder_feature(p, yhat_ref, feat_prev)
+    err = assert_close_fp16(np.asarray(feat_new)[sl8], f_ref[sl8], what + " f_t")
+    if bits_gpu is not None:
+        ref_bits = oracle.estimate_bits(q[sl16], oracle.sigma_from_s(s)[sl16])
+        assert abs(bits_gpu - ref_bits) <= 1e-2 * abs(ref_bits), (what, bits_gpu, ref_bits)
+    return f_ref, err
+
+
+def int_state(feat, yhat):
+    return ci.State(np.asarray(feat, np.int64), np.asarray(yhat, np.int64))

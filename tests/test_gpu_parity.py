@@ -1,0 +1,184 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+fp16 path: teacher-forced per frame (the oracle starts from the GPU's state),
+|gpu - oracle| <= 2e-2 max(1, |oracle|) on yhat, f_t and the reconstruction,
+q equal outside the rounding band, bits within 1e-2 relative.
+int path: free-running, bit-exact on q, yhat, f_t and the reconstruction.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from oracle import codec_float as cf
+from oracle import codec_int as ci
+from paper_2502_20762_amd.ncodec import Codec
+
+from parity_util import assert_close_fp16, check_fp16_encode, int_state, params_for
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def host_state(codec):
+    f, y = codec.get_state()
+    return host(f).astype(np.float64 if f.dtype == torch.float16 else np.int64), \
+        host(y).astype(np.float64 if y.dtype == torch.float16 else np.int64)
+
+
+def run_fp16_sequence(H, W, C, ne, nd, frames, what):
+    flat, p = params_for(C, ne, nd)
+    enc = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV)
+    dec = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV)
+    worst = 0.0
+    for t, x in enumerate(frames):
+        say(what, "frame", t, (H, W, C, ne, nd))
+        fprev, yprev = host_state(enc)
+        q, bits = enc.encode(gpu(x))
+        fnew, ynew = host_state(enc)
+        qh = host(q)
+        f_ref, err = check_fp16_encode(p, x, fprev, yprev, qh, float(host(bits)), fnew, ynew, f"{what} t={t}")
+        worst = max(worst, err)
+        xhat = host(dec.decode(q)).astype(np.float64)
+        df, dy = host_state(dec)
+        np.testing.assert_array_equal(df, fnew, err_msg="decoder f_t != encoder f_t")
+        np.testing.assert_array_equal(dy, ynew, err_msg="decoder yhat != encoder yhat")
+        assert_close_fp16(xhat, cf.reconstruct(p, f_ref), f"{what} t={t} xhat")
+    return worst
+
+
+def run_int_sequence(H, W, C, ne, nd, frames, what):
+    flat, p = params_for(C, ne, nd)
+    ip = ci.integerize(p)
+    enc = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
+    dec = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
+    st = ci.zero_state(ip, H, W)
+    for t, x in enumerate(frames):
+        say(what, "frame", t, (H, W, C, ne, nd))
+        r = ci.encode_frame(ip, x, st)
+        q, bits = enc.encode(gpu(x))
+        np.testing.assert_array_equal(host(q), r.q, err_msg=f"{what} t={t} q")
+        f, y = host_state(enc)
+        np.testing.assert_array_equal(f, r.state.feat, err_msg=f"{what} t={t} f_t")
+        np.testing.assert_array_equal(y, r.state.yhat, err_msg=f"{what} t={t} yhat")
+        assert abs(float(host(bits)) - r.bits) <= 1e-5 * abs(r.bits), (float(host(bits)), r.bits)
+        xhat_ref, sd = ci.decode_frame(ip, r.q, st)
+        xhat = host(dec.decode(q))
+        np.testing.assert_array_equal(xhat, xhat_ref, err_msg=f"{what} t={t} xhat")
+        st = r.state
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU test run without a GPU")
+
+
+def test_tiny_fp16_sequence():
+    frames = list(synth.frame_sequence("tiny", 3))
+    run_fp16_sequence(64, 64, 64, 2, 2, frames, "tiny fp16")
+
+
+def test_tiny_int_sequence_bit_exact():
+    frames = list(synth.frame_sequence("tiny_int", 3))
+    run_int_sequence(64, 64, 64, 2, 2, frames, "tiny int")
+
+
+@pytest.mark.parametrize("H,W,C,ne,nd", [
+    (16, 16, 64, 1, 1),      # one latent pixel, 4 pixels at 1/8
+    (48, 80, 128, 1, 2),     # ragged: 60 pixels at 1/8 (< one 128-pixel tile)
+    (112, 208, 256, 2, 1),   # 364 pixels at 1/8: three tiles, ragged tail
+    (32, 48, 64, 0, 0),      # no blocks at all
+])
+def test_edge_shapes_fp16(H, W, C, ne, nd):
+    frames = [synth.random_frame(H, W, seed=s) for s in (10, 11)]
+    run_fp16_sequence(H, W, C, ne, nd, frames, "edge fp16")
+
+
+@pytest.mark.parametrize("H,W,C,ne,nd", [
+    (16, 16, 64, 1, 1),
+    (48, 80, 128, 1, 2),
+    (112, 208, 256, 2, 1),
+    (32, 48, 64, 0, 0),
+])
+def test_edge_shapes_int(H, W, C, ne, nd):
+    frames = [synth.random_frame(H, W, seed=s) for s in (12, 13)]
+    run_int_sequence(H, W, C, ne, nd, frames, "edge int")
+
+
+def test_extreme_frames_int():
+    # all-zero, all-one and saturated-out-of-range inputs
+    H = W = 32
+    frames = [np.zeros((3, H, W), np.float16), np.ones((3, H, W), np.float16),
+              np.full((3, H, W), 100.0, np.float16)]
+    run_int_sequence(H, W, 64, 1, 1, frames, "extreme int")
+
+
+def test_wvga_fp16():
+    frames = list(synth.frame_sequence("wvga", 1))
+    run_fp16_sequence(480, 832, 128, 6, 6, frames, "wvga fp16")
+
+
+def test_wvga_int_bit_exact():
+    pre = synth.PRESETS["wvga"]
+    frames = list(synth.frame_sequence(pre, 2))
+    run_int_sequence(480, 832, 128, 6, 6, frames, "wvga int")
+
+
+def test_estimate_bits_matches_oracle():
+    flat, _ = params_for(64, 1, 1)
+    c = Codec(16, 16, 64, 1, 1, "fp16", flat, device=DEV)
+    rng = np.random.default_rng(5)
+    for n in (0, 1, 1000, 1 << 20, 2088960):
+        say("estimate_bits n =", n)
+        q = rng.integers(-40, 41, size=n).astype(np.int16)
+        sigma = rng.uniform(0.11, 20.0, size=n).astype(np.float32)
+        b = float(host(c.estimate_bits(gpu(q), gpu(sigma))))
+        ref = oracle.estimate_bits(q, sigma.astype(np.float64))
+        assert abs(b - ref) <= 1e-5 * max(abs(ref), 1e-30), (n, b, ref)
+    # deterministic: same inputs, same bits
+    q = gpu(rng.integers(-5, 6, size=100000).astype(np.int16))
+    s = gpu(rng.uniform(0.2, 3.0, size=100000).astype(np.float32))
+    assert float(host(c.estimate_bits(q, s))) == float(host(c.estimate_bits(q, s)))
+
+
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_determinism_reset_and_state_round_trip(path):
+    H, W, C = 64, 96, 128
+    flat, _ = params_for(C, 2, 2)
+    frames = [gpu(synth.random_frame(H, W, seed=s)) for s in (20, 21, 22)]
+    a = Codec(H, W, C, 2, 2, path, flat, device=DEV)
+    b = Codec(H, W, C, 2, 2, path, flat, device=DEV)
+    qa = [host(a.encode(f)[0]) for f in frames]
+    qb = [host(b.encode(f)[0]) for f in frames]
+    for u, v in zip(qa, qb):
+        np.testing.assert_array_equal(u, v)
+    # restore the state after frame 0 and re-encode frames 1, 2
+    c = Codec(H, W, C, 2, 2, path, flat, device=DEV)
+    c.encode(frames[0])
+    f0, y0 = c.get_state()
+    q1, bits1 = c.encode(frames[1])
+    c.set_state(f0, y0)
+    q1b, bits1b = c.encode(frames[1])
+    np.testing.assert_array_equal(host(q1), host(q1b))
+    assert float(host(bits1)) == float(host(bits1b))
+    # reset -> the next frame is coded as an I-frame again
+    c.reset()
+    np.testing.assert_array_equal(host(c.encode(frames[0])[0]), qa[0])
+    fz, yz = Codec(H, W, C, 2, 2, path, flat, device=DEV).get_state()
+    assert not host(fz).any() and not host(yz).any()
