@@ -26,6 +26,9 @@ DEVICE_FLAGS = [
     # packed fp32 VALU ops are kept off for all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-result",
+    # MFMA accumulators in ordinary VGPRs: avoids AGPR<->VGPR copies of
+    # loop-carried accumulators
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
 
 

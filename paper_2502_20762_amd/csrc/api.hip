@@ -164,18 +164,47 @@ struct Packer {
         for (int c = 0; c < C; ++c) wp[t * C + c] = q16(dw[c * 9 + t]);
       for (int c = 0; c < C; ++c) bp[c] = 512 * (int32_t)q16(dwb[c]);
     }
+    if (!is_int) {
+      // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1
+      // fragments (rows 32j..32j+31, all C inputs) followed by the 2*MT pw2
+      // fragments that consume that chunk.  The pw2 contraction index is
+      // permuted inside the chunk so that the pw1 accumulator registers are
+      // directly the pw2 operand.  One chunk is one contiguous copy into LDS.
+      const int KS = C / 16, MT = C / 32, NCH = 2 * C / 32, FR = KS + 2 * MT;
+      d.pw1.w = img.add((size_t)NCH * FR * 1024);
+      d.pw1.bias = img.add((size_t)2 * C * 4);
+      d.pw2.bias = img.add((size_t)C * 4);
+      f16* cp = img.at<f16>(d.pw1.w);
+      auto kmap = [](int k) { return 8 * ((k % 8) / 4) + 4 * ((k / 8) % 2) + (k % 4); };  // within 16
+      for (int j = 0; j < NCH; ++j)
+        for (int f = 0; f < FR; ++f)
+          for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 8; ++e) {
+              float v;
+              if (f < KS) {
+                const int n = 32 * j + (l & 31), k = 16 * f + 8 * (l >> 5) + e;
+                v = w1[(size_t)n * C + k];
+              } else {
+                const int t = (f - KS) / 2, u = (f - KS) % 2;
+                const int n = 32 * t + (l & 31);
+                const int hidden = 32 * j + 16 * u + kmap(8 * (l >> 5) + e);
+                v = w2[(size_t)n * 2 * C + hidden];
+              }
+              cp[(((size_t)j * FR + f) * 64 + l) * 8 + e] = (f16)v;
+            }
+      float* b1p = img.at<float>(d.pw1.bias);
+      float* b2p = img.at<float>(d.pw2.bias);
+      for (int n = 0; n < 2 * C; ++n) b1p[n] = (float)(f16)b1[n];
+      for (int n = 0; n < C; ++n) b2p[n] = (float)(f16)b2[n];
+      return d;
+    }
     d.pw1 = plain(w1, b1, 2 * C, C);
     // Second conv: its contraction index is permuted inside each 32-channel
     // hidden chunk so that the first conv's accumulator registers can be used
     // directly as this conv's operand.
-    if (!is_int)
-      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
-        return 32 * (k / 32) + 16 * ((k / 16) % 2) + 8 * ((k % 8) / 4) + 4 * ((k / 8) % 2) + (k % 4);
-      });
-    else
-      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
-        return 32 * (k / 32) + 8 * ((k % 16) / 4) + 4 * ((k / 16) % 2) + (k % 4);
-      });
+    d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
+      return 32 * (k / 32) + 8 * ((k % 16) / 4) + 4 * ((k / 16) % 2) + (k % 4);
+    });
     return d;
   }
 };
@@ -186,7 +215,7 @@ struct Layout {
   size_t sigma_tab = 0;
   size_t image_bytes = 0;
   // state and intermediates (offsets from the workspace base)
-  size_t feat[2], yhat[2], ed, zA, zB, y, partials;
+  size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad;
   int n_partials;
   size_t total;
 };
@@ -247,6 +276,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
   L.partials = alloc((size_t)L.n_partials * 8);
+  L.zpad = alloc((size_t)C * 2);  // zeroed at create and never written
   L.total = off;
   return pk.ok;
 }
@@ -377,7 +407,7 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
     const BlockDev& b = L.dec[k];
     BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                  ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
-                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8};
+                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
     NC_HIP(ctx, dcblock(ctx, ba), "decoder block");
     z = dst;
   }
@@ -485,7 +515,7 @@ ncodec_status ncodec_encode_frame(ncodec_ctx* ctx, const void* d_frame, int16_t*
     const BlockDev& b = L.enc[k];
     BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                  ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
-                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8};
+                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
     NC_HIP(ctx, dcblock(ctx, ba), "encoder block");
     z = dst;
   }

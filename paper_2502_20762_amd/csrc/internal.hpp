@@ -46,9 +46,10 @@ struct BlockArgs {
   const void* b2;
   const void* dww;  // [9][C]
   const void* dwb;  // [C]
-  const void* src;  // z (NHWC)
-  void* dst;        // z' (NHWC), must not alias src
+  const void* src;   // z (NHWC)
+  void* dst;         // z' (NHWC), must not alias src
   int h, w;
+  const void* zpad;  // C zero elements: the depthwise taps outside the image read these
 };
 
 struct PriorArgs {
@@ -83,6 +84,12 @@ hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n,
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);
+
+// DC-block kernels tile the 1/8-scale grid in 8 x 16 pixel tiles.
+inline int dc_grid(int h, int w) {
+  const int t = ((h + 7) / 8) * ((w + 15) / 16);
+  return (t + 7) / 8 * 8;
+}
 
 inline int grid_tiles(int P) {
   const int t = (P + 127) / 128;

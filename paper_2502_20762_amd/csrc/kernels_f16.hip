@@ -91,97 +91,234 @@ __global__ __launch_bounds__(256) void k_pw_f16(PwArgs a) {
   }
 }
 
+// One DC block (Supp. B.1) for a tile of 128 pixels, 8 waves.
+//
+// Waves w and w+4 share 32 pixels (pixel group w & 3) and sit on the same
+// SIMD; wave w >> 2 == hf owns output channels [hf C/2, (hf+1) C/2) of the
+// second pointwise conv and produces the hidden chunks j with j % 2 == hf of
+// the first one.  A hidden chunk (32 channels after bias + LeakyReLU, fp16)
+// goes to LDS in MFMA operand order so both waves of the pair consume it.
+//
+// Weights stream chunk by chunk (chunk j = the pw1 fragments producing hidden
+// chunk j followed by the pw2 fragments consuming it) into four LDS buffers,
+// three chunks ahead, with direct global->LDS loads.  The buffers are distinct
+// LDS objects indexed statically (the loop is unrolled by four), so LDS reads
+// never wait for loads into a different buffer.
 template <int C>
-__global__ __launch_bounds__(256) void k_dcblock_f16(BlockArgs a) {
-  constexpr int KS = C / 16;       // k-steps over the C input channels
-  constexpr int NCH = 2 * C / 32;  // hidden chunks of 32
-  constexpr int MT = C / 32;       // output row tiles
-  constexpr int KS2 = 2 * C / 16;  // k-steps over the hidden channels
-  const int P = a.h * a.w;
-  const int ntile = (P + 127) / 128;
+struct DcSmem {
+  static constexpr int KS = C / 16, MT = C / 32, FR = KS + 2 * MT, CHUNK = FR * 1024;
+};
+
+template <int C>
+__device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, int wave, int lane) {
+  constexpr int FR = DcSmem<C>::FR;
+#pragma unroll
+  for (int i = 0; i < FR / 8; ++i) {
+    const int f = wave + 8 * i;
+    const char* g = wchunks + ((size_t)j * FR + f) * 1024 + lane * 16;
+    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(buf + f * 1024), 16,
+                                     0, 0);
+  }
+}
+
+// Hidden chunk j from the pw1 fragments in `wb`: bias, LeakyReLU, fp16, stored
+// to `gx` as two B fragments (k = hidden in the permuted order the pw2
+// weights were packed with).
+template <int C>
+__device__ __forceinline__ void dc_hidden(const char* wb, const half8* av, const float* b1s, int j, int h,
+                                          int lane, half8* gx) {
+  constexpr int KS = DcSmem<C>::KS;
+  const half8* w = (const half8*)wb + lane;
+  floatx16 hacc = {};
+#pragma unroll
+  for (int s = 0; s < KS; ++s) hacc = mfma_f16(w[s * 64], av[s], hacc);
+  half8 g0, g1;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const floatx4 bv = *(const floatx4*)(b1s + 32 * j + 8 * g + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const f16 v = (f16)leaky(hacc[4 * g + e] + bv[e]);
+      if (g < 2) g0[4 * g + e] = v; else g1[4 * (g - 2) + e] = v;
+    }
+  }
+  gx[lane] = g0;
+  gx[64 + lane] = g1;
+}
+
+// Second pointwise conv, hidden chunk j, this wave's MT/2 output tiles.
+template <int C>
+__device__ __forceinline__ void dc_project(const char* wb, const half8* gx, int hf, int lane, floatx16* out) {
+  constexpr int KS = DcSmem<C>::KS, MT = DcSmem<C>::MT;
+  const half8* w = (const half8*)wb + lane;
+  const half8 g0 = gx[lane], g1 = gx[64 + lane];
+#pragma unroll
+  for (int t = 0; t < MT / 2; ++t) {
+    const int tt = hf * (MT / 2) + t;
+    out[t] = mfma_f16(w[(KS + 2 * tt) * 64], g0, out[t]);
+    out[t] = mfma_f16(w[(KS + 2 * tt + 1) * 64], g1, out[t]);
+  }
+}
+
+template <int C>
+__global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
+  constexpr int KS = DcSmem<C>::KS;
+  constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 (a multiple of 4)
+  constexpr int MT = DcSmem<C>::MT;
+  constexpr int CHUNK = DcSmem<C>::CHUNK;
+  constexpr int LDS_PER_WAVE = DcSmem<C>::FR / 8;  // outstanding direct loads per issued chunk
+  constexpr int TH = 8, TW = 16;                   // pixel tile (rows x columns at 1/8 scale)
+  constexpr int HW = TW + 2, HPX = (TH + 2) * HW;  // halo tile: 10 x 18 pixels
+  constexpr int CS = 64;                           // channels per staged halo slice (128 B per pixel)
+  constexpr int SLOTS = HPX * (CS / 8);            // 16-byte slots per slice
+  constexpr int SLICE_INSTR = (SLOTS + 63) / 64;
+  static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
+  constexpr int SLICE = (HPX * CS * 2 + 1023) / 1024 * 1024;
+  constexpr int BUF = CHUNK > SLICE ? CHUNK : SLICE;
+  __shared__ __attribute__((aligned(1024))) char wb0[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb1[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb2[BUF];  // also halo slices (even)
+  __shared__ __attribute__((aligned(1024))) char wb3[BUF];  // also halo slices (odd)
+  __shared__ half8 gx0[4][128];  // [pixel group][2 fragments x 64 lanes], even chunks
+  __shared__ half8 gx1[4][128];  // odd chunks
+  __shared__ float b1s[2 * C], b2s[C], dwbs[C];
+  __shared__ __attribute__((aligned(16))) f16 dws[9 * C];
+
+  const int tiles_x = (a.w + TW - 1) / TW;
+  const int ntile = tiles_x * ((a.h + TH - 1) / TH);
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < P;
-  const int y = valid ? p / a.w : 0, x = valid ? p - y * a.w : 0;
+  const int ty0 = (tile / tiles_x) * TH, tx0 = (tile % tiles_x) * TW;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pg = wave & 3, hf = wave >> 2;
+  const int r = 2 * pg + ((lane & 31) >> 4), c = lane & 15;  // this lane's pixel in the tile
+  const int y = ty0 + r, x = tx0 + c;
+  const bool valid = y < a.h && x < a.w;
+  const int p = y * a.w + x;
   const f16* z = (const f16*)a.src;
+  const char* wchunks = (const char*)a.w1;
 
-  // depthwise 3x3 (+ bias) for this lane's pixel, channels 16s + 8h + e.
-  half8 av[KS];
-  {
-    const half8* dww = (const half8*)a.dww;
-    const float* dwb = (const float*)a.dwb;
+  dc_issue<C>(wchunks, 0, wb0, wave, lane);
+  dc_issue<C>(wchunks, 1, wb1, wave, lane);
+
+  // Halo slice k (channels [64k, 64k+64)) -> LDS: slot S = 8 * halo_pixel +
+  // (v ^ (halo_pixel & 7)) holds channel vector v of that pixel, so the 3x3
+  // reads of 8 neighbouring pixels hit 8 different bank groups.
+  constexpr int SLICE_PER_WAVE = (SLICE_INSTR + 7) / 8;
+  const f16* slice_src[SLICE_PER_WAVE];  // slice-0 source of this lane's slot, per instruction
+  bool slice_on[SLICE_PER_WAVE];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+  for (int i = 0; i < SLICE_PER_WAVE; ++i) {
+    const int ins = wave + 8 * i;
+    const int S = ins * 64 + lane;
+    slice_on[i] = ins < SLICE_INSTR && S < SLOTS;
+    const int hp = S >> 3, v = (S & 7) ^ (hp & 7);
+    const int hy = ty0 - 1 + hp / HW, hx = tx0 - 1 + hp % HW;
+    const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+    // zpad holds C zeros, so adding a slice offset (< C) keeps it in bounds
+    slice_src[i] = (in ? z + (size_t)(hy * a.w + hx) * C : (const f16*)a.zpad) + 8 * v;
+  }
+  auto issue_slice = [&](int k, char* buf) {
+#pragma unroll
+    for (int i = 0; i < SLICE_PER_WAVE; ++i) {
+      if (slice_on[i])
+        __builtin_amdgcn_global_load_lds((const void*)(slice_src[i] + CS * k),
+                                         (__attribute__((address_space(3))) void*)(buf + (wave + 8 * i) * 1024), 16,
+                                         0, 0);
+    }
+  };
+  issue_slice(0, wb2);
+  for (int i = threadIdx.x; i < 2 * C; i += 512) b1s[i] = ((const float*)a.b1)[i];
+  for (int i = threadIdx.x; i < C; i += 512) {
+    b2s[i] = ((const float*)a.b2)[i];
+    dwbs[i] = ((const float*)a.dwb)[i];
+  }
+  for (int i = threadIdx.x; i < 9 * C / 8; i += 512) ((half8*)dws)[i] = ((const half8*)a.dww)[i];
+
+  // depthwise 3x3 (+ bias) for this lane's pixel, channels 16s + 8h + e,
+  // from the staged halo slices (double-buffered in wb2 / wb3).
+  half8 av[KS];
+  // byte offset of this lane's 9 taps inside a staged slice, for channel
+  // vector h (step ss of the slice XORs in 2 * ss, see the slot layout)
+  int tap_off[9];
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int hp = (r + ky) * HW + c + kx;
+      tap_off[ky * 3 + kx] = (hp << 7) | ((h ^ (hp & 7)) << 4);
+    }
+  auto dw_slice = [&](int k, const char* buf) {
+#pragma unroll
+    for (int ss = 0; ss < CS / 16; ++ss) {
+      const int s = k * (CS / 16) + ss;
       const int c0 = 16 * s + 8 * h;
       float acc[8];
-      const floatx4 b0 = *(const floatx4*)(dwb + c0), b1v = *(const floatx4*)(dwb + c0 + 4);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) { acc[e] = b0[e]; acc[4 + e] = b1v[e]; }
+      for (int e = 0; e < 8; ++e) acc[e] = dwbs[c0 + e];
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
+      for (int t = 0; t < 9; ++t) {
+        const half8 zv = *(const half8*)(buf + (tap_off[t] ^ (ss << 5)));
+        const half8 wv = *(const half8*)(dws + t * C + c0);
 #pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const int xx = x + kx - 1;
-          if (valid && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w) {
-            const half8 v = *(const half8*)(z + (size_t)(yy * a.w + xx) * C + c0);
-            const half8 wv = dww[(ky * 3 + kx) * (C / 8) + (c0 >> 3)];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)wv[e], (float)v[e], acc[e]);
-          }
-        }
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)wv[e], (float)zv[e], acc[e]);
       }
       half8 o;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = valid ? (f16)acc[e] : (f16)0.f;
+      for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
       av[s] = o;
+      __builtin_amdgcn_sched_barrier(0);  // keep the live range of one step's taps short
     }
+  };
+#pragma unroll
+  for (int k = 0; k < C / CS; ++k) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // slice k staged; slice k-1's buffer no longer read
+    if (k + 1 < C / CS) issue_slice(k + 1, (k & 1) ? wb2 : wb3);
+    dw_slice(k, (k & 1) ? wb3 : wb2);
   }
+  __syncthreads();  // all halo reads done: wb2 / wb3 become weight buffers
+  dc_issue<C>(wchunks, 2, wb2, wave, lane);
 
-  const half8* w1 = (const half8*)a.w1;
-  const half8* w2 = (const half8*)a.w2;
-  const float* b1 = (const float*)a.b1;
-  floatx16 out[MT];
+  floatx16 out[MT / 2];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) out[t] = floatx16{};
+  for (int t = 0; t < MT / 2; ++t) out[t] = floatx16{};
 
-  for (int j = 0; j < NCH; ++j) {
-    floatx16 hacc = {};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) hacc = mfma_f16(w1[((size_t)j * KS + s) * 64 + lane], av[s], hacc);
-    half8 g0, g1;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const floatx4 bv = *(const floatx4*)(b1 + 32 * j + 8 * g + 4 * h);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const f16 v = (f16)leaky(hacc[4 * g + e] + bv[e]);
-        if (g < 2) g0[4 * g + e] = v; else g1[4 * (g - 2) + e] = v;
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      out[t] = mfma_f16(w2[((size_t)t * KS2 + 2 * j) * 64 + lane], g0, out[t]);
-      out[t] = mfma_f16(w2[((size_t)t * KS2 + 2 * j + 1) * 64 + lane], g1, out[t]);
-    }
+  if (hf == 0) dc_hidden<C>(wb0, av, b1s, 0, h, lane, gx0[pg]);
+  __syncthreads();
+
+  // Iteration j: issue chunk j+3, produce hidden chunk j+1 (one wave of each
+  // pair), project hidden chunk j (both waves).
+  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, half8* gcur, half8* gnxt) {
+    const bool more = j + 3 < NCH;
+    if (more) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
+    if (j + 1 < NCH && hf == ((j + 1) & 1)) dc_hidden<C>(wnxt, av, b1s, j + 1, h, lane, gnxt);
+    dc_project<C>(wcur, gcur, hf, lane, out);
+    if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+  for (int j = 0; j < NCH; j += 4) {
+    step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
+    step(j + 1, wb1, wb2, wb0, gx1[pg], gx0[pg]);
+    step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
+    step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
   }
   if (!valid) return;
 
-  const float* b2 = (const float*)a.b2;
   f16* dst = (f16*)a.dst;
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
+  for (int t = 0; t < MT / 2; ++t) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int c = 32 * t + 8 * g + 4 * h;
-      const floatx4 bv = *(const floatx4*)(b2 + c);
-      const half4 zv = *(const half4*)(z + (size_t)p * C + c);
+      const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
+      const floatx4 bv = *(const floatx4*)(b2s + cc);
+      const half4 zv = *(const half4*)(z + (size_t)p * C + cc);
       half4 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = (f16)(out[t][4 * g + e] + bv[e] + (float)zv[e]);
-      *(half4*)(dst + (size_t)p * C + c) = o;
+      *(half4*)(dst + (size_t)p * C + cc) = o;
     }
   }
 }
@@ -286,7 +423,7 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st) {
-  dim3 grid(grid_tiles(a.h * a.w)), block(256);
+  dim3 grid(dc_grid(a.h, a.w)), block(512);
   switch (C) {
     case 64: hipLaunchKernelGGL((k_dcblock_f16<64>), grid, block, 0, st, a); break;
     case 128: hipLaunchKernelGGL((k_dcblock_f16<128>), grid, block, 0, st, a); break;
