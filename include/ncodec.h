@@ -137,13 +137,14 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
 /* Kernel launches one ncodec_encode_frame / ncodec_decode_frame enqueues. */
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
 
-/* Optional per-kernel timing.  While enabled, each kernel the context
- * enqueues is bracketed by a pair of HIP events recorded on the context's
- * stream.  ncodec_timing_read() synchronises the stream, aggregates the
- * recorded pairs per kernel kind (launch count and summed milliseconds),
- * writes at most max_kinds records to out, sets *n_kinds, and clears the
- * log.  Kinds: "embed", "fuse", "dcblock", "down", "prior", "reduce", "up",
- * "recon".  Meant for measurement runs; off by default. */
+/* Optional per-kernel timing.  While enabled, every kernel the context
+ * enqueues is launched with a start / stop HIP event pair attached to its
+ * dispatch (hipExtLaunchKernel), so each interval is that kernel's execution
+ * time.  ncodec_timing_read() synchronises the stream, aggregates the
+ * intervals per kernel kind (launch count and summed milliseconds), writes at
+ * most max_kinds records to out, sets *n_kinds, and clears the log.  Kinds:
+ * "embed", "fuse", "dcblock", "down", "prior", "reduce", "up", "recon".
+ * Meant for measurement runs; off by default. */
 typedef struct {
   char kind[16];
   int32_t launches;

@@ -16,6 +16,10 @@
 
 using namespace nc;
 
+namespace nc {
+thread_local LaunchEvents g_launch_events;
+}
+
 namespace {
 
 thread_local std::string g_create_error;
@@ -318,16 +322,20 @@ ncodec_status hip_fail(ncodec_ctx* ctx, hipError_t e, const char* where) {
     if (_e != hipSuccess) return hip_fail(ctx, _e, where); \
   } while (0)
 
-// Runs one launch; in timing mode brackets it with events on the context stream.
+// Runs one launch.  In timing mode the launch's kernel dispatch carries a
+// start / stop event pair (hipExtLaunchKernelGGL), so the recorded interval
+// is that kernel's execution, without the dispatch gap before it.
 template <class F>
-hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch) {
-  if (!ctx->timing) return launch();
+hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch_fn) {
+  if (!ctx->timing) return launch_fn();
   ncodec_ctx::TimedLaunch t{kind, nullptr, nullptr};
   hipError_t e = hipEventCreate(&t.start);
   if (e == hipSuccess) e = hipEventCreate(&t.stop);
-  if (e == hipSuccess) e = hipEventRecord(t.start, ctx->stream);
-  if (e == hipSuccess) e = launch();
-  if (e == hipSuccess) e = hipEventRecord(t.stop, ctx->stream);
+  if (e == hipSuccess) {
+    g_launch_events = {t.start, t.stop};
+    e = launch_fn();
+    g_launch_events = {};
+  }
   ctx->log.push_back(t);
   return e;
 }

@@ -1,11 +1,28 @@
 // Host-visible launch interface between the scheduler (api.hip) and the
 // kernel translation units.  Not part of the public ABI.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace nc {
+
+// Events attached to the next kernel dispatch (timing mode of the C ABI): when
+// set, launches go through hipExtLaunchKernelGGL, whose start / stop events
+// bracket exactly that dispatch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, hipStream_t st, Args... args) {
+  if (g_launch_events.start)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, g_launch_events.start, g_launch_events.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+}
 
 // How a pointwise kernel gathers its activation operand (K index -> memory).
 enum Loader : int {

@@ -402,7 +402,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   dim3 grid(grid_tiles(a.P), a.N / NT), block(256);
 #define NC_PW(L, E)                                                            \
   if (loader == L && epi == E) {                                               \
-    hipLaunchKernelGGL((k_pw_f16<NT, L, E>), grid, block, 0, st, a);           \
+    launch(k_pw_f16<NT, L, E>, grid, block, st, a);           \
     return hipGetLastError();                                                  \
   }
   NC_PW(LD_NHWC, EP_NHWC)
@@ -425,9 +425,9 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
 hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st) {
   dim3 grid(dc_grid(a.h, a.w)), block(512);
   switch (C) {
-    case 64: hipLaunchKernelGGL((k_dcblock_f16<64>), grid, block, 0, st, a); break;
-    case 128: hipLaunchKernelGGL((k_dcblock_f16<128>), grid, block, 0, st, a); break;
-    case 256: hipLaunchKernelGGL((k_dcblock_f16<256>), grid, block, 0, st, a); break;
+    case 64: launch(k_dcblock_f16<64>, grid, block, st, a); break;
+    case 128: launch(k_dcblock_f16<128>, grid, block, st, a); break;
+    case 256: launch(k_dcblock_f16<256>, grid, block, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -439,10 +439,10 @@ hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials)
   const int ch = a.C >= 128 ? 128 : a.C;
   dim3 grid(grid_tiles(a.P), a.C / ch), block(256);
   if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / ch);
-  if (ch == 128 && a.decode) hipLaunchKernelGGL((k_prior_f16<128, true>), grid, block, 0, st, a);
-  else if (ch == 128) hipLaunchKernelGGL((k_prior_f16<128, false>), grid, block, 0, st, a);
-  else if (ch == 64 && a.decode) hipLaunchKernelGGL((k_prior_f16<64, true>), grid, block, 0, st, a);
-  else if (ch == 64) hipLaunchKernelGGL((k_prior_f16<64, false>), grid, block, 0, st, a);
+  if (ch == 128 && a.decode) launch(k_prior_f16<128, true>, grid, block, st, a);
+  else if (ch == 128) launch(k_prior_f16<128, false>, grid, block, st, a);
+  else if (ch == 64 && a.decode) launch(k_prior_f16<64, true>, grid, block, st, a);
+  else if (ch == 64) launch(k_prior_f16<64, false>, grid, block, st, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

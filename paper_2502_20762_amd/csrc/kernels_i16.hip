@@ -360,7 +360,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   dim3 grid(grid_tiles(a.P), a.N / NT), block(256);
 #define NC_PW(L, E)                                                            \
   if (loader == L && epi == E) {                                               \
-    hipLaunchKernelGGL((k_pw_i16<NT, L, E>), grid, block, 0, st, a);           \
+    launch(k_pw_i16<NT, L, E>, grid, block, st, a);           \
     return hipGetLastError();                                                  \
   }
   NC_PW(LD_NHWC, EP_NHWC)
@@ -381,9 +381,9 @@ hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
 hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
   dim3 grid(grid_tiles(a.h * a.w)), block(256);
   switch (C) {
-    case 64: hipLaunchKernelGGL((k_dcblock_i16<64>), grid, block, 0, st, a); break;
-    case 128: hipLaunchKernelGGL((k_dcblock_i16<128>), grid, block, 0, st, a); break;
-    case 256: hipLaunchKernelGGL((k_dcblock_i16<256>), grid, block, 0, st, a); break;
+    case 64: launch(k_dcblock_i16<64>, grid, block, st, a); break;
+    case 128: launch(k_dcblock_i16<128>, grid, block, st, a); break;
+    case 256: launch(k_dcblock_i16<256>, grid, block, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -394,8 +394,8 @@ int prior_partials_i16(int C, int P) { return grid_tiles(P) * (C / 64); }
 hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials) {
   dim3 grid(grid_tiles(a.P), a.C / 64), block(256);
   if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / 64);
-  if (a.decode) hipLaunchKernelGGL((k_prior_i16<64, true>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((k_prior_i16<64, false>), grid, block, 0, st, a);
+  if (a.decode) launch(k_prior_i16<64, true>, grid, block, st, a);
+  else launch(k_prior_i16<64, false>, grid, block, st, a);
   return hipGetLastError();
 }
 

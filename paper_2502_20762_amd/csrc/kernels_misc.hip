@@ -57,14 +57,14 @@ __global__ void k_planar_to_nhwc(const uint16_t* src, uint16_t* dst, int C, int 
 }
 
 hipError_t launch_reduce(const double* partials, int n, double* out, hipStream_t st) {
-  hipLaunchKernelGGL(k_reduce, dim3(1), dim3(256), 0, st, partials, n, out);
+  launch(k_reduce, dim3(1), dim3(256), st, partials, n, out);
   return hipGetLastError();
 }
 
 hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n, double* partials, double* out,
                                 hipStream_t st) {
   const int64_t chunk = n > 0 ? (n + kBitsBlocks - 1) / kBitsBlocks : 1;
-  hipLaunchKernelGGL(k_bits, dim3(kBitsBlocks), dim3(256), 0, st, q, sigma, n, chunk, partials);
+  launch(k_bits, dim3(kBitsBlocks), dim3(256), st, q, sigma, n, chunk, partials);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_reduce(partials, kBitsBlocks, out, st);
@@ -74,21 +74,21 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st) {
   const size_t n = bytes / 4;
   if (n == 0) return hipSuccess;
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
-  hipLaunchKernelGGL(k_fill_zero, dim3(blocks), dim3(256), 0, st, (uint32_t*)p, n);
+  launch(k_fill_zero, dim3(blocks), dim3(256), st, (uint32_t*)p, n);
   return hipGetLastError();
 }
 
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st) {
   const size_t n = (size_t)C * P;
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 8192);
-  hipLaunchKernelGGL(k_nhwc_to_planar, dim3(blocks), dim3(256), 0, st, (const uint16_t*)src, (uint16_t*)dst, C, P);
+  launch(k_nhwc_to_planar, dim3(blocks), dim3(256), st, (const uint16_t*)src, (uint16_t*)dst, C, P);
   return hipGetLastError();
 }
 
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st) {
   const size_t n = (size_t)C * P;
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 8192);
-  hipLaunchKernelGGL(k_planar_to_nhwc, dim3(blocks), dim3(256), 0, st, (const uint16_t*)src, (uint16_t*)dst, C, P);
+  launch(k_planar_to_nhwc, dim3(blocks), dim3(256), st, (const uint16_t*)src, (uint16_t*)dst, C, P);
   return hipGetLastError();
 }
 

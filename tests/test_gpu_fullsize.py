@@ -1,0 +1,109 @@
+"""Full-size (1920x1088, C = 256, 8 + 8 blocks) parity, in the configuration bench.py times.
+
+The GPU codes whole 1080p frames.  The oracle recomputes sampled regions: every output
+of the transform depends only on inputs within a bounded neighbourhood (each 3x3
+depthwise conv widens it by one pixel at 1/8 scale; everything else is 1x1, 2x2/s2 or
+a pixel shuffle), so the oracle run on a crop of the frame and of the GPU's state
+reproduces the full-frame result exactly away from the crop's artificial borders.
+Crops touching the real frame border keep that border (zero padding is then the same).
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import codec_float as cf
+from oracle import codec_int as ci
+from paper_2502_20762_amd.ncodec import Codec
+
+from parity_util import assert_close_fp16, check_fp16_encode, params_for
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+DEV = "cuda:0"
+PRE = synth.PRESETS["hd1080"]
+H, W, C, NE, ND = PRE.height, PRE.width, PRE.channels, PRE.n_enc, PRE.n_dec
+H16, W16 = H // 16, W // 16
+S = 28        # crop size in latent (1/16) pixels
+MARGIN = 10   # latent pixels discarded at crop borders interior to the frame
+CROPS = [(0, 0), (H16 - S, W16 - S), (20, 46)]  # top-left corner, bottom-right corner, interior
+
+
+def say(*a):
+    print("[gpu-fullsize]", *a, flush=True)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def crop_views(Y0, X0):
+    """Slices of the crop inside the full arrays, and of the valid region inside the crop."""
+    lo_y = MARGIN if Y0 > 0 else 0
+    lo_x = MARGIN if X0 > 0 else 0
+    hi_y = S - (MARGIN if Y0 + S < H16 else 0)
+    hi_x = S - (MARGIN if X0 + S < W16 else 0)
+    full = {k: (slice(f * Y0, f * (Y0 + S)), slice(f * X0, f * (X0 + S))) for k, f in (("l", 1), ("f", 2), ("x", 16))}
+    valid = {k: (slice(f * lo_y, f * hi_y), slice(f * lo_x, f * hi_x)) for k, f in (("l", 1), ("f", 2), ("x", 16))}
+    return full, valid
+
+
+def frames():
+    return list(synth.frame_sequence(PRE, 2))
+
+
+def test_hd1080_int_sampled_bit_exact():
+    flat, p = params_for(C, NE, ND)
+    ip = ci.integerize(p)
+    enc = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
+    dec = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
+    for t, x in enumerate(frames()):
+        say("int frame", t)
+        f0, y0 = (host(v).astype(np.int64) for v in enc.get_state())
+        q, _ = enc.encode(torch.from_numpy(x).to(DEV))
+        xhat = host(dec.decode(q))
+        f1, y1 = (host(v).astype(np.int64) for v in enc.get_state())
+        d1, e1 = (host(v).astype(np.int64) for v in dec.get_state())
+        np.testing.assert_array_equal(d1, f1)
+        np.testing.assert_array_equal(e1, y1)
+        qh = host(q).astype(np.int64)
+        for (Y0, X0) in CROPS:
+            full, valid = crop_views(Y0, X0)
+            say("  crop", (Y0, X0))
+            st = ci.State(f0[(slice(None),) + full["f"]], y0[(slice(None),) + full["l"]])
+            r = ci.encode_frame(ip, x[(slice(None),) + full["x"]], st)
+            xr, _ = ci.decode_frame(ip, r.q, st)
+            sl, sf, sx = ((slice(None),) + valid[k] for k in ("l", "f", "x"))
+            np.testing.assert_array_equal(qh[(slice(None),) + full["l"]][sl], r.q[sl])
+            np.testing.assert_array_equal(y1[(slice(None),) + full["l"]][sl], r.state.yhat[sl])
+            np.testing.assert_array_equal(f1[(slice(None),) + full["f"]][sf], r.state.feat[sf])
+            np.testing.assert_array_equal(xhat[(slice(None),) + full["x"]][sx], xr[sx])
+
+
+def test_hd1080_fp16_sampled_within_tolerance():
+    flat, p = params_for(C, NE, ND)
+    enc = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
+    dec = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
+    for t, x in enumerate(frames()):
+        say("fp16 frame", t)
+        f0, y0 = (host(v).astype(np.float64) for v in enc.get_state())
+        q, bits = enc.encode(torch.from_numpy(x).to(DEV))
+        xhat = host(dec.decode(q)).astype(np.float64)
+        f1, y1 = (host(v).astype(np.float64) for v in enc.get_state())
+        d1, _ = (host(v).astype(np.float64) for v in dec.get_state())
+        np.testing.assert_array_equal(d1, f1)
+        qh = host(q).astype(np.float64)
+        assert np.isfinite(float(host(bits)))
+        for (Y0, X0) in CROPS:
+            full, valid = crop_views(Y0, X0)
+            say("  crop", (Y0, X0))
+            fp = f0[(slice(None),) + full["f"]]
+            yp = y0[(slice(None),) + full["l"]]
+            sl, sf, sx = ((slice(None),) + valid[k] for k in ("l", "f", "x"))
+            f_ref, _ = check_fp16_encode(p, x[(slice(None),) + full["x"]], fp, yp,
+                                         qh[(slice(None),) + full["l"]], None,
+                                         f1[(slice(None),) + full["f"]], y1[(slice(None),) + full["l"]],
+                                         what=f"1080p fp16 t={t} crop {(Y0, X0)}", valid=(sl, sf))
+            assert_close_fp16(xhat[(slice(None),) + full["x"]][sx], cf.reconstruct(p, f_ref)[sx],
+                              f"1080p fp16 t={t} crop {(Y0, X0)} xhat")

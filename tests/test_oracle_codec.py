@@ -158,3 +158,30 @@ def test_activations_stay_in_int16_range(name):
         r = ci.encode_frame(ip, x, st)   # raises OverflowError on any int32 overflow
         st = r.state
         assert np.max(np.abs(st.feat)) < 16 * 512
+
+
+def test_crop_locality_used_by_full_size_sampling():
+    # The full-size GPU tests compare crops: with 8 + 8 blocks every output more than
+    # 10 latent pixels from a crop border depends only on inputs inside the crop.
+    import test_gpu_fullsize as fs
+    C, ne, nd = 64, 8, 8
+    Hf, Wf = 32 * 16, 48 * 16
+    p = oracle.unpack(synth.make_weights(C, ne, nd), C, ne, nd)
+    ip = ci.integerize(p)
+    rng = np.random.default_rng(3)
+    x = rng.uniform(0, 1, (3, Hf, Wf)).astype(np.float16)
+    st = ci.State(rng.integers(-2000, 2000, (C, Hf // 8, Wf // 8)), rng.integers(-2000, 2000, (C, Hf // 16, Wf // 16)))
+    r = ci.encode_frame(ip, x, st)
+    xr, _ = ci.decode_frame(ip, r.q, st)
+    S, M = fs.S, fs.MARGIN
+    for (Y0, X0) in [(0, 0), (32 - S, 48 - S), (2, 11)]:
+        sub = ci.State(st.feat[:, 2 * Y0:2 * (Y0 + S), 2 * X0:2 * (X0 + S)], st.yhat[:, Y0:Y0 + S, X0:X0 + S])
+        rc = ci.encode_frame(ip, x[:, 16 * Y0:16 * (Y0 + S), 16 * X0:16 * (X0 + S)], sub)
+        xc, _ = ci.decode_frame(ip, rc.q, sub)
+        ly, lx = (M if Y0 > 0 else 0), (M if X0 > 0 else 0)
+        hy, hx = S - (M if Y0 + S < 32 else 0), S - (M if X0 + S < 48 else 0)
+        np.testing.assert_array_equal(rc.q[:, ly:hy, lx:hx], r.q[:, Y0 + ly:Y0 + hy, X0 + lx:X0 + hx])
+        np.testing.assert_array_equal(rc.state.feat[:, 2 * ly:2 * hy, 2 * lx:2 * hx],
+                                      r.state.feat[:, 2 * (Y0 + ly):2 * (Y0 + hy), 2 * (X0 + lx):2 * (X0 + hx)])
+        np.testing.assert_array_equal(xc[:, 16 * ly:16 * hy, 16 * lx:16 * hx],
+                                      xr[:, 16 * (Y0 + ly):16 * (Y0 + hy), 16 * (X0 + lx):16 * (X0 + hx)])
