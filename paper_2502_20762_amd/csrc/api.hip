@@ -202,13 +202,55 @@ struct Packer {
       for (int n = 0; n < C; ++n) b2p[n] = (float)(f16)b2[n];
       return d;
     }
-    d.pw1 = plain(w1, b1, 2 * C, C);
-    // Second conv: its contraction index is permuted inside each 32-channel
-    // hidden chunk so that the first conv's accumulator registers can be used
-    // directly as this conv's operand.
-    d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) {
-      return 32 * (k / 32) + 8 * ((k % 16) / 4) + 4 * ((k / 16) % 2) + (k % 4);
-    });
+    // Integer chunk-major image: per hidden chunk j, the pw1 hi-digit
+    // fragments (KSI k-steps of 32), the pw1 lo-digit fragments, then the pw2
+    // hi and lo fragments (one k-step: the chunk's 32 hidden channels, in the
+    // order of the pw1 accumulator registers).
+    const int KSI = C / 32, MT = C / 32, NCH = 2 * C / 32, FR = 2 * KSI + 2 * MT;
+    d.pw1.w = img.add((size_t)NCH * FR * 1024);
+    d.pw1.bias = img.add((size_t)2 * C * 4);
+    d.pw2.bias = img.add((size_t)C * 4);
+    int8_t* cp = img.at<int8_t>(d.pw1.w);
+    auto kmap = [](int k) { return 8 * ((k % 16) / 4) + 4 * ((k / 16) % 2) + (k % 4); };  // within 32
+    auto digit = [&](int wi, bool hi) {
+      if (wi > 32639) {
+        if (ok && err) *err = "integer weight above 32639 (|w| >= 3.984) cannot be split into int8 digits";
+        ok = false;
+      }
+      const int lo = ((wi + 128) & 255) - 128;
+      return (int8_t)(hi ? (wi - lo) / 256 : lo);
+    };
+    for (int j = 0; j < NCH; ++j)
+      for (int f = 0; f < FR; ++f)
+        for (int l = 0; l < 64; ++l)
+          for (int e = 0; e < 16; ++e) {
+            int wi;
+            bool hi;
+            if (f < 2 * KSI) {
+              const int sstep = f % KSI;
+              hi = f < KSI;
+              const int n = 32 * j + (l & 31), k = 32 * sstep + 16 * (l >> 5) + e;
+              wi = q16(w1[(size_t)n * C + k]);
+            } else {
+              const int t = (f - 2 * KSI) % MT;
+              hi = f < 2 * KSI + MT;
+              const int n = 32 * t + (l & 31);
+              wi = q16(w2[(size_t)n * 2 * C + 32 * j + kmap(16 * (l >> 5) + e)]);
+            }
+            cp[(((size_t)j * FR + f) * 64 + l) * 16 + e] = digit(wi, hi);
+          }
+    int32_t* c1 = img.at<int32_t>(d.pw1.bias);
+    int32_t* c2 = img.at<int32_t>(d.pw2.bias);
+    for (int n = 0; n < 2 * C; ++n) {
+      int64_t sum = 0;
+      for (int k = 0; k < C; ++k) sum += q16(w1[(size_t)n * C + k]);
+      c1[n] = (int32_t)(uint32_t)(uint64_t)(512 * (int64_t)q16(b1[n]) + 128 * sum);
+    }
+    for (int n = 0; n < C; ++n) {
+      int64_t sum = 0;
+      for (int k = 0; k < 2 * C; ++k) sum += q16(w2[(size_t)n * 2 * C + k]);
+      c2[n] = (int32_t)(uint32_t)(uint64_t)(512 * (int64_t)q16(b2[n]) + 128 * sum);
+    }
     return d;
   }
 };

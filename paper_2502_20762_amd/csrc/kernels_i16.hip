@@ -132,127 +132,247 @@ __global__ __launch_bounds__(256) void k_pw_i16(PwArgs a) {
   }
 }
 
-// Whole DC block on the integer path.  The hidden activations g (2C per
-// pixel) are kept in registers as int8 digit fragments, then the second
-// pointwise conv runs one output tile at a time with three accumulators.
+// Whole DC block on the integer path; same dataflow as the fp16 block kernel
+// (8 waves per 8 x 16 pixel tile, LDS-staged halo and chunk-major weights,
+// hidden chunks exchanged between the two waves of a pixel group), with every
+// contraction done as int8 digit products:
+//   pw1 (per hidden chunk): three accumulators hh, hl + lh, ll, combined and
+//       rescaled once per chunk;
+//   pw2 (per output tile and chunk): t = hh; t <<= 8; t += hl + lh (MFMA);
+//       acc += t << 8; acc += ll (MFMA).  All in wrapping int32, which equals
+//       the exact sum whenever that fits int32.
 template <int C>
-__global__ __launch_bounds__(256) void k_dcblock_i16(BlockArgs a) {
-  constexpr int KS = C / 32;       // k-steps (32 channels) over C
-  constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 = k-steps of the second conv
-  constexpr int MT = C / 32;
-  const int P = a.h * a.w;
-  const int ntile = (P + 127) / 128;
+struct DcSmemI {
+  static constexpr int KSI = C / 32, MT = C / 32, FR = 2 * KSI + 2 * MT, CHUNK = FR * 1024;
+};
+
+template <int C>
+__device__ __forceinline__ void dci_issue(const char* wchunks, int j, char* buf, int wave, int lane) {
+  constexpr int FR = DcSmemI<C>::FR;
+#pragma unroll
+  for (int i = 0; i < FR / 8; ++i) {
+    const int f = wave + 8 * i;
+    const char* g = wchunks + ((size_t)j * FR + f) * 1024 + lane * 16;
+    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(buf + f * 1024), 16,
+                                     0, 0);
+  }
+}
+
+template <int C>
+__device__ __forceinline__ void dci_hidden(const char* wb, const intx4* ah, const intx4* al, const int* c1s, int j,
+                                           int h, int lane, intx4* gx) {
+  constexpr int KSI = DcSmemI<C>::KSI;
+  const intx4* w = (const intx4*)wb + lane;
+  intx16 hh = {}, mid = {}, ll = {};
+#pragma unroll
+  for (int s = 0; s < KSI; ++s) {
+    const intx4 wa = w[s * 64], wl = w[(KSI + s) * 64];
+    hh = mfma_i8(wa, ah[s], hh);
+    mid = mfma_i8(wa, al[s], mid);
+    mid = mfma_i8(wl, ah[s], mid);
+    ll = mfma_i8(wl, al[s], ll);
+  }
+  int gv[16];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const intx4 cv = *(const intx4*)(c1s + 32 * j + 8 * g + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 4 * g + e;
+      const int hv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
+      gv[r] = hv >= 0 ? hv : rhe_shift(819 * hv, 13);
+    }
+  }
+  uint32_t d[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[e] = pack2(gv[2 * e], gv[2 * e + 1]);
+  intx4 gh, gl;
+  split16(d, gh, gl);
+  gx[lane] = gh;
+  gx[64 + lane] = gl;
+}
+
+template <int C>
+__device__ __forceinline__ void dci_project(const char* wb, const intx4* gx, int hf, int lane, intx16* out) {
+  constexpr int KSI = DcSmemI<C>::KSI, MT = DcSmemI<C>::MT;
+  const intx4* w = (const intx4*)wb + lane;
+  const intx4 gh = gx[lane], gl = gx[64 + lane];
+#pragma unroll
+  for (int t = 0; t < MT / 2; ++t) {
+    const int tt = hf * (MT / 2) + t;
+    const intx4 wa = w[(2 * KSI + tt) * 64], wl = w[(2 * KSI + MT + tt) * 64];
+    intx16 v = mfma_i8(wa, gh, intx16{});
+#pragma unroll
+    for (int r = 0; r < 16; ++r) v[r] = (int)((uint32_t)v[r] << 8);
+    v = mfma_i8(wa, gl, v);
+    v = mfma_i8(wl, gh, v);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) out[t][r] = (int)(((uint32_t)v[r] << 8) + (uint32_t)out[t][r]);
+    out[t] = mfma_i8(wl, gl, out[t]);
+  }
+}
+
+template <int C>
+__global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
+  constexpr int KSI = DcSmemI<C>::KSI;
+  constexpr int NCH = 2 * C / 32;
+  constexpr int MT = DcSmemI<C>::MT;
+  constexpr int CHUNK = DcSmemI<C>::CHUNK;
+  constexpr int LDS_PER_WAVE = DcSmemI<C>::FR / 8;
+  constexpr int TH = 8, TW = 16;
+  constexpr int HW = TW + 2, HPX = (TH + 2) * HW;
+  constexpr int CS = 64;
+  constexpr int SLOTS = HPX * (CS / 8);
+  constexpr int SLICE_INSTR = (SLOTS + 63) / 64;
+  constexpr int SLICE = (HPX * CS * 2 + 1023) / 1024 * 1024;
+  constexpr int BUF = CHUNK > SLICE ? CHUNK : SLICE;
+  static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
+  __shared__ __attribute__((aligned(1024))) char wb0[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb1[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb2[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb3[BUF];
+  __shared__ intx4 gx0[4][128];
+  __shared__ intx4 gx1[4][128];
+  __shared__ int c1s[2 * C], c2s[C], dwbs[C];
+  __shared__ __attribute__((aligned(16))) int16_t dws[9 * C];
+
+  const int tiles_x = (a.w + TW - 1) / TW;
+  const int ntile = tiles_x * ((a.h + TH - 1) / TH);
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < P;
-  const int y = valid ? p / a.w : 0, x = valid ? p - y * a.w : 0;
+  const int ty0 = (tile / tiles_x) * TH, tx0 = (tile % tiles_x) * TW;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pg = wave & 3, hf = wave >> 2;
+  const int r = 2 * pg + ((lane & 31) >> 4), c = lane & 15;
+  const int y = ty0 + r, x = tx0 + c;
+  const bool valid = y < a.h && x < a.w;
+  const int p = y * a.w + x;
   const int16_t* z = (const int16_t*)a.src;
+  const char* wchunks = (const char*)a.w1;
 
-  intx4 ah[KS], al[KS];
-  {
-    const int16_t* dww = (const int16_t*)a.dww;
-    const int* dwb = (const int*)a.dwb;
+  dci_issue<C>(wchunks, 0, wb0, wave, lane);
+  dci_issue<C>(wchunks, 1, wb1, wave, lane);
+
+  constexpr int SLICE_PER_WAVE = (SLICE_INSTR + 7) / 8;
+  const int16_t* slice_src[SLICE_PER_WAVE];
+  bool slice_on[SLICE_PER_WAVE];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+  for (int i = 0; i < SLICE_PER_WAVE; ++i) {
+    const int ins = wave + 8 * i;
+    const int S = ins * 64 + lane;
+    slice_on[i] = ins < SLICE_INSTR && S < SLOTS;
+    const int hp = S >> 3, v = (S & 7) ^ (hp & 7);
+    const int hy = ty0 - 1 + hp / HW, hx = tx0 - 1 + hp % HW;
+    const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+    slice_src[i] = (in ? z + (size_t)(hy * a.w + hx) * C : (const int16_t*)a.zpad) + 8 * v;
+  }
+  auto issue_slice = [&](int k, char* buf) {
+#pragma unroll
+    for (int i = 0; i < SLICE_PER_WAVE; ++i) {
+      if (slice_on[i])
+        __builtin_amdgcn_global_load_lds((const void*)(slice_src[i] + CS * k),
+                                         (__attribute__((address_space(3))) void*)(buf + (wave + 8 * i) * 1024), 16,
+                                         0, 0);
+    }
+  };
+  issue_slice(0, wb2);
+  for (int i = threadIdx.x; i < 2 * C; i += 512) c1s[i] = ((const int*)a.b1)[i];
+  for (int i = threadIdx.x; i < C; i += 512) {
+    c2s[i] = ((const int*)a.b2)[i];
+    dwbs[i] = ((const int*)a.dwb)[i];
+  }
+  for (int i = threadIdx.x; i < 9 * C / 8; i += 512) ((intx4*)dws)[i] = ((const intx4*)a.dww)[i];
+
+  // depthwise 3x3: lane = pixel, channels 32s + 16h + e (two 8-channel vectors
+  // per tap), exact int32 sums, rescaled to int16 and split into int8 digits.
+  intx4 ah[KSI], al[KSI];
+  int tap_off[9];
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int hp = (r + ky) * HW + c + kx;
+      tap_off[ky * 3 + kx] = (hp << 7) | (((2 * h) ^ (hp & 7)) << 4);
+    }
+  auto dw_slice = [&](int k, const char* buf) {
+#pragma unroll
+    for (int ss = 0; ss < CS / 32; ++ss) {
+      const int s = k * (CS / 32) + ss;
       const int c0 = 32 * s + 16 * h;
       int acc[16];
 #pragma unroll
-      for (int e = 0; e < 16; e += 4) {
-        const intx4 bv = *(const intx4*)(dwb + c0 + e);
+      for (int e = 0; e < 16; ++e) acc[e] = dwbs[c0 + e];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc[e + u] = bv[u];
-      }
+      for (int t = 0; t < 9; ++t) {
+        // vectors v0 = 4 ss + 2h and v0 + 1 of the slice (see the slot layout)
+        const int o0 = tap_off[t] ^ (ss << 6);
+        const shortx8 z0 = *(const shortx8*)(buf + o0);
+        const shortx8 z1 = *(const shortx8*)(buf + (o0 ^ 16));
+        const shortx8 w0 = *(const shortx8*)(dws + t * C + c0);
+        const shortx8 w1 = *(const shortx8*)(dws + t * C + c0 + 8);
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
-#pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const int xx = x + kx - 1;
-          if (valid && yy >= 0 && yy < a.h && xx >= 0 && xx < a.w) {
-            const shortx8* vp = (const shortx8*)(z + (size_t)(yy * a.w + xx) * C + c0);
-            const shortx8* wp = (const shortx8*)(dww + (ky * 3 + kx) * C + c0);
-            const shortx8 v0 = vp[0], v1 = vp[1], w0 = wp[0], w1 = wp[1];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              acc[e] += (int)w0[e] * (int)v0[e];
-              acc[8 + e] += (int)w1[e] * (int)v1[e];
-            }
-          }
+        for (int e = 0; e < 8; ++e) {
+          acc[e] += (int)w0[e] * (int)z0[e];
+          acc[8 + e] += (int)w1[e] * (int)z1[e];
         }
       }
       uint32_t d[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) d[e] = pack2(rescale13(acc[2 * e]), rescale13(acc[2 * e + 1]));
       split16(d, ah[s], al[s]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+  };
+#pragma unroll
+  for (int k = 0; k < C / CS; ++k) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (k + 1 < C / CS) issue_slice(k + 1, (k & 1) ? wb2 : wb3);
+    dw_slice(k, (k & 1) ? wb3 : wb2);
   }
+  __syncthreads();
+  dci_issue<C>(wchunks, 2, wb2, wave, lane);
 
-  const intx4* w1h = (const intx4*)a.w1;
-  const intx4* w1l = (const intx4*)a.w1lo;
-  const int* c1 = (const int*)a.b1;
-  intx4 gh[NCH], gl[NCH];
+  intx16 out[MT / 2];
 #pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    intx16 hh = {}, mid = {}, ll = {};
+  for (int t = 0; t < MT / 2; ++t) out[t] = intx16{};
+
+  if (hf == 0) dci_hidden<C>(wb0, ah, al, c1s, 0, h, lane, gx0[pg]);
+  __syncthreads();
+
+  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, intx4* gcur, intx4* gnxt) {
+    const bool more = j + 3 < NCH;
+    if (more) dci_issue<C>(wchunks, j + 3, wiss, wave, lane);
+    if (j + 1 < NCH && hf == ((j + 1) & 1)) dci_hidden<C>(wnxt, ah, al, c1s, j + 1, h, lane, gnxt);
+    dci_project<C>(wcur, gcur, hf, lane, out);
+    if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+  for (int j = 0; j < NCH; j += 4) {
+    step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
+    step(j + 1, wb1, wb2, wb0, gx1[pg], gx0[pg]);
+    step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
+    step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
+  }
+  if (!valid) return;
+
+  int16_t* dst = (int16_t*)a.dst;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const size_t idx = ((size_t)j * KS + s) * 64 + lane;
-      const intx4 wa = w1h[idx], wb = w1l[idx];
-      hh = mfma_i8(wa, ah[s], hh);
-      mid = mfma_i8(wa, al[s], mid);
-      mid = mfma_i8(wb, ah[s], mid);
-      ll = mfma_i8(wb, al[s], ll);
-    }
-    int gv[16];
+  for (int t = 0; t < MT / 2; ++t) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const intx4 cv = *(const intx4*)(c1 + 32 * j + 8 * g + 4 * h);
+      const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
+      const intx4 cv = *(const intx4*)(c2s + cc);
+      const shortx4 zv = *(const shortx4*)(z + (size_t)p * C + cc);
+      shortx4 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int r = 4 * g + e;
-        const int hv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
-        gv[r] = hv >= 0 ? hv : rhe_shift(819 * hv, 13);
+        const int pv = rescale13((int)((uint32_t)out[t][4 * g + e] + (uint32_t)cv[e]));
+        o[e] = (short)clip16((int)zv[e] + pv);
       }
-    }
-    uint32_t d[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) d[e] = pack2(gv[2 * e], gv[2 * e + 1]);
-    split16(d, gh[j], gl[j]);
-  }
-
-  const intx4* w2h = (const intx4*)a.w2;
-  const intx4* w2l = (const intx4*)a.w2lo;
-  const int* c2 = (const int*)a.b2;
-  int16_t* dst = (int16_t*)a.dst;
-#pragma unroll 1
-  for (int t = 0; t < MT; ++t) {
-    intx16 hh = {}, mid = {}, ll = {};
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      const size_t idx = ((size_t)t * NCH + j) * 64 + lane;
-      const intx4 wa = w2h[idx], wb = w2l[idx];
-      hh = mfma_i8(wa, gh[j], hh);
-      mid = mfma_i8(wa, gl[j], mid);
-      mid = mfma_i8(wb, gh[j], mid);
-      ll = mfma_i8(wb, gl[j], ll);
-    }
-    if (valid) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = 32 * t + 8 * g + 4 * h;
-        const intx4 cv = *(const intx4*)(c2 + c);
-        const shortx4 zv = *(const shortx4*)(z + (size_t)p * C + c);
-        shortx4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * g + e;
-          const int pv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
-          o[e] = (short)clip16((int)zv[e] + pv);
-        }
-        *(shortx4*)(dst + (size_t)p * C + c) = o;
-      }
+      *(shortx4*)(dst + (size_t)p * C + cc) = o;
     }
   }
 }
@@ -379,7 +499,7 @@ hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
-  dim3 grid(grid_tiles(a.h * a.w)), block(256);
+  dim3 grid(dc_grid(a.h, a.w)), block(512);
   switch (C) {
     case 64: launch(k_dcblock_i16<64>, grid, block, st, a); break;
     case 128: launch(k_dcblock_i16<128>, grid, block, st, a); break;
