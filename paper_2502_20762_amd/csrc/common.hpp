@@ -85,6 +85,12 @@ __device__ __forceinline__ void split16(const uint32_t* d, intx4& hi, intx4& lo)
   }
 }
 
+// Workgroup barrier for LDS hand-offs inside a pipelined loop.  It waits for
+// this wave's LDS operations (lgkmcnt) but, unlike __syncthreads(), not for
+// outstanding global->LDS loads: callers wait for those explicitly with
+// s_waitcnt vmcnt(N) so that later chunks stay in flight across the barrier.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ __forceinline__ float leaky(float v) { return v >= 0.f ? v : 0.1f * v; }
 
 // Gaussian rate of one symbol, -log2(max(L, 1e-9)),

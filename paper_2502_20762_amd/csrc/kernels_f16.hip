@@ -121,17 +121,27 @@ __device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, 
   }
 }
 
-// Hidden chunk j from the pw1 fragments in `wb`: bias, LeakyReLU, fp16, stored
-// to `gx` as two B fragments (k = hidden in the permuted order the pw2
-// weights were packed with).
+// pw1 for hidden chunk j from the fragments in `wb` (32 hidden x 32 pixels).
 template <int C>
-__device__ __forceinline__ void dc_hidden(const char* wb, const half8* av, const float* b1s, int j, int h,
-                                          int lane, half8* gx) {
+__device__ __forceinline__ floatx16 dc_hidden_mfma(const char* wb, const half8* av, int lane) {
   constexpr int KS = DcSmem<C>::KS;
   const half8* w = (const half8*)wb + lane;
+  // All fragment reads are issued before the dependent MFMA chain starts, so
+  // the chain does not pay an LDS round trip per link.
+  half8 wf[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) wf[s] = w[s * 64];
+  __builtin_amdgcn_sched_barrier(0);
   floatx16 hacc = {};
 #pragma unroll
-  for (int s = 0; s < KS; ++s) hacc = mfma_f16(w[s * 64], av[s], hacc);
+  for (int s = 0; s < KS; ++s) hacc = mfma_f16(wf[s], av[s], hacc);
+  return hacc;
+}
+
+// Bias, LeakyReLU, fp16; stored to `gx` as two B fragments (k = hidden in the
+// permuted order the pw2 weights were packed with).
+__device__ __forceinline__ void dc_hidden_store(const floatx16& hacc, const float* b1s, int j, int h, int lane,
+                                                half8* gx) {
   half8 g0, g1;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
@@ -199,9 +209,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   const f16* z = (const f16*)a.src;
   const char* wchunks = (const char*)a.w1;
 
-  dc_issue<C>(wchunks, 0, wb0, wave, lane);
-  dc_issue<C>(wchunks, 1, wb1, wave, lane);
-
   // Halo slice k (channels [64k, 64k+64)) -> LDS: slot S = 8 * halo_pixel +
   // (v ^ (halo_pixel & 7)) holds channel vector v of that pixel, so the 3x3
   // reads of 8 neighbouring pixels hit 8 different bank groups.
@@ -228,7 +235,11 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
                                          0, 0);
     }
   };
-  issue_slice(0, wb2);
+  // all halo slices up front (one buffer each); the weight stream starts after the depthwise
+  static_assert(C / CS <= 4, "one LDS buffer per halo slice");
+  char* const slice_buf[4] = {wb0, wb1, wb2, wb3};
+#pragma unroll
+  for (int k = 0; k < C / CS; ++k) issue_slice(k, slice_buf[k]);
   for (int i = threadIdx.x; i < 2 * C; i += 512) b1s[i] = ((const float*)a.b1)[i];
   for (int i = threadIdx.x; i < C; i += 512) {
     b2s[i] = ((const float*)a.b2)[i];
@@ -237,7 +248,7 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   for (int i = threadIdx.x; i < 9 * C / 8; i += 512) ((half8*)dws)[i] = ((const half8*)a.dww)[i];
 
   // depthwise 3x3 (+ bias) for this lane's pixel, channels 16s + 8h + e,
-  // from the staged halo slices (double-buffered in wb2 / wb3).
+  // from the staged halo slices.
   half8 av[KS];
   // byte offset of this lane's 9 taps inside a staged slice, for channel
   // vector h (step ss of the slice XORs in 2 * ss, see the slot layout)
@@ -271,33 +282,37 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
       __builtin_amdgcn_sched_barrier(0);  // keep the live range of one step's taps short
     }
   };
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();  // all slices staged
 #pragma unroll
-  for (int k = 0; k < C / CS; ++k) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();  // slice k staged; slice k-1's buffer no longer read
-    if (k + 1 < C / CS) issue_slice(k + 1, (k & 1) ? wb2 : wb3);
-    dw_slice(k, (k & 1) ? wb3 : wb2);
-  }
-  __syncthreads();  // all halo reads done: wb2 / wb3 become weight buffers
+  for (int k = 0; k < C / CS; ++k) dw_slice(k, slice_buf[k]);
+  __syncthreads();  // all halo reads done: the buffers hold weights from here on
+  dc_issue<C>(wchunks, 0, wb0, wave, lane);
+  dc_issue<C>(wchunks, 1, wb1, wave, lane);
   dc_issue<C>(wchunks, 2, wb2, wave, lane);
 
   floatx16 out[MT / 2];
 #pragma unroll
   for (int t = 0; t < MT / 2; ++t) out[t] = floatx16{};
 
-  if (hf == 0) dc_hidden<C>(wb0, av, b1s, 0, h, lane, gx0[pg]);
-  __syncthreads();
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
+  lds_barrier();  // chunks 0 and 1 staged
+  if (hf == 0) dc_hidden_store(dc_hidden_mfma<C>(wb0, av, lane), b1s, 0, h, lane, gx0[pg]);
+  lds_barrier();
 
   // Iteration j: issue chunk j+3, produce hidden chunk j+1 (one wave of each
   // pair), project hidden chunk j (both waves).
   auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, half8* gcur, half8* gnxt) {
     const bool more = j + 3 < NCH;
     if (more) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
-    if (j + 1 < NCH && hf == ((j + 1) & 1)) dc_hidden<C>(wnxt, av, b1s, j + 1, h, lane, gnxt);
+    const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
+    floatx16 hacc;
+    if (produce) hacc = dc_hidden_mfma<C>(wnxt, av, lane);
     dc_project<C>(wcur, gcur, hf, lane, out);
+    if (produce) dc_hidden_store(hacc, b1s, j + 1, h, lane, gnxt);
     if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
     step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
@@ -305,21 +320,61 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
     step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
   }
-  if (!valid) return;
-
+  // Epilogue through LDS: each wave parks its 32 px x C/2 accumulators (+ bias)
+  // as fp32 in the buffer of its pixel group (row = pixel, 16-byte chunk k of
+  // the row stored at k ^ (row & SWZ)), then all threads add the residual and
+  // store whole pixel rows with coalesced 16-byte accesses.  The residual
+  // loads are issued first so their latency overlaps the parking.
+  static_assert(32 * C * 4 <= BUF, "a pixel group's fp32 output fits one buffer");
+  constexpr int SWZ = (C / 4 - 1) & 31;  // keeps the swizzled chunk inside its row
+  constexpr int CH8 = C / 8;             // 8-channel chunks per pixel
+  constexpr int PER = 128 * CH8 / 512;   // chunks per thread
+  half8 zres[PER];
+  size_t gofs[PER];
+  bool gok[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int idx = i * 512 + threadIdx.x;
+    const int px = idx / CH8, k8 = idx % CH8;
+    const int gpx = px >> 5, row = px & 31;
+    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
+    gok[i] = yy < a.h && xx < a.w;
+    gofs[i] = (size_t)(gok[i] ? yy * a.w + xx : 0) * C + 8 * k8;
+    zres[i] = *(const half8*)(z + gofs[i]);
+  }
+  {
+    char* ob = pg == 0 ? wb0 : pg == 1 ? wb1 : pg == 2 ? wb2 : wb3;
+    const int row = lane & 31;
+#pragma unroll
+    for (int t = 0; t < MT / 2; ++t) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
+        const floatx4 bv = *(const floatx4*)(b2s + cc);
+        floatx4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e] + bv[e];
+        *(floatx4*)(ob + row * (C * 4) + (((cc >> 2) ^ (row & SWZ)) << 4)) = o;
+      }
+    }
+  }
+  lds_barrier();
   f16* dst = (f16*)a.dst;
 #pragma unroll
-  for (int t = 0; t < MT / 2; ++t) {
+  for (int i = 0; i < PER; ++i) {
+    const int idx = i * 512 + threadIdx.x;
+    const int px = idx / CH8, k8 = idx % CH8;
+    const int gpx = px >> 5, row = px & 31;
+    const char* ob = gpx == 0 ? wb0 : gpx == 1 ? wb1 : gpx == 2 ? wb2 : wb3;
+    const floatx4 o0 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
+    const floatx4 o1 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
+    half8 r;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-      const floatx4 bv = *(const floatx4*)(b2s + cc);
-      const half4 zv = *(const half4*)(z + (size_t)p * C + cc);
-      half4 o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = (f16)(out[t][4 * g + e] + bv[e] + (float)zv[e]);
-      *(half4*)(dst + (size_t)p * C + cc) = o;
+    for (int e = 0; e < 4; ++e) {
+      r[e] = (f16)(o0[e] + (float)zres[i][e]);
+      r[4 + e] = (f16)(o1[e] + (float)zres[i][4 + e]);
     }
+    if (gok[i]) *(half8*)(dst + gofs[i]) = r;
   }
 }
 
@@ -414,11 +469,21 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   return hipErrorInvalidValue;
 }
 
+// Rows per workgroup pass: the widest that still gives at least 512
+// workgroups (two per CU), so the latent-resolution convolutions, which have a
+// quarter of the pixels, still fill the chip.
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  if (a.N % 256 == 0) return pw_dispatch<256>(loader, epi, a, st);
-  if (a.N % 192 == 0) return pw_dispatch<192>(loader, epi, a, st);
-  if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
-  if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
+  const int tiles = (a.P + 127) / 128;
+  const int cands[4] = {256, 192, 128, 64};
+  int nt = 0;
+  for (int c : cands)
+    if (a.N % c == 0 && (nt == 0 || tiles * (a.N / c) < 512)) nt = c;
+  switch (nt) {
+    case 256: return pw_dispatch<256>(loader, epi, a, st);
+    case 192: return pw_dispatch<192>(loader, epi, a, st);
+    case 128: return pw_dispatch<128>(loader, epi, a, st);
+    case 64: return pw_dispatch<64>(loader, epi, a, st);
+  }
   return hipErrorInvalidValue;
 }
 
@@ -433,10 +498,12 @@ hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-int prior_partials_f16(int C, int P) { return grid_tiles(P) * (C >= 128 ? C / 128 : 1); }
+// Channels per workgroup: 64 (mu and s rows, 128 accumulator registers), which
+// gives C / 64 workgroups per pixel tile.
+int prior_partials_f16(int C, int P) { return grid_tiles(P) * (C / 64); }
 
 hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials) {
-  const int ch = a.C >= 128 ? 128 : a.C;
+  const int ch = 64;
   dim3 grid(grid_tiles(a.P), a.C / ch), block(256);
   if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / ch);
   if (ch == 128 && a.decode) launch(k_prior_f16<128, true>, grid, block, st, a);

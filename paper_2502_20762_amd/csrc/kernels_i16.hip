@@ -16,7 +16,13 @@
 
 namespace nc {
 
-__device__ __forceinline__ int rescale13(int a) { return clip16(rhe_shift(a, 13)); }
+// clip(RHE(a / 8192)) for any int32 a.  |a| >= 2^28 saturates either way, so a
+// is first clamped to +-2^28; then the round-half-even bias can be added
+// without overflow: RHE(a / 2^s) = (a + 2^(s-1) - 1 + ((a >> s) & 1)) >> s.
+__device__ __forceinline__ int rescale13(int a) {
+  const int ac = min(max(a, -(1 << 28)), 1 << 28);
+  return clip16((ac + 4095 + ((ac >> 13) & 1)) >> 13);
+}
 
 __device__ __forceinline__ uint32_t pack2(int lo, int hi) {
   return ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
@@ -158,20 +164,41 @@ __device__ __forceinline__ void dci_issue(const char* wchunks, int j, char* buf,
   }
 }
 
+struct I16Acc {
+  intx16 hh, mid, ll;
+};
+
 template <int C>
-__device__ __forceinline__ void dci_hidden(const char* wb, const intx4* ah, const intx4* al, const int* c1s, int j,
-                                           int h, int lane, intx4* gx) {
+__device__ __forceinline__ I16Acc dci_hidden_mfma(const char* wb, const intx4* ah, const intx4* al, int lane) {
   constexpr int KSI = DcSmemI<C>::KSI;
   const intx4* w = (const intx4*)wb + lane;
-  intx16 hh = {}, mid = {}, ll = {};
+  // Fragment reads are issued ahead of the MFMAs in groups of half a chunk.
+  constexpr int G = KSI >= 4 ? KSI / 2 : KSI;
+  I16Acc acc{{}, {}, {}};
 #pragma unroll
-  for (int s = 0; s < KSI; ++s) {
-    const intx4 wa = w[s * 64], wl = w[(KSI + s) * 64];
-    hh = mfma_i8(wa, ah[s], hh);
-    mid = mfma_i8(wa, al[s], mid);
-    mid = mfma_i8(wl, ah[s], mid);
-    ll = mfma_i8(wl, al[s], ll);
+  for (int s0 = 0; s0 < KSI; s0 += G) {
+    intx4 wa[G], wl[G];
+#pragma unroll
+    for (int s = 0; s < G; ++s) {
+      wa[s] = w[(s0 + s) * 64];
+      wl[s] = w[(KSI + s0 + s) * 64];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < G; ++s) {
+      acc.hh = mfma_i8(wa[s], ah[s0 + s], acc.hh);
+      acc.mid = mfma_i8(wa[s], al[s0 + s], acc.mid);
+      acc.mid = mfma_i8(wl[s], ah[s0 + s], acc.mid);
+      acc.ll = mfma_i8(wl[s], al[s0 + s], acc.ll);
+    }
   }
+  return acc;
+}
+
+// Combine, rescale, integer LeakyReLU (slope 819 / 8192), split into int8
+// digits, store as the pw2 operand fragments.
+__device__ __forceinline__ void dci_hidden_store(const I16Acc& acc, const int* c1s, int j, int h, int lane,
+                                                 intx4* gx) {
   int gv[16];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
@@ -179,8 +206,9 @@ __device__ __forceinline__ void dci_hidden(const char* wb, const intx4* ah, cons
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = 4 * g + e;
-      const int hv = rescale13(combine_i16(hh[r], mid[r], ll[r], cv[e]));
-      gv[r] = hv >= 0 ? hv : rhe_shift(819 * hv, 13);
+      const int hv = rescale13(combine_i16(acc.hh[r], acc.mid[r], acc.ll[r], cv[e]));
+      const int m = 819 * hv;  // |m| < 2^25: the bias form of RHE cannot overflow
+      gv[r] = hv >= 0 ? hv : (m + 4095 + ((m >> 13) & 1)) >> 13;
     }
   }
   uint32_t d[8];
@@ -251,9 +279,6 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   const int16_t* z = (const int16_t*)a.src;
   const char* wchunks = (const char*)a.w1;
 
-  dci_issue<C>(wchunks, 0, wb0, wave, lane);
-  dci_issue<C>(wchunks, 1, wb1, wave, lane);
-
   constexpr int SLICE_PER_WAVE = (SLICE_INSTR + 7) / 8;
   const int16_t* slice_src[SLICE_PER_WAVE];
   bool slice_on[SLICE_PER_WAVE];
@@ -276,7 +301,10 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
                                          0, 0);
     }
   };
-  issue_slice(0, wb2);
+  static_assert(C / CS <= 4, "one LDS buffer per halo slice");
+  char* const slice_buf[4] = {wb0, wb1, wb2, wb3};
+#pragma unroll
+  for (int k = 0; k < C / CS; ++k) issue_slice(k, slice_buf[k]);
   for (int i = threadIdx.x; i < 2 * C; i += 512) c1s[i] = ((const int*)a.b1)[i];
   for (int i = threadIdx.x; i < C; i += 512) {
     c2s[i] = ((const int*)a.b2)[i];
@@ -324,31 +352,35 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();  // all slices staged
 #pragma unroll
-  for (int k = 0; k < C / CS; ++k) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (k + 1 < C / CS) issue_slice(k + 1, (k & 1) ? wb2 : wb3);
-    dw_slice(k, (k & 1) ? wb3 : wb2);
-  }
-  __syncthreads();
+  for (int k = 0; k < C / CS; ++k) dw_slice(k, slice_buf[k]);
+  __syncthreads();  // all halo reads done: the buffers hold weights from here on
+  dci_issue<C>(wchunks, 0, wb0, wave, lane);
+  dci_issue<C>(wchunks, 1, wb1, wave, lane);
   dci_issue<C>(wchunks, 2, wb2, wave, lane);
 
   intx16 out[MT / 2];
 #pragma unroll
   for (int t = 0; t < MT / 2; ++t) out[t] = intx16{};
 
-  if (hf == 0) dci_hidden<C>(wb0, ah, al, c1s, 0, h, lane, gx0[pg]);
-  __syncthreads();
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
+  lds_barrier();  // chunks 0 and 1 staged
+  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, lane), c1s, 0, h, lane, gx0[pg]);
+  lds_barrier();
 
   auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, intx4* gcur, intx4* gnxt) {
     const bool more = j + 3 < NCH;
     if (more) dci_issue<C>(wchunks, j + 3, wiss, wave, lane);
-    if (j + 1 < NCH && hf == ((j + 1) & 1)) dci_hidden<C>(wnxt, ah, al, c1s, j + 1, h, lane, gnxt);
+    const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
+    I16Acc hacc;
+    if (produce) hacc = dci_hidden_mfma<C>(wnxt, ah, al, lane);
     dci_project<C>(wcur, gcur, hf, lane, out);
+    if (produce) dci_hidden_store(hacc, c1s, j + 1, h, lane, gnxt);
     if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
     step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
@@ -492,8 +524,10 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   return hipErrorInvalidValue;
 }
 
+// Rows per workgroup pass: 128 unless that leaves fewer than 512 workgroups.
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
+  const int tiles = (a.P + 127) / 128;
+  if (a.N % 128 == 0 && tiles * (a.N / 128) >= 512) return pw_dispatch<128>(loader, epi, a, st);
   if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
   return hipErrorInvalidValue;
 }
