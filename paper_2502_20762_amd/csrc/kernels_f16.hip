@@ -13,79 +13,210 @@
 
 namespace nc {
 
+// ---------------------------------------------------------------- pointwise
+// out^T[rows n0 .. n0+NT)[128 pixels] = W * act^T (+ bias) for one tile of
+// 128 consecutive output pixels.  8 waves: wave w owns pixels 32 (w & 3) ..
+// +31 and rows (w >> 2) NT/2 .. +NT/2.  K is consumed 64 at a time through four
+// LDS stages (distinct objects, statically indexed), each holding the
+// activation slice (128 pixels x 64 channels, one 128-byte row per pixel,
+// 16-byte vector v of pixel px stored at slot v ^ (px & 7)) and the weight
+// fragments of those 64 contraction indices, filled by direct global->LDS
+// loads three stages ahead.  The result is parked in LDS and written with
+// coalesced 16-byte stores.
+template <int NT>
+struct PwSmem {
+  static constexpr int ACT = 128 * 128;               // activation slice bytes
+  static constexpr int WGT = NT / 32 * 4 * 1024;      // weight fragments bytes
+  static constexpr int STAGE = ACT + WGT;
+  static constexpr int DMA_PER_WAVE = (ACT / 1024 + WGT / 1024) / 8;
+};
+
+// Global address of 16-byte activation vector v (8 contraction indices
+// starting at 64 kc + 8 v) of output pixel gp.
 template <int LOADER>
-__device__ __forceinline__ half8 load_b_f16(const PwArgs& a, int p, int k0) {
+__device__ __forceinline__ const char* pw_act_src(const PwArgs& a, int gp, int kc, int v) {
+  const int k = 64 * kc + 8 * v;
   if constexpr (LOADER == LD_NHWC) {
-    if (k0 < a.C0) return *(const half8*)((const f16*)a.src0 + (size_t)p * a.C0 + k0);
-    return *(const half8*)((const f16*)a.src1 + (size_t)p * a.C1 + (k0 - a.C0));
+    if (k < a.C0) return (const char*)((const f16*)a.src0 + (size_t)gp * a.C0 + k);
+    return (const char*)((const f16*)a.src1 + (size_t)gp * a.C1 + (k - a.C0));
   } else if constexpr (LOADER == LD_FRAME) {
-    const int py = p / a.w8, px = p - py * a.w8;
-    const int c = k0 >> 6, i = (k0 >> 3) & 7;
-    return *(const half8*)((const f16*)a.src0 + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px);
+    // unshuffle x8: k = 64 c + 8 i + j -> colour c = kc, frame row 8 py + i = 8 py + v, columns 8 px .. +7
+    const int py = gp / a.w8, px = gp - py * a.w8;
+    return (const char*)((const f16*)a.src0 + (size_t)kc * a.H * a.W + (size_t)(8 * py + v) * a.W + 8 * px);
   } else {
+    // 2x2 stride 2: k = (2 i + j) Csrc + c from pixel (2 Y + i, 2 X + j)
     const int w16 = a.w8 >> 1;
-    const int Y = p / w16, X = p - Y * w16;
-    const int tap = k0 / a.Csrc, c = k0 - tap * a.Csrc;
+    const int Y = gp / w16, X = gp - Y * w16;
+    const int tap = k / a.Csrc, c = k - tap * a.Csrc;
     const int pix = (2 * Y + (tap >> 1)) * a.w8 + 2 * X + (tap & 1);
-    return *(const half8*)((const f16*)a.src0 + (size_t)pix * a.Csrc + c);
+    return (const char*)((const f16*)a.src0 + (size_t)pix * a.Csrc + c);
   }
 }
 
+template <int NT, int LOADER>
+__device__ __forceinline__ void pw_issue(const PwArgs& a, int tile, int n0, int kc, char* stage, int wave, int lane) {
+  using S = PwSmem<NT>;
+  constexpr int ACT_INSTR = S::ACT / 1024;  // 16
+#pragma unroll
+  for (int i = 0; i < ACT_INSTR / 8; ++i) {
+    const int ins = wave + 8 * i;
+    const int slot = ins * 64 + lane;
+    const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
+    const int gp = min(tile * 128 + px, a.P - 1);  // pixels past the end reload the last one
+    __builtin_amdgcn_global_load_lds((const void*)pw_act_src<LOADER>(a, gp, kc, v),
+                                     (__attribute__((address_space(3))) void*)(stage + ins * 1024), 16, 0, 0);
+  }
+  const int ks = a.K / 16;
+  const char* w = (const char*)a.wfrag;
+#pragma unroll
+  for (int i = 0; i < S::WGT / 1024 / 8; ++i) {
+    const int f = wave + 8 * i;  // fragment f of the stage: row tile f / 4, k-step f % 4
+    const int mt = n0 / 32 + (f >> 2), sk = 4 * kc + (f & 3);
+    __builtin_amdgcn_global_load_lds((const void*)(w + (((size_t)mt * ks + sk) * 64 + lane) * 16),
+                                     (__attribute__((address_space(3))) void*)(stage + S::ACT + f * 1024), 16, 0, 0);
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void pw_compute(const char* stage, int pg, int hf, int lane, floatx16* acc) {
+  using S = PwSmem<NT>;
+  constexpr int RT = NT / 64;  // row tiles per wave
+  const int pl = pg * 32 + (lane & 31), h = lane >> 5;
+  half8 b[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) b[ks] = *(const half8*)(stage + pl * 128 + ((((2 * ks + h) ^ (pl & 7))) << 4));
+  half8 w[RT][4];
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) w[t][ks] = *(const half8*)(stage + S::ACT + ((hf * RT + t) * 4 + ks) * 1024 + lane * 16);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int t = 0; t < RT; ++t) acc[t] = mfma_f16(w[t][ks], b[ks], acc[t]);
+}
+
 template <int NT, int LOADER, int EPI>
-__global__ __launch_bounds__(256) void k_pw_f16(PwArgs a) {
-  constexpr int MT = NT / 32;
+__global__ __launch_bounds__(512) void k_pw_f16(PwArgs a) {
+  using S = PwSmem<NT>;
+  constexpr int RT = NT / 64;
+  __shared__ __attribute__((aligned(1024))) char st0[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st1[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st2[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st3[S::STAGE];
   const int ntile = (a.P + 127) / 128;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < a.P;
-  const int mt0 = blockIdx.y * MT;
-  const int ks = a.K / 16;
-  const half8* wf = (const half8*)a.wfrag;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pg = wave & 3, hf = wave >> 2;
+  const int n0 = blockIdx.y * NT;
+  const int nk = a.K / 64;
 
-  floatx16 acc[MT];
+  floatx16 acc[RT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = floatx16{};
+  for (int t = 0; t < RT; ++t) acc[t] = floatx16{};
+  floatx4 bias[RT][4];
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) bias[t][g] = *(const floatx4*)((const float*)a.bias + n0 + 32 * (hf * RT + t) + 8 * g + 4 * h);
 
-  for (int s = 0; s < ks; ++s) {
-    half8 b = {};
-    if (valid) b = load_b_f16<LOADER>(a, p, 16 * s + 8 * h);
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const half8 w = wf[((size_t)(mt0 + t) * ks + s) * 64 + lane];
-      acc[t] = mfma_f16(w, b, acc[t]);
-    }
+  pw_issue<NT, LOADER>(a, tile, n0, 0, st0, wave, lane);
+  if (nk > 1) pw_issue<NT, LOADER>(a, tile, n0, 1, st1, wave, lane);
+  if (nk > 2) pw_issue<NT, LOADER>(a, tile, n0, 2, st2, wave, lane);
+  // Stage kc: wait until at most the later-issued stages are in flight, make
+  // every wave's loads visible, refill the buffer freed in the previous
+  // iteration with stage kc + 3, then compute.
+  auto step = [&](int kc, const char* cur, char* refill) {
+    const int ahead = min(nk - 1 - kc, 2);  // stages issued after kc still in flight
+    if (ahead == 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * S::DMA_PER_WAVE) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(S::DMA_PER_WAVE) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    if (kc + 3 < nk) pw_issue<NT, LOADER>(a, tile, n0, kc + 3, refill, wave, lane);
+    pw_compute<NT>(cur, pg, hf, lane, acc);
+  };
+  for (int kc = 0; kc < nk; kc += 4) {
+    step(kc, st0, st3);
+    if (kc + 1 < nk) step(kc + 1, st1, st0);
+    if (kc + 2 < nk) step(kc + 2, st2, st1);
+    if (kc + 3 < nk) step(kc + 3, st3, st2);
   }
-  if (!valid) return;
+  lds_barrier();  // every wave is done reading the stages
 
-  const float* bias = (const float*)a.bias;
+  // park acc + bias as fp32: pixel group pg in stage buffer pg, row = pixel,
+  // NT floats per row, 16-byte chunk c of a row at c ^ (row & SWZ)
+  constexpr int SWZ = (NT / 4 - 1) & 31;
+  static_assert(32 * NT * 4 <= S::STAGE, "a pixel group's output fits one stage buffer");
+  {
+    char* ob = pg == 0 ? st0 : pg == 1 ? st1 : pg == 2 ? st2 : st3;
+    const int row = lane & 31;
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = 32 * (mt0 + t) + 8 * g + 4 * h;
-      const floatx4 bv = *(const floatx4*)(bias + n);
-      half4 o;
-      if constexpr (EPI == EP_REC) {
+      for (int g = 0; g < 4; ++g) {
+        const int nl = 32 * (hf * RT + t) + 8 * g + 4 * h;  // row of the pass
+        floatx4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (f16)fminf(fmaxf(acc[t][4 * g + e] + bv[e], 0.f), 1.f);
-        const int c = n >> 6, i = (n >> 3) & 7, j0 = n & 7;
-        const int py = p / a.w8, px = p - py * a.w8;
-        *(half4*)((f16*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px + j0) = o;
-      } else {
+        for (int e = 0; e < 4; ++e) o[e] = acc[t][4 * g + e] + bias[t][g][e];
+        *(floatx4*)(ob + row * (NT * 4) + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
+      }
+  }
+  lds_barrier();
+
+  auto parked = [&](int px, int nl8) {  // 8 floats: pass rows nl8 * 8 .. +7 of tile pixel px
+    const int gpx = px >> 5, row = px & 31;
+    const char* ob = gpx == 0 ? st0 : gpx == 1 ? st1 : gpx == 2 ? st2 : st3;
+    const floatx4 o0 = *(const floatx4*)(ob + row * (NT * 4) + (((2 * nl8) ^ (row & SWZ)) << 4));
+    const floatx4 o1 = *(const floatx4*)(ob + row * (NT * 4) + (((2 * nl8 + 1) ^ (row & SWZ)) << 4));
+    floatx16 r;  // only [0, 8) used
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (f16)(acc[t][4 * g + e] + bv[e]);
+    for (int e = 0; e < 4; ++e) { r[e] = o0[e]; r[4 + e] = o1[e]; }
+    return r;
+  };
+  if constexpr (EPI == EP_REC) {
+    // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
+    // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
+    constexpr int UNITS = 128 * (NT / 8);
+#pragma unroll
+    for (int it = 0; it < UNITS / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int nl8 = idx >> 7, px = idx & 127;  // consecutive threads walk pixels
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        const floatx16 r = parked(px, nl8);
+        const int n = n0 + 8 * nl8, c = n >> 6, i = (n >> 3) & 7;
+        const int py = gp / a.w8, pxx = gp - py * a.w8;
+        half8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (f16)fminf(fmaxf(r[e], 0.f), 1.f);
+        *(half8*)((f16*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * pxx) = o;
+      }
+    }
+  } else {
+    constexpr int UNITS = 128 * (NT / 8);
+#pragma unroll
+    for (int it = 0; it < UNITS / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int px = idx / (NT / 8), nl8 = idx % (NT / 8);  // consecutive threads walk a pixel's row
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        const floatx16 r = parked(px, nl8);
+        half8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
+        size_t off;
         if constexpr (EPI == EP_NHWC) {
-          *(half4*)((f16*)a.dst + (size_t)p * a.Cdst + n) = o;
-        } else {  // EP_UP: row n = sp * C + c
-          const int C = a.Cdst;
+          off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
+        } else {  // EP_UP: pass rows n = sp * C + c, all in one sub-position sp
+          const int C = a.Cdst, n = n0 + 8 * nl8;
           const int sp = n / C, c = n - sp * C;
           const int w16 = a.w8 >> 1;
-          const int Y = p / w16, X = p - Y * w16;
-          const int pix = (2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1);
-          *(half4*)((f16*)a.dst + (size_t)pix * C + c) = o;
+          const int Y = gp / w16, X = gp - Y * w16;
+          off = (size_t)((2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1)) * C + c;
         }
+        *(half8*)((f16*)a.dst + off) = o;
       }
     }
   }
@@ -454,10 +585,10 @@ __global__ __launch_bounds__(256) void k_prior_f16(PriorArgs a) {
 
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  dim3 grid(grid_tiles(a.P), a.N / NT), block(256);
+  dim3 grid(grid_tiles(a.P), a.N / NT), block(512);
 #define NC_PW(L, E)                                                            \
   if (loader == L && epi == E) {                                               \
-    launch(k_pw_f16<NT, L, E>, grid, block, st, a);           \
+    launch(k_pw_f16<NT, L, E>, grid, block, st, a);                            \
     return hipGetLastError();                                                  \
   }
   NC_PW(LD_NHWC, EP_NHWC)
@@ -469,21 +600,14 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   return hipErrorInvalidValue;
 }
 
-// Rows per workgroup pass: the widest that still gives at least 512
-// workgroups (two per CU), so the latent-resolution convolutions, which have a
-// quarter of the pixels, still fill the chip.
+// Rows per workgroup pass: 128, or 64 where 128 leaves fewer than 512
+// workgroups (the latent-resolution convolutions) or does not divide N.
+// K must be a multiple of 64 (C = 64, 128, 256; 192 for the patch embed).
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
+  if (a.K % 64) return hipErrorInvalidValue;
   const int tiles = (a.P + 127) / 128;
-  const int cands[4] = {256, 192, 128, 64};
-  int nt = 0;
-  for (int c : cands)
-    if (a.N % c == 0 && (nt == 0 || tiles * (a.N / c) < 512)) nt = c;
-  switch (nt) {
-    case 256: return pw_dispatch<256>(loader, epi, a, st);
-    case 192: return pw_dispatch<192>(loader, epi, a, st);
-    case 128: return pw_dispatch<128>(loader, epi, a, st);
-    case 64: return pw_dispatch<64>(loader, epi, a, st);
-  }
+  if (a.N % 128 == 0 && tiles * (a.N / 128) >= 512) return pw_dispatch<128>(loader, epi, a, st);
+  if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
   return hipErrorInvalidValue;
 }
 
