@@ -28,111 +28,222 @@ __device__ __forceinline__ uint32_t pack2(int lo, int hi) {
   return ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
 }
 
-// 16 consecutive int16 activations of pixel p starting at channel k0 -> hi/lo fragments.
+// ---------------------------------------------------------------- pointwise
+// Same tiling and LDS pipeline as the fp16 pointwise kernel: 8 waves per tile
+// of 128 output pixels, K consumed 64 at a time through four LDS stages.  A
+// stage holds the activation slice (int16, or the fp16 frame for the patch
+// embed, converted with x_i = round(512 x) when the operand is read) and, per
+// 32-row tile, four int8 fragments: hi digits for k-steps 0 and 1, then lo
+// digits for k-steps 0 and 1 (32 contraction indices each).
+struct PwSmemI {
+  static constexpr int ACT = 128 * 128;
+};
+template <int NT>
+struct PwSmemIN {
+  static constexpr int WGT = NT / 32 * 4 * 1024;
+  static constexpr int STAGE = PwSmemI::ACT + WGT;
+  static constexpr int DMA_PER_WAVE = (PwSmemI::ACT / 1024 + WGT / 1024) / 8;
+};
+
 template <int LOADER>
-__device__ __forceinline__ void load_b_i16(const PwArgs& a, int p, int k0, intx4& bh, intx4& bl) {
-  uint32_t d[8];
-  if constexpr (LOADER == LD_FRAME) {
-    const int py = p / a.w8, px = p - py * a.w8;
-    const int c = k0 >> 6, i = (k0 >> 3) & 7;  // rows i and i + 1, 8 pixels each
-    const f16* base = (const f16*)a.src0 + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px;
-    const half8 r0 = *(const half8*)base;
-    const half8 r1 = *(const half8*)(base + a.W);
-    int v[16];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      v[e] = clip16((int)rintf((float)r0[e] * 512.f));
-      v[8 + e] = clip16((int)rintf((float)r1[e] * 512.f));
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) d[e] = pack2(v[2 * e], v[2 * e + 1]);
+__device__ __forceinline__ const char* pwi_act_src(const PwArgs& a, int gp, int kc, int v) {
+  const int k = 64 * kc + 8 * v;
+  if constexpr (LOADER == LD_NHWC) {
+    if (k < a.C0) return (const char*)((const int16_t*)a.src0 + (size_t)gp * a.C0 + k);
+    return (const char*)((const int16_t*)a.src1 + (size_t)gp * a.C1 + (k - a.C0));
+  } else if constexpr (LOADER == LD_FRAME) {
+    const int py = gp / a.w8, px = gp - py * a.w8;
+    return (const char*)((const f16*)a.src0 + (size_t)kc * a.H * a.W + (size_t)(8 * py + v) * a.W + 8 * px);
   } else {
-    const int16_t* ptr;
-    if constexpr (LOADER == LD_NHWC) {
-      ptr = (k0 < a.C0) ? (const int16_t*)a.src0 + (size_t)p * a.C0 + k0
-                        : (const int16_t*)a.src1 + (size_t)p * a.C1 + (k0 - a.C0);
-    } else {
-      const int w16 = a.w8 >> 1;
-      const int Y = p / w16, X = p - Y * w16;
-      const int tap = k0 / a.Csrc, c = k0 - tap * a.Csrc;
-      const int pix = (2 * Y + (tap >> 1)) * a.w8 + 2 * X + (tap & 1);
-      ptr = (const int16_t*)a.src0 + (size_t)pix * a.Csrc + c;
-    }
-    const intx4 q0 = *(const intx4*)ptr;
-    const intx4 q1 = *(const intx4*)(ptr + 8);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
+    const int w16 = a.w8 >> 1;
+    const int Y = gp / w16, X = gp - Y * w16;
+    const int tap = k / a.Csrc, c = k - tap * a.Csrc;
+    const int pix = (2 * Y + (tap >> 1)) * a.w8 + 2 * X + (tap & 1);
+    return (const char*)((const int16_t*)a.src0 + (size_t)pix * a.Csrc + c);
   }
-  split16(d, bh, bl);
+}
+
+template <int NT, int LOADER>
+__device__ __forceinline__ void pwi_issue(const PwArgs& a, int tile, int n0, int kc, char* stage, int wave, int lane) {
+  constexpr int ACT_INSTR = PwSmemI::ACT / 1024;
+#pragma unroll
+  for (int i = 0; i < ACT_INSTR / 8; ++i) {
+    const int ins = wave + 8 * i;
+    const int slot = ins * 64 + lane;
+    const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
+    const int gp = min(tile * 128 + px, a.P - 1);
+    __builtin_amdgcn_global_load_lds((const void*)pwi_act_src<LOADER>(a, gp, kc, v),
+                                     (__attribute__((address_space(3))) void*)(stage + ins * 1024), 16, 0, 0);
+  }
+  const int ks = a.K / 32;
+#pragma unroll
+  for (int i = 0; i < PwSmemIN<NT>::WGT / 1024 / 8; ++i) {
+    const int f = wave + 8 * i;  // row tile f / 4; f % 4: hi k0, hi k1, lo k0, lo k1
+    const int mt = n0 / 32 + (f >> 2), sk = 2 * kc + (f & 1);
+    const char* plane = (f & 2) ? (const char*)a.wfrag_lo : (const char*)a.wfrag;
+    __builtin_amdgcn_global_load_lds((const void*)(plane + (((size_t)mt * ks + sk) * 64 + lane) * 16),
+                                     (__attribute__((address_space(3))) void*)(stage + PwSmemI::ACT + f * 1024), 16,
+                                     0, 0);
+  }
+}
+
+template <int NT, int LOADER>
+__device__ __forceinline__ void pwi_compute(const char* stage, int pg, int hf, int lane, intx16 (*acc)[3]) {
+  constexpr int RT = NT / 64;
+  const int pl = pg * 32 + (lane & 31), h = lane >> 5;
+  intx4 bh[2], bl[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    // contraction indices 32 ks + 16 h .. +15 = vectors 4 ks + 2 h and + 1
+    const int v0 = 4 * ks + 2 * h;
+    uint32_t d[8];
+    if constexpr (LOADER == LD_FRAME) {
+      const half8 x0 = *(const half8*)(stage + pl * 128 + ((v0 ^ (pl & 7)) << 4));
+      const half8 x1 = *(const half8*)(stage + pl * 128 + (((v0 + 1) ^ (pl & 7)) << 4));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        d[e] = pack2(clip16((int)rintf((float)x0[2 * e] * 512.f)), clip16((int)rintf((float)x0[2 * e + 1] * 512.f)));
+        d[4 + e] = pack2(clip16((int)rintf((float)x1[2 * e] * 512.f)), clip16((int)rintf((float)x1[2 * e + 1] * 512.f)));
+      }
+    } else {
+      const intx4 q0 = *(const intx4*)(stage + pl * 128 + ((v0 ^ (pl & 7)) << 4));
+      const intx4 q1 = *(const intx4*)(stage + pl * 128 + (((v0 + 1) ^ (pl & 7)) << 4));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
+    }
+    split16(d, bh[ks], bl[ks]);
+  }
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const char* wt = stage + PwSmemI::ACT + (hf * RT + t) * 4 * 1024 + lane * 16;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const intx4 wh = *(const intx4*)(wt + ks * 1024), wl = *(const intx4*)(wt + (2 + ks) * 1024);
+      acc[t][0] = mfma_i8(wh, bh[ks], acc[t][0]);
+      acc[t][1] = mfma_i8(wh, bl[ks], acc[t][1]);
+      acc[t][1] = mfma_i8(wl, bh[ks], acc[t][1]);
+      acc[t][2] = mfma_i8(wl, bl[ks], acc[t][2]);
+    }
+  }
 }
 
 template <int NT, int LOADER, int EPI>
-__global__ __launch_bounds__(256) void k_pw_i16(PwArgs a) {
-  constexpr int MT = NT / 32;
+__global__ __launch_bounds__(512) void k_pw_i16(PwArgs a) {
+  using S = PwSmemIN<NT>;
+  constexpr int RT = NT / 64;
+  __shared__ __attribute__((aligned(1024))) char st0[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st1[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st2[S::STAGE];
+  __shared__ __attribute__((aligned(1024))) char st3[S::STAGE];
   const int ntile = (a.P + 127) / 128;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < a.P;
-  const int mt0 = blockIdx.y * MT;
-  const int ks = a.K / 32;
-  const intx4* wh = (const intx4*)a.wfrag;
-  const intx4* wl = (const intx4*)a.wfrag_lo;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pg = wave & 3, hf = wave >> 2;
+  const int n0 = blockIdx.y * NT;
+  const int nk = a.K / 64;
 
-  intx16 ahh[MT], amid[MT], all[MT];
+  intx16 acc[RT][3];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) { ahh[t] = intx16{}; amid[t] = intx16{}; all[t] = intx16{}; }
+  for (int t = 0; t < RT; ++t) acc[t][0] = acc[t][1] = acc[t][2] = intx16{};
+  intx4 corr[RT][4];
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) corr[t][g] = *(const intx4*)((const int*)a.bias + n0 + 32 * (hf * RT + t) + 8 * g + 4 * h);
 
-  for (int s = 0; s < ks; ++s) {
-    intx4 bh = {}, bl = {};
-    if (valid) load_b_i16<LOADER>(a, p, 32 * s + 16 * h, bh, bl);
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const size_t idx = ((size_t)(mt0 + t) * ks + s) * 64 + lane;
-      const intx4 ah = wh[idx], al = wl[idx];
-      ahh[t] = mfma_i8(ah, bh, ahh[t]);
-      amid[t] = mfma_i8(ah, bl, amid[t]);
-      amid[t] = mfma_i8(al, bh, amid[t]);
-      all[t] = mfma_i8(al, bl, all[t]);
-    }
+  pwi_issue<NT, LOADER>(a, tile, n0, 0, st0, wave, lane);
+  if (nk > 1) pwi_issue<NT, LOADER>(a, tile, n0, 1, st1, wave, lane);
+  if (nk > 2) pwi_issue<NT, LOADER>(a, tile, n0, 2, st2, wave, lane);
+  auto step = [&](int kc, const char* cur, char* refill) {
+    const int ahead = min(nk - 1 - kc, 2);
+    if (ahead == 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * S::DMA_PER_WAVE) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(S::DMA_PER_WAVE) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    if (kc + 3 < nk) pwi_issue<NT, LOADER>(a, tile, n0, kc + 3, refill, wave, lane);
+    pwi_compute<NT, LOADER>(cur, pg, hf, lane, acc);
+  };
+  for (int kc = 0; kc < nk; kc += 4) {
+    step(kc, st0, st3);
+    if (kc + 1 < nk) step(kc + 1, st1, st0);
+    if (kc + 2 < nk) step(kc + 2, st2, st1);
+    if (kc + 3 < nk) step(kc + 3, st3, st2);
   }
-  if (!valid) return;
+  lds_barrier();
 
-  const int* corr = (const int*)a.bias;
+  // park the rescaled int16 results as int32, as in the fp16 kernel
+  constexpr int SWZ = (NT / 4 - 1) & 31;
+  static_assert(32 * NT * 4 <= S::STAGE, "a pixel group's output fits one stage buffer");
+  {
+    char* ob = pg == 0 ? st0 : pg == 1 ? st1 : pg == 2 ? st2 : st3;
+    const int row = lane & 31;
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = 32 * (mt0 + t) + 8 * g + 4 * h;
-      const intx4 cv = *(const intx4*)(corr + n);
-      int v[4];
+      for (int g = 0; g < 4; ++g) {
+        const int nl = 32 * (hf * RT + t) + 8 * g + 4 * h;
+        intx4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 4 * g + e;
-        v[e] = rescale13(combine_i16(ahh[t][r], amid[t][r], all[t][r], cv[e]));
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          o[e] = rescale13(combine_i16(acc[t][0][r], acc[t][1][r], acc[t][2][r], corr[t][g][e]));
+        }
+        *(intx4*)(ob + row * (NT * 4) + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
       }
-      if constexpr (EPI == EP_REC) {
-        shortx4 o;
+  }
+  lds_barrier();
+
+  auto parked = [&](int px, int nl8, int* v) {
+    const int gpx = px >> 5, row = px & 31;
+    const char* ob = gpx == 0 ? st0 : gpx == 1 ? st1 : gpx == 2 ? st2 : st3;
+    const intx4 o0 = *(const intx4*)(ob + row * (NT * 4) + (((2 * nl8) ^ (row & SWZ)) << 4));
+    const intx4 o1 = *(const intx4*)(ob + row * (NT * 4) + (((2 * nl8 + 1) ^ (row & SWZ)) << 4));
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (short)min(max(v[e], 0), 512);
-        const int c = n >> 6, i = (n >> 3) & 7, j0 = n & 7;
-        const int py = p / a.w8, px = p - py * a.w8;
-        *(shortx4*)((int16_t*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * px + j0) = o;
-      } else {
-        shortx4 o;
+    for (int e = 0; e < 4; ++e) { v[e] = o0[e]; v[4 + e] = o1[e]; }
+  };
+  constexpr int UNITS = 128 * (NT / 8);
+  if constexpr (EPI == EP_REC) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (short)v[e];
+    for (int it = 0; it < UNITS / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int nl8 = idx >> 7, px = idx & 127;
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        int v[8];
+        parked(px, nl8, v);
+        const int n = n0 + 8 * nl8, c = n >> 6, i = (n >> 3) & 7;
+        const int py = gp / a.w8, pxx = gp - py * a.w8;
+        shortx8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (short)min(max(v[e], 0), 512);
+        *(shortx8*)((int16_t*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * pxx) = o;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < UNITS / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int px = idx / (NT / 8), nl8 = idx % (NT / 8);
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        int v[8];
+        parked(px, nl8, v);
+        shortx8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
+        size_t off;
         if constexpr (EPI == EP_NHWC) {
-          *(shortx4*)((int16_t*)a.dst + (size_t)p * a.Cdst + n) = o;
+          off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {
-          const int C = a.Cdst;
+          const int C = a.Cdst, n = n0 + 8 * nl8;
           const int sp = n / C, c = n - sp * C;
           const int w16 = a.w8 >> 1;
-          const int Y = p / w16, X = p - Y * w16;
-          const int pix = (2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1);
-          *(shortx4*)((int16_t*)a.dst + (size_t)pix * C + c) = o;
+          const int Y = gp / w16, X = gp - Y * w16;
+          off = (size_t)((2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1)) * C + c;
         }
+        *(shortx8*)((int16_t*)a.dst + off) = o;
       }
     }
   }
@@ -509,10 +620,10 @@ __global__ __launch_bounds__(256) void k_prior_i16(PriorArgs a) {
 
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  dim3 grid(grid_tiles(a.P), a.N / NT), block(256);
+  dim3 grid(grid_tiles(a.P), a.N / NT), block(512);
 #define NC_PW(L, E)                                                            \
   if (loader == L && epi == E) {                                               \
-    launch(k_pw_i16<NT, L, E>, grid, block, st, a);           \
+    launch(k_pw_i16<NT, L, E>, grid, block, st, a);                            \
     return hipGetLastError();                                                  \
   }
   NC_PW(LD_NHWC, EP_NHWC)
@@ -524,8 +635,10 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   return hipErrorInvalidValue;
 }
 
-// Rows per workgroup pass: 128 unless that leaves fewer than 512 workgroups.
+// Rows per workgroup pass: 128 unless that leaves fewer than 512 workgroups
+// or does not divide N (then 64).  K must be a multiple of 64.
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
+  if (a.K % 64) return hipErrorInvalidValue;
   const int tiles = (a.P + 127) / 128;
   if (a.N % 128 == 0 && tiles * (a.N / 128) >= 512) return pw_dispatch<128>(loader, epi, a, st);
   if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
