@@ -11,6 +11,8 @@
 #include "common.hpp"
 #include "internal.hpp"
 
+#include <type_traits>
+
 namespace nc {
 
 // ---------------------------------------------------------------- pointwise
@@ -307,23 +309,27 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 (a multiple of 4)
   constexpr int MT = DcSmem<C>::MT;
   constexpr int CHUNK = DcSmem<C>::CHUNK;
-  constexpr int LDS_PER_WAVE = DcSmem<C>::FR / 8;  // outstanding direct loads per issued chunk
+  constexpr int LDS_PER_WAVE = DcSmem<C>::FR / 8;  // direct loads per wave per weight chunk
   constexpr int TH = 8, TW = 16;                   // pixel tile (rows x columns at 1/8 scale)
-  constexpr int HW = TW + 2, HPX = (TH + 2) * HW;  // halo tile: 10 x 18 pixels
-  constexpr int CS = 64;                           // channels per staged halo slice (128 B per pixel)
-  constexpr int SLOTS = HPX * (CS / 8);            // 16-byte slots per slice
-  constexpr int SLICE_INSTR = (SLOTS + 63) / 64;
-  static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
-  constexpr int SLICE = (HPX * CS * 2 + 1023) / 1024 * 1024;
-  constexpr int BUF = CHUNK > SLICE ? CHUNK : SLICE;
+  constexpr int HW = TW + 2;                       // halo row length
+  // Depthwise role: wave w filters a band of 4 tile rows (sg) for a quarter of
+  // the channels (cq), lane l = pixel (row 4 sg + l / 16, column l % 16).
+  constexpr int NG = C / 32;                 // 8-channel groups per wave (= 16-byte vectors per halo pixel)
+  constexpr int NS = NG / 2;                 // 16-channel MFMA steps per wave
+  constexpr int BPX = 6 * HW;                // halo pixels of a 4-row band
+  constexpr int RINSTR = (BPX * NG + 63) / 64;  // direct loads per wave for its halo band
+  constexpr int REGION = 16 * 1024;          // per-wave LDS region: halo band, then the exchange
+  constexpr int SWS = NG == 8 ? 0 : NG == 4 ? 1 : 2;  // swizzle: vector v of pixel hp at v ^ ((hp >> SWS) & (NG-1))
+  static_assert(RINSTR * 1024 <= REGION && 2 * NG * 1024 <= REGION, "band and exchange fit a region");
+  static_assert(NG >= 2 && NG <= 8 && NCH % 4 == 0, "C in {64, 128, 256}");
+  constexpr int BUF = CHUNK > 2 * REGION ? CHUNK : 2 * REGION;
   __shared__ __attribute__((aligned(1024))) char wb0[BUF];
   __shared__ __attribute__((aligned(1024))) char wb1[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb2[BUF];  // also halo slices (even)
-  __shared__ __attribute__((aligned(1024))) char wb3[BUF];  // also halo slices (odd)
+  __shared__ __attribute__((aligned(1024))) char wb2[BUF];
+  __shared__ __attribute__((aligned(1024))) char wb3[BUF];
   __shared__ half8 gx0[4][128];  // [pixel group][2 fragments x 64 lanes], even chunks
   __shared__ half8 gx1[4][128];  // odd chunks
-  __shared__ float b1s[2 * C], b2s[C], dwbs[C];
-  __shared__ __attribute__((aligned(16))) f16 dws[9 * C];
+  __shared__ float b1s[2 * C], b2s[C];
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -332,108 +338,159 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   const int ty0 = (tile / tiles_x) * TH, tx0 = (tile % tiles_x) * TW;
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int pg = wave & 3, hf = wave >> 2;
-  const int r = 2 * pg + ((lane & 31) >> 4), c = lane & 15;  // this lane's pixel in the tile
-  const int y = ty0 + r, x = tx0 + c;
-  const bool valid = y < a.h && x < a.w;
-  const int p = y * a.w + x;
+  const int pg = wave & 3, hf = wave >> 2;                       // MFMA role: 32 pixels, half the outputs
+  const int sg = pg >> 1, cq = (wave & 1) | ((wave >> 2) << 1);  // depthwise role
+  const int cb = cq * (C / 4);
   const f16* z = (const f16*)a.src;
   const char* wchunks = (const char*)a.w1;
-
-  // Halo slice k (channels [64k, 64k+64)) -> LDS: slot S = 8 * halo_pixel +
-  // (v ^ (halo_pixel & 7)) holds channel vector v of that pixel, so the 3x3
-  // reads of 8 neighbouring pixels hit 8 different bank groups.
-  constexpr int SLICE_PER_WAVE = (SLICE_INSTR + 7) / 8;
-  const f16* slice_src[SLICE_PER_WAVE];  // slice-0 source of this lane's slot, per instruction
-  bool slice_on[SLICE_PER_WAVE];
-#pragma unroll
-  for (int i = 0; i < SLICE_PER_WAVE; ++i) {
-    const int ins = wave + 8 * i;
-    const int S = ins * 64 + lane;
-    slice_on[i] = ins < SLICE_INSTR && S < SLOTS;
-    const int hp = S >> 3, v = (S & 7) ^ (hp & 7);
-    const int hy = ty0 - 1 + hp / HW, hx = tx0 - 1 + hp % HW;
-    const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-    // zpad holds C zeros, so adding a slice offset (< C) keeps it in bounds
-    slice_src[i] = (in ? z + (size_t)(hy * a.w + hx) * C : (const f16*)a.zpad) + 8 * v;
-  }
-  auto issue_slice = [&](int k, char* buf) {
-#pragma unroll
-    for (int i = 0; i < SLICE_PER_WAVE; ++i) {
-      if (slice_on[i])
-        __builtin_amdgcn_global_load_lds((const void*)(slice_src[i] + CS * k),
-                                         (__attribute__((address_space(3))) void*)(buf + (wave + 8 * i) * 1024), 16,
-                                         0, 0);
-    }
+  auto bufp = [&](int k) __attribute__((always_inline)) -> char* {
+    return k == 0 ? wb0 : k == 1 ? wb1 : k == 2 ? wb2 : wb3;
   };
-  // all halo slices up front (one buffer each); the weight stream starts after the depthwise
-  static_assert(C / CS <= 4, "one LDS buffer per halo slice");
-  char* const slice_buf[4] = {wb0, wb1, wb2, wb3};
-#pragma unroll
-  for (int k = 0; k < C / CS; ++k) issue_slice(k, slice_buf[k]);
-  for (int i = threadIdx.x; i < 2 * C; i += 512) b1s[i] = ((const float*)a.b1)[i];
-  for (int i = threadIdx.x; i < C; i += 512) {
-    b2s[i] = ((const float*)a.b2)[i];
-    dwbs[i] = ((const float*)a.dwb)[i];
-  }
-  for (int i = threadIdx.x; i < 9 * C / 8; i += 512) ((half8*)dws)[i] = ((const half8*)a.dww)[i];
+  // region of the wave with depthwise role (sg, cq): buffer 2 (cq >> 1) + sg, half cq & 1
+  auto region = [&](int sg_, int cq_) __attribute__((always_inline)) -> char* {
+    return bufp(2 * (cq_ >> 1) + sg_) + (cq_ & 1) * REGION;
+  };
+  char* const own = region(sg, cq);
 
-  // depthwise 3x3 (+ bias) for this lane's pixel, channels 16s + 8h + e,
-  // from the staged halo slices.
-  half8 av[KS];
-  // byte offset of this lane's 9 taps inside a staged slice, for channel
-  // vector h (step ss of the slice XORs in 2 * ss, see the slot layout)
+  // Per-block constants to registers first, so that waiting for them does not
+  // also wait for the halo loads issued next.
+  constexpr int NB1 = (2 * C + 511) / 512, NB2 = (C + 511) / 512;
+  float rb1[NB1], rb2[NB2];
+#pragma unroll
+  for (int i = 0; i < NB1; ++i) {
+    const int k = threadIdx.x + 512 * i;
+    rb1[i] = k < 2 * C ? ((const float*)a.b1)[k] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < NB2; ++i) {
+    const int k = threadIdx.x + 512 * i;
+    rb2[i] = k < C ? ((const float*)a.b2)[k] : 0.f;
+  }
+
+  // Halo band: slot S = 16-byte unit S of the region; pixel hp = S / NG of the
+  // 6 x 18 band, position S % NG holds channel vector (S % NG) ^ swizzle(hp).
+  // Out-of-image pixels and padding slots read the zero row (C zeros).
+#pragma unroll
+  for (int i = 0; i < RINSTR; ++i) {
+    const int S = i * 64 + lane;
+    const int hp = S / NG, v = (S % NG) ^ ((hp >> SWS) & (NG - 1));
+    const int hy = ty0 - 1 + 4 * sg + hp / HW, hx = tx0 - 1 + hp % HW;
+    const bool in = hp < BPX && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+    const f16* src = in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const f16*)a.zpad;
+    __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(own + i * 1024), 16,
+                                     0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < NB1; ++i)
+    if (threadIdx.x + 512 * i < 2 * C) b1s[threadIdx.x + 512 * i] = rb1[i];
+#pragma unroll
+  for (int i = 0; i < NB2; ++i)
+    if (threadIdx.x + 512 * i < C) b2s[threadIdx.x + 512 * i] = rb2[i];
+
+  // Depthwise 3x3 + bias for 64 pixels x 8 channels per group, weights and
+  // bias wave-uniform (scalar loads); the centre tap is kept as the residual.
   int tap_off[9];
 #pragma unroll
   for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int hp = (r + ky) * HW + c + kx;
-      tap_off[ky * 3 + kx] = (hp << 7) | ((h ^ (hp & 7)) << 4);
+      const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
+      tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
     }
-  auto dw_slice = [&](int k, const char* buf) {
+  // constant address space: wave-uniform loads become scalar loads
+  typedef const __attribute__((address_space(4))) half8 cwhalf8;
+  typedef const __attribute__((address_space(4))) float cwfloat;
+  cwhalf8* dww = (cwhalf8*)((const half8*)a.dww + cb / 8);
+  cwfloat* dwb = (cwfloat*)((const float*)a.dwb + cb);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band (only this wave reads it)
+  half8 dv[NG], zc[NG];
 #pragma unroll
-    for (int ss = 0; ss < CS / 16; ++ss) {
-      const int s = k * (CS / 16) + ss;
-      const int c0 = 16 * s + 8 * h;
-      float acc[8];
+  for (int g = 0; g < NG; ++g) {
+    float acc[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = dwbs[c0 + e];
+    for (int e = 0; e < 8; ++e) acc[e] = dwb[8 * g + e];
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const half8 zv = *(const half8*)(buf + (tap_off[t] ^ (ss << 5)));
-        const half8 wv = *(const half8*)(dws + t * C + c0);
+    for (int t = 0; t < 9; ++t) {
+      const half8 zv = *(const half8*)(own + (tap_off[t] ^ (g << 4)));
+      const half8 wv = dww[t * (C / 8) + g];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)wv[e], (float)zv[e], acc[e]);
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)wv[e], (float)zv[e], acc[e]);
+      if (t == 4) zc[g] = zv;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dv[g][e] = (f16)acc[e];
+  }
+  // Lanes 0-31 hold pixel group 2 sg, lanes 32-63 group 2 sg + 1.  Swapping
+  // the upper half of group 2p with the lower half of group 2p+1 gives, for
+  // each pixel group, the MFMA B fragment of channels cb + 16 p .. +15
+  // (lanes 0-31: +0..7, lanes 32-63: +8..15).  The band is dead now, so the
+  // fragments overwrite it: [pixel group & 1][step p] for the filtered values,
+  // then the same for the centre taps.
+  auto swap_store = [&](half8* v, int off) __attribute__((always_inline)) {
+#pragma unroll
+    for (int p = 0; p < NS; ++p) {
+      uint32_t* x = (uint32_t*)&v[2 * p];
+      uint32_t* y = (uint32_t*)&v[2 * p + 1];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const auto r2 = __builtin_amdgcn_permlane32_swap(x[i], y[i], false, false);
+        x[i] = r2[0];
+        y[i] = r2[1];
       }
-      half8 o;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
-      av[s] = o;
-      __builtin_amdgcn_sched_barrier(0);  // keep the live range of one step's taps short
+      *(half8*)(own + off + p * 1024 + lane * 16) = v[2 * p];
+      *(half8*)(own + off + (NS + p) * 1024 + lane * 16) = v[2 * p + 1];
     }
   };
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();  // all slices staged
+  swap_store(dv, 0);
+  swap_store(zc, NG * 1024);
+  lds_barrier();
+
+  // MFMA role: all C filtered channels of this wave's 32 pixels, and the
+  // residual in the layout of its output tiles (tile t = channels
+  // 32 (hf MT/2 + t) .. +31, register 4 g + e = channel 8 g + 4 h + e), which
+  // with the bias initialises the accumulators.
+  half8 av[KS];
 #pragma unroll
-  for (int k = 0; k < C / CS; ++k) dw_slice(k, slice_buf[k]);
-  __syncthreads();  // all halo reads done: the buffers hold weights from here on
+  for (int s = 0; s < KS; ++s) {
+    const char* src = region(sg, s / NS) + ((pg & 1) * NS + s % NS) * 1024;
+    av[s] = *(const half8*)(src + lane * 16);
+  }
+  half4 zr[MT / 2][4];  // residual, converted once the first hidden chunk is done
+#pragma unroll
+  for (int t = 0; t < MT / 2; ++t) {
+    const int tt = hf * (MT / 2) + t;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int s = 2 * tt + (g >> 1);  // step holding channels 32 tt + 8 g .. +7
+      const char* src = region(sg, s / NS) + NG * 1024 + ((pg & 1) * NS + s % NS) * 1024;
+      zr[t][g] = *(const half4*)(src + ((lane & 31) + 32 * (g & 1)) * 16 + 8 * h);
+    }
+  }
+  lds_barrier();  // exchange read: the buffers take weight chunks from here on
+
   dc_issue<C>(wchunks, 0, wb0, wave, lane);
   dc_issue<C>(wchunks, 1, wb1, wave, lane);
   dc_issue<C>(wchunks, 2, wb2, wave, lane);
-
-  floatx16 out[MT / 2];
-#pragma unroll
-  for (int t = 0; t < MT / 2; ++t) out[t] = floatx16{};
-
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
   lds_barrier();  // chunks 0 and 1 staged
   if (hf == 0) dc_hidden_store(dc_hidden_mfma<C>(wb0, av, lane), b1s, 0, h, lane, gx0[pg]);
+  floatx16 out[MT / 2];
+#pragma unroll
+  for (int t = 0; t < MT / 2; ++t) {
+    const int tt = hf * (MT / 2) + t;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const floatx4 bv = *(const floatx4*)(b2s + 32 * tt + 8 * g + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[t][4 * g + e] = (float)zr[t][g][e] + bv[e];
+    }
+  }
   lds_barrier();
 
   // Iteration j: issue chunk j+3, produce hidden chunk j+1 (one wave of each
   // pair), project hidden chunk j (both waves).
-  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, half8* gcur, half8* gnxt) {
+  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, half8* gcur, half8* gnxt)
+                  __attribute__((always_inline)) {
     const bool more = j + 3 < NCH;
     if (more) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
     const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
@@ -451,61 +508,49 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
     step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
   }
-  // Epilogue through LDS: each wave parks its 32 px x C/2 accumulators (+ bias)
-  // as fp32 in the buffer of its pixel group (row = pixel, 16-byte chunk k of
-  // the row stored at k ^ (row & SWZ)), then all threads add the residual and
-  // store whole pixel rows with coalesced 16-byte accesses.  The residual
-  // loads are issued first so their latency overlaps the parking.
+
+  // Epilogue through LDS: each wave parks its 32 px x C/2 results as fp32 in
+  // the buffer of its pixel group (row = pixel, 16-byte chunk k of the row at
+  // k ^ (row & SWZ)); then all threads convert and store whole pixel rows with
+  // coalesced 16-byte stores.
   static_assert(32 * C * 4 <= BUF, "a pixel group's fp32 output fits one buffer");
   constexpr int SWZ = (C / 4 - 1) & 31;  // keeps the swizzled chunk inside its row
-  constexpr int CH8 = C / 8;             // 8-channel chunks per pixel
-  constexpr int PER = 128 * CH8 / 512;   // chunks per thread
-  half8 zres[PER];
-  size_t gofs[PER];
-  bool gok[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int idx = i * 512 + threadIdx.x;
-    const int px = idx / CH8, k8 = idx % CH8;
-    const int gpx = px >> 5, row = px & 31;
-    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
-    gok[i] = yy < a.h && xx < a.w;
-    gofs[i] = (size_t)(gok[i] ? yy * a.w + xx : 0) * C + 8 * k8;
-    zres[i] = *(const half8*)(z + gofs[i]);
-  }
   {
-    char* ob = pg == 0 ? wb0 : pg == 1 ? wb1 : pg == 2 ? wb2 : wb3;
+    char* ob = bufp(pg);
     const int row = lane & 31;
 #pragma unroll
-    for (int t = 0; t < MT / 2; ++t) {
+    for (int t = 0; t < MT / 2; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-        const floatx4 bv = *(const floatx4*)(b2s + cc);
         floatx4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e] + bv[e];
+        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e];
         *(floatx4*)(ob + row * (C * 4) + (((cc >> 2) ^ (row & SWZ)) << 4)) = o;
       }
-    }
   }
   lds_barrier();
+  constexpr int CH8 = C / 8;            // 8-channel chunks per pixel
+  constexpr int PER = 128 * CH8 / 512;  // chunks per thread
   f16* dst = (f16*)a.dst;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int idx = i * 512 + threadIdx.x;
     const int px = idx / CH8, k8 = idx % CH8;
     const int gpx = px >> 5, row = px & 31;
-    const char* ob = gpx == 0 ? wb0 : gpx == 1 ? wb1 : gpx == 2 ? wb2 : wb3;
-    const floatx4 o0 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
-    const floatx4 o1 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
-    half8 r;
+    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
+    if (yy < a.h && xx < a.w) {
+      const char* ob = bufp(gpx);
+      const floatx4 o0 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
+      const floatx4 o1 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
+      half8 o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      r[e] = (f16)(o0[e] + (float)zres[i][e]);
-      r[4 + e] = (f16)(o1[e] + (float)zres[i][4 + e]);
+      for (int e = 0; e < 4; ++e) {
+        o[e] = (f16)o0[e];
+        o[4 + e] = (f16)o1[e];
+      }
+      *(half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8) = o;
     }
-    if (gok[i]) *(half8*)(dst + gofs[i]) = r;
   }
 }
 
