@@ -170,11 +170,13 @@ struct Packer {
     }
     if (!is_int) {
       // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1
-      // fragments (rows 32j..32j+31, all C inputs) followed by the 2*MT pw2
-      // fragments that consume that chunk.  The pw2 contraction index is
-      // permuted inside the chunk so that the pw1 accumulator registers are
-      // directly the pw2 operand.  One chunk is one contiguous copy into LDS.
-      const int KS = C / 16, MT = C / 32, NCH = 2 * C / 32, FR = KS + 2 * MT;
+      // fragments (rows 32j..32j+31, all C inputs), one bias fragment (column
+      // C of the pw1 matrix extended by its bias, contracted with a constant
+      // one), then the 2*MT pw2 fragments that consume that chunk.  The pw2
+      // contraction index is permuted inside the chunk so that the pw1
+      // accumulator registers are directly the pw2 operand.  One chunk is one
+      // contiguous copy into LDS.
+      const int KS = C / 16, MT = C / 32, NCH = 2 * C / 32, FR = KS + 1 + 2 * MT;
       d.pw1.w = img.add((size_t)NCH * FR * 1024);
       d.pw1.bias = img.add((size_t)2 * C * 4);
       d.pw2.bias = img.add((size_t)C * 4);
@@ -188,8 +190,10 @@ struct Packer {
               if (f < KS) {
                 const int n = 32 * j + (l & 31), k = 16 * f + 8 * (l >> 5) + e;
                 v = w1[(size_t)n * C + k];
+              } else if (f == KS) {
+                v = (l < 32 && e == 0) ? b1[32 * j + l] : 0.f;
               } else {
-                const int t = (f - KS) / 2, u = (f - KS) % 2;
+                const int t = (f - KS - 1) / 2, u = (f - KS - 1) % 2;
                 const int n = 32 * t + (l & 31);
                 const int hidden = 32 * j + 16 * u + kmap(8 * (l >> 5) + e);
                 v = w2[(size_t)n * 2 * C + hidden];

@@ -85,11 +85,37 @@ __device__ __forceinline__ void split16(const uint32_t* d, intx4& hi, intx4& lo)
   }
 }
 
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// lds_wave_base + 16 l (the base is wave-uniform and goes through M0).  It is
+// issued from inline asm so that the compiler does not treat every later LDS
+// read as dependent on it (it would otherwise wait for all outstanding loads
+// before each LDS read); callers wait explicitly with s_waitcnt vmcnt(N),
+// counting these loads, before reading the destination.
+__device__ __forceinline__ void dma16(const void* g, const void* lds_wave_base) {
+  const uint32_t m = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_wave_base;
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m) : "memory", "m0");
+}
+
+// Read-only kernel data seen through the constant address space: loads at
+// wave-uniform addresses become scalar loads.
+typedef const __attribute__((address_space(4))) float cfloat;
+typedef const __attribute__((address_space(4))) int32_t cint;
+typedef const __attribute__((address_space(4))) half8 chalf8;
+typedef const __attribute__((address_space(4))) shortx8 cshortx8;
+
 // Workgroup barrier for LDS hand-offs inside a pipelined loop.  It waits for
 // this wave's LDS operations (lgkmcnt) but, unlike __syncthreads(), not for
 // outstanding global->LDS loads: callers wait for those explicitly with
 // s_waitcnt vmcnt(N) so that later chunks stay in flight across the barrier.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// The wait is the builtin (0xC07F = lgkmcnt(0), other counters unconstrained)
+// so that the compiler knows every LDS read before it has completed; the empty
+// asm statements keep memory accesses from moving across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 __device__ __forceinline__ float leaky(float v) { return v >= 0.f ? v : 0.1f * v; }
 

@@ -65,8 +65,7 @@ __device__ __forceinline__ void pw_issue(const PwArgs& a, int tile, int n0, int 
     const int slot = ins * 64 + lane;
     const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
     const int gp = min(tile * 128 + px, a.P - 1);  // pixels past the end reload the last one
-    __builtin_amdgcn_global_load_lds((const void*)pw_act_src<LOADER>(a, gp, kc, v),
-                                     (__attribute__((address_space(3))) void*)(stage + ins * 1024), 16, 0, 0);
+    dma16(pw_act_src<LOADER>(a, gp, kc, v), stage + ins * 1024);
   }
   const int ks = a.K / 16;
   const char* w = (const char*)a.wfrag;
@@ -74,8 +73,7 @@ __device__ __forceinline__ void pw_issue(const PwArgs& a, int tile, int n0, int 
   for (int i = 0; i < S::WGT / 1024 / 8; ++i) {
     const int f = wave + 8 * i;  // fragment f of the stage: row tile f / 4, k-step f % 4
     const int mt = n0 / 32 + (f >> 2), sk = 4 * kc + (f & 3);
-    __builtin_amdgcn_global_load_lds((const void*)(w + (((size_t)mt * ks + sk) * 64 + lane) * 16),
-                                     (__attribute__((address_space(3))) void*)(stage + S::ACT + f * 1024), 16, 0, 0);
+    dma16(w + (((size_t)mt * ks + sk) * 64 + lane) * 16, stage + S::ACT + f * 1024);
   }
 }
 
@@ -233,58 +231,68 @@ __global__ __launch_bounds__(512) void k_pw_f16(PwArgs a) {
 // goes to LDS in MFMA operand order so both waves of the pair consume it.
 //
 // Weights stream chunk by chunk (chunk j = the pw1 fragments producing hidden
-// chunk j followed by the pw2 fragments consuming it) into four LDS buffers,
-// three chunks ahead, with direct global->LDS loads.  The buffers are distinct
-// LDS objects indexed statically (the loop is unrolled by four), so LDS reads
-// never wait for loads into a different buffer.
+// DC block.  The weights of one block are streamed in NCH = 2C/32 chunks:
+// chunk j holds the KS = C/16 pw1 fragments of hidden channels 32 j .. +31,
+// their bias as one more fragment (contracted with a constant-one B
+// fragment), then the 2 MT pw2 fragments that consume them (one 1 KiB MFMA A
+// fragment each), into a ring of four LDS buffers with direct global->LDS
+// loads.  The buffers are distinct LDS objects indexed statically (the loop is
+// unrolled by four).
 template <int C>
 struct DcSmem {
-  static constexpr int KS = C / 16, MT = C / 32, FR = KS + 2 * MT, CHUNK = FR * 1024;
+  static constexpr int KS = C / 16, MT = C / 32, FR = KS + 1 + 2 * MT, CHUNK = FR * 1024;
 };
 
+// Chunk j -> buf; fragment f is loaded by wave f % 8.
 template <int C>
 __device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, int wave, int lane) {
   constexpr int FR = DcSmem<C>::FR;
 #pragma unroll
-  for (int i = 0; i < FR / 8; ++i) {
+  for (int i = 0; i < (FR + 7) / 8; ++i) {
     const int f = wave + 8 * i;
-    const char* g = wchunks + ((size_t)j * FR + f) * 1024 + lane * 16;
-    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(buf + f * 1024), 16,
-                                     0, 0);
+    if (FR % 8 == 0 || f < FR) dma16(wchunks + ((size_t)j * FR + f) * 1024 + lane * 16, buf + f * 1024);
   }
 }
 
-// pw1 for hidden chunk j from the fragments in `wb` (32 hidden x 32 pixels).
+// The first half of the pw1 fragments of one chunk, to registers.
 template <int C>
-__device__ __forceinline__ floatx16 dc_hidden_mfma(const char* wb, const half8* av, int lane) {
+__device__ __forceinline__ void dc_load_w1(const char* wb, int lane, half8* wf) {
+  const half8* w = (const half8*)wb + lane;
+#pragma unroll
+  for (int s = 0; s < DcSmem<C>::KS / 2; ++s) wf[s] = w[s * 64];
+}
+
+// pw1 chain of one hidden chunk (bias included): the first half of the
+// fragments comes from registers (loaded an iteration earlier), the second
+// half and the bias fragment are read from the chunk's buffer while the first
+// half runs.
+template <int C>
+__device__ __forceinline__ floatx16 dc_hidden(const half8* wf, const char* wb, const half8* av, half8 ones, int lane) {
   constexpr int KS = DcSmem<C>::KS;
   const half8* w = (const half8*)wb + lane;
-  // All fragment reads are issued before the dependent MFMA chain starts, so
-  // the chain does not pay an LDS round trip per link.
-  half8 wf[KS];
+  half8 w2[KS / 2 + 1];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) wf[s] = w[s * 64];
+  for (int s = 0; s <= KS / 2; ++s) w2[s] = w[(KS / 2 + s) * 64];
   __builtin_amdgcn_sched_barrier(0);
   floatx16 hacc = {};
 #pragma unroll
-  for (int s = 0; s < KS; ++s) hacc = mfma_f16(wf[s], av[s], hacc);
-  return hacc;
+  for (int s = 0; s < KS / 2; ++s) hacc = mfma_f16(wf[s], av[s], hacc);
+#pragma unroll
+  for (int s = 0; s < KS / 2; ++s) hacc = mfma_f16(w2[s], av[KS / 2 + s], hacc);
+  return mfma_f16(w2[KS / 2], ones, hacc);
 }
 
-// Bias, LeakyReLU, fp16; stored to `gx` as two B fragments (k = hidden in the
+// LeakyReLU, fp16; stored to `gx` as two B fragments (k = hidden in the
 // permuted order the pw2 weights were packed with).
-__device__ __forceinline__ void dc_hidden_store(const floatx16& hacc, const float* b1s, int j, int h, int lane,
-                                                half8* gx) {
+__device__ __forceinline__ void dc_hidden_store(const floatx16& hacc, int lane, half8* gx) {
   half8 g0, g1;
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const floatx4 bv = *(const floatx4*)(b1s + 32 * j + 8 * g + 4 * h);
+  for (int g = 0; g < 4; ++g)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const f16 v = (f16)leaky(hacc[4 * g + e] + bv[e]);
+      const f16 v = (f16)leaky(hacc[4 * g + e]);
       if (g < 2) g0[4 * g + e] = v; else g1[4 * (g - 2) + e] = v;
     }
-  }
   gx[lane] = g0;
   gx[64 + lane] = g1;
 }
@@ -298,8 +306,8 @@ __device__ __forceinline__ void dc_project(const char* wb, const half8* gx, int 
 #pragma unroll
   for (int t = 0; t < MT / 2; ++t) {
     const int tt = hf * (MT / 2) + t;
-    out[t] = mfma_f16(w[(KS + 2 * tt) * 64], g0, out[t]);
-    out[t] = mfma_f16(w[(KS + 2 * tt + 1) * 64], g1, out[t]);
+    out[t] = mfma_f16(w[(KS + 1 + 2 * tt) * 64], g0, out[t]);
+    out[t] = mfma_f16(w[(KS + 1 + 2 * tt + 1) * 64], g1, out[t]);
   }
 }
 
@@ -309,7 +317,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 (a multiple of 4)
   constexpr int MT = DcSmem<C>::MT;
   constexpr int CHUNK = DcSmem<C>::CHUNK;
-  constexpr int LDS_PER_WAVE = DcSmem<C>::FR / 8;  // direct loads per wave per weight chunk
   constexpr int TH = 8, TW = 16;                   // pixel tile (rows x columns at 1/8 scale)
   constexpr int HW = TW + 2;                       // halo row length
   // Depthwise role: wave w filters a band of 4 tile rows (sg) for a quarter of
@@ -329,7 +336,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   __shared__ __attribute__((aligned(1024))) char wb3[BUF];
   __shared__ half8 gx0[4][128];  // [pixel group][2 fragments x 64 lanes], even chunks
   __shared__ half8 gx1[4][128];  // odd chunks
-  __shared__ float b1s[2 * C], b2s[C];
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -352,21 +358,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   };
   char* const own = region(sg, cq);
 
-  // Per-block constants to registers first, so that waiting for them does not
-  // also wait for the halo loads issued next.
-  constexpr int NB1 = (2 * C + 511) / 512, NB2 = (C + 511) / 512;
-  float rb1[NB1], rb2[NB2];
-#pragma unroll
-  for (int i = 0; i < NB1; ++i) {
-    const int k = threadIdx.x + 512 * i;
-    rb1[i] = k < 2 * C ? ((const float*)a.b1)[k] : 0.f;
-  }
-#pragma unroll
-  for (int i = 0; i < NB2; ++i) {
-    const int k = threadIdx.x + 512 * i;
-    rb2[i] = k < C ? ((const float*)a.b2)[k] : 0.f;
-  }
-
   // Halo band: slot S = 16-byte unit S of the region; pixel hp = S / NG of the
   // 6 x 18 band, position S % NG holds channel vector (S % NG) ^ swizzle(hp).
   // Out-of-image pixels and padding slots read the zero row (C zeros).
@@ -376,16 +367,8 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     const int hp = S / NG, v = (S % NG) ^ ((hp >> SWS) & (NG - 1));
     const int hy = ty0 - 1 + 4 * sg + hp / HW, hx = tx0 - 1 + hp % HW;
     const bool in = hp < BPX && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-    const f16* src = in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const f16*)a.zpad;
-    __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(own + i * 1024), 16,
-                                     0, 0);
+    dma16(in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const f16*)a.zpad, own + i * 1024);
   }
-#pragma unroll
-  for (int i = 0; i < NB1; ++i)
-    if (threadIdx.x + 512 * i < 2 * C) b1s[threadIdx.x + 512 * i] = rb1[i];
-#pragma unroll
-  for (int i = 0; i < NB2; ++i)
-    if (threadIdx.x + 512 * i < C) b2s[threadIdx.x + 512 * i] = rb2[i];
 
   // Depthwise 3x3 + bias for 64 pixels x 8 channels per group, weights and
   // bias wave-uniform (scalar loads); the centre tap is kept as the residual.
@@ -397,11 +380,8 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
       const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
       tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
     }
-  // constant address space: wave-uniform loads become scalar loads
-  typedef const __attribute__((address_space(4))) half8 cwhalf8;
-  typedef const __attribute__((address_space(4))) float cwfloat;
-  cwhalf8* dww = (cwhalf8*)((const half8*)a.dww + cb / 8);
-  cwfloat* dwb = (cwfloat*)((const float*)a.dwb + cb);
+  chalf8* dww = (chalf8*)((const half8*)a.dww + cb / 8);
+  cfloat* dwb = (cfloat*)((const float*)a.dwb + cb);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band (only this wave reads it)
   half8 dv[NG], zc[NG];
 #pragma unroll
@@ -468,45 +448,56 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   }
   lds_barrier();  // exchange read: the buffers take weight chunks from here on
 
+  // Pipeline: in iteration j one wave of each pair runs the pw1 chain of
+  // hidden chunk j+1 from fragments it loaded in iteration j-1, the other loads
+  // the fragments of chunk j+2 for its next chain; both project hidden chunk
+  // j.  Chunk c sits in buffer c % 4; chunk j+3 is loaded during iteration j.
   dc_issue<C>(wchunks, 0, wb0, wave, lane);
   dc_issue<C>(wchunks, 1, wb1, wave, lane);
   dc_issue<C>(wchunks, 2, wb2, wave, lane);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
-  lds_barrier();  // chunks 0 and 1 staged
-  if (hf == 0) dc_hidden_store(dc_hidden_mfma<C>(wb0, av, lane), b1s, 0, h, lane, gx0[pg]);
+  half8 ones = {};  // B fragment of the bias step: k = 0 is one for every pixel
+  if (lane < 32) ones[0] = (f16)1.f;
+  half8 wf[KS / 2];  // first half of the next chain's pw1 fragments
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  lds_barrier();  // chunks 0 to 2 staged
+  dc_load_w1<C>(hf == 0 ? wb0 : wb1, lane, wf);  // hf 1: chunk 1, for its chain in iteration 0
+  if (hf == 0) dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0[pg]);
   floatx16 out[MT / 2];
+  {
+    cfloat* b2 = (cfloat*)a.b2;
 #pragma unroll
-  for (int t = 0; t < MT / 2; ++t) {
-    const int tt = hf * (MT / 2) + t;
+    for (int t = 0; t < MT / 2; ++t) {
+      const int tt = hf * (MT / 2) + t;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const floatx4 bv = *(const floatx4*)(b2s + 32 * tt + 8 * g + 4 * h);
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) out[t][4 * g + e] = (float)zr[t][g][e] + bv[e];
+        for (int e = 0; e < 4; ++e) {
+          const float bv = h ? b2[32 * tt + 8 * g + 4 + e] : b2[32 * tt + 8 * g + e];
+          out[t][4 * g + e] = (float)zr[t][g][e] + bv;
+        }
     }
   }
-  lds_barrier();
+  lds_barrier();  // hidden chunk 0 visible
 
-  // Iteration j: issue chunk j+3, produce hidden chunk j+1 (one wave of each
-  // pair), project hidden chunk j (both waves).
-  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, half8* gcur, half8* gnxt)
+  auto step = [&](int j, const char* wcur, const char* wnxt, const char* wpre, char* wiss, half8* gcur, half8* gnxt)
                   __attribute__((always_inline)) {
-    const bool more = j + 3 < NCH;
-    if (more) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
+    const bool dma = j + 3 < NCH;
+    if (dma) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
     const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
+    const bool prefetch = j + 2 < NCH && hf == (j & 1);
     floatx16 hacc;
-    if (produce) hacc = dc_hidden_mfma<C>(wnxt, av, lane);
+    if (produce) hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
     dc_project<C>(wcur, gcur, hf, lane, out);
-    if (produce) dc_hidden_store(hacc, b1s, j + 1, h, lane, gnxt);
-    if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (prefetch) dc_load_w1<C>(wpre, lane, wf);
+    if (produce) dc_hidden_store(hacc, lane, gnxt);
+    if (dma) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // chunk j+3: prefetched next iteration
     lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
-    step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
-    step(j + 1, wb1, wb2, wb0, gx1[pg], gx0[pg]);
-    step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
-    step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
+    step(j + 0, wb0, wb1, wb2, wb3, gx0[pg], gx1[pg]);
+    step(j + 1, wb1, wb2, wb3, wb0, gx1[pg], gx0[pg]);
+    step(j + 2, wb2, wb3, wb0, wb1, gx0[pg], gx1[pg]);
+    step(j + 3, wb3, wb0, wb1, wb2, gx1[pg], gx0[pg]);
   }
 
   // Epilogue through LDS: each wave parks its 32 px x C/2 results as fp32 in

@@ -72,8 +72,7 @@ __device__ __forceinline__ void pwi_issue(const PwArgs& a, int tile, int n0, int
     const int slot = ins * 64 + lane;
     const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
     const int gp = min(tile * 128 + px, a.P - 1);
-    __builtin_amdgcn_global_load_lds((const void*)pwi_act_src<LOADER>(a, gp, kc, v),
-                                     (__attribute__((address_space(3))) void*)(stage + ins * 1024), 16, 0, 0);
+    dma16(pwi_act_src<LOADER>(a, gp, kc, v), stage + ins * 1024);
   }
   const int ks = a.K / 32;
 #pragma unroll
@@ -81,9 +80,7 @@ __device__ __forceinline__ void pwi_issue(const PwArgs& a, int tile, int n0, int
     const int f = wave + 8 * i;  // row tile f / 4; f % 4: hi k0, hi k1, lo k0, lo k1
     const int mt = n0 / 32 + (f >> 2), sk = 2 * kc + (f & 1);
     const char* plane = (f & 2) ? (const char*)a.wfrag_lo : (const char*)a.wfrag;
-    __builtin_amdgcn_global_load_lds((const void*)(plane + (((size_t)mt * ks + sk) * 64 + lane) * 16),
-                                     (__attribute__((address_space(3))) void*)(stage + PwSmemI::ACT + f * 1024), 16,
-                                     0, 0);
+    dma16(plane + (((size_t)mt * ks + sk) * 64 + lane) * 16, stage + PwSmemI::ACT + f * 1024);
   }
 }
 
@@ -270,8 +267,7 @@ __device__ __forceinline__ void dci_issue(const char* wchunks, int j, char* buf,
   for (int i = 0; i < FR / 8; ++i) {
     const int f = wave + 8 * i;
     const char* g = wchunks + ((size_t)j * FR + f) * 1024 + lane * 16;
-    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(buf + f * 1024), 16,
-                                     0, 0);
+    dma16(g, buf + f * 1024);
   }
 }
 
@@ -407,9 +403,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 #pragma unroll
     for (int i = 0; i < SLICE_PER_WAVE; ++i) {
       if (slice_on[i])
-        __builtin_amdgcn_global_load_lds((const void*)(slice_src[i] + CS * k),
-                                         (__attribute__((address_space(3))) void*)(buf + (wave + 8 * i) * 1024), 16,
-                                         0, 0);
+        dma16(slice_src[i] + CS * k, buf + (wave + 8 * i) * 1024);
     }
   };
   static_assert(C / CS <= 4, "one LDS buffer per halo slice");
