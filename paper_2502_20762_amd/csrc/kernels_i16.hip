@@ -30,7 +30,7 @@ __device__ __forceinline__ uint32_t pack2(int lo, int hi) {
 
 // ---------------------------------------------------------------- pointwise
 // Same tiling and LDS pipeline as the fp16 pointwise kernel: 8 waves per tile
-// of 128 output pixels, K consumed 64 at a time through four LDS stages.  A
+// of 128 output pixels, K consumed 64 at a time through three LDS stages.  A
 // stage holds the activation slice (int16, or the fp16 frame for the patch
 // embed, converted with x_i = round(512 x) when the operand is read) and, per
 // 32-row tile, four int8 fragments: hi digits for k-steps 0 and 1, then lo
@@ -125,20 +125,24 @@ __device__ __forceinline__ void pwi_compute(const char* stage, int pg, int hf, i
 }
 
 template <int NT, int LOADER, int EPI>
-__global__ __launch_bounds__(512) void k_pw_i16(PwArgs a) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 4 : 2))) void k_pw_i16(PwArgs a) {
   using S = PwSmemIN<NT>;
   constexpr int RT = NT / 64;
   __shared__ __attribute__((aligned(1024))) char st0[S::STAGE];
   __shared__ __attribute__((aligned(1024))) char st1[S::STAGE];
   __shared__ __attribute__((aligned(1024))) char st2[S::STAGE];
-  __shared__ __attribute__((aligned(1024))) char st3[S::STAGE];
   const int ntile = (a.P + 127) / 128;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  // (tile, row pass) pairs with the row pass fastest, each XCD taking a
+  // contiguous range: the passes over one pixel tile run together and share
+  // its activations in L2.
+  const int npass = a.N / NT;
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = lin / npass;
   if (tile >= ntile) return;
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pg = wave & 3, hf = wave >> 2;
-  const int n0 = blockIdx.y * NT;
+  const int n0 = (lin - tile * npass) * NT;
   const int nk = a.K / 64;
 
   intx16 acc[RT][3];
@@ -152,29 +156,31 @@ __global__ __launch_bounds__(512) void k_pw_i16(PwArgs a) {
 
   pwi_issue<NT, LOADER>(a, tile, n0, 0, st0, wave, lane);
   if (nk > 1) pwi_issue<NT, LOADER>(a, tile, n0, 1, st1, wave, lane);
-  if (nk > 2) pwi_issue<NT, LOADER>(a, tile, n0, 2, st2, wave, lane);
   auto step = [&](int kc, const char* cur, char* refill) {
-    const int ahead = min(nk - 1 - kc, 2);
-    if (ahead == 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * S::DMA_PER_WAVE) : "memory");
-    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(S::DMA_PER_WAVE) : "memory");
+    const int ahead = min(nk - 1 - kc, 1);  // stages issued after kc still in flight
+    if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(S::DMA_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
-    if (kc + 3 < nk) pwi_issue<NT, LOADER>(a, tile, n0, kc + 3, refill, wave, lane);
+    if (kc + 2 < nk) pwi_issue<NT, LOADER>(a, tile, n0, kc + 2, refill, wave, lane);
     pwi_compute<NT, LOADER>(cur, pg, hf, lane, acc);
   };
-  for (int kc = 0; kc < nk; kc += 4) {
-    step(kc, st0, st3);
+  for (int kc = 0; kc < nk; kc += 3) {
+    step(kc, st0, st2);
     if (kc + 1 < nk) step(kc + 1, st1, st0);
     if (kc + 2 < nk) step(kc + 2, st2, st1);
-    if (kc + 3 < nk) step(kc + 3, st3, st2);
   }
   lds_barrier();
 
   // park the rescaled int16 results as int32, as in the fp16 kernel
   constexpr int SWZ = (NT / 4 - 1) & 31;
-  static_assert(32 * NT * 4 <= S::STAGE, "a pixel group's output fits one stage buffer");
+  // pixel group g parks at offset (g % GPS) * PARK of stage g / GPS
+  constexpr int PARK = 32 * NT * 4, GPS = S::STAGE / PARK;
+  static_assert(GPS >= 2, "four pixel groups fit three stage buffers");
+  auto park = [&](int g) __attribute__((always_inline)) -> char* {
+    return (g / GPS == 0 ? st0 : g / GPS == 1 ? st1 : st2) + (g % GPS) * PARK;
+  };
   {
-    char* ob = pg == 0 ? st0 : pg == 1 ? st1 : pg == 2 ? st2 : st3;
+    char* ob = park(pg);
     const int row = lane & 31;
 #pragma unroll
     for (int t = 0; t < RT; ++t)
@@ -194,7 +200,7 @@ __global__ __launch_bounds__(512) void k_pw_i16(PwArgs a) {
 
   auto parked = [&](int px, int nl8, int* v) {
     const int gpx = px >> 5, row = px & 31;
-    const char* ob = gpx == 0 ? st0 : gpx == 1 ? st1 : gpx == 2 ? st2 : st3;
+    const char* ob = park(gpx);
     const intx4 o0 = *(const intx4*)(ob + row * (NT * 4) + (((2 * nl8) ^ (row & SWZ)) << 4));
     const intx4 o1 = *(const intx4*)(ob + row * (NT * 4) + (((2 * nl8 + 1) ^ (row & SWZ)) << 4));
 #pragma unroll
@@ -614,7 +620,7 @@ __global__ __launch_bounds__(256) void k_prior_i16(PriorArgs a) {
 
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  dim3 grid(grid_tiles(a.P), a.N / NT), block(512);
+  dim3 grid(grid_tiles(a.P) * (a.N / NT)), block(512);
 #define NC_PW(L, E)                                                            \
   if (loader == L && epi == E) {                                               \
     launch(k_pw_i16<NT, L, E>, grid, block, st, a);                            \
@@ -629,14 +635,12 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   return hipErrorInvalidValue;
 }
 
-// Rows per workgroup pass: 128 unless that leaves fewer than 512 workgroups
-// or does not divide N (then 64).  K must be a multiple of 64.
+// 64 rows per workgroup pass: two workgroups fit a CU, and the passes over one
+// pixel tile run side by side on one XCD.  K must be a multiple of 64 (C = 64,
+// 128, 256; 192 for the patch embed) and N a multiple of 64.
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
-  if (a.K % 64) return hipErrorInvalidValue;
-  const int tiles = (a.P + 127) / 128;
-  if (a.N % 128 == 0 && tiles * (a.N / 128) >= 512) return pw_dispatch<128>(loader, epi, a, st);
-  if (a.N % 64 == 0) return pw_dispatch<64>(loader, epi, a, st);
-  return hipErrorInvalidValue;
+  if (a.K % 64 || a.N % 64) return hipErrorInvalidValue;
+  return pw_dispatch<64>(loader, epi, a, st);
 }
 
 hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
