@@ -290,7 +290,14 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   // packed k' = (2i + j) * C + c  <-  source column c * 4 + 2i + j
   L.down = pk.gemm(dn_w, dn_b, C, 4 * C, 4 * C, [](int n) { return n; }, [C](int k) { return (k % C) * 4 + k / C; });
   const float* hd_w = take((size_t)2 * C * C); const float* hd_b = take(2 * C);
-  L.head = pk.plain(hd_w, hd_b, 2 * C, C);
+  if (is_int) {
+    L.head = pk.plain(hd_w, hd_b, 2 * C, C);
+  } else {
+    // packed row n' = 64 t + r: mu row 32 t + r (r < 32), else s row C + 32 t + r - 32
+    L.head = pk.gemm(hd_w, hd_b, 2 * C, C, C,
+                     [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
+                     [](int k) { return k; });
+  }
   const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
   // packed row n' = sp * C + c  <-  source row 4c + sp
   L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });

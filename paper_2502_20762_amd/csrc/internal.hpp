@@ -35,6 +35,8 @@ enum Epi : int {
   EP_NHWC = 0,  // dst[p*Cdst + n]
   EP_UP = 1,    // rows ordered (sub-position, channel): pixel-shuffle x2 into the 1/8 grid
   EP_REC = 2,   // rows 64c+8i+j: pixel-shuffle x8 into a planar 3xHxW frame, clamped
+  EP_PRIOR = 3,      // rows (32 mu, 32 s) per pass: quantise y, write q, yhat, bit partials
+  EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
 };
 
 struct PwArgs {
@@ -52,6 +54,12 @@ struct PwArgs {
   int Csrc;              // channels of the LD_DOWN source
   void* dst;
   int Cdst;
+  // prior head (EP_PRIOR*): dst = yhat_t (NHWC, Cdst = C)
+  const void* y;        // NHWC latent to quantise (encode)
+  const int16_t* q_in;  // planar symbols (decode)
+  int16_t* q_out;       // planar symbols (encode)
+  double* partials;     // one per (tile, pass) of the encoder
+  const float* sigma_tab;
 };
 
 struct BlockArgs {

@@ -11,6 +11,7 @@
 #include "common.hpp"
 #include "internal.hpp"
 
+#include <cstring>
 #include <type_traits>
 
 namespace nc {
@@ -170,6 +171,24 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(floatx4*)(ob + row * (NT * 4) + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
       }
   }
+  // prior head: a pass covers channels c0 .. c0+31 (rows 0-31 mu, 32-63 s);
+  // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
+  const int c0 = n0 / 2;
+  int16_t* qt = (int16_t*)st2;
+  if constexpr (EPI == EP_PRIOR_DEC) {
+    static_assert(NT == 64, "prior passes are 64 rows");
+    const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;  // 32 channels x 16 chunks of 8 pixels
+    const int p0 = tile * 128 + 8 * k;
+    const int16_t* src = a.q_in + (size_t)(c0 + ch) * a.P + p0;
+    shortx8 v = {};
+    if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+      v = *(const shortx8*)src;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p0 + e < a.P ? src[e] : (short)0;
+    }
+    *(shortx8*)(qt + ch * 128 + 8 * k) = v;
+  }
   lds_barrier();
 
   auto parked = [&](int px, int nl8) {  // 8 floats: pass rows nl8 * 8 .. +7 of tile pixel px
@@ -182,7 +201,62 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { r[e] = o0[e]; r[4 + e] = o1[e]; }
     return r;
   };
-  if constexpr (EPI == EP_REC) {
+  if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
+    // thread = (pixel px, 8 channels g8): mu and s from the park, y / q, yhat
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    const int c = c0 + 8 * g8;
+    const floatx16 mu = parked(px, g8), sg = parked(px, 4 + g8);
+    double bsum = 0.0;
+    if constexpr (EPI == EP_PRIOR) {
+      half8 yv = {};
+      if (gp < a.P) yv = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + c);
+      half8 yh;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float q = rintf((float)yv[e] - mu[e]);
+        q = fminf(fmaxf(q, -32768.f), 32767.f);
+        qt[(8 * g8 + e) * 128 + px] = (int16_t)q;
+        yh[e] = (f16)(q + mu[e]);
+        if (gp < a.P) bsum += (double)symbol_bits(q, softplus_sigma(sg[e]));
+      }
+      if (gp < a.P) *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
+      __shared__ double red[8];
+      bsum = wave_sum(bsum);
+      if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = bsum;
+      lds_barrier();
+      {
+        const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
+        const int p0 = tile * 128 + 8 * k;
+        const shortx8 v = *(const shortx8*)(qt + ch * 128 + 8 * k);
+        int16_t* dq = a.q_out + (size_t)(c0 + ch) * a.P + p0;
+        if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+          *(shortx8*)dq = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (p0 + e < a.P) dq[e] = v[e];
+        }
+      }
+      if (threadIdx.x == 0) {
+        double t = 0.0;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) t += red[w];
+        a.partials[(size_t)tile * npass + n0 / NT] = t;
+      }
+    } else {
+      if (gp < a.P) {
+        half8 yh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          // same operation order as the encoder: mu first, then q + mu
+          const float q = (float)qt[(8 * g8 + e) * 128 + px];
+          yh[e] = (f16)(q + mu[e]);
+        }
+        *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
+      }
+    }
+  } else if constexpr (EPI == EP_REC) {
     // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
     // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
     constexpr int UNITS = 128 * (NT / 8);
@@ -552,80 +626,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   }
 }
 
-// Prior head, quantiser and bits.  One wave = 32 latent pixels x CH channels
-// (their mu rows and their s rows).  Workgroup partial sums are written per
-// (tile, channel slice) and reduced in a fixed order by k_reduce.
-template <int CH, bool DECODE>
-__global__ __launch_bounds__(256) void k_prior_f16(PriorArgs a) {
-  constexpr int MT = CH / 32;
-  const int ntile = (a.P + 127) / 128;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < a.P;
-  const int C = a.C;
-  const int ct0 = blockIdx.y * MT;
-  const int ks = C / 16;
-  const half8* wf = (const half8*)a.wfrag;
-  const f16* yp = (const f16*)a.yhat_prev;
-
-  floatx16 amu[MT], asg[MT];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) { amu[t] = floatx16{}; asg[t] = floatx16{}; }
-  for (int s = 0; s < ks; ++s) {
-    half8 b = {};
-    if (valid) b = *(const half8*)(yp + (size_t)p * C + 16 * s + 8 * h);
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      amu[t] = mfma_f16(wf[((size_t)(ct0 + t) * ks + s) * 64 + lane], b, amu[t]);
-      if constexpr (!DECODE) asg[t] = mfma_f16(wf[((size_t)(C / 32 + ct0 + t) * ks + s) * 64 + lane], b, asg[t]);
-    }
-  }
-
-  const float* bias = (const float*)a.bias;
-  double bsum = 0.0;
-  if (valid) {
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = 32 * (ct0 + t) + 8 * g + 4 * h;
-        const floatx4 bm = *(const floatx4*)(bias + c);
-        half4 yh;
-        if constexpr (DECODE) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            // same operation order as the encoder: mu first, then q + mu
-            const float mu = amu[t][4 * g + e] + bm[e];
-            const float q = (float)a.q_in[(size_t)(c + e) * a.P + p];
-            yh[e] = (f16)(q + mu);
-          }
-        } else {
-          const floatx4 bs = *(const floatx4*)(bias + C + c);
-          const half4 yv = *(const half4*)((const f16*)a.y + (size_t)p * C + c);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float mu = amu[t][4 * g + e] + bm[e];
-            float q = rintf((float)yv[e] - mu);
-            q = fminf(fmaxf(q, -32768.f), 32767.f);
-            a.q_out[(size_t)(c + e) * a.P + p] = (int16_t)q;
-            yh[e] = (f16)(q + mu);
-            bsum += (double)symbol_bits(q, softplus_sigma(asg[t][4 * g + e] + bs[e]));
-          }
-        }
-        *(half4*)((f16*)a.yhat_new + (size_t)p * C + c) = yh;
-      }
-    }
-  }
-  if constexpr (DECODE) return;
-  __shared__ double red[4];
-  bsum = wave_sum(bsum);
-  if (lane == 0) red[wave] = bsum;
-  __syncthreads();
-  if (threadIdx.x == 0) a.partials[(size_t)tile * gridDim.y + blockIdx.y] = ((red[0] + red[1]) + red[2]) + red[3];
-}
-
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
   dim3 grid(grid_tiles(a.P) * (a.N / NT)), block(512);
@@ -639,6 +639,8 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
+  NC_PW(LD_NHWC, EP_PRIOR)
+  NC_PW(LD_NHWC, EP_PRIOR_DEC)
 #undef NC_PW
   return hipErrorInvalidValue;
 }
@@ -664,18 +666,32 @@ hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st) {
 
 // Channels per workgroup: 64 (mu and s rows, 128 accumulator registers), which
 // gives C / 64 workgroups per pixel tile.
-int prior_partials_f16(int C, int P) { return grid_tiles(P) * (C / 64); }
+// Prior head, quantiser and bits (Fig. 4 "Q", Supp. B.2) as the epilogue of
+// the pointwise kernel: the head's rows are packed in passes of 32 mu rows
+// followed by the 32 s rows of the same channels, so one workgroup holds both
+// for its 128 latent pixels x 32 channels.  Bit partial sums: one per
+// (tile, pass), reduced in a fixed order by k_reduce.
+int prior_partials_f16(int C, int P) { return ((P + 127) / 128) * (C / 32); }
 
-hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials) {
-  const int ch = 64;
-  dim3 grid(grid_tiles(a.P), a.C / ch), block(256);
-  if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / ch);
-  if (ch == 128 && a.decode) launch(k_prior_f16<128, true>, grid, block, st, a);
-  else if (ch == 128) launch(k_prior_f16<128, false>, grid, block, st, a);
-  else if (ch == 64 && a.decode) launch(k_prior_f16<64, true>, grid, block, st, a);
-  else if (ch == 64) launch(k_prior_f16<64, false>, grid, block, st, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+hipError_t launch_prior_f16(const PriorArgs& pa, hipStream_t st, int* n_partials) {
+  if (pa.C % 32) return hipErrorInvalidValue;
+  PwArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.wfrag = pa.wfrag;
+  a.bias = pa.bias;
+  a.K = pa.C;
+  a.N = 2 * pa.C;
+  a.P = pa.P;
+  a.src0 = pa.yhat_prev;
+  a.C0 = pa.C;
+  a.dst = pa.yhat_new;
+  a.Cdst = pa.C;
+  a.y = pa.y;
+  a.q_in = pa.q_in;
+  a.q_out = pa.q_out;
+  a.partials = pa.partials;
+  if (n_partials) *n_partials = prior_partials_f16(pa.C, pa.P);
+  return pw_dispatch<64>(LD_NHWC, pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
 }
 
 }  // namespace nc
