@@ -361,21 +361,29 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   constexpr int CHUNK = DcSmemI<C>::CHUNK;
   constexpr int LDS_PER_WAVE = DcSmemI<C>::FR / 8;
   constexpr int TH = 8, TW = 16;
-  constexpr int HW = TW + 2, HPX = (TH + 2) * HW;
-  constexpr int CS = 64;
-  constexpr int SLOTS = HPX * (CS / 8);
-  constexpr int SLICE_INSTR = (SLOTS + 63) / 64;
-  constexpr int SLICE = (HPX * CS * 2 + 1023) / 1024 * 1024;
-  constexpr int BUF = CHUNK > SLICE ? CHUNK : SLICE;
+  constexpr int HW = TW + 2;
+  // Depthwise role: band sg of 4 tile rows x channel part cp (CP parts of CPC
+  // channels); lane l = pixel (row 4 sg + l / 16, column l % 16).  With C = 64
+  // there are only two parts and waves 4-7 sit the depthwise out.
+  constexpr int CP = C / 32 < 4 ? C / 32 : 4;
+  constexpr int CPC = C / CP;                  // channels per part
+  constexpr int NG = CPC / 8;                  // 8-channel groups (16-byte vectors per halo pixel)
+  constexpr int NS = CPC / 32;                 // 32-channel MFMA steps per part
+  constexpr int BPX = 6 * HW;
+  constexpr int RINSTR = (BPX * NG + 63) / 64;
+  constexpr int REGION = 16 * 1024;
+  constexpr int SWS = NG == 8 ? 0 : 1;         // vector v of pixel hp at v ^ ((hp >> SWS) & (NG-1))
+  static_assert(NG == 4 || NG == 8, "C in {64, 128, 256}");
+  static_assert(RINSTR * 1024 <= REGION && 4 * NS * 1024 <= REGION, "band and exchange fit a region");
   static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
+  constexpr int BUF = CHUNK > 2 * REGION ? CHUNK : 2 * REGION;
   __shared__ __attribute__((aligned(1024))) char wb0[BUF];
   __shared__ __attribute__((aligned(1024))) char wb1[BUF];
   __shared__ __attribute__((aligned(1024))) char wb2[BUF];
   __shared__ __attribute__((aligned(1024))) char wb3[BUF];
   __shared__ intx4 gx0[4][128];
   __shared__ intx4 gx1[4][128];
-  __shared__ int c1s[2 * C], c2s[C], dwbs[C];
-  __shared__ __attribute__((aligned(16))) int16_t dws[9 * C];
+  __shared__ int c1s[2 * C];
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -385,89 +393,127 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pg = wave & 3, hf = wave >> 2;
-  const int r = 2 * pg + ((lane & 31) >> 4), c = lane & 15;
-  const int y = ty0 + r, x = tx0 + c;
-  const bool valid = y < a.h && x < a.w;
-  const int p = y * a.w + x;
+  const int sg = pg >> 1;
+  const int cp = CP == 4 ? (wave & 1) | ((wave >> 2) << 1) : (wave & 1);
+  const bool dw_on = CP == 4 || wave < 4;
+  const int cb = cp * CPC;
   const int16_t* z = (const int16_t*)a.src;
   const char* wchunks = (const char*)a.w1;
-
-  constexpr int SLICE_PER_WAVE = (SLICE_INSTR + 7) / 8;
-  const int16_t* slice_src[SLICE_PER_WAVE];
-  bool slice_on[SLICE_PER_WAVE];
-#pragma unroll
-  for (int i = 0; i < SLICE_PER_WAVE; ++i) {
-    const int ins = wave + 8 * i;
-    const int S = ins * 64 + lane;
-    slice_on[i] = ins < SLICE_INSTR && S < SLOTS;
-    const int hp = S >> 3, v = (S & 7) ^ (hp & 7);
-    const int hy = ty0 - 1 + hp / HW, hx = tx0 - 1 + hp % HW;
-    const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-    slice_src[i] = (in ? z + (size_t)(hy * a.w + hx) * C : (const int16_t*)a.zpad) + 8 * v;
-  }
-  auto issue_slice = [&](int k, char* buf) {
-#pragma unroll
-    for (int i = 0; i < SLICE_PER_WAVE; ++i) {
-      if (slice_on[i])
-        dma16(slice_src[i] + CS * k, buf + (wave + 8 * i) * 1024);
-    }
+  auto bufp = [&](int k) __attribute__((always_inline)) -> char* {
+    return k == 0 ? wb0 : k == 1 ? wb1 : k == 2 ? wb2 : wb3;
   };
-  static_assert(C / CS <= 4, "one LDS buffer per halo slice");
-  char* const slice_buf[4] = {wb0, wb1, wb2, wb3};
-#pragma unroll
-  for (int k = 0; k < C / CS; ++k) issue_slice(k, slice_buf[k]);
-  for (int i = threadIdx.x; i < 2 * C; i += 512) c1s[i] = ((const int*)a.b1)[i];
-  for (int i = threadIdx.x; i < C; i += 512) {
-    c2s[i] = ((const int*)a.b2)[i];
-    dwbs[i] = ((const int*)a.dwb)[i];
-  }
-  for (int i = threadIdx.x; i < 9 * C / 8; i += 512) ((intx4*)dws)[i] = ((const intx4*)a.dww)[i];
+  auto region = [&](int sg_, int cp_) __attribute__((always_inline)) -> char* {
+    return bufp(2 * (cp_ >> 1) + sg_) + (cp_ & 1) * REGION;
+  };
+  char* const own = region(sg, cp);
 
-  // depthwise 3x3: lane = pixel, channels 32s + 16h + e (two 8-channel vectors
-  // per tap), exact int32 sums, rescaled to int16 and split into int8 digits.
-  intx4 ah[KSI], al[KSI];
-  int tap_off[9];
+  // pw1 corrections to registers before the halo loads, stored after the depthwise
+  constexpr int NB1 = (2 * C + 511) / 512;
+  int rc1[NB1];
 #pragma unroll
-  for (int ky = 0; ky < 3; ++ky)
+  for (int i = 0; i < NB1; ++i) {
+    const int k = threadIdx.x + 512 * i;
+    rc1[i] = k < 2 * C ? ((const int*)a.b1)[k] : 0;
+  }
+
+  // Halo band (as in the fp16 block): slot S = 16-byte unit S of the region.
+  if (dw_on) {
 #pragma unroll
-    for (int kx = 0; kx < 3; ++kx) {
-      const int hp = (r + ky) * HW + c + kx;
-      tap_off[ky * 3 + kx] = (hp << 7) | (((2 * h) ^ (hp & 7)) << 4);
+    for (int i = 0; i < RINSTR; ++i) {
+      const int S = i * 64 + lane;
+      const int hp = S / NG, v = (S % NG) ^ ((hp >> SWS) & (NG - 1));
+      const int hy = ty0 - 1 + 4 * sg + hp / HW, hx = tx0 - 1 + hp % HW;
+      const bool in = hp < BPX && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+      dma16(in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const int16_t*)a.zpad, own + i * 1024);
     }
-  auto dw_slice = [&](int k, const char* buf) {
+  }
+
+  if (dw_on) {
+    // Depthwise 3x3: exact int32 sums with v_dot2_i32_i16 (one weight of each
+    // scalar pair masked to zero selects the channel), bias 512 b_i, rescaled
+    // to int16 and split into int8 digits.
+    int tap_off[9];
 #pragma unroll
-    for (int ss = 0; ss < CS / 32; ++ss) {
-      const int s = k * (CS / 32) + ss;
-      const int c0 = 32 * s + 16 * h;
-      int acc[16];
+    for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = dwbs[c0 + e];
+      for (int kx = 0; kx < 3; ++kx) {
+        const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
+        tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
+      }
+    cint* dww = (cint*)((const int16_t*)a.dww + cb);  // [9][C] int16, as pairs
+    cint* dwb = (cint*)((const int*)a.dwb + cb);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band
+    typedef short short2v __attribute__((ext_vector_type(2)));
+    uint32_t dv[NG][4];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      int acc[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = dwb[8 * g + e];
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
-        // vectors v0 = 4 ss + 2h and v0 + 1 of the slice (see the slot layout)
-        const int o0 = tap_off[t] ^ (ss << 6);
-        const shortx8 z0 = *(const shortx8*)(buf + o0);
-        const shortx8 z1 = *(const shortx8*)(buf + (o0 ^ 16));
-        const shortx8 w0 = *(const shortx8*)(dws + t * C + c0);
-        const shortx8 w1 = *(const shortx8*)(dws + t * C + c0 + 8);
+        const intx4 zv = *(const intx4*)(own + (tap_off[t] ^ (g << 4)));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          acc[e] += (int)w0[e] * (int)z0[e];
-          acc[8 + e] += (int)w1[e] * (int)z1[e];
+        for (int i = 0; i < 4; ++i) {
+          const int wp = dww[(t * C + 8 * g) / 2 + i];
+          // (a bit_cast applied directly to the vector element zv[i] reads element 0
+          // with this compiler; going through a scalar keeps the element)
+          const int zi = zv[i];
+          const short2v zz = __builtin_bit_cast(short2v, zi);
+          acc[2 * i] = __builtin_amdgcn_sdot2(zz, __builtin_bit_cast(short2v, wp & 0xFFFF), acc[2 * i], false);
+          acc[2 * i + 1] =
+              __builtin_amdgcn_sdot2(zz, __builtin_bit_cast(short2v, (int)(wp & 0xFFFF0000u)), acc[2 * i + 1], false);
         }
       }
-      uint32_t d[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) d[e] = pack2(rescale13(acc[2 * e]), rescale13(acc[2 * e + 1]));
-      split16(d, ah[s], al[s]);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < 4; ++i) dv[g][i] = pack2(rescale13(acc[2 * i]), rescale13(acc[2 * i + 1]));
     }
-  };
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();  // all slices staged
+    // 16-channel unit u = groups 2u, 2u+1 -> hi / lo digit vectors; units 2p and
+    // 2p+1 swap lane halves into the B fragments of step cb / 32 + p for pixel
+    // groups 2 sg (lanes 0-31) and 2 sg + 1; they overwrite the dead band:
+    // [pixel group & 1][step p][hi, lo] x 1 KiB.
 #pragma unroll
-  for (int k = 0; k < C / CS; ++k) dw_slice(k, slice_buf[k]);
-  __syncthreads();  // all halo reads done: the buffers hold weights from here on
+    for (int p = 0; p < NS; ++p) {
+      intx4 xh, xl, yh, yl;
+      {
+        uint32_t d[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { d[i] = dv[4 * p][i]; d[4 + i] = dv[4 * p + 1][i]; }
+        split16(d, xh, xl);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { d[i] = dv[4 * p + 2][i]; d[4 + i] = dv[4 * p + 3][i]; }
+        split16(d, yh, yl);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const auto rh = __builtin_amdgcn_permlane32_swap((uint32_t)xh[i], (uint32_t)yh[i], false, false);
+        xh[i] = (int)rh[0];
+        yh[i] = (int)rh[1];
+        const auto rl = __builtin_amdgcn_permlane32_swap((uint32_t)xl[i], (uint32_t)yl[i], false, false);
+        xl[i] = (int)rl[0];
+        yl[i] = (int)rl[1];
+      }
+      *(intx4*)(own + ((0 * NS + p) * 2 + 0) * 1024 + lane * 16) = xh;
+      *(intx4*)(own + ((0 * NS + p) * 2 + 1) * 1024 + lane * 16) = xl;
+      *(intx4*)(own + ((1 * NS + p) * 2 + 0) * 1024 + lane * 16) = yh;
+      *(intx4*)(own + ((1 * NS + p) * 2 + 1) * 1024 + lane * 16) = yl;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NB1; ++i)
+    if (threadIdx.x + 512 * i < 2 * C) c1s[threadIdx.x + 512 * i] = rc1[i];
+  lds_barrier();
+
+  // MFMA role: the digit fragments of all C filtered channels of this wave's 32 pixels
+  intx4 ah[KSI], al[KSI];
+#pragma unroll
+  for (int s = 0; s < KSI; ++s) {
+    const char* src = region(sg, s / NS) + (((pg & 1) * NS + s % NS) * 2) * 1024 + lane * 16;
+    ah[s] = *(const intx4*)src;
+    al[s] = *(const intx4*)(src + 1024);
+  }
+  lds_barrier();  // exchange read: the buffers take weight chunks from here on
+
   dci_issue<C>(wchunks, 0, wb0, wave, lane);
   dci_issue<C>(wchunks, 1, wb1, wave, lane);
   dci_issue<C>(wchunks, 2, wb2, wave, lane);
@@ -481,7 +527,8 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, lane), c1s, 0, h, lane, gx0[pg]);
   lds_barrier();
 
-  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, intx4* gcur, intx4* gnxt) {
+  auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, intx4* gcur, intx4* gnxt)
+                  __attribute__((always_inline)) {
     const bool more = j + 3 < NCH;
     if (more) dci_issue<C>(wchunks, j + 3, wiss, wave, lane);
     const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
@@ -499,23 +546,51 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
     step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
   }
-  if (!valid) return;
 
+  // Epilogue through LDS: park the pw2 sums (int32) as in the fp16 block, then
+  // each thread takes 8 channels of one pixel: rescale(sum + correction), add
+  // the residual with saturation, coalesced 16-byte loads and stores.
+  static_assert(32 * C * 4 <= BUF, "a pixel group's int32 output fits one buffer");
+  constexpr int SWZ = (C / 4 - 1) & 31;
+  {
+    char* ob = bufp(pg);
+    const int row = lane & 31;
+#pragma unroll
+    for (int t = 0; t < MT / 2; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
+        intx4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e];
+        *(intx4*)(ob + row * (C * 4) + (((cc >> 2) ^ (row & SWZ)) << 4)) = o;
+      }
+  }
+  lds_barrier();
+  constexpr int CH8 = C / 8;
+  constexpr int PER = 128 * CH8 / 512;
   int16_t* dst = (int16_t*)a.dst;
+  const int* c2 = (const int*)a.b2;
 #pragma unroll
-  for (int t = 0; t < MT / 2; ++t) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-      const intx4 cv = *(const intx4*)(c2s + cc);
-      const shortx4 zv = *(const shortx4*)(z + (size_t)p * C + cc);
-      shortx4 o;
+  for (int i = 0; i < PER; ++i) {
+    const int idx = i * 512 + threadIdx.x;
+    const int px = idx / CH8, k8 = idx % CH8;
+    const int gpx = px >> 5, row = px & 31;
+    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
+    if (yy < a.h && xx < a.w) {
+      const char* ob = bufp(gpx);
+      const intx4 o0 = *(const intx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
+      const intx4 o1 = *(const intx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
+      const intx4 b0 = *(const intx4*)(c2 + 8 * k8), b1 = *(const intx4*)(c2 + 8 * k8 + 4);
+      const size_t off = (size_t)(yy * a.w + xx) * C + 8 * k8;
+      const shortx8 zv = *(const shortx8*)(z + off);
+      shortx8 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int pv = rescale13((int)((uint32_t)out[t][4 * g + e] + (uint32_t)cv[e]));
-        o[e] = (short)clip16((int)zv[e] + pv);
+        o[e] = (short)clip16((int)zv[e] + rescale13((int)((uint32_t)o0[e] + (uint32_t)b0[e])));
+        o[4 + e] = (short)clip16((int)zv[4 + e] + rescale13((int)((uint32_t)o1[e] + (uint32_t)b1[e])));
       }
-      *(shortx4*)(dst + (size_t)p * C + cc) = o;
+      *(shortx8*)(dst + off) = o;
     }
   }
 }
