@@ -102,6 +102,7 @@ typedef const __attribute__((address_space(4))) float cfloat;
 typedef const __attribute__((address_space(4))) int32_t cint;
 typedef const __attribute__((address_space(4))) half8 chalf8;
 typedef const __attribute__((address_space(4))) shortx8 cshortx8;
+typedef const __attribute__((address_space(4))) intx4 cintx4;
 
 // Workgroup barrier for LDS hand-offs inside a pipelined loop.  It waits for
 // this wave's LDS operations (lgkmcnt) but, unlike __syncthreads(), not for

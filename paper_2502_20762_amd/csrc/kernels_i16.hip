@@ -429,9 +429,9 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   }
 
   if (dw_on) {
-    // Depthwise 3x3: exact int32 sums with v_dot2_i32_i16 (one weight of each
-    // scalar pair masked to zero selects the channel), bias 512 b_i, rescaled
-    // to int16 and split into int8 digits.
+    // Depthwise 3x3: exact int32 sums, one v_mad_i32_i16 per tap and channel
+    // (op_sel picks the low or high int16 of the packed activation and of the
+    // wave-uniform weight pair), bias 512 b_i, rescaled to int16.
     int tap_off[9];
 #pragma unroll
     for (int ky = 0; ky < 3; ++ky)
@@ -440,10 +440,9 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
         const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
         tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
       }
-    cint* dww = (cint*)((const int16_t*)a.dww + cb);  // [9][C] int16, as pairs
+    cintx4* dww = (cintx4*)((const int16_t*)a.dww + cb);  // [9][C] int16, 8 per vector
     cint* dwb = (cint*)((const int*)a.dwb + cb);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band
-    typedef short short2v __attribute__((ext_vector_type(2)));
     uint32_t dv[NG][4];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -453,20 +452,18 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
         const intx4 zv = *(const intx4*)(own + (tap_off[t] ^ (g << 4)));
+        const intx4 wv = dww[(t * C + 8 * g) / 8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int wp = dww[(t * C + 8 * g) / 2 + i];
-          // (a bit_cast applied directly to the vector element zv[i] reads element 0
-          // with this compiler; going through a scalar keeps the element)
+          const int wp = wv[i];
           const int zi = zv[i];
-          const short2v zz = __builtin_bit_cast(short2v, zi);
-          acc[2 * i] = __builtin_amdgcn_sdot2(zz, __builtin_bit_cast(short2v, wp & 0xFFFF), acc[2 * i], false);
-          acc[2 * i + 1] =
-              __builtin_amdgcn_sdot2(zz, __builtin_bit_cast(short2v, (int)(wp & 0xFFFF0000u)), acc[2 * i + 1], false);
+          asm("v_mad_i32_i16 %0, %1, %2, %0" : "+v"(acc[2 * i]) : "v"(zi), "s"(wp));
+          asm("v_mad_i32_i16 %0, %1, %2, %0 op_sel:[1,1,0,0]" : "+v"(acc[2 * i + 1]) : "v"(zi), "s"(wp));
         }
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) dv[g][i] = pack2(rescale13(acc[2 * i]), rescale13(acc[2 * i + 1]));
+      __builtin_amdgcn_sched_barrier(0);  // one group's weights live at a time
     }
     // 16-channel unit u = groups 2u, 2u+1 -> hi / lo digit vectors; units 2p and
     // 2p+1 swap lane halves into the B fragments of step cb / 32 + p for pixel
