@@ -281,13 +281,22 @@ struct I16Acc {
   intx16 hh, mid, ll;
 };
 
+// pw1 for hidden chunk j; the low-digit accumulator starts at the chunk's
+// correction 512 b_i + 128 sum w (row 8 g + 4 h + e of register 4 g + e).
 template <int C>
-__device__ __forceinline__ I16Acc dci_hidden_mfma(const char* wb, const intx4* ah, const intx4* al, int lane) {
+__device__ __forceinline__ I16Acc dci_hidden_mfma(const char* wb, const intx4* ah, const intx4* al, const int* c1s,
+                                                  int j, int h, int lane) {
   constexpr int KSI = DcSmemI<C>::KSI;
   const intx4* w = (const intx4*)wb + lane;
   // Fragment reads are issued ahead of the MFMAs in groups of half a chunk.
   constexpr int G = KSI >= 4 ? KSI / 2 : KSI;
   I16Acc acc{{}, {}, {}};
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const intx4 cv = *(const intx4*)(c1s + 32 * j + 8 * g + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc.ll[4 * g + e] = cv[e];
+  }
 #pragma unroll
   for (int s0 = 0; s0 < KSI; s0 += G) {
     intx4 wa[G], wl[G];
@@ -309,20 +318,16 @@ __device__ __forceinline__ I16Acc dci_hidden_mfma(const char* wb, const intx4* a
 }
 
 // Combine, rescale, integer LeakyReLU (slope 819 / 8192), split into int8
-// digits, store as the pw2 operand fragments.
-__device__ __forceinline__ void dci_hidden_store(const I16Acc& acc, const int* c1s, int j, int h, int lane,
-                                                 intx4* gx) {
+// digits, store as the pw2 operand fragments.  The LeakyReLU is
+// max(h, RHE(819 h / 2^13)): for h >= 0 the scaled value never exceeds h, for
+// h < 0 it is never below h, so the maximum selects the right branch.
+__device__ __forceinline__ void dci_hidden_store(const I16Acc& acc, int lane, intx4* gx) {
   int gv[16];
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const intx4 cv = *(const intx4*)(c1s + 32 * j + 8 * g + 4 * h);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 4 * g + e;
-      const int hv = rescale13(combine_i16(acc.hh[r], acc.mid[r], acc.ll[r], cv[e]));
-      const int m = 819 * hv;  // |m| < 2^25: the bias form of RHE cannot overflow
-      gv[r] = hv >= 0 ? hv : (m + 4095 + ((m >> 13) & 1)) >> 13;
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int hv = rescale13(combine_i16(acc.hh[r], acc.mid[r], acc.ll[r], 0));
+    const int m = 819 * hv;  // |m| < 2^25: the bias form of RHE cannot overflow
+    gv[r] = max(hv, (m + 4095 + ((m >> 13) & 1)) >> 13);
   }
   uint32_t d[8];
 #pragma unroll
@@ -521,18 +526,35 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
   lds_barrier();  // chunks 0 and 1 staged
-  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, lane), c1s, 0, h, lane, gx0[pg]);
+  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0[pg]);
   lds_barrier();
 
+  // The residual tile (128 pixels x C int16, pixel px at byte 2 C px of
+  // buffers 0 and 1) is loaded during the last two chunks.
+  static_assert(128 * C * 2 <= 2 * BUF, "residual tile fits two buffers");
+  auto issue_residual = [&]() __attribute__((always_inline)) {
+    constexpr int CH8 = C / 8;
+#pragma unroll
+    for (int i = 0; i < C / 32; ++i) {
+      const int k = wave + 8 * i;  // 1 KiB unit k of the tile
+      const int S = k * 64 + lane;
+      const int px = S / CH8, k8 = S % CH8;
+      const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
+      const bool in = yy < a.h && xx < a.w;
+      char* dstl = (k * 1024 < BUF ? wb0 : wb1) + (k * 1024) % BUF;
+      dma16(in ? z + (size_t)(yy * a.w + xx) * C + 8 * k8 : (const int16_t*)a.zpad, dstl);
+    }
+  };
   auto step = [&](int j, const char* wcur, const char* wnxt, char* wiss, intx4* gcur, intx4* gnxt)
                   __attribute__((always_inline)) {
     const bool more = j + 3 < NCH;
     if (more) dci_issue<C>(wchunks, j + 3, wiss, wave, lane);
     const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
     I16Acc hacc;
-    if (produce) hacc = dci_hidden_mfma<C>(wnxt, ah, al, lane);
+    if (produce) hacc = dci_hidden_mfma<C>(wnxt, ah, al, c1s, j + 1, h, lane);
+    if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
     dci_project<C>(wcur, gcur, hf, lane, out);
-    if (produce) dci_hidden_store(hacc, c1s, j + 1, h, lane, gnxt);
+    if (produce) dci_hidden_store(hacc, lane, gnxt);
     if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
@@ -544,50 +566,49 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
   }
 
-  // Epilogue through LDS: park the pw2 sums (int32) as in the fp16 block, then
-  // each thread takes 8 channels of one pixel: rescale(sum + correction), add
-  // the residual with saturation, coalesced 16-byte loads and stores.
-  static_assert(32 * C * 4 <= BUF, "a pixel group's int32 output fits one buffer");
-  constexpr int SWZ = (C / 4 - 1) & 31;
+  // Epilogue: rescale(sum + correction) to int16 in registers, parked in
+  // buffers 2 (pixel groups 0, 1) and 3 (groups 2, 3), row = pixel, 8-byte unit
+  // u of the row at u ^ (row & 15); then each thread adds the residual to 8
+  // channels of one pixel with saturation and stores them with one 16-byte store.
   {
-    char* ob = bufp(pg);
+    const int* c2 = (const int*)a.b2;
+    char* ob = (pg < 2 ? wb2 : wb3) + (pg & 1) * (32 * C * 2);
     const int row = lane & 31;
 #pragma unroll
     for (int t = 0; t < MT / 2; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-        intx4 o;
+        const intx4 cv = *(const intx4*)(c2 + cc);
+        shortx4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e];
-        *(intx4*)(ob + row * (C * 4) + (((cc >> 2) ^ (row & SWZ)) << 4)) = o;
+        for (int e = 0; e < 4; ++e) o[e] = (short)rescale13((int)((uint32_t)out[t][4 * g + e] + (uint32_t)cv[e]));
+        *(shortx4*)(ob + row * (C * 2) + (((cc >> 2) ^ (row & 15)) << 3)) = o;
       }
   }
-  lds_barrier();
+  lds_barrier();  // the residual loads were waited for in the last chunk step
   constexpr int CH8 = C / 8;
   constexpr int PER = 128 * CH8 / 512;
   int16_t* dst = (int16_t*)a.dst;
-  const int* c2 = (const int*)a.b2;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int idx = i * 512 + threadIdx.x;
     const int px = idx / CH8, k8 = idx % CH8;
-    const int gpx = px >> 5, row = px & 31;
-    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
+    const int row = px & 31;
+    const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
     if (yy < a.h && xx < a.w) {
-      const char* ob = bufp(gpx);
-      const intx4 o0 = *(const intx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
-      const intx4 o1 = *(const intx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
-      const intx4 b0 = *(const intx4*)(c2 + 8 * k8), b1 = *(const intx4*)(c2 + 8 * k8 + 4);
-      const size_t off = (size_t)(yy * a.w + xx) * C + 8 * k8;
-      const shortx8 zv = *(const shortx8*)(z + off);
+      const char* ob = (px < 64 ? wb2 : wb3) + ((px >> 5) & 1) * (32 * C * 2) + row * (C * 2);
+      const shortx4 p0 = *(const shortx4*)(ob + (((2 * k8) ^ (row & 15)) << 3));
+      const shortx4 p1 = *(const shortx4*)(ob + (((2 * k8 + 1) ^ (row & 15)) << 3));
+      const int rb = px * (C * 2) + 16 * k8;  // residual byte offset in buffers 0, 1
+      const shortx8 zv = *(const shortx8*)((rb < BUF ? wb0 : wb1) + rb % BUF);
       shortx8 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        o[e] = (short)clip16((int)zv[e] + rescale13((int)((uint32_t)o0[e] + (uint32_t)b0[e])));
-        o[4 + e] = (short)clip16((int)zv[4 + e] + rescale13((int)((uint32_t)o1[e] + (uint32_t)b1[e])));
+        o[e] = (short)clip16((int)zv[e] + (int)p0[e]);
+        o[4 + e] = (short)clip16((int)zv[4 + e] + (int)p1[e]);
       }
-      *(shortx8*)(dst + off) = o;
+      *(shortx8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8) = o;
     }
   }
 }
