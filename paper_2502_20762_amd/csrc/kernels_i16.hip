@@ -388,7 +388,8 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   __shared__ __attribute__((aligned(1024))) char wb3[BUF];
   __shared__ intx4 gx0[4][128];
   __shared__ intx4 gx1[4][128];
-  __shared__ int c1s[2 * C];
+  __shared__ __attribute__((aligned(16))) int c1s[2 * C];  // pw1 corrections 512 b + 128 sum w
+  __shared__ __attribute__((aligned(16))) int c2s[C];      // pw2 corrections
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -412,13 +413,15 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   };
   char* const own = region(sg, cp);
 
-  // pw1 corrections to registers before the halo loads, stored after the depthwise
-  constexpr int NB1 = (2 * C + 511) / 512;
-  int rc1[NB1];
+  // Corrections straight into LDS (waves 0 and 1, before their halo loads;
+  // waited for with those loads and made visible by the exchange barrier).
+  if (wave < 2) {
+    const int* src = wave == 0 ? (const int*)a.b1 : (const int*)a.b2;
+    int* dstl = wave == 0 ? c1s : c2s;
+    const int n16 = (wave == 0 ? 2 * C : C) / 4;  // 16-byte units
 #pragma unroll
-  for (int i = 0; i < NB1; ++i) {
-    const int k = threadIdx.x + 512 * i;
-    rc1[i] = k < 2 * C ? ((const int*)a.b1)[k] : 0;
+    for (int i = 0; i < (2 * C / 4 + 63) / 64; ++i)
+      if (64 * i + lane < n16) dma16(src + 4 * (64 * i + lane), dstl + 4 * 64 * i);
   }
 
   // Halo band (as in the fp16 block): slot S = 16-byte unit S of the region.
@@ -501,9 +504,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
       *(intx4*)(own + ((1 * NS + p) * 2 + 1) * 1024 + lane * 16) = yl;
     }
   }
-#pragma unroll
-  for (int i = 0; i < NB1; ++i)
-    if (threadIdx.x + 512 * i < 2 * C) c1s[threadIdx.x + 512 * i] = rc1[i];
+  if (!dw_on) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // corrections (waves 0, 1 are depthwise waves)
   lds_barrier();
 
   // MFMA role: the digit fragments of all C filtered channels of this wave's 32 pixels
@@ -571,7 +572,6 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   // u of the row at u ^ (row & 15); then each thread adds the residual to 8
   // channels of one pixel with saturation and stores them with one 16-byte store.
   {
-    const int* c2 = (const int*)a.b2;
     char* ob = (pg < 2 ? wb2 : wb3) + (pg & 1) * (32 * C * 2);
     const int row = lane & 31;
 #pragma unroll
@@ -579,7 +579,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-        const intx4 cv = *(const intx4*)(c2 + cc);
+        const intx4 cv = *(const intx4*)(c2s + cc);
         shortx4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = (short)rescale13((int)((uint32_t)out[t][4 * g + e] + (uint32_t)cv[e]));
