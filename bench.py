@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import statistics
 import os
 import sys
 import time
@@ -92,38 +93,59 @@ def cpu_baseline(pre, weights, strip_rows):
                       f"of 1080p frame 0 ({dt:.1f} s), scaled by {frac:.3f}; host cpu_count={os.cpu_count()}"}
 
 
+def timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch):
+    """Encode then decode `steps` frames; per-frame event stamps on the codec stream."""
+    stream = torch.cuda.current_stream()
+    nfr = len(gframes)
+    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev_d = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev_e[0].record(stream)
+    for k in range(steps):
+        enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
+        ev_e[k + 1].record(stream)
+    ev_d[0].record(stream)
+    for k in range(steps):
+        dec.decode(qbuf[k], out=xout)
+        ev_d[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fe = [ev_e[k].elapsed_time(ev_e[k + 1]) for k in range(steps)]
+    fd = [ev_d[k].elapsed_time(ev_d[k + 1]) for k in range(steps)]
+    return {"enc_ms": sum(fe), "dec_ms": sum(fd), "wall_s": wall,
+            "enc_median_ms": statistics.median(fe), "dec_median_ms": statistics.median(fd)}
+
+
 def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
     H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
     enc = Codec(H, W, C, ne, nd, path, weights)
     dec = Codec(H, W, C, ne, nd, path, weights)
-    stream = torch.cuda.current_stream()
     odt = torch.int16 if path == "int16" else torch.float16
     qbuf = [torch.empty(enc.q_shape, dtype=torch.int16, device="cuda") for _ in range(steps)]
     bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
     xout = torch.empty(enc.frame_shape, dtype=odt, device="cuda")
     nfr = len(gframes)
-    for i in range(warmup):
-        q, _ = enc.encode(gframes[i % nfr])
-        dec.decode(q, out=xout)
-    torch.cuda.synchronize()
 
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e2 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    e0.record(stream)
-    for k in range(steps):
-        enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
-    e1.record(stream)
-    for k in range(steps):
-        dec.decode(qbuf[k], out=xout)
-    e2.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    enc_ms, dec_ms = e0.elapsed_time(e1), e1.elapsed_time(e2)
+    def warm():
+        enc.reset()
+        dec.reset()
+        for i in range(warmup):
+            q, _ = enc.encode(gframes[i % nfr])
+            dec.decode(q, out=xout)
+        torch.cuda.synchronize()
 
-    # instrumented pass: events around every kernel, same frames
+    # direct launches (the library default), then the same frames as hipGraph replays
+    warm()
+    r = timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch)
+    enc.graphs(True)
+    dec.graphs(True)
+    warm()
+    graph = timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch)
+    enc.graphs(False)
+    dec.graphs(False)
+
+    # instrumented pass: events around every kernel, same frames (always direct launches)
     enc.reset()
     dec.reset()
     enc.timing(True)
@@ -138,12 +160,13 @@ def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
             a = kern.setdefault(kind, [0, 0.0])
             a[0] += n
             a[1] += ms
-    return {
-        "enc_ms": enc_ms, "dec_ms": dec_ms, "wall_s": wall,
+    r.update({
+        "graph": graph,
         "bits_per_frame": float(bits.mean().item()),
         "kernels": {k: {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms} for k, (n, ms) in kern.items()},
         "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)],
-    }
+    })
+    return r
 
 
 def main():
@@ -185,11 +208,16 @@ def main():
         achieved = op_scale * fl / (kd["avg_us"] * 1e-6) / 1e12
         t_roof = roofline_seconds(kinds, enc_list + dec_list, peak_tflops * 1e12 / op_scale)
         step_ms = (r["enc_ms"] + r["dec_ms"]) / K
+        ga = r["graph"]
         return {
             "value": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3),
             "ms_per_step": step_ms,
             "encode_fps": K / (r["enc_ms"] * 1e-3),
             "decode_fps": K / (r["dec_ms"] * 1e-3),
+            "encode_fps_median": 1e3 / r["enc_median_ms"],
+            "decode_fps_median": 1e3 / r["dec_median_ms"],
+            "graph_replay": {"value": K / ((ga["enc_ms"] + ga["dec_ms"]) * 1e-3),
+                             "encode_fps": K / (ga["enc_ms"] * 1e-3), "decode_fps": K / (ga["dec_ms"] * 1e-3)},
             "roofline": {"kernel": "dcblock", "bound": "mfma", "achieved": achieved, "peak": peak_tflops,
                          "unit": unit, "frac": achieved / peak_tflops, "traffic": None,
                          "per_launch": {"algorithmic_ops": op_scale * fl, "algorithmic_bytes": by,
@@ -214,6 +242,8 @@ def main():
                    "height": H, "width": W, "channels": C, "n_enc_blocks": ne, "n_dec_blocks": nd,
                    "path": main_path},
         "encode_fps": s_main["encode_fps"], "decode_fps": s_main["decode_fps"],
+        "encode_fps_median": s_main["encode_fps_median"], "decode_fps_median": s_main["decode_fps_median"],
+        "launch_mode": "direct", "graph_replay": s_main["graph_replay"],
         "roofline": s_main["roofline"],
         "frame_roofline_fps": s_main["frame_roofline_fps"],
         "frac_of_frame_roofline": s_main["frac_of_frame_roofline"],

@@ -137,6 +137,18 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
 /* Kernel launches one ncodec_encode_frame / ncodec_decode_frame enqueues. */
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
 
+/* Graph replay of the per-frame launch sequence (Sec. 3: at this size the
+ * module count, not the MAC count, is what costs time).  When enabled, the
+ * first encode (decode) for each of the two state buffers captures its
+ * launches into a hipGraph on a private stream; later calls replay it on the
+ * context's stream, re-pointing only the nodes that read or write the
+ * caller's buffers (frame, q, bits, output frame).  Results are identical to
+ * the direct launches.  Off by default: on MI355X with ROCm 7 the replay of
+ * this linear launch chain measured slightly slower than direct launches.
+ * While per-kernel timing is enabled, calls launch directly.  Errors: EHIP if
+ * capture, instantiation, update or launch fails. */
+ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
+
 /* Optional per-kernel timing.  While enabled, every kernel the context
  * enqueues is launched with a start / stop HIP event pair attached to its
  * dispatch (hipExtLaunchKernel), so each interval is that kernel's execution

@@ -265,7 +265,7 @@ struct Layout {
   size_t sigma_tab = 0;
   size_t image_bytes = 0;
   // state and intermediates (offsets from the workspace base)
-  size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad;
+  size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
   int n_partials;
   size_t total;
 };
@@ -334,6 +334,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
   L.partials = alloc((size_t)L.n_partials * 8);
   L.zpad = alloc((size_t)C * 2);  // zeroed at create and never written
+  L.spare_bits = alloc(8);        // bit total of graph replays called without d_bits
   L.total = off;
   return pk.ok;
 }
@@ -354,6 +355,22 @@ struct ncodec_ctx {
   };
   bool timing = false;
   std::vector<TimedLaunch> log;
+  // Graph replay: one captured graph per (encode / decode, state parity), with
+  // the kernel nodes that touch caller buffers, updated when those change.
+  struct CapturedNode {
+    const char* kind;
+    hipGraphNode_t node;
+  };
+  struct GraphSlot {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    std::vector<CapturedNode> nodes;
+    const void* ptr[3] = {nullptr, nullptr, nullptr};
+  };
+  bool use_graphs = false;
+  GraphSlot graphs[2][2];  // [decode][cur]
+  hipStream_t cap_stream = nullptr;
+  std::vector<CapturedNode>* capturing = nullptr;
   bool is_int() const { return cfg.path == NCODEC_PATH_INT16; }
   template <class T = void> T* p(size_t off) const { return (T*)(ws + off); }
 };
@@ -380,6 +397,16 @@ ncodec_status hip_fail(ncodec_ctx* ctx, hipError_t e, const char* where) {
 // is that kernel's execution, without the dispatch gap before it.
 template <class F>
 hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch_fn) {
+  if (ctx->capturing) {
+    hipError_t e = launch_fn();
+    if (e != hipSuccess) return e;
+    hipStreamCaptureStatus cs;
+    const hipGraphNode_t* deps = nullptr;
+    size_t nd = 0;
+    e = hipStreamGetCaptureInfo_v2(ctx->stream, &cs, nullptr, nullptr, &deps, &nd);
+    if (e == hipSuccess && nd == 1) ctx->capturing->push_back({kind, deps[0]});
+    return e;
+  }
   if (!ctx->timing) return launch_fn();
   ncodec_ctx::TimedLaunch t{kind, nullptr, nullptr};
   hipError_t e = hipEventCreate(&t.start);
@@ -475,6 +502,200 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   return NCODEC_OK;
 }
 
+// Enqueues one encode on ctx->stream (or records it under capture).
+ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits) {
+  ncodec_status st;
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int h8 = c.height / 8, w8 = c.width / 8;
+  const int P8 = h8 * w8, P16 = P8 / 4;
+  const Layout& L = ctx->L;
+  const int cur = ctx->cur, nxt = 1 - cur;
+
+  PwArgs a = conv_args(ctx, L.pe, 192, C, P8);
+  a.src0 = d_frame;
+  a.dst = ctx->p(L.ed);
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "embed", LD_FRAME, EP_NHWC, a), "patch embed");
+
+  void* z = ctx->p(L.zA);
+  a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
+  a.src0 = ctx->p(L.ed);
+  a.C0 = C;
+  a.src1 = ctx->p(L.feat[cur]);
+  a.C1 = C;
+  a.dst = z;
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_enc");
+
+  for (int k = 0; k < c.n_enc_blocks; ++k) {
+    void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
+    const BlockDev& b = L.enc[k];
+    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
+                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
+                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
+    NC_HIP(ctx, dcblock(ctx, ba), "encoder block");
+    z = dst;
+  }
+
+  a = conv_args(ctx, L.down, 4 * C, C, P16);
+  a.src0 = z;
+  a.Csrc = C;
+  a.dst = ctx->p(L.y);
+  a.Cdst = C;
+  NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
+
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.head.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+  pa.bias = ctx->p(L.head.bias);
+  pa.yhat_prev = ctx->p(L.yhat[cur]);
+  pa.y = ctx->p(L.y);
+  pa.q_out = d_q;
+  pa.yhat_new = ctx->p(L.yhat[nxt]);
+  pa.partials = ctx->p<double>(L.partials);
+  pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
+  pa.C = C;
+  pa.P = P16;
+  pa.decode = 0;
+  int np = 0;
+  NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
+  if (d_bits)
+    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(pa.partials, np, d_bits, ctx->stream); }), "bits reduce");
+
+  st = run_decoder(ctx, nxt);
+  return st;
+}
+
+// Enqueues one decode on ctx->stream (or records it under capture).
+ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_out) {
+  ncodec_status st;
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int P8 = (c.height / 8) * (c.width / 8), P16 = P8 / 4;
+  const Layout& L = ctx->L;
+  const int cur = ctx->cur, nxt = 1 - cur;
+
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.head.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+  pa.bias = ctx->p(L.head.bias);
+  pa.yhat_prev = ctx->p(L.yhat[cur]);
+  pa.q_in = d_q;
+  pa.yhat_new = ctx->p(L.yhat[nxt]);
+  pa.C = C;
+  pa.P = P16;
+  pa.decode = 1;
+  NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
+  st = run_decoder(ctx, nxt);
+  if (st) return st;
+
+  PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
+  a.src0 = ctx->p(L.feat[nxt]);
+  a.C0 = C;
+  a.dst = d_frame_out;
+  NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
+  return NCODEC_OK;
+}
+
+// Replaces one pointer in the argument struct of a captured kernel node.
+template <class T, class F>
+hipError_t set_struct_arg(hipGraphExec_t x, hipGraphNode_t n, F&& edit) {
+  hipKernelNodeParams p;
+  hipError_t e = hipGraphKernelNodeGetParams(n, &p);
+  if (e != hipSuccess) return e;
+  if (!p.kernelParams) return hipErrorInvalidValue;
+  T v;
+  std::memcpy(&v, p.kernelParams[0], sizeof(T));
+  edit(v);
+  void* args[1] = {&v};
+  p.kernelParams = args;
+  p.extra = nullptr;
+  return hipGraphExecKernelNodeSetParams(x, n, &p);
+}
+
+hipError_t set_reduce_out(hipGraphExec_t x, hipGraphNode_t n, double* out) {
+  hipKernelNodeParams p;
+  hipError_t e = hipGraphKernelNodeGetParams(n, &p);
+  if (e != hipSuccess) return e;
+  if (!p.kernelParams) return hipErrorInvalidValue;
+  const double* part = *(const double* const*)p.kernelParams[0];
+  int np = *(const int*)p.kernelParams[1];
+  void* args[3] = {&part, &np, &out};
+  p.kernelParams = args;
+  p.extra = nullptr;
+  return hipGraphExecKernelNodeSetParams(x, n, &p);
+}
+
+// Points the caller-buffer nodes of a captured graph at this call's buffers:
+// encode ptr = {frame, q, bits}, decode ptr = {q, frame_out}.
+hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, const void* const* ptr) {
+  hipError_t e = hipSuccess;
+  for (const auto& cn : gs.nodes) {
+    if (e != hipSuccess) break;
+    if (!decode && !std::strcmp(cn.kind, "embed") && ptr[0] != gs.ptr[0]) {
+      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.src0 = ptr[0]; });
+    } else if (!std::strcmp(cn.kind, "prior") && ptr[decode ? 0 : 1] != gs.ptr[decode ? 0 : 1]) {
+      int16_t* q = (int16_t*)ptr[decode ? 0 : 1];
+      if (ctx->is_int())
+        e = set_struct_arg<PriorArgs>(gs.exec, cn.node, [&](PriorArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
+      else
+        e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
+    } else if (!decode && !std::strcmp(cn.kind, "reduce") && ptr[2] != gs.ptr[2]) {
+      e = set_reduce_out(gs.exec, cn.node, (double*)ptr[2]);
+    } else if (decode && !std::strcmp(cn.kind, "recon") && ptr[1] != gs.ptr[1]) {
+      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.dst = (void*)ptr[1]; });
+    }
+  }
+  if (e == hipSuccess) for (int i = 0; i < 3; ++i) gs.ptr[i] = ptr[i];
+  return e;
+}
+
+// Runs one encode or decode as a graph replay: the first call for a state
+// parity captures the launch sequence (on a private stream, so the caller's
+// stream may be the null stream), later calls only retarget caller buffers.
+ncodec_status run_graph(ncodec_ctx* ctx, bool decode, const void* p0, const void* p1, const void* p2) {
+  ncodec_ctx::GraphSlot& gs = ctx->graphs[decode][ctx->cur];
+  const void* ptr[3] = {p0, p1, p2};
+  if (!gs.exec) {
+    if (!ctx->cap_stream) NC_HIP(ctx, hipStreamCreateWithFlags(&ctx->cap_stream, hipStreamNonBlocking), "capture stream");
+    const hipStream_t user = ctx->stream;
+    ctx->stream = ctx->cap_stream;
+    gs.nodes.clear();
+    ctx->capturing = &gs.nodes;
+    hipError_t e = hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal);
+    ncodec_status st = NCODEC_OK;
+    if (e == hipSuccess) {
+      st = decode ? enqueue_decode(ctx, (const int16_t*)p0, (void*)p1)
+                  : enqueue_encode(ctx, p0, (int16_t*)p1, (double*)p2);
+      hipGraph_t g = nullptr;
+      const hipError_t e2 = hipStreamEndCapture(ctx->cap_stream, &g);
+      gs.graph = g;
+      if (e2 != hipSuccess && st == NCODEC_OK) st = hip_fail(ctx, e2, "graph capture");
+    } else {
+      st = hip_fail(ctx, e, "begin graph capture");
+    }
+    ctx->capturing = nullptr;
+    ctx->stream = user;
+    if (st == NCODEC_OK) {
+      e = hipGraphInstantiate(&gs.exec, gs.graph, nullptr, nullptr, 0);
+      if (e != hipSuccess) st = hip_fail(ctx, e, "graph instantiate");
+    }
+    if (st != NCODEC_OK) {
+      if (gs.graph) (void)hipGraphDestroy(gs.graph);
+      gs = ncodec_ctx::GraphSlot{};
+      return st;
+    }
+    for (int i = 0; i < 3; ++i) gs.ptr[i] = ptr[i];
+  } else {
+    NC_HIP(ctx, retarget(ctx, gs, decode, ptr), "graph update");
+  }
+  NC_HIP(ctx, hipGraphLaunch(gs.exec, ctx->stream), "graph launch");
+  return NCODEC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -548,68 +769,13 @@ ncodec_status ncodec_encode_frame(ncodec_ctx* ctx, const void* d_frame, int16_t*
   if (st) return st;
   if (!d_frame || !d_q) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be non-NULL");
   if ((uintptr_t)d_frame % 16 || (uintptr_t)d_q % 16) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be 16-byte aligned");
-  const ncodec_config& c = ctx->cfg;
-  const int C = c.channels;
-  const int h8 = c.height / 8, w8 = c.width / 8;
-  const int P8 = h8 * w8, P16 = P8 / 4;
-  const Layout& L = ctx->L;
-  const int cur = ctx->cur, nxt = 1 - cur;
-
-  PwArgs a = conv_args(ctx, L.pe, 192, C, P8);
-  a.src0 = d_frame;
-  a.dst = ctx->p(L.ed);
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "embed", LD_FRAME, EP_NHWC, a), "patch embed");
-
-  void* z = ctx->p(L.zA);
-  a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
-  a.src0 = ctx->p(L.ed);
-  a.C0 = C;
-  a.src1 = ctx->p(L.feat[cur]);
-  a.C1 = C;
-  a.dst = z;
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_enc");
-
-  for (int k = 0; k < c.n_enc_blocks; ++k) {
-    void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
-    const BlockDev& b = L.enc[k];
-    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
-                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
-                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
-    NC_HIP(ctx, dcblock(ctx, ba), "encoder block");
-    z = dst;
-  }
-
-  a = conv_args(ctx, L.down, 4 * C, C, P16);
-  a.src0 = z;
-  a.Csrc = C;
-  a.dst = ctx->p(L.y);
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
-
-  PriorArgs pa;
-  std::memset(&pa, 0, sizeof(pa));
-  pa.wfrag = ctx->p(L.head.w);
-  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
-  pa.bias = ctx->p(L.head.bias);
-  pa.yhat_prev = ctx->p(L.yhat[cur]);
-  pa.y = ctx->p(L.y);
-  pa.q_out = d_q;
-  pa.yhat_new = ctx->p(L.yhat[nxt]);
-  pa.partials = ctx->p<double>(L.partials);
-  pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
-  pa.C = C;
-  pa.P = P16;
-  pa.decode = 0;
-  int np = 0;
-  NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
-  if (d_bits)
-    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(pa.partials, np, d_bits, ctx->stream); }), "bits reduce");
-
-  st = run_decoder(ctx, nxt);
-  if (st) return st;
-  ctx->cur = nxt;
+  ncodec_status st2;
+  if (ctx->use_graphs && !ctx->timing)
+    st2 = run_graph(ctx, false, d_frame, d_q, d_bits ? (const void*)d_bits : ctx->p(ctx->L.spare_bits));
+  else
+    st2 = enqueue_encode(ctx, d_frame, d_q, d_bits);
+  if (st2) return st2;
+  ctx->cur = 1 - ctx->cur;
   return NCODEC_OK;
 }
 
@@ -619,33 +785,13 @@ ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_f
   if (!d_q || !d_frame_out) return fail(ctx, NCODEC_EINVAL, "d_q and d_frame_out must be non-NULL");
   if ((uintptr_t)d_frame_out % 16 || (uintptr_t)d_q % 16)
     return fail(ctx, NCODEC_EINVAL, "d_q and d_frame_out must be 16-byte aligned");
-  const ncodec_config& c = ctx->cfg;
-  const int C = c.channels;
-  const int P8 = (c.height / 8) * (c.width / 8), P16 = P8 / 4;
-  const Layout& L = ctx->L;
-  const int cur = ctx->cur, nxt = 1 - cur;
-
-  PriorArgs pa;
-  std::memset(&pa, 0, sizeof(pa));
-  pa.wfrag = ctx->p(L.head.w);
-  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
-  pa.bias = ctx->p(L.head.bias);
-  pa.yhat_prev = ctx->p(L.yhat[cur]);
-  pa.q_in = d_q;
-  pa.yhat_new = ctx->p(L.yhat[nxt]);
-  pa.C = C;
-  pa.P = P16;
-  pa.decode = 1;
-  NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
-  st = run_decoder(ctx, nxt);
-  if (st) return st;
-
-  PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
-  a.src0 = ctx->p(L.feat[nxt]);
-  a.C0 = C;
-  a.dst = d_frame_out;
-  NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
-  ctx->cur = nxt;
+  ncodec_status st2;
+  if (ctx->use_graphs && !ctx->timing)
+    st2 = run_graph(ctx, true, d_q, d_frame_out, nullptr);
+  else
+    st2 = enqueue_decode(ctx, d_q, d_frame_out);
+  if (st2) return st2;
+  ctx->cur = 1 - ctx->cur;
   return NCODEC_OK;
 }
 
@@ -685,6 +831,13 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   if (!ctx) return 0;
   if (decode) return 4 + ctx->cfg.n_dec_blocks;
   return 7 + ctx->cfg.n_enc_blocks + ctx->cfg.n_dec_blocks;
+}
+
+ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  ctx->use_graphs = enable != 0;
+  return NCODEC_OK;
 }
 
 ncodec_status ncodec_timing_enable(ncodec_ctx* ctx, int32_t enable) {
@@ -749,6 +902,12 @@ void ncodec_destroy(ncodec_ctx* ctx) {
     if (t.start) (void)hipEventDestroy(t.start);
     if (t.stop) (void)hipEventDestroy(t.stop);
   }
+  for (auto& row : ctx->graphs)
+    for (auto& gs : row) {
+      if (gs.exec) (void)hipGraphExecDestroy(gs.exec);
+      if (gs.graph) (void)hipGraphDestroy(gs.graph);
+    }
+  if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
   delete ctx;
 }
 

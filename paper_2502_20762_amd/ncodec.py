@@ -64,6 +64,7 @@ _SIGNATURES = {
     "ncodec_set_state": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_kernels_per_frame": (ctypes.c_int32, [_P, ctypes.c_int32]),
     "ncodec_timing_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "ncodec_graph_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
     "ncodec_timing_read": (ctypes.c_int, [_P, ctypes.POINTER(ncodec_kernel_timing), ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_int32)]),
     "ncodec_last_error": (ctypes.c_char_p, [_P]),
@@ -151,6 +152,10 @@ def ncodec_kernels_per_frame(ctx, decode: bool) -> int:
 
 def ncodec_timing_enable(ctx, enable: bool) -> None:
     _check(load_library().ncodec_timing_enable(ctx, 1 if enable else 0), ctx)
+
+
+def ncodec_graph_enable(ctx, enable: bool) -> None:
+    _check(load_library().ncodec_graph_enable(ctx, 1 if enable else 0), ctx)
 
 
 def ncodec_timing_read(ctx) -> dict:
@@ -246,6 +251,9 @@ class Codec:
 
     def timing(self, enable: bool):
         ncodec_timing_enable(self.ctx, enable)
+
+    def graphs(self, enable: bool):
+        ncodec_graph_enable(self.ctx, enable)
 
     def timing_read(self) -> dict:
         return ncodec_timing_read(self.ctx)
