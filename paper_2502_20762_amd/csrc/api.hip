@@ -290,14 +290,10 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   // packed k' = (2i + j) * C + c  <-  source column c * 4 + 2i + j
   L.down = pk.gemm(dn_w, dn_b, C, 4 * C, 4 * C, [](int n) { return n; }, [C](int k) { return (k % C) * 4 + k / C; });
   const float* hd_w = take((size_t)2 * C * C); const float* hd_b = take(2 * C);
-  if (is_int) {
-    L.head = pk.plain(hd_w, hd_b, 2 * C, C);
-  } else {
-    // packed row n' = 64 t + r: mu row 32 t + r (r < 32), else s row C + 32 t + r - 32
-    L.head = pk.gemm(hd_w, hd_b, 2 * C, C, C,
-                     [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
-                     [](int k) { return k; });
-  }
+  // packed row n' = 64 t + r: mu row 32 t + r (r < 32), else s row C + 32 t + r - 32
+  L.head = pk.gemm(hd_w, hd_b, 2 * C, C, C,
+                   [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
+                   [](int k) { return k; });
   const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
   // packed row n' = sp * C + c  <-  source row 4c + sp
   L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });
@@ -639,10 +635,7 @@ hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, con
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.src0 = ptr[0]; });
     } else if (!std::strcmp(cn.kind, "prior") && ptr[decode ? 0 : 1] != gs.ptr[decode ? 0 : 1]) {
       int16_t* q = (int16_t*)ptr[decode ? 0 : 1];
-      if (ctx->is_int())
-        e = set_struct_arg<PriorArgs>(gs.exec, cn.node, [&](PriorArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
-      else
-        e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
+      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
     } else if (!decode && !std::strcmp(cn.kind, "reduce") && ptr[2] != gs.ptr[2]) {
       e = set_reduce_out(gs.exec, cn.node, (double*)ptr[2]);
     } else if (decode && !std::strcmp(cn.kind, "recon") && ptr[1] != gs.ptr[1]) {

@@ -2,12 +2,11 @@
 //
 // k_pw_f16      pointwise / patch-embed / 2x2-s2 / upsample / reconstruction
 //               contractions (out^T = W * act^T + b) with gather-on-load and
-//               scatter-on-store, one wave = 32 pixels x NT output channels.
-// k_dcblock_f16 one whole DC block (Supp. B.1): depthwise 3x3 computed into
-//               registers, pw C->2C + LeakyReLU chained into pw 2C->C through
-//               registers 32 hidden channels at a time, residual add.
-// k_prior_f16   1x1 prior head on yhat_{t-1}, quantiser, yhat_t and the
-//               per-tile bit partial sums (Fig. 4 "Q", Supp. B.2).
+//               scatter-on-store, and the prior head with the quantiser and
+//               the bit partial sums as its epilogue (Fig. 4 "Q", Supp. B.2).
+// k_dcblock_f16 one whole DC block (Supp. B.1): depthwise 3x3, pw C->2C +
+//               LeakyReLU chained into pw 2C->C through registers 32 hidden
+//               channels at a time, residual add.
 #include "common.hpp"
 #include "internal.hpp"
 

@@ -14,6 +14,8 @@
 #include "common.hpp"
 #include "internal.hpp"
 
+#include <cstring>
+
 namespace nc {
 
 // clip(RHE(a / 8192)) for any int32 a.  |a| >= 2^28 saturates either way, so a
@@ -196,6 +198,24 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(intx4*)(ob + row * (NT * 4) + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
       }
   }
+  // prior head: a pass covers channels c0 .. c0+31 (rows 0-31 mu_i, 32-63 s_i);
+  // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
+  const int c0 = n0 / 2;
+  int16_t* qt = (int16_t*)st2;
+  if constexpr (EPI == EP_PRIOR_DEC) {
+    static_assert(NT == 64, "prior passes are 64 rows");
+    const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
+    const int p0 = tile * 128 + 8 * k;
+    const int16_t* src = a.q_in + (size_t)(c0 + ch) * a.P + p0;
+    shortx8 v = {};
+    if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+      v = *(const shortx8*)src;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p0 + e < a.P ? src[e] : (short)0;
+    }
+    *(shortx8*)(qt + ch * 128 + 8 * k) = v;
+  }
   lds_barrier();
 
   auto parked = [&](int px, int nl8, int* v) {
@@ -207,7 +227,60 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { v[e] = o0[e]; v[4 + e] = o1[e]; }
   };
   constexpr int UNITS = 128 * (NT / 8);
-  if constexpr (EPI == EP_REC) {
+  if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
+    // thread = (pixel px, 8 channels g8): q = RHE((y_i - mu_i) / 512),
+    // yhat_i = clip(512 q + mu_i), sigma from the table at s_i
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    const int c = c0 + 8 * g8;
+    int mu[8], sv[8];
+    parked(px, g8, mu);
+    parked(px, 4 + g8, sv);
+    if constexpr (EPI == EP_PRIOR) {
+      double bsum = 0.0;
+      shortx8 yv = {};
+      if (gp < a.P) yv = *(const shortx8*)((const int16_t*)a.y + (size_t)gp * a.Cdst + c);
+      shortx8 yh;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int q = rhe_shift((int)yv[e] - mu[e], 9);
+        qt[(8 * g8 + e) * 128 + px] = (int16_t)q;
+        yh[e] = (short)clip16(512 * q + mu[e]);
+        if (gp < a.P) bsum += (double)symbol_bits((float)q, a.sigma_tab[sv[e] + 32768]);
+      }
+      if (gp < a.P) *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c) = yh;
+      __shared__ double red[8];
+      bsum = wave_sum(bsum);
+      if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = bsum;
+      lds_barrier();
+      {
+        const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
+        const int p0 = tile * 128 + 8 * k;
+        const shortx8 v = *(const shortx8*)(qt + ch * 128 + 8 * k);
+        int16_t* dq = a.q_out + (size_t)(c0 + ch) * a.P + p0;
+        if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+          *(shortx8*)dq = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (p0 + e < a.P) dq[e] = v[e];
+        }
+      }
+      if (threadIdx.x == 0) {
+        double t = 0.0;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) t += red[w];
+        a.partials[(size_t)tile * npass + n0 / NT] = t;
+      }
+    } else {
+      if (gp < a.P) {
+        shortx8 yh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) yh[e] = (short)clip16(512 * (int)qt[(8 * g8 + e) * 128 + px] + mu[e]);
+        *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c) = yh;
+      }
+    }
+  } else if constexpr (EPI == EP_REC) {
 #pragma unroll
     for (int it = 0; it < UNITS / 512; ++it) {
       const int idx = it * 512 + threadIdx.x;
@@ -613,104 +686,6 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   }
 }
 
-// Integer prior head, quantiser q = round((y_i - mu_i) / 512), yhat = clip(512 q + mu_i)
-// and bits with sigma looked up from the 65536-entry table indexed by s_i.
-template <int CH, bool DECODE>
-__global__ __launch_bounds__(256) void k_prior_i16(PriorArgs a) {
-  constexpr int MT = CH / 32;
-  const int ntile = (a.P + 127) / 128;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  if (tile >= ntile) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5;
-  const int p = tile * 128 + wave * 32 + (lane & 31);
-  const bool valid = p < a.P;
-  const int C = a.C;
-  const int ct0 = blockIdx.y * MT;
-  const int ks = C / 32;
-  const intx4* wh = (const intx4*)a.wfrag;
-  const intx4* wl = (const intx4*)a.wfrag_lo;
-  const int16_t* yp = (const int16_t*)a.yhat_prev;
-
-  intx16 mhh[MT], mmid[MT], mll[MT], shh[MT], smid[MT], sll[MT];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    mhh[t] = intx16{}; mmid[t] = intx16{}; mll[t] = intx16{};
-    shh[t] = intx16{}; smid[t] = intx16{}; sll[t] = intx16{};
-  }
-  for (int s = 0; s < ks; ++s) {
-    intx4 bh = {}, bl = {};
-    if (valid) {
-      const int16_t* ptr = yp + (size_t)p * C + 32 * s + 16 * h;
-      const intx4 q0 = *(const intx4*)ptr, q1 = *(const intx4*)(ptr + 8);
-      uint32_t d[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
-      split16(d, bh, bl);
-    }
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      size_t idx = ((size_t)(ct0 + t) * ks + s) * 64 + lane;
-      intx4 xa = wh[idx], xb = wl[idx];
-      mhh[t] = mfma_i8(xa, bh, mhh[t]);
-      mmid[t] = mfma_i8(xa, bl, mmid[t]);
-      mmid[t] = mfma_i8(xb, bh, mmid[t]);
-      mll[t] = mfma_i8(xb, bl, mll[t]);
-      if constexpr (!DECODE) {
-        idx = ((size_t)(C / 32 + ct0 + t) * ks + s) * 64 + lane;
-        xa = wh[idx];
-        xb = wl[idx];
-        shh[t] = mfma_i8(xa, bh, shh[t]);
-        smid[t] = mfma_i8(xa, bl, smid[t]);
-        smid[t] = mfma_i8(xb, bh, smid[t]);
-        sll[t] = mfma_i8(xb, bl, sll[t]);
-      }
-    }
-  }
-
-  const int* corr = (const int*)a.bias;
-  double bsum = 0.0;
-  if (valid) {
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = 32 * (ct0 + t) + 8 * g + 4 * h;
-        const intx4 cm = *(const intx4*)(corr + c);
-        shortx4 yh;
-        if constexpr (DECODE) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * g + e;
-            const int mu = rescale13(combine_i16(mhh[t][r], mmid[t][r], mll[t][r], cm[e]));
-            const int q = a.q_in[(size_t)(c + e) * a.P + p];
-            yh[e] = (short)clip16(512 * q + mu);
-          }
-        } else {
-          const intx4 cs = *(const intx4*)(corr + C + c);
-          const shortx4 yv = *(const shortx4*)((const int16_t*)a.y + (size_t)p * C + c);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * g + e;
-            const int mu = rescale13(combine_i16(mhh[t][r], mmid[t][r], mll[t][r], cm[e]));
-            const int sv = rescale13(combine_i16(shh[t][r], smid[t][r], sll[t][r], cs[e]));
-            const int q = rhe_shift((int)yv[e] - mu, 9);
-            a.q_out[(size_t)(c + e) * a.P + p] = (int16_t)q;
-            yh[e] = (short)clip16(512 * q + mu);
-            bsum += (double)symbol_bits((float)q, a.sigma_tab[sv + 32768]);
-          }
-        }
-        *(shortx4*)((int16_t*)a.yhat_new + (size_t)p * C + c) = yh;
-      }
-    }
-  }
-  if constexpr (DECODE) return;
-  __shared__ double red[4];
-  bsum = wave_sum(bsum);
-  if (lane == 0) red[wave] = bsum;
-  __syncthreads();
-  if (threadIdx.x == 0) a.partials[(size_t)tile * gridDim.y + blockIdx.y] = ((red[0] + red[1]) + red[2]) + red[3];
-}
-
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
   dim3 grid(grid_tiles(a.P) * (a.N / NT)), block(512);
@@ -724,6 +699,8 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
+  NC_PW(LD_NHWC, EP_PRIOR)
+  NC_PW(LD_NHWC, EP_PRIOR_DEC)
 #undef NC_PW
   return hipErrorInvalidValue;
 }
@@ -747,14 +724,34 @@ hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-int prior_partials_i16(int C, int P) { return grid_tiles(P) * (C / 64); }
+// Integer prior head, quantiser q = RHE((y_i - mu_i) / 512),
+// yhat_i = clip(512 q + mu_i) and bits with sigma looked up from the
+// 65536-entry table indexed by s_i (Supp. B.2, Alg. 1), as the epilogue of the
+// pointwise kernel over passes of 32 mu rows + the 32 s rows of the same
+// channels.  Bit partial sums: one per (tile, pass).
+int prior_partials_i16(int C, int P) { return ((P + 127) / 128) * (C / 32); }
 
-hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials) {
-  dim3 grid(grid_tiles(a.P), a.C / 64), block(256);
-  if (n_partials) *n_partials = ((a.P + 127) / 128) * (a.C / 64);
-  if (a.decode) launch(k_prior_i16<64, true>, grid, block, st, a);
-  else launch(k_prior_i16<64, false>, grid, block, st, a);
-  return hipGetLastError();
+hipError_t launch_prior_i16(const PriorArgs& pa, hipStream_t st, int* n_partials) {
+  if (pa.C % 32) return hipErrorInvalidValue;
+  PwArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.wfrag = pa.wfrag;
+  a.wfrag_lo = pa.wfrag_lo;
+  a.bias = pa.bias;
+  a.K = pa.C;
+  a.N = 2 * pa.C;
+  a.P = pa.P;
+  a.src0 = pa.yhat_prev;
+  a.C0 = pa.C;
+  a.dst = pa.yhat_new;
+  a.Cdst = pa.C;
+  a.y = pa.y;
+  a.q_in = pa.q_in;
+  a.q_out = pa.q_out;
+  a.partials = pa.partials;
+  a.sigma_tab = pa.sigma_tab;
+  if (n_partials) *n_partials = prior_partials_i16(pa.C, pa.P);
+  return pw_dispatch<64>(LD_NHWC, pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
 }
 
 }  // namespace nc
