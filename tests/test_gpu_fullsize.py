@@ -1,6 +1,7 @@
-"""Full-size (1920x1088, C = 256, 8 + 8 blocks) parity, in the configuration bench.py times.
+"""Full-size parity in the configuration bench.py times: 1920x1088 (fp16 and int16)
+and 3840x2176 (fp16), C = 256, 8 + 8 blocks.
 
-The GPU codes whole 1080p frames.  The oracle recomputes sampled regions: every output
+The GPU codes whole frames.  The oracle recomputes sampled regions: every output
 of the transform depends only on inputs within a bounded neighbourhood (each 3x3
 depthwise conv widens it by one pixel at 1/8 scale; everything else is 1x1, 2x2/s2 or
 a pixel shuffle), so the oracle run on a crop of the frame and of the GPU's state
@@ -21,12 +22,15 @@ from parity_util import assert_close_fp16, check_fp16_encode, params_for
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
 DEV = "cuda:0"
-PRE = synth.PRESETS["hd1080"]
-H, W, C, NE, ND = PRE.height, PRE.width, PRE.channels, PRE.n_enc, PRE.n_dec
-H16, W16 = H // 16, W // 16
 S = 28        # crop size in latent (1/16) pixels
 MARGIN = 10   # latent pixels discarded at crop borders interior to the frame
-CROPS = [(0, 0), (H16 - S, W16 - S), (20, 46)]  # top-left corner, bottom-right corner, interior
+
+
+def geometry(pre):
+    H16, W16 = pre.height // 16, pre.width // 16
+    # top-left corner, bottom-right corner, an interior crop
+    crops = [(0, 0), (H16 - S, W16 - S), (H16 // 3, W16 // 2 - 14)]
+    return pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec, H16, W16, crops
 
 
 def say(*a):
@@ -38,7 +42,7 @@ def host(t):
     return t.cpu().numpy()
 
 
-def crop_views(Y0, X0):
+def crop_views(Y0, X0, H16, W16):
     """Slices of the crop inside the full arrays, and of the valid region inside the crop."""
     lo_y = MARGIN if Y0 > 0 else 0
     lo_x = MARGIN if X0 > 0 else 0
@@ -49,16 +53,17 @@ def crop_views(Y0, X0):
     return full, valid
 
 
-def frames():
-    return list(synth.frame_sequence(PRE, 2))
+def frames(pre):
+    return list(synth.frame_sequence(pre, 2))
 
 
 def test_hd1080_int_sampled_bit_exact():
+    H, W, C, NE, ND, H16, W16, CROPS = geometry(synth.PRESETS["hd1080_int"])
     flat, p = params_for(C, NE, ND)
     ip = ci.integerize(p)
     enc = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
     dec = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
-    for t, x in enumerate(frames()):
+    for t, x in enumerate(frames(synth.PRESETS["hd1080_int"])):
         say("int frame", t)
         f0, y0 = (host(v).astype(np.int64) for v in enc.get_state())
         q, _ = enc.encode(torch.from_numpy(x).to(DEV))
@@ -69,7 +74,7 @@ def test_hd1080_int_sampled_bit_exact():
         np.testing.assert_array_equal(e1, y1)
         qh = host(q).astype(np.int64)
         for (Y0, X0) in CROPS:
-            full, valid = crop_views(Y0, X0)
+            full, valid = crop_views(Y0, X0, H16, W16)
             say("  crop", (Y0, X0))
             st = ci.State(f0[(slice(None),) + full["f"]], y0[(slice(None),) + full["l"]])
             r = ci.encode_frame(ip, x[(slice(None),) + full["x"]], st)
@@ -81,12 +86,15 @@ def test_hd1080_int_sampled_bit_exact():
             np.testing.assert_array_equal(xhat[(slice(None),) + full["x"]][sx], xr[sx])
 
 
-def test_hd1080_fp16_sampled_within_tolerance():
+@pytest.mark.parametrize("preset", ["hd1080", "uhd4k"])
+def test_fullsize_fp16_sampled_within_tolerance(preset):
+    pre = synth.PRESETS[preset]
+    H, W, C, NE, ND, H16, W16, CROPS = geometry(pre)
     flat, p = params_for(C, NE, ND)
     enc = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
     dec = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
-    for t, x in enumerate(frames()):
-        say("fp16 frame", t)
+    for t, x in enumerate(frames(pre)):
+        say(preset, "fp16 frame", t)
         f0, y0 = (host(v).astype(np.float64) for v in enc.get_state())
         q, bits = enc.encode(torch.from_numpy(x).to(DEV))
         xhat = host(dec.decode(q)).astype(np.float64)
@@ -96,7 +104,7 @@ def test_hd1080_fp16_sampled_within_tolerance():
         qh = host(q).astype(np.float64)
         assert np.isfinite(float(host(bits)))
         for (Y0, X0) in CROPS:
-            full, valid = crop_views(Y0, X0)
+            full, valid = crop_views(Y0, X0, H16, W16)
             say("  crop", (Y0, X0))
             fp = f0[(slice(None),) + full["f"]]
             yp = y0[(slice(None),) + full["l"]]
@@ -104,6 +112,6 @@ def test_hd1080_fp16_sampled_within_tolerance():
             f_ref, _ = check_fp16_encode(p, x[(slice(None),) + full["x"]], fp, yp,
                                          qh[(slice(None),) + full["l"]], None,
                                          f1[(slice(None),) + full["f"]], y1[(slice(None),) + full["l"]],
-                                         what=f"1080p fp16 t={t} crop {(Y0, X0)}", valid=(sl, sf))
+                                         what=f"{preset} fp16 t={t} crop {(Y0, X0)}", valid=(sl, sf))
             assert_close_fp16(xhat[(slice(None),) + full["x"]][sx], cf.reconstruct(p, f_ref)[sx],
-                              f"1080p fp16 t={t} crop {(Y0, X0)} xhat")
+                              f"{preset} fp16 t={t} crop {(Y0, X0)} xhat")
