@@ -93,6 +93,33 @@ def cpu_baseline(pre, weights, strip_rows):
                       f"of 1080p frame 0 ({dt:.1f} s), scaled by {frac:.3f}; host cpu_count={os.cpu_count()}"}
 
 
+TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "dcblock_hd1080_hbm_traffic.md")
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2502_20762_amd", "csrc")
+SOURCES = {"k_dcblock_f16<256>": ["kernels_f16.hip", "common.hpp", "internal.hpp"],
+           "k_dcblock_i16<256>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
+
+
+def counted_traffic(kernel):
+    """HBM bytes per launch from the committed counter summary (FETCH_SIZE and WRITE_SIZE
+    passes scaled by a plain copy), or None if it is missing or the kernel sources changed
+    since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        h = hashlib.sha256()
+        for f in SOURCES[kernel]:
+            h.update(open(os.path.join(CSRC, f), "rb").read())
+    except (OSError, KeyError):
+        return None
+    for line in text.splitlines():
+        parts = line.split()
+        if len(parts) == 4 and parts[0] == "traffic" and parts[1] == kernel:
+            fields = dict(p.split("=", 1) for p in parts[2:])
+            if fields.get("sources_sha256") == h.hexdigest():
+                return int(fields["bytes_per_launch"])
+    return None
+
+
 def timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch):
     """Encode then decode `steps` frames; per-frame event stamps on the codec stream."""
     stream = torch.cuda.current_stream()
@@ -177,6 +204,9 @@ def main():
     ap.add_argument("--paths", default="fp16,int16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-strip-rows", type=int, default=272)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (3 times), as the reference "
+                         "kernel for scaling hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the per-frame transform runs on a single MI355X "
@@ -187,6 +217,15 @@ def main():
 
     import synth
     from paper_2502_20762_amd.ncodec import Codec
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     pre = synth.PRESETS["hd1080"]
     H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
@@ -202,6 +241,7 @@ def main():
         res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
 
     def summary(path, r, peak_tflops, op_scale, unit):
+        traffic = counted_traffic("k_dcblock_f16<256>" if path == "fp16" else "k_dcblock_i16<256>")
         K = args.steps
         fl, by = kinds["dcblock"]
         kd = r["kernels"]["dcblock"]
@@ -219,7 +259,7 @@ def main():
             "graph_replay": {"value": K / ((ga["enc_ms"] + ga["dec_ms"]) * 1e-3),
                              "encode_fps": K / (ga["enc_ms"] * 1e-3), "decode_fps": K / (ga["dec_ms"] * 1e-3)},
             "roofline": {"kernel": "dcblock", "bound": "mfma", "achieved": achieved, "peak": peak_tflops,
-                         "unit": unit, "frac": achieved / peak_tflops, "traffic": None,
+                         "unit": unit, "frac": achieved / peak_tflops, "traffic": traffic,
                          "per_launch": {"algorithmic_ops": op_scale * fl, "algorithmic_bytes": by,
                                         "avg_us": kd["avg_us"], "launches": kd["launches"]}},
             "frame_roofline_fps": 1.0 / t_roof,
