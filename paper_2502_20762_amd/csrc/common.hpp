@@ -118,7 +118,9 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-__device__ __forceinline__ float leaky(float v) { return v >= 0.f ? v : 0.1f * v; }
+// LeakyReLU with slope 0.1 as max(v, 0.1 v): the same value as the two-branch
+// form for every v (0.1 v <= v exactly when v >= 0), two VALU operations.
+__device__ __forceinline__ float leaky(float v) { return fmaxf(v, 0.1f * v); }
 
 // Gaussian rate of one symbol, -log2(max(L, 1e-9)),
 // L = 1/2 [erfc((|q| - 1/2) / (sigma sqrt2)) - erfc((|q| + 1/2) / (sigma sqrt2))].
