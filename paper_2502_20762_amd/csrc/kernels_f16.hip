@@ -620,7 +620,8 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
         o[e] = (f16)o0[e];
         o[4 + e] = (f16)o1[e];
       }
-      *(half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8) = o;
+      // streaming store: the block's output is read by the next launch, not this one
+      __builtin_nontemporal_store(o, (half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8));
     }
   }
 }

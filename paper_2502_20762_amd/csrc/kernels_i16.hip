@@ -681,7 +681,8 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
         o[e] = (short)clip16((int)zv[e] + (int)p0[e]);
         o[4 + e] = (short)clip16((int)zv[4 + e] + (int)p1[e]);
       }
-      *(shortx8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8) = o;
+      // streaming store: the block's output is read by the next launch, not this one
+      __builtin_nontemporal_store(o, (shortx8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8));
     }
   }
 }
