@@ -538,10 +538,15 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   half8 ones = {};  // B fragment of the bias step: k = 0 is one for every pixel
   if (lane < 32) ones[0] = (f16)1.f;
   half8 wf[KS / 2];  // first half of the next chain's pw1 fragments
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  lds_barrier();  // chunks 0 to 2 staged
-  dc_load_w1<C>(hf == 0 ? wb0 : wb1, lane, wf);  // hf 1: chunk 1, for its chain in iteration 0
-  if (hf == 0) dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0[pg]);
+  // Wait for chunk 0 only (every wave issues at least FR / 8 loads per chunk;
+  // a wave with more waits a little longer): hidden chunk 0 runs while
+  // chunks 1 and 2 are still arriving.
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (DcSmem<C>::FR / 8)) : "memory");
+  lds_barrier();  // chunk 0 staged
+  if (hf == 0) {
+    dc_load_w1<C>(wb0, lane, wf);
+    dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0[pg]);
+  }
   floatx16 out[MT / 2];
   {
     cfloat* b2 = (cfloat*)a.b2;
@@ -557,7 +562,9 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
         }
     }
   }
-  lds_barrier();  // hidden chunk 0 visible
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  lds_barrier();  // chunks 1 and 2 staged, hidden chunk 0 visible
+  if (hf == 1) dc_load_w1<C>(wb1, lane, wf);  // chunk 1, for its chain in iteration 0
 
   auto step = [&](int j, const char* wcur, const char* wnxt, const char* wpre, char* wiss, half8* gcur, half8* gnxt)
                   __attribute__((always_inline)) {
