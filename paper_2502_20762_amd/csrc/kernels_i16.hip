@@ -598,10 +598,11 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 #pragma unroll
   for (int t = 0; t < MT / 2; ++t) out[t] = intx16{};
 
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
-  lds_barrier();  // chunks 0 and 1 staged
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LDS_PER_WAVE) : "memory");
+  lds_barrier();  // chunk 0 staged; hidden chunk 0 runs while chunks 1 and 2 arrive
   if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0[pg]);
-  lds_barrier();
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
+  lds_barrier();  // chunk 1 staged, hidden chunk 0 visible
 
   // The residual tile (128 pixels x C int16, pixel px at byte 2 C px of
   // buffers 0 and 1) is loaded during the last two chunks.
