@@ -67,13 +67,15 @@ def macs_per_frame(H, W, C, ne, nd):
     return sum(kinds[n][0] for n in enc) / 2, sum(kinds[n][0] for n in dec) / 2
 
 
-def cpu_baseline(pre, weights, strip_rows):
-    """Oracle (float64 NumPy) encode + decode of a horizontal strip of the first frame."""
+def cpu_baseline(pre, weights, strip_rows, path="fp16"):
+    """Oracle (NumPy, float64 or exact integers) encode and decode of a horizontal strip
+    of the first frame, timed separately."""
     import numpy as np
 
     import oracle
     import synth
     from oracle import codec_float as cf
+    from oracle import codec_int as ci
 
     try:
         from threadpoolctl import threadpool_info
@@ -82,15 +84,22 @@ def cpu_baseline(pre, weights, strip_rows):
         threads = os.cpu_count()
     p = oracle.unpack(weights, pre.channels, pre.n_enc, pre.n_dec)
     x = next(synth.frame_sequence(pre, 1))[:, :strip_rows, :]
-    st = cf.zero_state(p, strip_rows, pre.width)
+    if path == "int16":
+        m, p = ci, ci.integerize(p)
+    else:
+        m = cf
+    st = m.zero_state(p, strip_rows, pre.width)
     t0 = time.perf_counter()
-    r = cf.encode_frame(p, x, st)
-    cf.decode_frame(p, r.q, st)
-    dt = time.perf_counter() - t0
+    r = m.encode_frame(p, x, st)
+    t1 = time.perf_counter()
+    m.decode_frame(p, r.q, st)
+    t2 = time.perf_counter()
     frac = strip_rows / pre.height
-    return {"value": frac / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"fp16-path oracle (float64 NumPy) encode + decode of the top {strip_rows} of {pre.height} rows "
-                      f"of 1080p frame 0 ({dt:.1f} s), scaled by {frac:.3f}; host cpu_count={os.cpu_count()}"}
+    kind = "float64 NumPy" if path == "fp16" else "exact-integer NumPy"
+    return {"value": frac / (t2 - t0), "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "encode_fps": frac / (t1 - t0), "decode_fps": frac / (t2 - t1),
+            "sample": f"{path}-path oracle ({kind}) encode + decode of the top {strip_rows} of {pre.height} rows "
+                      f"of 1080p frame 0 ({t2 - t0:.1f} s), scaled by {frac:.3f}; host cpu_count={os.cpu_count()}"}
 
 
 TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "dcblock_hd1080_hbm_traffic.md")
@@ -264,6 +273,10 @@ def main():
                                         "avg_us": kd["avg_us"], "launches": kd["launches"]}},
             "frame_roofline_fps": 1.0 / t_roof,
             "frac_of_frame_roofline": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3) * t_roof,
+            "encode_frac_of_roofline": roofline_seconds(kinds, enc_list, peak_tflops * 1e12 / op_scale)
+                                       / (r["enc_ms"] * 1e-3 / K),
+            "decode_frac_of_roofline": roofline_seconds(kinds, dec_list, peak_tflops * 1e12 / op_scale)
+                                       / (r["dec_ms"] * 1e-3 / K),
             "kernels_us": {k: round(v["avg_us"], 2) for k, v in r["kernels"].items()},
             "kernels_per_frame": r["kernels_per_frame"],
             "bits_per_frame": r["bits_per_frame"],
@@ -287,12 +300,16 @@ def main():
         "roofline": s_main["roofline"],
         "frame_roofline_fps": s_main["frame_roofline_fps"],
         "frac_of_frame_roofline": s_main["frac_of_frame_roofline"],
+        "encode_frac_of_roofline": s_main["encode_frac_of_roofline"],
+        "decode_frac_of_roofline": s_main["decode_frac_of_roofline"],
         "kernels_us": s_main["kernels_us"], "kernels_per_frame": s_main["kernels_per_frame"],
     })
     if "int16" in res and main_path != "int16":
         out["int16"] = summary("int16", res["int16"], MFMA_I8_PEAK_TOPS, 4, "TOP/s")
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(pre, weights, args.cpu_strip_rows)
+        out["cpu_baseline"] = cpu_baseline(pre, weights, args.cpu_strip_rows, main_path)
+        if "int16" in out:
+            out["int16"]["cpu_baseline"] = cpu_baseline(pre, weights, args.cpu_strip_rows, "int16")
     print(json.dumps(out), flush=True)
 
 
