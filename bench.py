@@ -212,7 +212,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--paths", default="fp16,int16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-strip-rows", type=int, default=272)
+    ap.add_argument("--cpu-strip-rows", type=int, default=1088)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (3 times), as the reference "
                          "kernel for scaling hardware byte counters")
