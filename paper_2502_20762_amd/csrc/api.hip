@@ -153,15 +153,31 @@ struct Packer {
     const float* b1 = cur; cur += 2 * C;
     const float* w2 = cur; cur += (size_t)2 * C * C;
     const float* b2 = cur; cur += C;
-    d.dww = img.add((size_t)9 * C * 2);
-    d.dwb = img.add((size_t)C * 4);
     if (!is_int) {
-      f16* wp = img.at<f16>(d.dww);
-      float* bp = img.at<float>(d.dwb);
-      for (int t = 0; t < 9; ++t)
-        for (int c = 0; c < C; ++c) wp[t * C + c] = (f16)dw[c * 9 + t];
-      for (int c = 0; c < C; ++c) bp[c] = (float)(f16)dwb[c];
+      // fp16: 48 bytes per channel pair (c, c+1): 9 taps as (w_c, w_c+1) fp16
+      // pairs, the two biases as fp32, one pad word; the block's depthwise
+      // lane for the pair loads it with three 16-byte loads.
+      d.dww = img.add((size_t)C / 2 * 48);
+      d.dwb = d.dww;
+      uint32_t* wp = img.at<uint32_t>(d.dww);
+      for (int p = 0; p < C / 2; ++p) {
+        uint32_t* q = wp + 12 * p;
+        for (int t = 0; t < 9; ++t) {
+          const f16 lo = (f16)dw[(2 * p) * 9 + t], hi = (f16)dw[(2 * p + 1) * 9 + t];
+          uint16_t ul, uh;
+          std::memcpy(&ul, &lo, 2);
+          std::memcpy(&uh, &hi, 2);
+          q[t] = (uint32_t)ul | ((uint32_t)uh << 16);
+        }
+        for (int e = 0; e < 2; ++e) {
+          const float bv = (float)(f16)dwb[2 * p + e];
+          std::memcpy(&q[9 + e], &bv, 4);
+        }
+        q[11] = 0;
+      }
     } else {
+      d.dww = img.add((size_t)9 * C * 2);
+      d.dwb = img.add((size_t)C * 4);
       int16_t* wp = img.at<int16_t>(d.dww);
       int32_t* bp = img.at<int32_t>(d.dwb);
       for (int t = 0; t < 9; ++t)

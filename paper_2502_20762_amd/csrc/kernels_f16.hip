@@ -310,20 +310,20 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
 // the first one.  A hidden chunk (32 channels after bias + LeakyReLU, fp16)
 // goes to LDS in MFMA operand order so both waves of the pair consume it.
 //
-// Weights stream chunk by chunk (chunk j = the pw1 fragments producing hidden
-// DC block.  The weights of one block are streamed in NCH = 2C/32 chunks:
-// chunk j holds the KS = C/16 pw1 fragments of hidden channels 32 j .. +31,
-// their bias as one more fragment (contracted with a constant-one B
-// fragment), then the 2 MT pw2 fragments that consume them (one 1 KiB MFMA A
-// fragment each), into a ring of four LDS buffers with direct global->LDS
-// loads.  The buffers are distinct LDS objects indexed statically (the loop is
-// unrolled by four).
+// The weights of one block are streamed in NCH = 2C/32 chunks: chunk j holds
+// the KS = C/16 pw1 fragments of hidden channels 32 j .. +31, their bias as
+// one more fragment (contracted with a constant-one B fragment), then the 2 MT
+// pw2 fragments that consume them (one 1 KiB MFMA A fragment each), into a
+// ring of four LDS buffers with direct global->LDS loads (the loop is unrolled
+// by four, so every buffer address is static).  The residual is added from
+// LDS in the epilogue, so the prologue only exchanges the filtered channels.
 template <int C>
 struct DcSmem {
   static constexpr int KS = C / 16, MT = C / 32, FR = KS + 1 + 2 * MT, CHUNK = FR * 1024;
 };
 
-// Chunk j -> buf; fragment f is loaded by wave f % 8.
+// Chunk j -> buf; fragment f is loaded by wave f % 8, so every wave issues at
+// least FR / 8 loads.
 template <int C>
 __device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, int wave, int lane) {
   constexpr int FR = DcSmem<C>::FR;
@@ -391,31 +391,66 @@ __device__ __forceinline__ void dc_project(const char* wb, const half8* gx, int 
   }
 }
 
+// Depthwise geometry of the DC block for C channels.  Wave w filters NCW
+// channels (block w % NCB) over NRW tile rows (block w / NCB); lane = channel
+// pair cp (fastest) x column slice colq of CPL columns, so each lane keeps its
+// 9 tap weights in registers and slides a 3 x 3 window over its columns.  The
+// wave's halo band ((NRW + 2) x 18 pixels x NCW channels) sits in its own LDS
+// region: halo pixel hp at position hp ^ ((hp >> 2) & 1), which puts the
+// pixels read by the column slices of one half-wave in different banks when
+// a pixel's slice is shorter than 128 bytes.  With C = 256 a wave takes 64
+// channels (whole 128-byte lines per halo pixel for its direct loads).
+template <int C>
+struct DcDw {
+  static constexpr int NCW = C == 256 ? 64 : C >= 128 ? C / 8 : 16;  // channels per wave
+  static constexpr int NRW = C / NCW;                 // tile rows per wave
+  static constexpr int NCB = C / NCW;                 // channel blocks
+  static constexpr int NCP = NCW / 2;                 // channel pairs
+  static constexpr int NCOLQ = 64 / NCP;              // column slices
+  static constexpr int CPL = 16 / NCOLQ;              // columns per lane
+  static constexpr int BP = (NRW + 2) * 18;           // halo pixels of the band
+  static constexpr int UPP = NCW / 8;                 // 16-byte units per halo pixel
+  static constexpr int SLOTS = BP * UPP;
+  static constexpr int RINSTR = (SLOTS + 63) / 64;    // direct loads per wave for the band
+  static constexpr int RB = SLOTS * 16;               // region bytes
+  static constexpr int XF = 1024 + 16;                // exchange fragment stride (padded against bank conflicts)
+  static constexpr int SPW = NCW / 16;                // 16-channel MFMA steps per wave
+  static_assert(NCB * (8 / NRW) == 8 && NCOLQ * CPL == 16 && BP % 2 == 0 && NRW % 2 == 0, "C in {64, 128, 256}");
+  static_assert(SPW * (NRW / 2) * XF <= RB, "the exchange fits the band's region");
+};
+
+__device__ __forceinline__ int dw_pos(int hp) { return hp ^ ((hp >> 2) & 1); }
+
 template <int C>
 __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
+  using G = DcDw<C>;
   constexpr int KS = DcSmem<C>::KS;
   constexpr int NCH = 2 * C / 32;  // hidden chunks of 32 (a multiple of 4)
   constexpr int MT = DcSmem<C>::MT;
-  constexpr int CHUNK = DcSmem<C>::CHUNK;
-  constexpr int TH = 8, TW = 16;                   // pixel tile (rows x columns at 1/8 scale)
-  constexpr int HW = TW + 2;                       // halo row length
-  // Depthwise role: wave w filters a band of 4 tile rows (sg) for a quarter of
-  // the channels (cq), lane l = pixel (row 4 sg + l / 16, column l % 16).
-  constexpr int NG = C / 32;                 // 8-channel groups per wave (= 16-byte vectors per halo pixel)
-  constexpr int NS = NG / 2;                 // 16-channel MFMA steps per wave
-  constexpr int BPX = 6 * HW;                // halo pixels of a 4-row band
-  constexpr int RINSTR = (BPX * NG + 63) / 64;  // direct loads per wave for its halo band
-  constexpr int REGION = 16 * 1024;          // per-wave LDS region: halo band, then the exchange
-  constexpr int SWS = NG == 8 ? 0 : NG == 4 ? 1 : 2;  // swizzle: vector v of pixel hp at v ^ ((hp >> SWS) & (NG-1))
-  static_assert(RINSTR * 1024 <= REGION && 2 * NG * 1024 <= REGION, "band and exchange fit a region");
-  static_assert(NG >= 2 && NG <= 8 && NCH % 4 == 0, "C in {64, 128, 256}");
-  constexpr int BUF = CHUNK > 2 * REGION ? CHUNK : 2 * REGION;
-  __shared__ __attribute__((aligned(1024))) char wb0[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb1[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb2[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb3[BUF];
-  __shared__ half8 gx0[4][128];  // [pixel group][2 fragments x 64 lanes], even chunks
-  __shared__ half8 gx1[4][128];  // odd chunks
+  constexpr int FR = DcSmem<C>::FR;
+  constexpr int TH = 8, TW = 16;   // pixel tile (rows x columns at 1/8 scale)
+  constexpr int CH8 = C / 8;       // 16-byte channel vectors per pixel
+  static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
+  // LDS: chunk buffers 0-3, the hidden-chunk buffers, the pw2 bias.  The
+  // eight band regions start after the pw1 part (fragments 0 .. KS) of buffer
+  // 1 and are laid over the rest, which is dead once the filtered channels have
+  // been exchanged.  So chunk 0 and the pw1 part of chunk 1 are loaded from
+  // the start, the pw2 part of chunk 1 after the exchange.  After the loop
+  // buffers 0-1 hold the residual tile and buffers 2-3 the parked output.
+  constexpr int BUF = DcSmem<C>::CHUNK;
+  constexpr int O1 = BUF, O2 = 2 * BUF, O3 = 3 * BUF, OGX = 4 * BUF;
+  constexpr int OR = BUF + (KS + 1) * 1024;  // first band region
+  constexpr int OB2 = (OR + 8 * G::RB > OGX + 16384 ? OR + 8 * G::RB : OGX + 16384);  // pw2 bias (C fp32)
+  constexpr int SMEM = OB2 + 1024;
+  static_assert(SMEM <= 160 * 1024, "fits the LDS of a CU");
+  static_assert(128 * C * 2 <= 2 * BUF && 2 * 32 * C * 2 <= BUF && BUF % 1024 == 0, "residual tile and parked output fit");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  char* const wb0 = smem;
+  char* const wb1 = smem + O1;
+  char* const wb2 = smem + O2;
+  char* const wb3 = smem + O3;
+  half8* const gx0 = (half8*)(smem + OGX);         // [pixel group][2 fragments x 64 lanes], even chunks
+  half8* const gx1 = (half8*)(smem + OGX + 8192);  // odd chunks
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -424,208 +459,248 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   const int ty0 = (tile / tiles_x) * TH, tx0 = (tile % tiles_x) * TW;
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int pg = wave & 3, hf = wave >> 2;                       // MFMA role: 32 pixels, half the outputs
-  const int sg = pg >> 1, cq = (wave & 1) | ((wave >> 2) << 1);  // depthwise role
-  const int cb = cq * (C / 4);
+  const int pg = wave & 3, hf = wave >> 2;  // MFMA role: 32 pixels, half the outputs
   const f16* z = (const f16*)a.src;
   const char* wchunks = (const char*)a.w1;
-  auto bufp = [&](int k) __attribute__((always_inline)) -> char* {
-    return k == 0 ? wb0 : k == 1 ? wb1 : k == 2 ? wb2 : wb3;
-  };
-  // region of the wave with depthwise role (sg, cq): buffer 2 (cq >> 1) + sg, half cq & 1
-  auto region = [&](int sg_, int cq_) __attribute__((always_inline)) -> char* {
-    return bufp(2 * (cq_ >> 1) + sg_) + (cq_ & 1) * REGION;
-  };
-  char* const own = region(sg, cq);
+  auto region = [&](int w_) __attribute__((always_inline)) -> char* { return smem + OR + w_ * G::RB; };
 
-  // Halo band: slot S = 16-byte unit S of the region; pixel hp = S / NG of the
-  // 6 x 18 band, position S % NG holds channel vector (S % NG) ^ swizzle(hp).
-  // Out-of-image pixels and padding slots read the zero row (C zeros).
+  // Depthwise role.
+  const int cbk = wave % G::NCB, rbk = wave / G::NCB;
+  const int cp = lane % G::NCP, colq = lane / G::NCP;
+  const int c0 = cbk * G::NCW + 2 * cp;  // this lane's channels c0, c0 + 1
+  char* const own = region(wave);
+  // this pair's 9 taps (fp16 pairs) and two fp32 biases: 48 bytes per pair
+  half2 wt[9];
+  float bias0, bias1;
+  {
+    // 11 words: a loaded word left unused would be reused as a temporary by
+    // the compiler, which then waits for this load before the band is issued
+    const intx4* wsrc = (const intx4*)a.dww + 3 * (c0 / 2);
+    const intx4 q0 = wsrc[0], q1 = wsrc[1];
+    const intx3 q2 = *(const intx3*)(wsrc + 2);
 #pragma unroll
-  for (int i = 0; i < RINSTR; ++i) {
+    for (int i = 0; i < 4; ++i) {
+      const int x0 = q0[i], x1 = q1[i];
+      wt[i] = __builtin_bit_cast(half2, x0);
+      wt[4 + i] = __builtin_bit_cast(half2, x1);
+    }
+    const int x8 = q2[0], xb0 = q2[1], xb1 = q2[2];
+    wt[8] = __builtin_bit_cast(half2, x8);
+    bias0 = __builtin_bit_cast(float, xb0);
+    bias1 = __builtin_bit_cast(float, xb1);
+  }
+  // pw2 bias to LDS (wave 0, before its band: waited for with the band)
+  if (wave == 0 && lane < C / 4) dma16((const float*)a.b2 + 4 * lane, smem + OB2);
+  // Halo band: slot S = 16-byte unit S of the region holds unit S % UPP of
+  // halo pixel dw_pos(S / UPP); out-of-image pixels read the zero row.
+#pragma unroll
+  for (int i = 0; i < G::RINSTR; ++i) {
     const int S = i * 64 + lane;
-    const int hp = S / NG, v = (S % NG) ^ ((hp >> SWS) & (NG - 1));
-    const int hy = ty0 - 1 + 4 * sg + hp / HW, hx = tx0 - 1 + hp % HW;
-    const bool in = hp < BPX && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-    dma16(in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const f16*)a.zpad, own + i * 1024);
+    if (G::SLOTS % 64 == 0 || S < G::SLOTS) {
+      const int hp = dw_pos(S / G::UPP), u = S % G::UPP;
+      const int hy = ty0 + rbk * G::NRW - 1 + hp / 18, hx = tx0 - 1 + hp % 18;
+      const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+      dma16(in ? z + (size_t)(hy * a.w + hx) * C + cbk * G::NCW + 8 * u : (const f16*)a.zpad, own + i * 1024);
+    }
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band
 
-  // Depthwise 3x3 + bias for 64 pixels x 8 channels per group, weights and
-  // bias wave-uniform (scalar loads); the centre tap is kept as the residual.
-  int tap_off[9];
+  // Chunk 0 and the pw1 part of chunk 1 (consumed after the depthwise) are
+  // requested a few fragments per output row, so that their direct loads,
+  // which the memory pipeline takes one at a time, queue behind the band
+  // instead of ahead of it.  Load m < NP0 is fragment wave + 8 m of chunk 0,
+  // the others fragment wave + 8 (m - NP0) of chunk 1.
+  constexpr int NP0 = (FR + 7) / 8, NP1 = (KS + 1 + 7) / 8;
+  constexpr int PER_ROW = (NP0 + NP1 + G::NRW - 1) / G::NRW;
+  auto issue_early = [&](int n) __attribute__((always_inline)) {
 #pragma unroll
-  for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-    for (int kx = 0; kx < 3; ++kx) {
-      const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
-      tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
-    }
-  chalf8* dww = (chalf8*)((const half8*)a.dww + cb / 8);
-  cfloat* dwb = (cfloat*)((const float*)a.dwb + cb);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band (only this wave reads it)
-  half8 dv[NG], zc[NG];
-#pragma unroll
-  for (int g = 0; g < NG; ++g) {
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = dwb[8 * g + e];
-#pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const half8 zv = *(const half8*)(own + (tap_off[t] ^ (g << 4)));
-      const half8 wv = dww[t * (C / 8) + g];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)wv[e], (float)zv[e], acc[e]);
-      if (t == 4) zc[g] = zv;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dv[g][e] = (f16)acc[e];
-  }
-  // Lanes 0-31 hold pixel group 2 sg, lanes 32-63 group 2 sg + 1.  Swapping
-  // the upper half of group 2p with the lower half of group 2p+1 gives, for
-  // each pixel group, the MFMA B fragment of channels cb + 16 p .. +15
-  // (lanes 0-31: +0..7, lanes 32-63: +8..15).  The band is dead now, so the
-  // fragments overwrite it: [pixel group & 1][step p] for the filtered values,
-  // then the same for the centre taps.
-  auto swap_store = [&](half8* v, int off) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < NS; ++p) {
-      uint32_t* x = (uint32_t*)&v[2 * p];
-      uint32_t* y = (uint32_t*)&v[2 * p + 1];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const auto r2 = __builtin_amdgcn_permlane32_swap(x[i], y[i], false, false);
-        x[i] = r2[0];
-        y[i] = r2[1];
-      }
-      *(half8*)(own + off + p * 1024 + lane * 16) = v[2 * p];
-      *(half8*)(own + off + (NS + p) * 1024 + lane * 16) = v[2 * p + 1];
+    for (int m = n * PER_ROW; m < (n + 1) * PER_ROW && m < NP0 + NP1; ++m) {
+      const int c1 = m >= NP0;
+      const int f = wave + 8 * (c1 ? m - NP0 : m);
+      if (f < (c1 ? KS + 1 : FR))
+        dma16(wchunks + ((size_t)c1 * FR + f) * 1024 + lane * 16, (c1 ? wb1 : wb0) + f * 1024);
     }
   };
-  swap_store(dv, 0);
-  swap_store(zc, NG * 1024);
+  // Depthwise 3x3 + bias: every band value this lane needs first, then the
+  // sliding window (fp32 accumulation), rounded to fp16.
+  half2 v[G::NRW + 2][G::CPL + 2];
+#pragma unroll
+  for (int y = 0; y < G::NRW + 2; ++y)
+#pragma unroll
+    for (int x = 0; x < G::CPL + 2; ++x)
+      v[y][x] = *(const half2*)(own + dw_pos(y * 18 + colq * G::CPL + x) * (G::UPP * 16) + cp * 4);
+  // The filtered pair goes straight to the MFMA B fragment of its pixel group
+  // and 16-channel step, in this wave's region (the band is dead once read):
+  // fragment (row pair j, step i) at (j SPW + i) XF; lane (pixel & 31) +
+  // 32 (bit 3 of the channel), element channel & 7.
+  const int xhalf = (cp >> 2) & 1;
+#pragma unroll
+  for (int rr = 0; rr < G::NRW; ++rr)
+#pragma unroll
+    for (int k = 0; k < G::CPL; ++k) {
+      float a0 = bias0, a1 = bias1;
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const half2 zz = v[rr + ky][k + kx], ww = wt[3 * ky + kx];
+          a0 = fmaf((float)ww[0], (float)zz[0], a0);
+          a1 = fmaf((float)ww[1], (float)zz[1], a1);
+        }
+      half2 o;
+      o[0] = (f16)a0;
+      o[1] = (f16)a1;
+      const int px = 16 * (rr & 1) + colq * G::CPL + k;  // pixel within the 32-pixel group
+      const int f = (rr >> 1) * G::SPW + (cp >> 3);
+      *(half2*)(own + f * G::XF + (px + 32 * xhalf) * 16 + (cp & 3) * 4) = o;
+      if (k == G::CPL - 1) issue_early(rr);
+    }
   lds_barrier();
 
-  // MFMA role: all C filtered channels of this wave's 32 pixels, and the
-  // residual in the layout of its output tiles (tile t = channels
-  // 32 (hf MT/2 + t) .. +31, register 4 g + e = channel 8 g + 4 h + e), which
-  // with the bias initialises the accumulators.
+  // MFMA role: all C filtered channels of this wave's 32 pixels.
   half8 av[KS];
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
-    const char* src = region(sg, s / NS) + ((pg & 1) * NS + s % NS) * 1024;
-    av[s] = *(const half8*)(src + lane * 16);
+    const int wcb = s / G::SPW, wrb = (2 * pg) / G::NRW;  // writer wave's channel and row blocks
+    const int f = (pg - wrb * (G::NRW / 2)) * G::SPW + (s - wcb * G::SPW);
+    av[s] = *(const half8*)(region(wrb * G::NCB + wcb) + f * G::XF + lane * 16);
   }
-  half4 zr[MT / 2][4];  // residual, converted once the first hidden chunk is done
-#pragma unroll
-  for (int t = 0; t < MT / 2; ++t) {
-    const int tt = hf * (MT / 2) + t;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int s = 2 * tt + (g >> 1);  // step holding channels 32 tt + 8 g .. +7
-      const char* src = region(sg, s / NS) + NG * 1024 + ((pg & 1) * NS + s % NS) * 1024;
-      zr[t][g] = *(const half4*)(src + ((lane & 31) + 32 * (g & 1)) * 16 + 8 * h);
-    }
-  }
-  lds_barrier();  // exchange read: the buffers take weight chunks from here on
+  lds_barrier();  // exchange read: the regions take buffers 2, 3 and the hidden chunks from here on
 
   // Pipeline: in iteration j one wave of each pair runs the pw1 chain of
   // hidden chunk j+1 from fragments it loaded in iteration j-1, the other loads
   // the fragments of chunk j+2 for its next chain; both project hidden chunk
   // j.  Chunk c sits in buffer c % 4; chunk j+3 is loaded during iteration j.
-  dc_issue<C>(wchunks, 0, wb0, wave, lane);
-  dc_issue<C>(wchunks, 1, wb1, wave, lane);
+  // Chunk 2 is only needed from iteration 1 on: it arrives during hidden
+  // chunk 0 and iteration 0, whose chain for chunk 2 loads its own fragments.
+  // the pw2 part of chunk 1 (2 MT fragments), then chunk 2
+#pragma unroll
+  for (int i = 0; i < (2 * MT + 7) / 8; ++i) {
+    const int f = KS + 1 + wave + 8 * i;
+    if ((2 * MT) % 8 == 0 || f < FR) dma16(wchunks + ((size_t)FR + f) * 1024 + lane * 16, wb1 + f * 1024);
+  }
   dc_issue<C>(wchunks, 2, wb2, wave, lane);
   half8 ones = {};  // B fragment of the bias step: k = 0 is one for every pixel
   if (lane < 32) ones[0] = (f16)1.f;
   half8 wf[KS / 2];  // first half of the next chain's pw1 fragments
-  // Wait for chunk 0 only (every wave issues at least FR / 8 loads per chunk;
-  // a wave with more waits a little longer): hidden chunk 0 runs while
-  // chunks 1 and 2 are still arriving.
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (DcSmem<C>::FR / 8)) : "memory");
-  lds_barrier();  // chunk 0 staged
+  // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + FR / 8) : "memory");
+  lds_barrier();  // chunks 0 and 1 staged
   if (hf == 0) {
     dc_load_w1<C>(wb0, lane, wf);
-    dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0[pg]);
+    dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0 + 128 * pg);
   }
-  floatx16 out[MT / 2];
-  {
-    cfloat* b2 = (cfloat*)a.b2;
+  floatx16 out[MT / 2];  // pw2 accumulators, starting from the bias
 #pragma unroll
-    for (int t = 0; t < MT / 2; ++t) {
-      const int tt = hf * (MT / 2) + t;
+  for (int t = 0; t < MT / 2; ++t) {
+    const int tt = hf * (MT / 2) + t;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+    for (int g = 0; g < 4; ++g) {
+      const floatx4 bv = *(const floatx4*)(smem + OB2 + (32 * tt + 8 * g + 4 * h) * 4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float bv = h ? b2[32 * tt + 8 * g + 4 + e] : b2[32 * tt + 8 * g + e];
-          out[t][4 * g + e] = (float)zr[t][g][e] + bv;
-        }
+      for (int e = 0; e < 4; ++e) out[t][4 * g + e] = bv[e];
     }
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  lds_barrier();  // chunks 1 and 2 staged, hidden chunk 0 visible
   if (hf == 1) dc_load_w1<C>(wb1, lane, wf);  // chunk 1, for its chain in iteration 0
+  lds_barrier();  // hidden chunk 0 visible
 
+  // The residual tile (128 pixels x C fp16; 16-byte unit u of pixel px holds
+  // channel vector u ^ (px & 7); byte b of the tile in buffer 0 below BUF, in
+  // buffer 1 above) is loaded during the last two chunks.
+  auto rtile = [&](int b) __attribute__((always_inline)) -> char* { return b < BUF ? wb0 + b : wb1 + (b - BUF); };
+  auto issue_residual = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < C / 32; ++i) {
+      const int k = wave + 8 * i;  // 1 KiB unit k of the tile
+      const int S = k * 64 + lane;
+      const int px = S / CH8, k8 = (S % CH8) ^ (px & 7);
+      const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
+      const bool in = yy < a.h && xx < a.w;
+      dma16(in ? z + (size_t)(yy * a.w + xx) * C + 8 * k8 : (const f16*)a.zpad, rtile(k * 1024));
+    }
+  };
   auto step = [&](int j, const char* wcur, const char* wnxt, const char* wpre, char* wiss, half8* gcur, half8* gnxt)
                   __attribute__((always_inline)) {
     const bool dma = j + 3 < NCH;
     if (dma) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
     const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
-    const bool prefetch = j + 2 < NCH && hf == (j & 1);
+    const bool prefetch = j >= 1 && j + 2 < NCH && hf == (j & 1);
     floatx16 hacc;
-    if (produce) hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
+    if (produce) {
+      if (j == 1) dc_load_w1<C>(wnxt, lane, wf);  // iteration 0 had no prefetch
+      hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
+    }
+    if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
     dc_project<C>(wcur, gcur, hf, lane, out);
     if (prefetch) dc_load_w1<C>(wpre, lane, wf);
     if (produce) dc_hidden_store(hacc, lane, gnxt);
-    if (dma) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // chunk j+3: prefetched next iteration
+    // chunk j+3 (in iteration 0 also chunk 2), or the residual in the last step
+    if (dma || j == NCH - 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
-    step(j + 0, wb0, wb1, wb2, wb3, gx0[pg], gx1[pg]);
-    step(j + 1, wb1, wb2, wb3, wb0, gx1[pg], gx0[pg]);
-    step(j + 2, wb2, wb3, wb0, wb1, gx0[pg], gx1[pg]);
-    step(j + 3, wb3, wb0, wb1, wb2, gx1[pg], gx0[pg]);
+    step(j + 0, wb0, wb1, wb2, wb3, gx0 + 128 * pg, gx1 + 128 * pg);
+    step(j + 1, wb1, wb2, wb3, wb0, gx1 + 128 * pg, gx0 + 128 * pg);
+    step(j + 2, wb2, wb3, wb0, wb1, gx0 + 128 * pg, gx1 + 128 * pg);
+    step(j + 3, wb3, wb0, wb1, wb2, gx1 + 128 * pg, gx0 + 128 * pg);
   }
 
-  // Epilogue through LDS: each wave parks its 32 px x C/2 results as fp32 in
-  // the buffer of its pixel group (row = pixel, 16-byte chunk k of the row at
-  // k ^ (row & SWZ)); then all threads convert and store whole pixel rows with
-  // coalesced 16-byte stores.
-  static_assert(32 * C * 4 <= BUF, "a pixel group's fp32 output fits one buffer");
-  constexpr int SWZ = (C / 4 - 1) & 31;  // keeps the swizzled chunk inside its row
+  // Epilogue.  The residual enters the accumulators through the MFMA: for
+  // output tile tt, out += E0 z[32 tt .. +15] + E1 z[32 tt + 16 .. +31] with
+  // E0, E1 the two 32 x 16 halves of the identity (exact in fp32), the z
+  // fragments read from the residual tile in B layout.  Then the sums are
+  // rounded once to fp16 and parked in buffers 2 (pixel groups 0, 1) and 3
+  // (groups 2, 3), row = pixel, 8-byte unit u of the row at u ^ (row & 15);
+  // each thread finally stores 8 channels of one pixel with one 16-byte store.
   {
-    char* ob = bufp(pg);
-    const int row = lane & 31;
+    const int row = lane & 31, px = 32 * pg + row;
+    half8 e0, e1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      e0[e] = (f16)(row == 8 * h + e ? 1.f : 0.f);
+      e1[e] = (f16)(row == 16 + 8 * h + e ? 1.f : 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < MT / 2; ++t) {
+      const int tt = hf * (MT / 2) + t;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int k8 = 4 * tt + 2 * q + h;
+        const half8 zb = *(const half8*)rtile((px * CH8 + (k8 ^ (px & 7))) * 16);
+        out[t] = mfma_f16(q ? e1 : e0, zb, out[t]);
+      }
+    }
+    char* ob = (pg < 2 ? wb2 : wb3) + (pg & 1) * (32 * C * 2);
 #pragma unroll
     for (int t = 0; t < MT / 2; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-        floatx4 o;
+        half4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = out[t][4 * g + e];
-        *(floatx4*)(ob + row * (C * 4) + (((cc >> 2) ^ (row & SWZ)) << 4)) = o;
+        for (int e = 0; e < 4; ++e) o[e] = (f16)out[t][4 * g + e];
+        *(half4*)(ob + row * (C * 2) + (((cc >> 2) ^ (row & 15)) << 3)) = o;
       }
   }
   lds_barrier();
-  constexpr int CH8 = C / 8;            // 8-channel chunks per pixel
-  constexpr int PER = 128 * CH8 / 512;  // chunks per thread
+  constexpr int PER = 128 * CH8 / 512;  // 16-byte units per thread
   f16* dst = (f16*)a.dst;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int idx = i * 512 + threadIdx.x;
     const int px = idx / CH8, k8 = idx % CH8;
-    const int gpx = px >> 5, row = px & 31;
-    const int yy = ty0 + 2 * gpx + (row >> 4), xx = tx0 + (row & 15);
+    const int row = px & 31;
+    const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
     if (yy < a.h && xx < a.w) {
-      const char* ob = bufp(gpx);
-      const floatx4 o0 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8) ^ (row & SWZ)) << 4));
-      const floatx4 o1 = *(const floatx4*)(ob + row * (C * 4) + (((2 * k8 + 1) ^ (row & SWZ)) << 4));
+      // units 2 k8 and 2 k8 + 1 are the aligned pair at 2 k8 ^ (row & 14),
+      // in swapped order when row is odd
+      const char* ob = (px < 64 ? wb2 : wb3) + ((px >> 5) & 1) * (32 * C * 2) + row * (C * 2);
+      const half8 pv = *(const half8*)(ob + (((2 * k8) ^ (row & 14)) << 3));
       half8 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        o[e] = (f16)o0[e];
-        o[4 + e] = (f16)o1[e];
+        o[e] = (row & 1) ? pv[4 + e] : pv[e];
+        o[4 + e] = (row & 1) ? pv[e] : pv[4 + e];
       }
       // streaming store: the block's output is read by the next launch, not this one
       __builtin_nontemporal_store(o, (half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8));
