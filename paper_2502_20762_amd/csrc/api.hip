@@ -176,13 +176,26 @@ struct Packer {
         q[11] = 0;
       }
     } else {
-      d.dww = img.add((size_t)9 * C * 2);
-      d.dwb = img.add((size_t)C * 4);
-      int16_t* wp = img.at<int16_t>(d.dww);
-      int32_t* bp = img.at<int32_t>(d.dwb);
-      for (int t = 0; t < 9; ++t)
-        for (int c = 0; c < C; ++c) wp[t * C + c] = q16(dw[c * 9 + t]);
-      for (int c = 0; c < C; ++c) bp[c] = 512 * (int32_t)q16(dwb[c]);
+      // int16: 96 bytes per channel quad (c .. c+3): for each of the 9 taps the
+      // int16 pairs (w_c, w_c+1) and (w_c+2, w_c+3), then the four biases
+      // 512 b (int32), two pad words.
+      d.dww = img.add((size_t)C / 4 * 96);
+      d.dwb = d.dww;
+      uint32_t* wp = img.at<uint32_t>(d.dww);
+      for (int q = 0; q < C / 4; ++q) {
+        uint32_t* o = wp + 24 * q;
+        for (int t = 0; t < 9; ++t)
+          for (int e = 0; e < 2; ++e) {
+            const uint32_t lo = (uint16_t)q16(dw[(4 * q + 2 * e) * 9 + t]);
+            const uint32_t hi = (uint16_t)q16(dw[(4 * q + 2 * e + 1) * 9 + t]);
+            o[2 * t + e] = lo | (hi << 16);
+          }
+        for (int e = 0; e < 4; ++e) {
+          const int32_t bv = 512 * (int32_t)q16(dwb[4 * q + e]);
+          std::memcpy(&o[18 + e], &bv, 4);
+        }
+        o[22] = o[23] = 0;
+      }
     }
     if (!is_int) {
       // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1

@@ -431,38 +431,67 @@ __device__ __forceinline__ void dci_project(const char* wb, const intx4* gx, int
   }
 }
 
+// Depthwise geometry of the integer DC block for C channels: wave w filters
+// NCW channels (block w % NCB) over NRW tile rows (block w / NCB); lane =
+// channel quad cq (fastest) x column slice colq of CPL columns, with its 9
+// tap weights (int16 pairs) in registers and a sliding 3 x 3 window.  The
+// wave's halo band ((NRW + 2) x 18 pixels x NCW channels) sits in its own LDS
+// region, halo pixel hp at position hp ^ ((hp >> SWZ) & 1) so that the column
+// slices of one 16-lane read group hit different banks when a pixel's slice is
+// shorter than 128 bytes.  With C = 256 a wave takes 64 channels (whole
+// 128-byte lines per halo pixel for its direct loads).
+template <int C>
+struct DcDwI {
+  static constexpr int NCW = C == 256 ? 64 : 32;      // channels per wave
+  static constexpr int NRW = C / NCW;                 // tile rows per wave
+  static constexpr int NCB = C / NCW;                 // channel blocks
+  static constexpr int NCQ = NCW / 4;                 // channel quads
+  static constexpr int NCOLQ = 64 / NCQ;              // column slices
+  static constexpr int CPL = 16 / NCOLQ;              // columns per lane
+  static constexpr int SWZ = CPL == 4 ? 2 : 1;
+  static constexpr int BP = (NRW + 2) * 18;           // halo pixels of the band
+  static constexpr int UPP = NCW / 8;                 // 16-byte units per halo pixel
+  static constexpr int SLOTS = BP * UPP;
+  static constexpr int RINSTR = (SLOTS + 63) / 64;    // direct loads per wave for the band
+  static constexpr int RB = SLOTS * 16;               // region bytes
+  static constexpr int XF = 1024 + 16;                // exchange fragment stride (padded against bank conflicts)
+  static constexpr int SPW = NCW / 32;                // 32-channel MFMA steps per wave
+  static_assert(NCB * (8 / NRW) == 8 && NCOLQ * CPL == 16 && NRW % 2 == 0, "C in {64, 128, 256}");
+  static_assert(2 * SPW * (NRW / 2) * XF <= RB, "the exchange fits the band's region");
+};
+
 template <int C>
 __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
+  using G = DcDwI<C>;
   constexpr int KSI = DcSmemI<C>::KSI;
   constexpr int NCH = 2 * C / 32;
   constexpr int MT = DcSmemI<C>::MT;
-  constexpr int CHUNK = DcSmemI<C>::CHUNK;
-  constexpr int LDS_PER_WAVE = DcSmemI<C>::FR / 8;
+  constexpr int FR = DcSmemI<C>::FR;
+  constexpr int LDS_PER_WAVE = FR / 8;
   constexpr int TH = 8, TW = 16;
-  constexpr int HW = TW + 2;
-  // Depthwise role: band sg of 4 tile rows x channel part cp (CP parts of CPC
-  // channels); lane l = pixel (row 4 sg + l / 16, column l % 16).  With C = 64
-  // there are only two parts and waves 4-7 sit the depthwise out.
-  constexpr int CP = C / 32 < 4 ? C / 32 : 4;
-  constexpr int CPC = C / CP;                  // channels per part
-  constexpr int NG = CPC / 8;                  // 8-channel groups (16-byte vectors per halo pixel)
-  constexpr int NS = CPC / 32;                 // 32-channel MFMA steps per part
-  constexpr int BPX = 6 * HW;
-  constexpr int RINSTR = (BPX * NG + 63) / 64;
-  constexpr int REGION = 16 * 1024;
-  constexpr int SWS = NG == 8 ? 0 : 1;         // vector v of pixel hp at v ^ ((hp >> SWS) & (NG-1))
-  static_assert(NG == 4 || NG == 8, "C in {64, 128, 256}");
-  static_assert(RINSTR * 1024 <= REGION && 4 * NS * 1024 <= REGION, "band and exchange fit a region");
-  static_assert(NCH % 4 == 0, "chunk loop is unrolled by four");
-  constexpr int BUF = CHUNK > 2 * REGION ? CHUNK : 2 * REGION;
-  __shared__ __attribute__((aligned(1024))) char wb0[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb1[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb2[BUF];
-  __shared__ __attribute__((aligned(1024))) char wb3[BUF];
-  __shared__ intx4 gx0[4][128];
-  __shared__ intx4 gx1[4][128];
-  __shared__ __attribute__((aligned(16))) int c1s[2 * C];  // pw1 corrections 512 b + 128 sum w
-  __shared__ __attribute__((aligned(16))) int c2s[C];      // pw2 corrections
+  static_assert(NCH % 4 == 0 && FR % 8 == 0, "chunk loop is unrolled by four");
+  // LDS: chunk buffers 0-3, the hidden-chunk buffers, the corrections.  The
+  // eight band regions start after the pw1 part (fragments 0 .. 2 KSI - 1) of
+  // buffer 1 and are laid over the rest, which is dead once the filtered
+  // channels have been exchanged: chunk 0 and the pw1 part of chunk 1 are
+  // loaded from the start, the pw2 part of chunk 1 after the exchange.  After
+  // the loop buffers 0-1 hold the residual tile and buffers 2-3 the parked
+  // output.
+  constexpr int BUF = DcSmemI<C>::CHUNK;
+  constexpr int O1 = BUF, O2 = 2 * BUF, O3 = 3 * BUF, OGX = 4 * BUF;
+  constexpr int OR = BUF + 2 * KSI * 1024;  // first band region
+  constexpr int OC = (OR + 8 * G::RB > OGX + 16384 ? OR + 8 * G::RB : OGX + 16384);
+  constexpr int SMEM = OC + 3 * C * 4;      // c1s: 2 C ints, c2s: C ints
+  static_assert(SMEM <= 160 * 1024, "fits the LDS of a CU");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  char* const wb0 = smem;
+  char* const wb1 = smem + O1;
+  char* const wb2 = smem + O2;
+  char* const wb3 = smem + O3;
+  intx4* const gx0 = (intx4*)(smem + OGX);         // [pixel group][2 fragments x 64 lanes], even chunks
+  intx4* const gx1 = (intx4*)(smem + OGX + 8192);  // odd chunks
+  int* const c1s = (int*)(smem + OC);              // pw1 corrections 512 b + 128 sum w
+  int* const c2s = c1s + 2 * C;                    // pw2 corrections
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -472,22 +501,12 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pg = wave & 3, hf = wave >> 2;
-  const int sg = pg >> 1;
-  const int cp = CP == 4 ? (wave & 1) | ((wave >> 2) << 1) : (wave & 1);
-  const bool dw_on = CP == 4 || wave < 4;
-  const int cb = cp * CPC;
   const int16_t* z = (const int16_t*)a.src;
   const char* wchunks = (const char*)a.w1;
-  auto bufp = [&](int k) __attribute__((always_inline)) -> char* {
-    return k == 0 ? wb0 : k == 1 ? wb1 : k == 2 ? wb2 : wb3;
-  };
-  auto region = [&](int sg_, int cp_) __attribute__((always_inline)) -> char* {
-    return bufp(2 * (cp_ >> 1) + sg_) + (cp_ & 1) * REGION;
-  };
-  char* const own = region(sg, cp);
+  auto region = [&](int w_) __attribute__((always_inline)) -> char* { return smem + OR + w_ * G::RB; };
 
-  // Corrections straight into LDS (waves 0 and 1, before their halo loads;
-  // waited for with those loads and made visible by the exchange barrier).
+  // Corrections straight into LDS (waves 0 and 1, before their bands: waited
+  // for with them and made visible by the exchange barrier).
   if (wave < 2) {
     const int* src = wave == 0 ? (const int*)a.b1 : (const int*)a.b2;
     int* dstl = wave == 0 ? c1s : c2s;
@@ -497,112 +516,152 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
       if (64 * i + lane < n16) dma16(src + 4 * (64 * i + lane), dstl + 4 * 64 * i);
   }
 
-  // Halo band (as in the fp16 block): slot S = 16-byte unit S of the region.
-  if (dw_on) {
+  // Depthwise role.
+  const int cbk = wave % G::NCB, rbk = wave / G::NCB;
+  const int cq = lane % G::NCQ, colq = lane / G::NCQ;
+  char* const own = region(wave);
+  // this quad's 9 taps (int16 pairs) and four 512 b biases: 96 bytes per quad,
+  // 22 words loaded (a loaded word left unused would be reused as a temporary
+  // by the compiler, which then waits for this load before the band is issued)
+  uint32_t wq[18];
+  int bq[4];
+  {
+    const intx4* wsrc = (const intx4*)a.dww + 6 * (cbk * G::NCQ + cq);
 #pragma unroll
-    for (int i = 0; i < RINSTR; ++i) {
-      const int S = i * 64 + lane;
-      const int hp = S / NG, v = (S % NG) ^ ((hp >> SWS) & (NG - 1));
-      const int hy = ty0 - 1 + 4 * sg + hp / HW, hx = tx0 - 1 + hp % HW;
-      const bool in = hp < BPX && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-      dma16(in ? z + (size_t)(hy * a.w + hx) * C + cb + 8 * v : (const int16_t*)a.zpad, own + i * 1024);
+    for (int i = 0; i < 4; ++i) {
+      const intx4 v = wsrc[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int x = v[e];
+        wq[4 * i + e] = (uint32_t)x;
+      }
+    }
+    const intx4 v4 = wsrc[4];
+    const intx2 v5 = *(const intx2*)(wsrc + 5);
+    const int x0 = v4[0], x1 = v4[1], x2 = v4[2], x3 = v4[3], x4 = v5[0], x5 = v5[1];
+    wq[16] = (uint32_t)x0;
+    wq[17] = (uint32_t)x1;
+    bq[0] = x2;
+    bq[1] = x3;
+    bq[2] = x4;
+    bq[3] = x5;
+  }
+  // Halo band: slot S = 16-byte unit S of the region holds unit S % UPP of
+  // halo pixel pos(S / UPP); out-of-image pixels read the zero row.
+  auto pos = [&](int hp) __attribute__((always_inline)) { return hp ^ ((hp >> G::SWZ) & 1); };
+#pragma unroll
+  for (int i = 0; i < G::RINSTR; ++i) {
+    const int S = i * 64 + lane;
+    if (G::SLOTS % 64 == 0 || S < G::SLOTS) {
+      const int hp = pos(S / G::UPP), u = S % G::UPP;
+      const int hy = ty0 + rbk * G::NRW - 1 + hp / 18, hx = tx0 - 1 + hp % 18;
+      const bool in = hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+      dma16(in ? z + (size_t)(hy * a.w + hx) * C + cbk * G::NCW + 8 * u : (const int16_t*)a.zpad, own + i * 1024);
     }
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band (and the corrections)
 
-  if (dw_on) {
-    // Depthwise 3x3: exact int32 sums, one v_mad_i32_i16 per tap and channel
-    // (op_sel picks the low or high int16 of the packed activation and of the
-    // wave-uniform weight pair), bias 512 b_i, rescaled to int16.
-    int tap_off[9];
+  // Chunk 0 and the pw1 part of chunk 1 (consumed after the depthwise) are
+  // requested a few fragments per output row, behind the band.  Load m < NP0
+  // is fragment wave + 8 m of chunk 0, the others fragment wave + 8 (m - NP0)
+  // of chunk 1.
+  constexpr int NP0 = FR / 8, NP1 = (2 * KSI + 7) / 8;
+  constexpr int PER_ROW = (NP0 + NP1 + G::NRW - 1) / G::NRW;
+  auto issue_early = [&](int n) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ky = 0; ky < 3; ++ky)
+    for (int m = n * PER_ROW; m < (n + 1) * PER_ROW && m < NP0 + NP1; ++m) {
+      const int c1 = m >= NP0;
+      const int f = wave + 8 * (c1 ? m - NP0 : m);
+      if (f < (c1 ? 2 * KSI : FR))
+        dma16(wchunks + ((size_t)c1 * FR + f) * 1024 + lane * 16, (c1 ? wb1 : wb0) + f * 1024);
+    }
+  };
+
+  // Depthwise 3x3: every band value this lane needs first (4 channels per
+  // read), then the sliding window with exact int32 sums, one v_mad_i32_i16
+  // per tap and channel (op_sel picks the low or high int16 of the packed
+  // activation and weight), bias 512 b, rescaled to int16.
+  uint32_t v[G::NRW + 2][G::CPL + 2][2];
 #pragma unroll
-      for (int kx = 0; kx < 3; ++kx) {
-        const int hp = ((lane >> 4) + ky) * HW + (lane & 15) + kx;
-        tap_off[ky * 3 + kx] = hp * (NG * 16) + (((hp >> SWS) & (NG - 1)) << 4);
-      }
-    cintx4* dww = (cintx4*)((const int16_t*)a.dww + cb);  // [9][C] int16, 8 per vector
-    cint* dwb = (cint*)((const int*)a.dwb + cb);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's band
-    uint32_t dv[NG][4];
+  for (int y = 0; y < G::NRW + 2; ++y)
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      int acc[8];
+    for (int x = 0; x < G::CPL + 2; ++x) {
+      const intx2 r = *(const intx2*)(own + pos(y * 18 + colq * G::CPL + x) * (G::UPP * 16) + cq * 8);
+      const int r0 = r[0], r1 = r[1];
+      v[y][x][0] = (uint32_t)r0;
+      v[y][x][1] = (uint32_t)r1;
+    }
+  // The filtered quad is split into int8 digits and written straight into the
+  // MFMA B fragments of its pixel group and 32-channel step, in this wave's
+  // region (the band is dead once read): fragment (row pair j, step i, digit
+  // d) at ((j SPW + i) 2 + d) XF; lane (pixel & 31) + 32 (bit 4 of the
+  // channel), word (channel & 15) / 4.
+  const int xhalf = (cq >> 2) & 1;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = dwb[8 * g + e];
+  for (int rr = 0; rr < G::NRW; ++rr)
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const intx4 zv = *(const intx4*)(own + (tap_off[t] ^ (g << 4)));
-        const intx4 wv = dww[(t * C + 8 * g) / 8];
+    for (int k = 0; k < G::CPL; ++k) {
+      int acc[4] = {bq[0], bq[1], bq[2], bq[3]};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int wp = wv[i];
-          const int zi = zv[i];
-          asm("v_mad_i32_i16 %0, %1, %2, %0" : "+v"(acc[2 * i]) : "v"(zi), "s"(wp));
-          asm("v_mad_i32_i16 %0, %1, %2, %0 op_sel:[1,1,0,0]" : "+v"(acc[2 * i + 1]) : "v"(zi), "s"(wp));
+      for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const int t = 3 * ky + kx;
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const uint32_t zz = v[rr + ky][k + kx][e], ww = wq[2 * t + e];
+            asm("v_mad_i32_i16 %0, %1, %2, %0" : "+v"(acc[2 * e]) : "v"(zz), "v"(ww));
+            asm("v_mad_i32_i16 %0, %1, %2, %0 op_sel:[1,1,0,0]" : "+v"(acc[2 * e + 1]) : "v"(zz), "v"(ww));
+          }
         }
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dv[g][i] = pack2(rescale13(acc[2 * i]), rescale13(acc[2 * i + 1]));
-      __builtin_amdgcn_sched_barrier(0);  // one group's weights live at a time
+      uint32_t dh, dl;
+      split4(pack2(rescale13(acc[0]), rescale13(acc[1])), pack2(rescale13(acc[2]), rescale13(acc[3])), dh, dl);
+      const int px = 16 * (rr & 1) + colq * G::CPL + k;  // pixel within the 32-pixel group
+      const int f = ((rr >> 1) * G::SPW + (cq >> 3)) * 2;
+      char* o = own + (px + 32 * xhalf) * 16 + (cq & 3) * 4;
+      *(uint32_t*)(o + f * G::XF) = dh;
+      *(uint32_t*)(o + (f + 1) * G::XF) = dl;
+      if (k == G::CPL - 1) issue_early(rr);
     }
-    // 16-channel unit u = groups 2u, 2u+1 -> hi / lo digit vectors; units 2p and
-    // 2p+1 swap lane halves into the B fragments of step cb / 32 + p for pixel
-    // groups 2 sg (lanes 0-31) and 2 sg + 1; they overwrite the dead band:
-    // [pixel group & 1][step p][hi, lo] x 1 KiB.
-#pragma unroll
-    for (int p = 0; p < NS; ++p) {
-      intx4 xh, xl, yh, yl;
-      {
-        uint32_t d[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { d[i] = dv[4 * p][i]; d[4 + i] = dv[4 * p + 1][i]; }
-        split16(d, xh, xl);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { d[i] = dv[4 * p + 2][i]; d[4 + i] = dv[4 * p + 3][i]; }
-        split16(d, yh, yl);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const auto rh = __builtin_amdgcn_permlane32_swap((uint32_t)xh[i], (uint32_t)yh[i], false, false);
-        xh[i] = (int)rh[0];
-        yh[i] = (int)rh[1];
-        const auto rl = __builtin_amdgcn_permlane32_swap((uint32_t)xl[i], (uint32_t)yl[i], false, false);
-        xl[i] = (int)rl[0];
-        yl[i] = (int)rl[1];
-      }
-      *(intx4*)(own + ((0 * NS + p) * 2 + 0) * 1024 + lane * 16) = xh;
-      *(intx4*)(own + ((0 * NS + p) * 2 + 1) * 1024 + lane * 16) = xl;
-      *(intx4*)(own + ((1 * NS + p) * 2 + 0) * 1024 + lane * 16) = yh;
-      *(intx4*)(own + ((1 * NS + p) * 2 + 1) * 1024 + lane * 16) = yl;
-    }
-  }
-  if (!dw_on) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // corrections (waves 0, 1 are depthwise waves)
   lds_barrier();
 
   // MFMA role: the digit fragments of all C filtered channels of this wave's 32 pixels
   intx4 ah[KSI], al[KSI];
 #pragma unroll
   for (int s = 0; s < KSI; ++s) {
-    const char* src = region(sg, s / NS) + (((pg & 1) * NS + s % NS) * 2) * 1024 + lane * 16;
-    ah[s] = *(const intx4*)src;
-    al[s] = *(const intx4*)(src + 1024);
+    const int wcb = s / G::SPW, wrb = (2 * pg) / G::NRW;  // writer wave's channel and row blocks
+    const int f = ((pg - wrb * (G::NRW / 2)) * G::SPW + (s - wcb * G::SPW)) * 2;
+    const char* src = region(wrb * G::NCB + wcb) + lane * 16;
+    ah[s] = *(const intx4*)(src + f * G::XF);
+    al[s] = *(const intx4*)(src + (f + 1) * G::XF);
   }
-  lds_barrier();  // exchange read: the buffers take weight chunks from here on
+  lds_barrier();  // exchange read: the regions take buffers 2, 3 and the hidden chunks from here on
 
-  dci_issue<C>(wchunks, 0, wb0, wave, lane);
-  dci_issue<C>(wchunks, 1, wb1, wave, lane);
+  // the pw2 part of chunk 1 (2 MT fragments), then chunk 2
+#pragma unroll
+  for (int i = 0; i < (2 * MT + 7) / 8; ++i) {
+    const int f = 2 * KSI + wave + 8 * i;
+    if ((2 * MT) % 8 == 0 || f < FR) dma16(wchunks + ((size_t)FR + f) * 1024 + lane * 16, wb1 + f * 1024);
+  }
   dci_issue<C>(wchunks, 2, wb2, wave, lane);
 
+  // pw2 accumulators start at the correction 512 b + 128 sum w (wrapping int32
+  // addition is associative, so the sum is the same as adding it at the end)
   intx16 out[MT / 2];
 #pragma unroll
-  for (int t = 0; t < MT / 2; ++t) out[t] = intx16{};
+  for (int t = 0; t < MT / 2; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const intx4 cv = *(const intx4*)(c2s + 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[t][4 * g + e] = cv[e];
+    }
 
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LDS_PER_WAVE) : "memory");
-  lds_barrier();  // chunk 0 staged; hidden chunk 0 runs while chunks 1 and 2 arrive
-  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0[pg]);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
-  lds_barrier();  // chunk 1 staged, hidden chunk 0 visible
+  // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + LDS_PER_WAVE) : "memory");
+  lds_barrier();
+  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0 + 128 * pg);
+  lds_barrier();  // hidden chunk 0 visible
 
   // The residual tile (128 pixels x C int16, pixel px at byte 2 C px of
   // buffers 0 and 1) is loaded during the last two chunks.
@@ -635,13 +694,14 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
-    step(j + 0, wb0, wb1, wb3, gx0[pg], gx1[pg]);
-    step(j + 1, wb1, wb2, wb0, gx1[pg], gx0[pg]);
-    step(j + 2, wb2, wb3, wb1, gx0[pg], gx1[pg]);
-    step(j + 3, wb3, wb0, wb2, gx1[pg], gx0[pg]);
+    step(j + 0, wb0, wb1, wb3, gx0 + 128 * pg, gx1 + 128 * pg);
+    step(j + 1, wb1, wb2, wb0, gx1 + 128 * pg, gx0 + 128 * pg);
+    step(j + 2, wb2, wb3, wb1, gx0 + 128 * pg, gx1 + 128 * pg);
+    step(j + 3, wb3, wb0, wb2, gx1 + 128 * pg, gx0 + 128 * pg);
   }
 
-  // Epilogue: rescale(sum + correction) to int16 in registers, parked in
+  // Epilogue: rescale(sum) to int16 in registers (the sums started at the
+  // corrections), parked in
   // buffers 2 (pixel groups 0, 1) and 3 (groups 2, 3), row = pixel, 8-byte unit
   // u of the row at u ^ (row & 15); then each thread adds the residual to 8
   // channels of one pixel with saturation and stores them with one 16-byte store.
@@ -653,10 +713,9 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cc = 32 * (hf * (MT / 2) + t) + 8 * g + 4 * h;
-        const intx4 cv = *(const intx4*)(c2s + cc);
         shortx4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (short)rescale13((int)((uint32_t)out[t][4 * g + e] + (uint32_t)cv[e]));
+        for (int e = 0; e < 4; ++e) o[e] = (short)rescale13(out[t][4 * g + e]);
         *(shortx4*)(ob + row * (C * 2) + (((cc >> 2) ^ (row & 15)) << 3)) = o;
       }
   }
