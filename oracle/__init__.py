@@ -13,12 +13,14 @@ CVPR 2025):
 * ``codec_int``    -- the integerised transform (Sec. 4.5, Eq. 3; Supp. B.4,
                       Alg. 1).
 * ``bits``         -- the Gaussian likelihood / bit estimate.
+* ``entropy``      -- the coder: quantised-scale Gaussian tables and
+                      interleaved rANS streams (Fig. 4 "AE"/"AD", Fig. 6).
 * ``params``       -- its own reading of the canonical flat parameter list.
 
 Parity status of each function is stated in its docstring; every function is
 pinned by ``tests/test_oracle_*.py`` against closed forms, brute force or
 library routines (none is "parity unpinned").
 """
-from . import bits, codec_float, codec_int, ops, params  # noqa: F401
+from . import bits, codec_float, codec_int, entropy, ops, params  # noqa: F401
 from .bits import estimate_bits, likelihood, sigma_from_s  # noqa: F401
 from .params import Params, unpack  # noqa: F401
