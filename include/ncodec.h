@@ -128,6 +128,67 @@ ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_f
 ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const float* d_sigma,
                                    int64_t n, double* d_bits);
 
+/* ---- Entropy coding (Fig. 4 "AE" / "AD", Fig. 6; Supp. B.2) ----------------
+ * The symbols are coded with rANS (Duda 2013; 32-bit state in [2^16, 2^32),
+ * 16-bit words, 16-bit frequencies) under quantised-scale Gaussian tables:
+ * NS = 64 scales sigma_j = fp32(0.11 (256/0.11)^(j/63)); table j codes
+ * q = -R .. R (R = ceil(8 sigma_j)) and an escape for larger |q|, which is
+ * followed by uniform sub-symbols (sign, hex digit count, hex digits of
+ * |q| - R - 1).  Frequencies: f = 1 + floor(p (2^16 - n)) for each of the
+ * n = 2R + 2 symbols of the Gaussian of scale sigma_j, the remainder added at
+ * q = 0.  The scale index of a symbol is the smallest j with
+ * sigma_j >= sigma = max(softplus(s), 0.11) (s the prior's scale output; on the
+ * int path s is an int16 and the index comes from a table of all 65,536
+ * values, so encoder and decoder agree on any device, Sec. 4.5).
+ *
+ * Container (little-endian bytes): u32 magic "NCRS", u32 version 1, u32 number
+ * of symbols, u32 symbols per stream (8192), u32 number of streams, u16 length
+ * in words of each stream, zero padding to 4 bytes, then the streams' 16-bit
+ * words.  A stream's 8192 symbols are coded by 64 interleaved rANS states
+ * (symbol i by state i % 64); it opens with the 64 final states.
+ *
+ * All calls enqueue on the context's stream; byte counts and status words are
+ * device outputs, valid after the stream synchronises.  Buffers must be device
+ * memory; d_stream must be 4-byte aligned. */
+
+/* Worst-case container size in bytes for one frame of cfg (what d_stream
+ * must hold for ncodec_encode_frame_coded).  0 for an invalid cfg. */
+size_t ncodec_stream_capacity(const ncodec_config* cfg);
+
+/* Scale indices (uint8, C x H/16 x W/16 planar) of the symbols of the next
+ * frame, from the current state (the prior head on yhat_{t-1}). */
+ncodec_status ncodec_scale_indices(ncodec_ctx* ctx, uint8_t* d_k);
+
+/* Code n symbols d_q (int16) with scale indices d_k (uint8, values >= 64 are
+ * taken as 63) into the container d_stream (capacity bytes, at least the
+ * worst case for n symbols: ncodec_stream_capacity of a frame with n symbols).
+ * *d_stream_bytes (device u64) receives the container size.
+ * n must be in [1, C H W / 256] of the context's frame.  EINVAL otherwise. */
+ncodec_status ncodec_rans_encode(ncodec_ctx* ctx, const int16_t* d_q, const uint8_t* d_k, int64_t n,
+                                 void* d_stream, size_t capacity, uint64_t* d_stream_bytes);
+
+/* Decode n symbols from a container of stream_bytes bytes with scale indices
+ * d_k into d_q.  *d_status (device int32, may be NULL) receives 0 for a clean
+ * decode, else a bit set: 1 bad or truncated container, 2 a stream ran past
+ * its length, 4 a stream ended in an inconsistent state.  The decoder never
+ * reads outside [d_stream, d_stream + stream_bytes); on error the symbols are
+ * unspecified but written in full. */
+ncodec_status ncodec_rans_decode(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes, const uint8_t* d_k,
+                                 int64_t n, int16_t* d_q, int32_t* d_status);
+
+/* ncodec_encode_frame, then the frame's symbols coded into d_stream
+ * (capacity >= ncodec_stream_capacity(cfg)); *d_stream_bytes (device u64)
+ * receives the container size.  d_q (symbols) and d_bits (estimate) may be
+ * NULL. */
+ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits,
+                                        void* d_stream, size_t capacity, uint64_t* d_stream_bytes);
+
+/* Decode one frame from its container: scale indices from the state, symbols
+ * from the container, then ncodec_decode_frame.  *d_status as for
+ * ncodec_rans_decode (may be NULL); the state advances even on error. */
+ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes,
+                                        void* d_frame_out, int32_t* d_status);
+
 /* Copy the state out of / into the context (enqueued).  d_feat: C x H/8 x W/8
  * planar, d_yhat: C x H/16 x W/16 planar; fp16 (fp16 path) or int16 (int
  * path).  Either pointer may be NULL to skip that tensor. */

@@ -292,12 +292,83 @@ struct Layout {
   ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
   std::vector<BlockDev> enc, dec;
   size_t sigma_tab = 0;
+  // entropy coder tables
+  size_t c_scales = 0, c_R = 0, c_off = 0, c_ent = 0, c_bkt = 0, c_ktab = 0;
   size_t image_bytes = 0;
   // state and intermediates (offsets from the workspace base)
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
+  // entropy coder: scale indices, symbols, per-stream scratch, lengths,
+  // offsets, status words, byte count
+  size_t kmap, qtmp, rscratch, rlens, roffs, rstatus, rbytes;
+  int64_t n_sym, n_streams;
   int n_partials;
   size_t total;
 };
+
+// Entropy-coder tables (Fig. 4 "AE" / "AD"): NS = 64 scales sigma_j =
+// fp32(0.11 (256 / 0.11)^(j / 63)); for each, symbols q = -R .. R (R =
+// ceil(8 sigma_j)) and an escape, probabilities of the Gaussian of scale sigma_j
+// quantised to 16-bit frequencies f = 1 + floor(p (2^16 - n)) with the
+// remainder added at q = 0.
+void build_coder_tables(Image& img, Layout& L, bool is_int) {
+  constexpr int NS = kCoderScales;
+  float sc[NS];
+  for (int j = 0; j < NS; ++j) sc[j] = (float)(0.11 * std::pow(256.0 / 0.11, (double)j / (NS - 1)));
+  std::vector<int32_t> Rv(NS), offv(NS);
+  std::vector<uint32_t> ent;
+  std::vector<uint16_t> bkt((size_t)NS * 257);
+  for (int j = 0; j < NS; ++j) {
+    const int R = (int)std::ceil(8.0 * (double)sc[j]);
+    const int n = 2 * R + 2;
+    const double sg = (double)sc[j] * std::sqrt(2.0);
+    std::vector<int64_t> f(n);
+    int64_t sum = 0;
+    for (int i = 0; i < n; ++i) {
+      double p;
+      if (i < n - 1) {
+        const double a = std::fabs((double)(i - R));
+        p = 0.5 * (std::erfc((a - 0.5) / sg) - std::erfc((a + 0.5) / sg));
+      } else {
+        p = std::erfc((R + 0.5) / sg);
+      }
+      f[i] = 1 + (int64_t)std::floor(p * (double)(65536 - n));
+      sum += f[i];
+    }
+    f[R] += 65536 - sum;
+    Rv[j] = R;
+    offv[j] = (int32_t)ent.size();
+    uint32_t start = 0;
+    int b = 0;
+    for (int i = 0; i < n; ++i) {
+      ent.push_back((start << 16) | (uint32_t)f[i]);
+      while (b < 256 && (uint32_t)(256 * b) < start + (uint32_t)f[i]) bkt[(size_t)j * 257 + b++] = (uint16_t)i;
+      start += (uint32_t)f[i];
+    }
+    bkt[(size_t)j * 257 + 256] = (uint16_t)(n - 1);
+  }
+  L.c_scales = img.add(NS * 4);
+  std::memcpy(img.at<float>(L.c_scales), sc, NS * 4);
+  L.c_R = img.add(NS * 4);
+  std::memcpy(img.at<int32_t>(L.c_R), Rv.data(), NS * 4);
+  L.c_off = img.add(NS * 4);
+  std::memcpy(img.at<int32_t>(L.c_off), offv.data(), NS * 4);
+  L.c_ent = img.add(ent.size() * 4);
+  std::memcpy(img.at<uint32_t>(L.c_ent), ent.data(), ent.size() * 4);
+  L.c_bkt = img.add(bkt.size() * 2);
+  std::memcpy(img.at<uint16_t>(L.c_bkt), bkt.data(), bkt.size() * 2);
+  if (is_int) {
+    // scale index of every int16 s_i: sigma = max(softplus(s_i / 512), 0.11)
+    L.c_ktab = img.add(65536);
+    uint8_t* kt = img.at<uint8_t>(L.c_ktab);
+    for (int i = 0; i < 65536; ++i) {
+      const double s = (double)(i - 32768) / 512.0;
+      const double sigma = std::fmax(s > 30.0 ? s : std::log1p(std::exp(s)), 0.11);
+      int j = 0;
+      while (j < NS - 1 && (double)sc[j] < sigma) ++j;
+      kt[i] = (uint8_t)j;
+    }
+  }
+}
 
 bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err) {
   const int C = cfg.channels;
@@ -344,6 +415,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
       tab[i] = (float)std::fmax(sp, 0.11);
     }
   }
+  build_coder_tables(img, L, is_int);
   L.image_bytes = align_up(img.bytes.size());
 
   const size_t P8 = (size_t)(cfg.height / 8) * (cfg.width / 8);
@@ -360,6 +432,15 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.partials = alloc((size_t)L.n_partials * 8);
   L.zpad = alloc((size_t)C * 2);  // zeroed at create and never written
   L.spare_bits = alloc(8);        // bit total of graph replays called without d_bits
+  L.n_sym = (int64_t)P16 * C;
+  L.n_streams = (L.n_sym + kRansStream - 1) / kRansStream;
+  L.kmap = alloc((size_t)L.n_sym);
+  L.qtmp = alloc((size_t)L.n_sym * 2);
+  L.rscratch = alloc((size_t)L.n_streams * kRansMaxWords * 2);
+  L.rlens = alloc((size_t)L.n_streams * 4);
+  L.roffs = alloc((size_t)L.n_streams * 4);
+  L.rstatus = alloc(8);
+  L.rbytes = alloc(8);
   L.total = off;
   return pk.ok;
 }
@@ -528,7 +609,8 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
 }
 
 // Enqueues one encode on ctx->stream (or records it under capture).
-ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits) {
+ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits,
+                             uint8_t* d_k = nullptr) {
   ncodec_status st;
   const ncodec_config& c = ctx->cfg;
   const int C = c.channels;
@@ -581,6 +663,9 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   pa.yhat_new = ctx->p(L.yhat[nxt]);
   pa.partials = ctx->p<double>(L.partials);
   pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
+  pa.k_out = d_k;
+  pa.scales = ctx->p<float>(L.c_scales);
+  pa.k_tab = ctx->is_int() ? ctx->p<uint8_t>(L.c_ktab) : nullptr;
   pa.C = C;
   pa.P = P16;
   pa.decode = 0;
@@ -623,6 +708,38 @@ ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_
   a.dst = d_frame_out;
   NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
   return NCODEC_OK;
+}
+
+RansTab rans_tab(const ncodec_ctx* ctx) {
+  const Layout& L = ctx->L;
+  return {ctx->p<uint32_t>(L.c_ent), ctx->p<int32_t>(L.c_off), ctx->p<int32_t>(L.c_R), ctx->p<uint16_t>(L.c_bkt)};
+}
+
+// Scale indices of the next frame's symbols, from the current state (the
+// prior head on yhat_{t-1}, Supp. B.2), into d_k (planar, C x h16 x w16).
+ncodec_status enqueue_scales(ncodec_ctx* ctx, uint8_t* d_k) {
+  const int C = ctx->cfg.channels;
+  const int P16 = (ctx->cfg.height / 16) * (ctx->cfg.width / 16);
+  const Layout& L = ctx->L;
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.head.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+  pa.bias = ctx->p(L.head.bias);
+  pa.yhat_prev = ctx->p(L.yhat[ctx->cur]);
+  pa.k_out = d_k;
+  pa.scales = ctx->p<float>(L.c_scales);
+  pa.k_tab = ctx->is_int() ? ctx->p<uint8_t>(L.c_ktab) : nullptr;
+  pa.C = C;
+  pa.P = P16;
+  pa.decode = 2;
+  NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (scale indices)");
+  return NCODEC_OK;
+}
+
+size_t stream_capacity(int64_t n) {
+  const int64_t ns = (n + kRansStream - 1) / kRansStream;
+  return (size_t)rans_payload_offset((int)ns) + (size_t)ns * kRansMaxWords * 2;
 }
 
 // Replaces one pointer in the argument struct of a captured kernel node.
@@ -826,6 +943,99 @@ ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const fl
   if (n > 0 && (!d_q || !d_sigma)) return fail(ctx, NCODEC_EINVAL, "d_q and d_sigma must be non-NULL");
   NC_HIP(ctx, launch_estimate_bits(d_q, d_sigma, n, ctx->p<double>(ctx->L.partials), d_bits, ctx->stream),
          "estimate_bits");
+  return NCODEC_OK;
+}
+
+size_t ncodec_stream_capacity(const ncodec_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  return stream_capacity((int64_t)(cfg->height / 16) * (cfg->width / 16) * cfg->channels);
+}
+
+ncodec_status ncodec_scale_indices(ncodec_ctx* ctx, uint8_t* d_k) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_k) return fail(ctx, NCODEC_EINVAL, "d_k is NULL");
+  return enqueue_scales(ctx, d_k);
+}
+
+ncodec_status ncodec_rans_encode(ncodec_ctx* ctx, const int16_t* d_q, const uint8_t* d_k, int64_t n, void* d_stream,
+                                 size_t capacity, uint64_t* d_stream_bytes) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (n <= 0 || n > ctx->L.n_sym) return fail(ctx, NCODEC_EINVAL, "n must be in [1, symbols per frame]");
+  if (!d_q || !d_k || !d_stream || !d_stream_bytes) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
+  if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  if (capacity < stream_capacity(n))
+    return fail(ctx, NCODEC_EINVAL, "capacity below the worst case of " + std::to_string(stream_capacity(n)) + " bytes");
+  const Layout& L = ctx->L;
+  NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
+           return launch_rans_encode(d_q, d_k, n, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch), kRansMaxWords,
+                                     ctx->p<uint32_t>(L.rlens), ctx->p<uint32_t>(L.roffs), (uint8_t*)d_stream,
+                                     d_stream_bytes, ctx->stream);
+         }),
+         "rans encode");
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_rans_decode(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes, const uint8_t* d_k,
+                                 int64_t n, int16_t* d_q, int32_t* d_status) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (n <= 0 || n > ctx->L.n_sym) return fail(ctx, NCODEC_EINVAL, "n must be in [1, symbols per frame]");
+  if (!d_stream || !d_k || !d_q) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
+  if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  const Layout& L = ctx->L;
+  NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
+           return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, d_k, n, rans_tab(ctx),
+                                     ctx->p<uint32_t>(L.roffs), ctx->p<uint32_t>(L.rlens), d_q,
+                                     ctx->p<int32_t>(L.rstatus), d_status, ctx->stream);
+         }),
+         "rans decode");
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits,
+                                        void* d_stream, size_t capacity, uint64_t* d_stream_bytes) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_frame || !d_stream || !d_stream_bytes) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
+  if ((uintptr_t)d_frame % 16 || (d_q && (uintptr_t)d_q % 16)) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be 16-byte aligned");
+  if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  const Layout& L = ctx->L;
+  if (capacity < stream_capacity(L.n_sym))
+    return fail(ctx, NCODEC_EINVAL, "capacity below ncodec_stream_capacity()");
+  int16_t* q = d_q ? d_q : ctx->p<int16_t>(L.qtmp);
+  st = enqueue_encode(ctx, d_frame, q, d_bits, ctx->p<uint8_t>(L.kmap));
+  if (st) return st;
+  NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
+           return launch_rans_encode(q, ctx->p<uint8_t>(L.kmap), L.n_sym, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch),
+                                     kRansMaxWords, ctx->p<uint32_t>(L.rlens), ctx->p<uint32_t>(L.roffs),
+                                     (uint8_t*)d_stream, d_stream_bytes, ctx->stream);
+         }),
+         "rans encode");
+  ctx->cur = 1 - ctx->cur;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes, void* d_frame_out,
+                                        int32_t* d_status) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!d_stream || !d_frame_out) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
+  if ((uintptr_t)d_frame_out % 16) return fail(ctx, NCODEC_EINVAL, "d_frame_out must be 16-byte aligned");
+  if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  const Layout& L = ctx->L;
+  st = enqueue_scales(ctx, ctx->p<uint8_t>(L.kmap));
+  if (st) return st;
+  NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
+           return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, ctx->p<uint8_t>(L.kmap), L.n_sym,
+                                     rans_tab(ctx), ctx->p<uint32_t>(L.roffs), ctx->p<uint32_t>(L.rlens),
+                                     ctx->p<int16_t>(L.qtmp), ctx->p<int32_t>(L.rstatus), d_status, ctx->stream);
+         }),
+         "rans decode");
+  st = enqueue_decode(ctx, ctx->p<int16_t>(L.qtmp), d_frame_out);
+  if (st) return st;
+  ctx->cur = 1 - ctx->cur;
   return NCODEC_OK;
 }
 

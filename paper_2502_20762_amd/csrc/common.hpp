@@ -139,6 +139,21 @@ __device__ __forceinline__ float softplus_sigma(float s) {
   return fmaxf(sp, 0.11f);
 }
 
+// Entropy-coder scales: sigma_j = SMIN (SMAX / SMIN)^(j / (NS - 1)), j < NS.
+constexpr int kCoderScales = 64;
+constexpr float kCoderSMin = 0.11f;
+constexpr float kCoderLogStepInv = 63.0f / 7.7524524f;  // (NS - 1) / ln(SMAX / SMIN), SMAX = 256
+
+// Scale index of sigma: the smallest j with scales[j] >= sigma (NS - 1 if
+// none).  The logarithm only seeds the search; the comparisons decide.
+__device__ __forceinline__ int coder_scale_index(float sigma, const float* scales) {
+  int j = (int)ceilf(__logf(sigma * (1.f / kCoderSMin)) * kCoderLogStepInv);
+  j = min(max(j, 0), kCoderScales - 1);
+  while (j > 0 && scales[j - 1] >= sigma) --j;
+  while (j < kCoderScales - 1 && scales[j] < sigma) ++j;
+  return j;
+}
+
 // Deterministic (fixed-order) wave reduction of a double.
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll

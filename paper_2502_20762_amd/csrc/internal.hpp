@@ -37,6 +37,7 @@ enum Epi : int {
   EP_REC = 2,   // rows 64c+8i+j: pixel-shuffle x8 into a planar 3xHxW frame, clamped
   EP_PRIOR = 3,      // rows (32 mu, 32 s) per pass: quantise y, write q, yhat, bit partials
   EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
+  EP_SCALES = 5,     // same rows: only the scale index of every symbol (entropy decoding)
 };
 
 struct PwArgs {
@@ -60,6 +61,9 @@ struct PwArgs {
   int16_t* q_out;       // planar symbols (encode)
   double* partials;     // one per (tile, pass) of the encoder
   const float* sigma_tab;
+  uint8_t* k_out;          // planar scale indices of the entropy coder (nullable for EP_PRIOR)
+  const float* scales;     // fp16 path: the NS coder scales sigma_j (fp32)
+  const uint8_t* k_tab;    // int path: scale index for s_i + 32768
 };
 
 struct BlockArgs {
@@ -88,10 +92,36 @@ struct PriorArgs {
   void* yhat_new;         // NHWC latent
   double* partials;       // one per (tile, channel slice) (encode)
   const float* sigma_tab; // int path: sigma for s_i + 32768
+  uint8_t* k_out;         // planar scale indices (nullable; required when scales_only)
+  const float* scales;    // fp16 path: coder scales
+  const uint8_t* k_tab;   // int path: scale index for s_i + 32768
   int C;
   int P;
-  int decode;
+  int decode;             // 0 encode, 1 decode (q given), 2 scale indices only
 };
+
+// Entropy coder (container and stream geometry; the tables live in the
+// weights image).
+constexpr int kRansStream = 8192;  // symbols per stream: 64 lanes x 128 steps
+constexpr int kRansHeader = 20;    // magic, version, symbols, symbols per stream, streams
+constexpr uint32_t kRansMagic = 0x5352434Eu;  // "NCRS"
+constexpr uint32_t kRansVersion = 1;
+constexpr int64_t kRansMaxWords = 128 + 7 * (int64_t)kRansStream;  // worst case per stream
+__host__ __device__ constexpr int rans_payload_offset(int ns) { return kRansHeader + 4 * ((ns + 1) / 2); }
+
+struct RansTab {
+  const uint32_t* ent;  // (start << 16) | freq; per scale 2 R + 2 entries: q = -R .. R, then escape
+  const int32_t* off;   // [NS] first entry of each scale
+  const int32_t* R;     // [NS]
+  const uint16_t* bkt;  // [NS][257]: entry holding slot 256 b (b < 256); [256] = last entry
+};
+
+hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const RansTab& t, uint16_t* scratch,
+                              int64_t max_words, uint32_t* lens, uint32_t* offs, uint8_t* out, uint64_t* nbytes,
+                              hipStream_t st);
+hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const RansTab& t,
+                              uint32_t* offs, uint32_t* lens, int16_t* q, int32_t* status, int32_t* status_out,
+                              hipStream_t st);
 
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);

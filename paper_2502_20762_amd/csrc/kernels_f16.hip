@@ -174,6 +174,21 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
   const int c0 = n0 / 2;
   int16_t* qt = (int16_t*)st2;
+  uint8_t* kt = (uint8_t*)(st2 + 8192);  // scale indices, [channel][pixel]
+  // planar store of the staged scale indices (after a barrier)
+  auto store_k = [&]() __attribute__((always_inline)) {
+    const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
+    const int p0 = tile * 128 + 8 * k;
+    uint8_t* dk = a.k_out + (size_t)(c0 + ch) * a.P + p0;
+    const uint8_t* sk = kt + ch * 128 + 8 * k;
+    if ((a.P & 7) == 0 && p0 + 8 <= a.P && ((uintptr_t)a.k_out & 7) == 0) {
+      *(uint64_t*)dk = *(const uint64_t*)sk;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (p0 + e < a.P) dk[e] = sk[e];
+    }
+  };
   if constexpr (EPI == EP_PRIOR_DEC) {
     static_assert(NT == 64, "prior passes are 64 rows");
     const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;  // 32 channels x 16 chunks of 8 pixels
@@ -200,7 +215,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { r[e] = o0[e]; r[4 + e] = o1[e]; }
     return r;
   };
-  if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
+  if constexpr (EPI == EP_SCALES) {
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const floatx16 sg = parked(px, 4 + g8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), a.scales);
+    lds_barrier();
+    store_k();
+  } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
     // thread = (pixel px, 8 channels g8): mu and s from the park, y / q, yhat
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
     const int gp = tile * 128 + px;
@@ -208,6 +230,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     const floatx16 mu = parked(px, g8), sg = parked(px, 4 + g8);
     double bsum = 0.0;
     if constexpr (EPI == EP_PRIOR) {
+      if (a.k_out) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), a.scales);
+      }
       half8 yv = {};
       if (gp < a.P) yv = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + c);
       half8 yh;
@@ -237,6 +264,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
             if (p0 + e < a.P) dq[e] = v[e];
         }
       }
+      if (a.k_out) store_k();
       if (threadIdx.x == 0) {
         double t = 0.0;
 #pragma unroll
@@ -723,6 +751,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_NHWC, EP_REC)
   NC_PW(LD_NHWC, EP_PRIOR)
   NC_PW(LD_NHWC, EP_PRIOR_DEC)
+  NC_PW(LD_NHWC, EP_SCALES)
 #undef NC_PW
   return hipErrorInvalidValue;
 }
@@ -772,8 +801,10 @@ hipError_t launch_prior_f16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.q_in = pa.q_in;
   a.q_out = pa.q_out;
   a.partials = pa.partials;
+  a.k_out = pa.k_out;
+  a.scales = pa.scales;
   if (n_partials) *n_partials = prior_partials_f16(pa.C, pa.P);
-  return pw_dispatch<64>(LD_NHWC, pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
+  return pw_dispatch<64>(LD_NHWC, pa.decode == 2 ? EP_SCALES : pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
 }
 
 }  // namespace nc

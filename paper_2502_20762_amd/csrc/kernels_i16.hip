@@ -202,6 +202,21 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
   const int c0 = n0 / 2;
   int16_t* qt = (int16_t*)st2;
+  uint8_t* kt = (uint8_t*)(st2 + 8192);  // scale indices, [channel][pixel]
+  // planar store of the staged scale indices (after a barrier)
+  auto store_k = [&]() __attribute__((always_inline)) {
+    const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
+    const int p0 = tile * 128 + 8 * k;
+    uint8_t* dk = a.k_out + (size_t)(c0 + ch) * a.P + p0;
+    const uint8_t* sk = kt + ch * 128 + 8 * k;
+    if ((a.P & 7) == 0 && p0 + 8 <= a.P && ((uintptr_t)a.k_out & 7) == 0) {
+      *(uint64_t*)dk = *(const uint64_t*)sk;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (p0 + e < a.P) dk[e] = sk[e];
+    }
+  };
   if constexpr (EPI == EP_PRIOR_DEC) {
     static_assert(NT == 64, "prior passes are 64 rows");
     const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
@@ -227,7 +242,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { v[e] = o0[e]; v[4 + e] = o1[e]; }
   };
   constexpr int UNITS = 128 * (NT / 8);
-  if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
+  if constexpr (EPI == EP_SCALES) {
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    int sv[8];
+    parked(px, 4 + g8, sv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = a.k_tab[sv[e] + 32768];
+    lds_barrier();
+    store_k();
+  } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
     // thread = (pixel px, 8 channels g8): q = RHE((y_i - mu_i) / 512),
     // yhat_i = clip(512 q + mu_i), sigma from the table at s_i
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
@@ -241,6 +264,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       shortx8 yv = {};
       if (gp < a.P) yv = *(const shortx8*)((const int16_t*)a.y + (size_t)gp * a.Cdst + c);
       shortx8 yh;
+      if (a.k_out) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = a.k_tab[sv[e] + 32768];
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int q = rhe_shift((int)yv[e] - mu[e], 9);
@@ -266,6 +293,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
             if (p0 + e < a.P) dq[e] = v[e];
         }
       }
+      if (a.k_out) store_k();
       if (threadIdx.x == 0) {
         double t = 0.0;
 #pragma unroll
@@ -762,6 +790,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_NHWC, EP_REC)
   NC_PW(LD_NHWC, EP_PRIOR)
   NC_PW(LD_NHWC, EP_PRIOR_DEC)
+  NC_PW(LD_NHWC, EP_SCALES)
 #undef NC_PW
   return hipErrorInvalidValue;
 }
@@ -811,8 +840,10 @@ hipError_t launch_prior_i16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.q_out = pa.q_out;
   a.partials = pa.partials;
   a.sigma_tab = pa.sigma_tab;
+  a.k_out = pa.k_out;
+  a.k_tab = pa.k_tab;
   if (n_partials) *n_partials = prior_partials_i16(pa.C, pa.P);
-  return pw_dispatch<64>(LD_NHWC, pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
+  return pw_dispatch<64>(LD_NHWC, pa.decode == 2 ? EP_SCALES : pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
 }
 
 }  // namespace nc

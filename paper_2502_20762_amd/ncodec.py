@@ -60,6 +60,12 @@ _SIGNATURES = {
     "ncodec_encode_frame": (ctypes.c_int, [_P, _P, _P, _P]),
     "ncodec_decode_frame": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_estimate_bits": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P]),
+    "ncodec_stream_capacity": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
+    "ncodec_scale_indices": (ctypes.c_int, [_P, _P]),
+    "ncodec_rans_encode": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P, ctypes.c_size_t, _P]),
+    "ncodec_rans_decode": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P, ctypes.c_int64, _P, _P]),
+    "ncodec_encode_frame_coded": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "ncodec_decode_frame_coded": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P, _P]),
     "ncodec_get_state": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_set_state": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_kernels_per_frame": (ctypes.c_int32, [_P, ctypes.c_int32]),
@@ -95,6 +101,11 @@ def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path) -> nc
     if isinstance(path, str):
         path = PATHS[path]
     return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path)
+
+
+def _p(v: int):
+    """Device address for a pointer argument (0 -> NULL)."""
+    return v or None
 
 
 def _check(st: int, ctx=None) -> None:
@@ -138,6 +149,33 @@ def ncodec_estimate_bits(ctx, d_q: int, d_sigma: int, n: int, d_bits: int) -> No
     _check(load_library().ncodec_estimate_bits(ctx, d_q or None, d_sigma or None, n, d_bits), ctx)
 
 
+def ncodec_stream_capacity(cfg: ncodec_config) -> int:
+    return int(load_library().ncodec_stream_capacity(ctypes.byref(cfg)))
+
+
+def ncodec_scale_indices(ctx, d_k: int) -> None:
+    _check(load_library().ncodec_scale_indices(ctx, _p(d_k)), ctx)
+
+
+def ncodec_rans_encode(ctx, d_q: int, d_k: int, n: int, d_stream: int, capacity: int, d_stream_bytes: int) -> None:
+    _check(load_library().ncodec_rans_encode(ctx, _p(d_q), _p(d_k), n, _p(d_stream), capacity, _p(d_stream_bytes)), ctx)
+
+
+def ncodec_rans_decode(ctx, d_stream: int, stream_bytes: int, d_k: int, n: int, d_q: int, d_status: int = 0) -> None:
+    _check(load_library().ncodec_rans_decode(ctx, _p(d_stream), stream_bytes, _p(d_k), n, _p(d_q), _p(d_status)), ctx)
+
+
+def ncodec_encode_frame_coded(ctx, d_frame: int, d_q: int, d_bits: int, d_stream: int, capacity: int,
+                              d_stream_bytes: int) -> None:
+    _check(load_library().ncodec_encode_frame_coded(ctx, _p(d_frame), _p(d_q), _p(d_bits), _p(d_stream), capacity,
+                                                    _p(d_stream_bytes)), ctx)
+
+
+def ncodec_decode_frame_coded(ctx, d_stream: int, stream_bytes: int, d_frame_out: int, d_status: int = 0) -> None:
+    _check(load_library().ncodec_decode_frame_coded(ctx, _p(d_stream), stream_bytes, _p(d_frame_out), _p(d_status)),
+           ctx)
+
+
 def ncodec_get_state(ctx, d_feat: int, d_yhat: int) -> None:
     _check(load_library().ncodec_get_state(ctx, d_feat or None, d_yhat or None), ctx)
 
@@ -176,6 +214,12 @@ def ncodec_status_string(st: int) -> str:
 
 def ncodec_destroy(ctx) -> None:
     load_library().ncodec_destroy(ctx)
+
+
+def _capacity(n: int) -> int:
+    """Worst-case container bytes for n symbols (the ABI's bound)."""
+    ns = (n + 8191) // 8192
+    return 20 + 4 * ((ns + 1) // 2) + ns * (128 + 7 * 8192) * 2
 
 
 # ---------------------------------------------------------------- convenience
@@ -231,6 +275,55 @@ class Codec:
         bits = bits_out if bits_out is not None else self._empty((), torch.float64)
         ncodec_estimate_bits(self.ctx, q.data_ptr(), sigma.data_ptr(), q.numel(), bits.data_ptr())
         return bits
+
+    # ---- entropy coding
+    def stream_capacity(self) -> int:
+        return ncodec_stream_capacity(self.cfg)
+
+    def scale_indices(self, out=None):
+        k = out if out is not None else self._empty(self.q_shape, self.torch.uint8)
+        ncodec_scale_indices(self.ctx, k.data_ptr())
+        return k
+
+    def rans_encode(self, q, k, stream=None, nbytes_out=None):
+        """Container of the symbols q under scale indices k (flattened): returns
+        (stream buffer, device byte count)."""
+        torch = self.torch
+        assert q.dtype == torch.int16 and k.dtype == torch.uint8 and q.numel() == k.numel()
+        assert q.is_contiguous() and k.is_contiguous()
+        n = q.numel()
+        cap = _capacity(n)
+        buf = stream if stream is not None else self._empty((cap,), torch.uint8)
+        nb = nbytes_out if nbytes_out is not None else self._empty((), torch.int64)
+        ncodec_rans_encode(self.ctx, q.data_ptr(), k.data_ptr(), n, buf.data_ptr(), buf.numel(), nb.data_ptr())
+        return buf, nb
+
+    def rans_decode(self, stream, nbytes, k, out=None, status_out=None):
+        torch = self.torch
+        assert stream.dtype == torch.uint8 and k.dtype == torch.uint8 and k.is_contiguous()
+        q = out if out is not None else self._empty(tuple(k.shape), torch.int16)
+        st = status_out if status_out is not None else self._empty((), torch.int32)
+        ncodec_rans_decode(self.ctx, stream.data_ptr(), int(nbytes), k.data_ptr(), k.numel(), q.data_ptr(),
+                           st.data_ptr())
+        return q, st
+
+    def encode_coded(self, frame, stream=None, nbytes_out=None, q_out=None, bits_out=None):
+        torch = self.torch
+        assert frame.dtype == torch.float16 and tuple(frame.shape) == self.frame_shape and frame.is_contiguous()
+        buf = stream if stream is not None else self._empty((self.stream_capacity(),), torch.uint8)
+        nb = nbytes_out if nbytes_out is not None else self._empty((), torch.int64)
+        ncodec_encode_frame_coded(self.ctx, frame.data_ptr(), q_out.data_ptr() if q_out is not None else 0,
+                                  bits_out.data_ptr() if bits_out is not None else 0, buf.data_ptr(), buf.numel(),
+                                  nb.data_ptr())
+        return buf, nb
+
+    def decode_coded(self, stream, nbytes, out=None, status_out=None):
+        torch = self.torch
+        odt = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float16
+        x = out if out is not None else self._empty(self.frame_shape, odt)
+        st = status_out if status_out is not None else self._empty((), torch.int32)
+        ncodec_decode_frame_coded(self.ctx, stream.data_ptr(), int(nbytes), x.data_ptr(), st.data_ptr())
+        return x, st
 
     def get_state(self):
         feat = self._empty(self.feat_shape, self.state_dtype)

@@ -110,7 +110,24 @@ def test_null_context_calls(lib):
     assert lib.ncodec_estimate_bits(None, None, None, 0, None) == nc.NCODEC_EINVAL
     assert lib.ncodec_get_state(None, None, None) == nc.NCODEC_EINVAL
     assert lib.ncodec_kernels_per_frame(None, 0) == 0
+    assert lib.ncodec_scale_indices(None, None) == nc.NCODEC_EINVAL
+    assert lib.ncodec_rans_encode(None, None, None, 1, None, 0, None) == nc.NCODEC_EINVAL
+    assert lib.ncodec_rans_decode(None, None, 0, None, 1, None, None) == nc.NCODEC_EINVAL
+    assert lib.ncodec_encode_frame_coded(None, None, None, None, None, 0, None) == nc.NCODEC_EINVAL
+    assert lib.ncodec_decode_frame_coded(None, None, 0, None, None) == nc.NCODEC_EINVAL
     lib.ncodec_destroy(None)
+
+
+def test_stream_capacity_is_the_worst_case_bound():
+    # 20-byte header, 2 bytes per stream length (padded to 4), and per stream of
+    # 8192 symbols 64 two-word final states plus at most 7 words per symbol
+    for H, W, C in [(64, 64, 64), (480, 832, 128), (1088, 1920, 256)]:
+        n = (H // 16) * (W // 16) * C
+        ns = -(-n // 8192)
+        want = 20 + 4 * ((ns + 1) // 2) + ns * (128 + 7 * 8192) * 2
+        assert nc.ncodec_stream_capacity(nc.make_config(H, W, C, 1, 1, "fp16")) == want
+        assert nc._capacity(n) == want
+    assert nc.ncodec_stream_capacity(nc.make_config(63, 64, 64, 1, 1, "fp16")) == 0
 
 
 def test_status_strings():
