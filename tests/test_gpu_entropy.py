@@ -100,7 +100,8 @@ def test_damaged_containers_are_flagged(coder):
 
 
 @pytest.mark.parametrize("path,H,W,C,ne,nd", [("fp16", 64, 64, 64, 2, 2), ("int16", 64, 64, 64, 2, 2),
-                                              ("fp16", 480, 832, 128, 2, 2), ("int16", 480, 832, 128, 2, 2)])
+                                              ("fp16", 480, 832, 128, 2, 2), ("int16", 480, 832, 128, 2, 2),
+                                              ("fp16", 1088, 1920, 256, 8, 8), ("int16", 1088, 1920, 256, 8, 8)])
 def test_coded_frames_round_trip(path, H, W, C, ne, nd):
     flat, _ = params_for(C, ne, nd)
     enc = Codec(H, W, C, ne, nd, path, flat, device=DEV)
