@@ -132,9 +132,9 @@ ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const fl
  * The symbols are coded with rANS (Duda 2013; 32-bit state in [2^16, 2^32),
  * 16-bit words, 16-bit frequencies) under quantised-scale Gaussian tables:
  * NS = 64 scales sigma_j = fp32(0.11 (256/0.11)^(j/63)); table j codes
- * q = -R .. R (R = ceil(8 sigma_j)) and an escape for larger |q|, which is
- * followed by uniform sub-symbols (sign, hex digit count, hex digits of
- * |q| - R - 1).  Frequencies: f = 1 + floor(p (2^16 - n)) for each of the
+ * q = -R .. R (R = max(ceil(8 sigma_j), 32)) and an escape for larger |q|,
+ * which is followed by one 16-bit field of frequency 1,
+ * 32768 * sign + |q| - R - 1.  Frequencies: f = 1 + floor(p (2^16 - n)) for each of the
  * n = 2R + 2 symbols of the Gaussian of scale sigma_j, the remainder added at
  * q = 0.  The scale index of a symbol is the smallest j with
  * sigma_j >= sigma = max(softplus(s), 0.11) (s the prior's scale output; on the
@@ -149,7 +149,8 @@ ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const fl
  *
  * All calls enqueue on the context's stream; byte counts and status words are
  * device outputs, valid after the stream synchronises.  Buffers must be device
- * memory; d_stream must be 4-byte aligned. */
+ * memory; d_stream must be 4-byte aligned, symbol and scale-index arrays
+ * 16-byte aligned.  A stream holds at most 128 + 2 * 8192 words. */
 
 /* Worst-case container size in bytes for one frame of cfg (what d_stream
  * must hold for ncodec_encode_frame_coded).  0 for an invalid cfg. */

@@ -10,7 +10,7 @@ format; the numbers below are its definition, not tuning knobs.
 
 Distribution tables (one per scale index j = 0 .. NS-1):
   sigma_j  = float32(SMIN * (SMAX / SMIN) ** (j / (NS - 1)))
-  R_j      = ceil(TAIL * sigma_j)
+  R_j      = max(ceil(TAIL * sigma_j), RMIN)
   symbols  q = -R_j .. R_j, then ESC (|q| > R_j)
   p(q)     = 1/2 [erfc((|q| - 1/2) / (sigma_j sqrt2)) - erfc((|q| + 1/2) / (sigma_j sqrt2))]
   p(ESC)   = erfc((R_j + 1/2) / (sigma_j sqrt2))
@@ -29,10 +29,9 @@ rANS (Duda, "Asymmetric numeral systems", 2013; the range variant with a
   The encoder runs over the symbols in reverse; its words, read backwards,
   are the decoder's input.  Each state starts at L and ends as two words.
 
-An escaped symbol continues with uniform sub-symbols (frequency M / m for m
-values): the sign (m = 2), n - 1 where n is the number of hex digits of
-v = |q| - R_j - 1 (m = 4), then the n digits of v, most significant first
-(m = 16).
+An escaped symbol continues with one uniform sub-symbol of frequency 1 (a
+plain 16-bit field): 32768 * sign + v with v = |q| - R_j - 1 (v < 32768
+because |q| <= 32768 and R_j >= 32).
 
 Streams: the symbols are cut into streams of LANES * STEPS; inside a stream,
 symbol i belongs to lane i mod LANES at step i div LANES, and the LANES lanes
@@ -59,6 +58,7 @@ NS = 64
 SMIN = 0.11
 SMAX = 256.0
 TAIL = 8.0
+RMIN = 32
 PREC = 16
 M = 1 << PREC
 L = 1 << 16
@@ -86,7 +86,7 @@ def scale_index(sigma) -> np.ndarray:
 def table(j: int):
     """(R, freq, start) of scale j; entries are q = -R .. R then ESC."""
     sigma = float(scale_table()[j])
-    R = int(math.ceil(TAIL * sigma))
+    R = max(int(math.ceil(TAIL * sigma)), RMIN)
     n = 2 * R + 2
     sg = sigma * math.sqrt(2.0)
     a = np.abs(np.arange(-R, R + 1, dtype=np.float64))
@@ -114,16 +114,8 @@ def _subsymbols(q: int, j: int):
     R, f, c = tables()[j]
     if -R <= q <= R:
         return [(int(c[q + R]), int(f[q + R]))]
-    out = [(int(c[-1]), int(f[-1]))]
     v = abs(q) - R - 1
-    out.append(((1 if q < 0 else 0) * (M // 2), M // 2))
-    nd = 1
-    while v >= 16 ** nd:
-        nd += 1
-    out.append(((nd - 1) * (M // 4), M // 4))
-    for d in range(nd - 1, -1, -1):
-        out.append((((v >> (4 * d)) & 15) * (M // 16), M // 16))
-    return out
+    return [(int(c[-1]), int(f[-1])), ((32768 if q < 0 else 0) + v, 1)]
 
 
 def encode_stream(q: np.ndarray, k: np.ndarray) -> list:
@@ -195,37 +187,15 @@ def decode_stream(words, k: np.ndarray):
             i = _find(j, x[ln] & (M - 1))
             x[ln] = take(x[ln], ln, int(c[i]), int(f[i]))
             if i == 2 * R + 1:
-                esc[ln] = {"R": R}
+                esc[ln] = R
             else:
                 out[t * LANES + ln] = i - R
-        # escaped symbols: sign, digit count, digits (lanes in order at each sub-step)
-        u = 1
-        while any(u < e.get("nsub", 3 if u < 3 else 0) for e in esc.values()):
-            for ln in sorted(esc):
-                e = esc[ln]
-                if u >= e.get("nsub", 3 if u < 3 else 0):
-                    continue
-                if u == 1:
-                    m = 2
-                elif u == 2:
-                    m = 4
-                else:
-                    m = 16
-                fq = M // m
-                v = (x[ln] & (M - 1)) // fq
-                x[ln] = take(x[ln], ln, v * fq, fq)
-                if u == 1:
-                    e["neg"] = v
-                elif u == 2:
-                    e["nd"] = v + 1
-                    e["nsub"] = 3 + v + 1
-                    e["val"] = 0
-                else:
-                    e["val"] = e["val"] * 16 + v
-            u += 1
-        for ln, e in esc.items():
-            mag = e["R"] + 1 + e["val"]
-            out[t * LANES + ln] = -mag if e["neg"] else mag
+        # escaped symbols: one 16-bit field each, lanes in order
+        for ln in sorted(esc):
+            fld = x[ln] & (M - 1)
+            x[ln] = take(x[ln], ln, fld, 1)
+            mag = esc[ln] + 1 + (fld & 32767)
+            out[t * LANES + ln] = -mag if fld >= 32768 else mag
     ok = ok and pos == len(words) and all(v == L for v in x)
     return out, ok
 

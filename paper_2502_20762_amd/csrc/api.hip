@@ -293,7 +293,7 @@ struct Layout {
   std::vector<BlockDev> enc, dec;
   size_t sigma_tab = 0;
   // entropy coder tables
-  size_t c_scales = 0, c_R = 0, c_off = 0, c_ent = 0, c_bkt = 0, c_ktab = 0;
+  size_t c_scales = 0, c_tab = 0, c_ktab = 0;
   size_t image_bytes = 0;
   // state and intermediates (offsets from the workspace base)
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
@@ -310,15 +310,13 @@ struct Layout {
 // ceil(8 sigma_j)) and an escape, probabilities of the Gaussian of scale sigma_j
 // quantised to 16-bit frequencies f = 1 + floor(p (2^16 - n)) with the
 // remainder added at q = 0.
-void build_coder_tables(Image& img, Layout& L, bool is_int) {
+void build_coder_tables(Image& img, Layout& L, bool is_int, std::string* err) {
   constexpr int NS = kCoderScales;
   float sc[NS];
   for (int j = 0; j < NS; ++j) sc[j] = (float)(0.11 * std::pow(256.0 / 0.11, (double)j / (NS - 1)));
-  std::vector<int32_t> Rv(NS), offv(NS);
-  std::vector<uint32_t> ent;
-  std::vector<uint16_t> bkt((size_t)NS * 257);
+  std::vector<uint16_t> tab(kTabStarts), bkt((size_t)NS * 257);
   for (int j = 0; j < NS; ++j) {
-    const int R = (int)std::ceil(8.0 * (double)sc[j]);
+    const int R = std::max((int)std::ceil(8.0 * (double)sc[j]), 32);
     const int n = 2 * R + 2;
     const double sg = (double)sc[j] * std::sqrt(2.0);
     std::vector<int64_t> f(n);
@@ -335,27 +333,28 @@ void build_coder_tables(Image& img, Layout& L, bool is_int) {
       sum += f[i];
     }
     f[R] += 65536 - sum;
-    Rv[j] = R;
-    offv[j] = (int32_t)ent.size();
+    tab[j] = (uint16_t)R;
+    tab[NS + j] = (uint16_t)(tab.size() - kTabStarts);
     uint32_t start = 0;
     int b = 0;
     for (int i = 0; i < n; ++i) {
-      ent.push_back((start << 16) | (uint32_t)f[i]);
+      tab.push_back((uint16_t)start);
       while (b < 256 && (uint32_t)(256 * b) < start + (uint32_t)f[i]) bkt[(size_t)j * 257 + b++] = (uint16_t)i;
       start += (uint32_t)f[i];
     }
+    tab.push_back(0);  // closing start, 2^16 mod 2^16
     bkt[(size_t)j * 257 + 256] = (uint16_t)(n - 1);
   }
+  if (tab.size() != (size_t)kTabBuckets) {
+    if (err) *err = "coder tables: " + std::to_string(tab.size() - kTabStarts) + " starts, expected " +
+                    std::to_string(kCoderStarts);
+    return;
+  }
+  tab.insert(tab.end(), bkt.begin(), bkt.end());
   L.c_scales = img.add(NS * 4);
   std::memcpy(img.at<float>(L.c_scales), sc, NS * 4);
-  L.c_R = img.add(NS * 4);
-  std::memcpy(img.at<int32_t>(L.c_R), Rv.data(), NS * 4);
-  L.c_off = img.add(NS * 4);
-  std::memcpy(img.at<int32_t>(L.c_off), offv.data(), NS * 4);
-  L.c_ent = img.add(ent.size() * 4);
-  std::memcpy(img.at<uint32_t>(L.c_ent), ent.data(), ent.size() * 4);
-  L.c_bkt = img.add(bkt.size() * 2);
-  std::memcpy(img.at<uint16_t>(L.c_bkt), bkt.data(), bkt.size() * 2);
+  L.c_tab = img.add(tab.size() * 2);
+  std::memcpy(img.at<uint16_t>(L.c_tab), tab.data(), tab.size() * 2);
   if (is_int) {
     // scale index of every int16 s_i: sigma = max(softplus(s_i / 512), 0.11)
     L.c_ktab = img.add(65536);
@@ -415,7 +414,12 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
       tab[i] = (float)std::fmax(sp, 0.11);
     }
   }
-  build_coder_tables(img, L, is_int);
+  std::string terr;
+  build_coder_tables(img, L, is_int, &terr);
+  if (!terr.empty()) {
+    if (err) *err = "internal: " + terr;
+    return false;
+  }
   L.image_bytes = align_up(img.bytes.size());
 
   const size_t P8 = (size_t)(cfg.height / 8) * (cfg.width / 8);
@@ -710,10 +714,7 @@ ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_
   return NCODEC_OK;
 }
 
-RansTab rans_tab(const ncodec_ctx* ctx) {
-  const Layout& L = ctx->L;
-  return {ctx->p<uint32_t>(L.c_ent), ctx->p<int32_t>(L.c_off), ctx->p<int32_t>(L.c_R), ctx->p<uint16_t>(L.c_bkt)};
-}
+const uint16_t* rans_tab(const ncodec_ctx* ctx) { return ctx->p<uint16_t>(ctx->L.c_tab); }
 
 // Scale indices of the next frame's symbols, from the current state (the
 // prior head on yhat_{t-1}, Supp. B.2), into d_k (planar, C x h16 x w16).
@@ -965,6 +966,7 @@ ncodec_status ncodec_rans_encode(ncodec_ctx* ctx, const int16_t* d_q, const uint
   if (n <= 0 || n > ctx->L.n_sym) return fail(ctx, NCODEC_EINVAL, "n must be in [1, symbols per frame]");
   if (!d_q || !d_k || !d_stream || !d_stream_bytes) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
   if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  if ((uintptr_t)d_q % 16 || (uintptr_t)d_k % 16) return fail(ctx, NCODEC_EINVAL, "d_q and d_k must be 16-byte aligned");
   if (capacity < stream_capacity(n))
     return fail(ctx, NCODEC_EINVAL, "capacity below the worst case of " + std::to_string(stream_capacity(n)) + " bytes");
   const Layout& L = ctx->L;
@@ -984,6 +986,7 @@ ncodec_status ncodec_rans_decode(ncodec_ctx* ctx, const void* d_stream, size_t s
   if (n <= 0 || n > ctx->L.n_sym) return fail(ctx, NCODEC_EINVAL, "n must be in [1, symbols per frame]");
   if (!d_stream || !d_k || !d_q) return fail(ctx, NCODEC_EINVAL, "NULL buffer");
   if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
+  if ((uintptr_t)d_k % 16) return fail(ctx, NCODEC_EINVAL, "d_k must be 16-byte aligned");
   const Layout& L = ctx->L;
   NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
            return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, d_k, n, rans_tab(ctx),

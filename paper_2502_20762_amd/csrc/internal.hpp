@@ -106,20 +106,28 @@ constexpr int kRansStream = 8192;  // symbols per stream: 64 lanes x 128 steps
 constexpr int kRansHeader = 20;    // magic, version, symbols, symbols per stream, streams
 constexpr uint32_t kRansMagic = 0x5352434Eu;  // "NCRS"
 constexpr uint32_t kRansVersion = 1;
-constexpr int64_t kRansMaxWords = 128 + 7 * (int64_t)kRansStream;  // worst case per stream
+constexpr int64_t kRansMaxWords = 128 + 2 * (int64_t)kRansStream;  // worst case per stream
 __host__ __device__ constexpr int rans_payload_offset(int ns) { return kRansHeader + 4 * ((ns + 1) / 2); }
 
-struct RansTab {
-  const uint32_t* ent;  // (start << 16) | freq; per scale 2 R + 2 entries: q = -R .. R, then escape
-  const int32_t* off;   // [NS] first entry of each scale
-  const int32_t* R;     // [NS]
-  const uint16_t* bkt;  // [NS][257]: entry holding slot 256 b (b < 256); [256] = last entry
-};
+// Coder tables: one block of uint16 in the weights image (16-byte aligned),
+// staged whole into LDS by the coder kernels.
+//   [0, 64)              R_j
+//   [64, 128)            first start of scale j (index into the starts)
+//   [128, 128 + STARTS)  starts: per scale the 2 R_j + 2 entry starts
+//                        (q = -R .. R, then the escape) and a closing 0
+//                        (standing for 2^16), so f_i = (start_{i+1} - start_i) mod 2^16
+//   then [NS][257]       buckets: entry holding slot 256 b (b < 256); [256] = last entry
+constexpr int kCoderStarts = 36976;  // sum over j of 2 R_j + 3
+constexpr int kTabStarts = 128;
+constexpr int kTabBuckets = kTabStarts + kCoderStarts;
+constexpr int kTabEncU16 = kTabBuckets;                       // what the encoder stages
+constexpr int kTabU16 = kTabBuckets + kCoderScales * 257;     // what the decoder stages
+static_assert(kTabEncU16 % 8 == 0 && kTabU16 % 8 == 0, "coder table block must be whole 16-byte chunks");
 
-hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const RansTab& t, uint16_t* scratch,
+hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const uint16_t* tab, uint16_t* scratch,
                               int64_t max_words, uint32_t* lens, uint32_t* offs, uint8_t* out, uint64_t* nbytes,
                               hipStream_t st);
-hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const RansTab& t,
+hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const uint16_t* tab,
                               uint32_t* offs, uint32_t* lens, int16_t* q, int32_t* status, int32_t* status_out,
                               hipStream_t st);
 

@@ -3,12 +3,16 @@
 // M = 2^16) on quantised-scale Gaussian tables.
 //
 // A stream is 8192 symbols coded by the 64 lanes of one wave in lock step:
-// symbol i of the stream belongs to lane i % 64 at step i / 64, so symbol and
-// scale-index loads are coalesced.  At every (step, sub-symbol) the lanes that
-// move a word do so in lane order (ballot + popcount give each its slot), so a
-// stream is one contiguous run of words.  Escaped symbols (|q| beyond the
-// table) continue with uniform sub-symbols: the sign, the digit count, then
-// the hex digits of |q| - R - 1, most significant first.
+// symbol i of the stream belongs to lane i % 64 at step i / 64.  At every
+// (step, sub-symbol) the lanes that move a word do so in lane order (ballot +
+// popcount give each its slot), so a stream is one contiguous run of words.
+// An escaped symbol (|q| beyond its table) continues with one 16-bit field
+// of frequency 1: 32768 * sign + |q| - R - 1.
+//
+// Every coder kernel first stages what its sequential loop touches into LDS
+// with direct global->LDS loads issued back to back and one wait (the tables,
+// the stream's symbols and scale indices, the decoder also the stream's
+// words), so the loop over the 128 steps never waits on global memory.
 //
 // k_rans_encode  one wave per stream: encodes backwards into the stream's
 //                scratch slot, words ending at the slot's end
@@ -28,76 +32,111 @@ namespace {
 
 constexpr uint32_t kRansL = 1u << 16;
 
-struct Sub {
-  uint32_t c, f;
-};
-
-// Sub-symbol u of a symbol (decoding order): u = 0 the table entry (or ESC),
-// then for an escape the sign (M / 2 each), the digit count minus one
-// (M / 4 each) and the digits (M / 16 each).
-__device__ __forceinline__ Sub rans_sub(int u, uint32_t ent, bool neg, int nd, uint32_t v) {
-  if (u == 0) return {ent >> 16, ent & 0xFFFFu};
-  if (u == 1) return {neg ? 32768u : 0u, 32768u};
-  if (u == 2) return {(uint32_t)(nd - 1) * 16384u, 16384u};
-  return {((v >> (4 * (nd - 1 - (u - 3)))) & 15u) * 4096u, 4096u};
+// Direct global->LDS load of 4 bytes per lane: lane l's bytes land at
+// lds_wave_base + 4 l.  Callers wait with s_waitcnt vmcnt before reading.
+__device__ __forceinline__ void dma4(const void* g, const void* lds_wave_base) {
+  const uint32_t m = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_wave_base;
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(m) : "memory", "m0");
 }
 
-__device__ __forceinline__ int wave_max(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, 64));
-  return v;
+// Stages n16 16-byte chunks from g into LDS at lds (one wave).
+__device__ __forceinline__ void stage16(const void* g, void* lds, int n16, int lane) {
+  for (int i = 0; i < n16; i += 64)
+    if (i + lane < n16) dma16((const uint8_t*)g + 16 * (i + lane), (uint8_t*)lds + 16 * i);
+}
+
+// x / f and x mod f for 1 <= f < 2^16 and x < f 2^16 (the quotient is below
+// 2^16): the fp32 estimate x * rcp(f) is within 2^-6 of x / f (relative error
+// at most about 2^-22 on a quotient below 2^16), so its truncation is off by
+// at most one and a single correction each way makes it exact.
+__device__ __forceinline__ uint32_t divmod16(uint32_t x, uint32_t f, uint32_t& r) {
+  uint32_t qd = (uint32_t)((float)x * __builtin_amdgcn_rcpf((float)f));
+  int32_t rr = (int32_t)(x - __umul24(qd, f));
+  if (rr < 0) {
+    --qd;
+    rr += (int32_t)f;
+  } else if (rr >= (int32_t)f) {
+    ++qd;
+    rr -= (int32_t)f;
+  }
+  r = (uint32_t)rr;
+  return qd;
 }
 
 }  // namespace
 
-__global__ __launch_bounds__(256) void k_rans_encode(const int16_t* q, const uint8_t* kidx, int64_t n, RansTab t,
-                                                   uint16_t* scratch, int64_t max_words, uint32_t* lens) {
-  const int lane = threadIdx.x & 63;
-  const int64_t s = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int64_t ns = (n + kRansStream - 1) / kRansStream;
-  if (s >= ns) return;  // whole waves
+// One wave (workgroup) per stream.  After staging, a parallel pass turns
+// every symbol into its table entry (start << 16 | frequency); the sequential
+// loop then reads one LDS word per step.
+__global__ __launch_bounds__(64) void k_rans_encode(const int16_t* q, const uint8_t* kidx, int64_t n,
+                                                  const uint16_t* tab, uint16_t* scratch, int64_t max_words,
+                                                  uint32_t* lens) {
+  __shared__ __align__(16) uint16_t st[kTabEncU16];
+  __shared__ __align__(16) uint32_t scf[kRansStream];
+  __shared__ __align__(16) int16_t sq[kRansStream];
+  __shared__ __align__(16) uint8_t sk[kRansStream];
+  const int lane = threadIdx.x;
+  const int64_t s = blockIdx.x;
   const int64_t base = s * kRansStream;
   const int cnt = (int)min((int64_t)kRansStream, n - base);
   const int steps = (cnt + 63) / 64;
+  stage16(tab, st, kTabEncU16 / 8, lane);
+  const int nq = cnt / 8, nk = cnt / 16;  // whole 16-byte chunks; q and k are 16-byte aligned
+  stage16(q + base, sq, nq, lane);
+  stage16(kidx + base, sk, nk, lane);
+  if (8 * nq + lane < cnt) sq[8 * nq + lane] = q[base + 8 * nq + lane];
+  if (16 * nk + lane < cnt) sk[16 * nk + lane] = kidx[base + 16 * nk + lane];
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  // table entry of every symbol (positions past cnt get values that are never used)
+  const uint16_t* sst = st + kTabStarts;
+#pragma unroll 8
+  for (int t = 0; t < steps; ++t) {
+    const int li = t * 64 + lane;
+    const int qv = sq[li];
+    const int k = min((int)sk[li], kCoderScales - 1);
+    const int R = st[k], o = st[kCoderScales + k];
+    const int i = (qv < -R || qv > R) ? 2 * R + 1 : qv + R;
+    const uint32_t c = sst[o + i], cn = sst[o + i + 1];
+    scf[li] = (c << 16) | ((cn - c) & 0xFFFFu);
+  }
+  __syncthreads();
   uint16_t* end = scratch + (s + 1) * max_words;
-  int64_t p = 0;  // words written, counted back from the end
+  const uint64_t below = (1ull << lane) - 1;
+  int p = 0;  // words written, counted back from the end
   uint32_t x = kRansL;
-  for (int st = steps - 1; st >= 0; --st) {
-    const int li = st * 64 + lane;
+  for (int t = steps - 1; t >= 0; --t) {
+    const int li = t * 64 + lane;
     const bool act = li < cnt;
-    int nsub = 0, nd = 1;
-    uint32_t ent = 0, v = 0;
-    bool neg = false;
-    if (act) {
-      const int qv = q[base + li];
-      const int k = min((int)kidx[base + li], kCoderScales - 1);
-      const int R = t.R[k];
-      const int off = t.off[k];
-      if (qv >= -R && qv <= R) {
-        ent = t.ent[off + qv + R];
-        nsub = 1;
-      } else {
-        ent = t.ent[off + 2 * R + 1];
-        neg = qv < 0;
-        v = (uint32_t)(abs(qv) - R - 1);
-        while (nd < 4 && v >= (1u << (4 * nd))) ++nd;
-        nsub = 3 + nd;
-      }
-    }
-    const int maxsub = wave_max(nsub);
-    for (int u = maxsub - 1; u >= 0; --u) {
-      const bool part = u < nsub;
-      const Sub sb = rans_sub(u, ent, neg, nd, v);
-      const bool emit = part && x >= (sb.f << 16);
-      const uint64_t m = __ballot(emit);
-      const int cw = __popcll(m);
-      if (emit) {
-        const int rank = __popcll(m & ((1ull << lane) - 1));
-        end[-(p + cw) + rank] = (uint16_t)(x & 0xFFFFu);
-        x >>= 16;
+    const uint32_t e = scf[li];
+    const uint32_t c = e >> 16, f = act ? (e & 0xFFFFu) : 1u;
+    const bool esc = act && c + f == 65536u;  // the last entry of a table is the escape
+    if (__ballot(esc)) {
+      // the field follows the escape in decoding order, so it is coded first;
+      // with frequency 1 every escaped state moves a word out
+      const uint64_t m = __ballot(esc);
+      const int cw = (int)__popcll(m);  // __popcll is unsigned: keep the slot arithmetic signed
+      if (esc) {
+        const int qv = sq[li];
+        const int R = st[min((int)sk[li], kCoderScales - 1)];
+        const uint32_t fld = (qv < 0 ? 32768u : 0u) + (uint32_t)(abs(qv) - R - 1);
+        end[(int)__popcll(m & below) - (p + cw)] = (uint16_t)(x & 0xFFFFu);
+        x = (x & 0xFFFF0000u) | fld;
       }
       p += cw;
-      if (part) x = (x / sb.f) * 65536u + (x % sb.f) + sb.c;
+    }
+    const bool emit = act && x >= (f << 16);
+    const uint64_t m = __ballot(emit);
+    const int cw = (int)__popcll(m);
+    if (emit) {
+      end[(int)__popcll(m & below) - (p + cw)] = (uint16_t)(x & 0xFFFFu);
+      x >>= 16;
+    }
+    p += cw;
+    if (act) {
+      uint32_t r;
+      const uint32_t qd = divmod16(x, f, r);
+      x = (qd << 16) + r + c;
     }
   }
   // the 64 final states open the stream: lane l at words 2l (high) and 2l + 1
@@ -212,87 +251,92 @@ __global__ __launch_bounds__(1024) void k_rans_index(const uint8_t* in, uint64_t
   }
 }
 
-__global__ __launch_bounds__(256) void k_rans_decode(const uint8_t* in, const uint8_t* kidx, int64_t n, RansTab t,
-                                                   const uint32_t* offs, const uint32_t* lens, int16_t* q,
-                                                   int32_t* status) {
-  const int lane = threadIdx.x & 63;
-  const int64_t s = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int64_t ns = (n + kRansStream - 1) / kRansStream;
-  if (s >= ns) return;
+// One wave (workgroup) per stream.  LDS holds the whole coder table block,
+// the stream's scale indices and the stream's words (word i at sw[par + i],
+// par the parity of the stream's start, so that whole dwords can be staged).
+__global__ __launch_bounds__(64) void k_rans_decode(const uint8_t* in, const uint8_t* kidx, int64_t n,
+                                                  const uint16_t* tab, const uint32_t* offs, const uint32_t* lens,
+                                                  int16_t* q, int32_t* status) {
+  __shared__ __align__(16) uint16_t st[kTabU16];
+  __shared__ __align__(16) uint8_t sk[kRansStream];
+  __shared__ __align__(16) uint16_t sw[kRansMaxWords + 2];
+  const int lane = threadIdx.x;
+  const int64_t s = blockIdx.x;
+  const int ns = (int)((n + kRansStream - 1) / kRansStream);
   const int64_t base = s * kRansStream;
   const int cnt = (int)min((int64_t)kRansStream, n - base);
   const int steps = (cnt + 63) / 64;
   const bool head_ok = status[0] == 0;  // status[0]: container check, status[1]: stream errors
-  const uint32_t len = head_ok ? lens[s] : 0u;
-  const uint16_t* w = (const uint16_t*)(in + rans_payload_offset((int)ns)) + (head_ok ? offs[s] : 0u);
   int err = 0;
-  auto word = [&](uint32_t i) -> uint32_t {
-    if (i < len) return w[i];
+  uint32_t len = head_ok ? lens[s] : 0u;
+  if (len > (uint32_t)kRansMaxWords) {
     err |= 2;
-    return 0u;
-  };
+    len = 0;
+  }
+  if (len < 128) err |= 2;
+  // the stream's words are u16 indices [g0, g1) of the container
+  const uint64_t g0 = (uint64_t)(rans_payload_offset(ns) / 2) + (head_ok ? offs[s] : 0u), g1 = g0 + len;
+  const int par = (int)(g0 & 1);
+  stage16(tab, st, kTabU16 / 8, lane);
+  const int nk = cnt / 16;  // k is 16-byte aligned
+  stage16(kidx + base, sk, nk, lane);
+  if (16 * nk + lane < cnt) sk[16 * nk + lane] = kidx[base + 16 * nk + lane];
+  {
+    // whole dwords d0 .. d1 - 1 inside [g0, g1); dword d lands at sw[2 (d - g0 / 2)]
+    const uint64_t d0 = (g0 + 1) / 2, d1 = g1 / 2;
+    const int nd = d1 > d0 ? (int)(d1 - d0) : 0;
+    const uint32_t* src = (const uint32_t*)in + d0;
+    uint16_t* dst = sw + 2 * (d0 - g0 / 2);
+    for (int i = 0; i < nd; i += 64)
+      if (i + lane < nd) dma4(src + i + lane, dst + 2 * i);
+    const uint16_t* in16 = (const uint16_t*)in;
+    if (lane == 0 && len > 0 && par) sw[1] = in16[g0];                          // odd first word
+    if (lane == 1 && len > 0 && (g1 & 1)) sw[par + len - 1] = in16[g1 - 1];   // odd last word
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  const uint16_t* sst = st + kTabStarts;
+  const uint16_t* sbk = st + kTabBuckets;
+  const uint64_t below = (1ull << lane) - 1;
+  auto word = [&](uint32_t i) -> uint32_t { return i < len ? (uint32_t)sw[par + i] : 0u; };
   uint32_t x = (word(2 * lane) << 16) | word(2 * lane + 1);
   uint32_t pos = 128;
-  // one decoding step of a sub-symbol with start c and frequency f, plus the
-  // lane-ordered renormalisation reads
-  auto advance = [&](bool part, uint32_t c, uint32_t f) {
-    if (part) x = f * (x >> 16) + (x & 0xFFFFu) - c;
-    const bool need = part && x < kRansL;
+  // lane-ordered renormalisation reads of the lanes in need
+  auto refill = [&](bool need) {
     const uint64_t m = __ballot(need);
-    if (need) x = (x << 16) | word(pos + __popcll(m & ((1ull << lane) - 1)));
-    pos += __popcll(m);
-  };
-  for (int st = 0; st < steps; ++st) {
-    const int li = st * 64 + lane;
-    const bool act = li < cnt;
-    int k = 0, R = 0, off = 0, qv = 0;
-    bool esc = false;
-    uint32_t c = 0, f = 1;
-    if (act) {
-      k = min((int)kidx[base + li], kCoderScales - 1);
-      R = t.R[k];
-      off = t.off[k];
-      // entry holding the slot: the bucket bounds it, a binary search finds it
-      const uint32_t slot = x & 0xFFFFu;
-      const int b = (int)(slot >> 8);
-      int lo = t.bkt[k * 257 + b], hi = t.bkt[k * 257 + b + 1];
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if ((t.ent[off + mid] >> 16) <= slot) lo = mid;
-        else hi = mid - 1;
-      }
-      const uint32_t e = t.ent[off + lo];
-      c = e >> 16;
-      f = e & 0xFFFFu;
-      esc = lo == 2 * R + 1;
-      qv = lo - R;
+    if (need) {
+      const uint32_t i = pos + (uint32_t)__popcll(m & below);
+      if (i >= len) err |= 2;
+      x = (x << 16) | word(i);
     }
-    advance(act, c, f);
+    pos += (uint32_t)__popcll(m);
+  };
+  for (int t = 0; t < steps; ++t) {
+    const int li = t * 64 + lane;
+    const bool act = li < cnt;
+    // positions past cnt read values that are never used; every index stays inside the tables
+    const int k = min((int)sk[li], kCoderScales - 1);
+    const int R = st[k], o = st[kCoderScales + k];
+    const uint32_t slot = x & 0xFFFFu;
+    // the bucket bounds the entry holding the slot; a binary search finds it
+    int lo = sbk[k * 257 + (slot >> 8)], hi = sbk[k * 257 + (slot >> 8) + 1];
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (sst[o + mid] <= slot) lo = mid;
+      else hi = mid - 1;
+    }
+    const uint32_t c = sst[o + lo], f = ((uint32_t)sst[o + lo + 1] - c) & 0xFFFFu;
+    const bool esc = act && lo == 2 * R + 1;
+    if (act) x = f * (x >> 16) + slot - c;
+    refill(act && x < kRansL);
+    int qv = lo - R;
     if (__ballot(esc)) {
-      bool neg = false;
-      int nd = 0;
-      uint32_t v = 0;
-      // sign, digit count
-      {
-        const uint32_t u = esc ? (x & 0xFFFFu) >> 15 : 0u;
-        advance(esc, u * 32768u, 32768u);
-        neg = u != 0;
-      }
-      {
-        const uint32_t u = esc ? (x & 0xFFFFu) >> 14 : 0u;
-        advance(esc, u * 16384u, 16384u);
-        nd = (int)u + 1;
-      }
-      const int maxd = wave_max(esc ? nd : 0);
-      for (int d = 0; d < maxd; ++d) {
-        const bool part = esc && d < nd;
-        const uint32_t u = part ? (x & 0xFFFFu) >> 12 : 0u;
-        advance(part, u * 4096u, 4096u);
-        if (part) v = v * 16u + u;
-      }
+      const uint32_t fld = x & 0xFFFFu;
+      if (esc) x >>= 16;
+      refill(esc);
       if (esc) {
-        const int mag = R + 1 + (int)v;
-        qv = neg ? -mag : mag;
+        const int mag = R + 1 + (int)(fld & 32767u);
+        qv = (fld >> 15) ? -mag : mag;
       }
     }
     if (act) q[base + li] = (int16_t)max(min(qv, 32767), -32768);
@@ -303,26 +347,26 @@ __global__ __launch_bounds__(256) void k_rans_decode(const uint8_t* in, const ui
 
 __global__ void k_rans_status(const int32_t* status, int32_t* out) { *out = status[0] | status[1]; }
 
-hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const RansTab& t, uint16_t* scratch,
+hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const uint16_t* tab, uint16_t* scratch,
                               int64_t max_words, uint32_t* lens, uint32_t* offs, uint8_t* out, uint64_t* nbytes,
                               hipStream_t st) {
   const int64_t ns = (n + kRansStream - 1) / kRansStream;
   if (ns <= 0 || ns > 65535) return hipErrorInvalidValue;
-  launch(k_rans_encode, dim3((unsigned)((ns + 3) / 4)), dim3(256), st, q, k, n, t, scratch, max_words, lens);
+  launch(k_rans_encode, dim3((unsigned)ns), dim3(64), st, q, k, n, tab, scratch, max_words, lens);
   launch(k_rans_frame, dim3(1), dim3(1024), st, (const uint32_t*)lens, n, offs, out, nbytes);
   launch(k_rans_pack, dim3((unsigned)ns), dim3(256), st, (const uint16_t*)scratch, max_words, (const uint32_t*)lens,
          (const uint32_t*)offs, n, out);
   return hipGetLastError();
 }
 
-hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const RansTab& t,
+hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const uint16_t* tab,
                               uint32_t* offs, uint32_t* lens, int16_t* q, int32_t* status, int32_t* status_out,
                               hipStream_t st) {
   const int64_t ns = (n + kRansStream - 1) / kRansStream;
   if (ns <= 0 || ns > 65535) return hipErrorInvalidValue;
   launch(k_rans_index, dim3(1), dim3(1024), st, in, in_bytes, n, offs, lens, status);
-  launch(k_rans_decode, dim3((unsigned)((ns + 3) / 4)), dim3(256), st, in, k, n, t, (const uint32_t*)offs,
-         (const uint32_t*)lens, q, status);
+  launch(k_rans_decode, dim3((unsigned)ns), dim3(64), st, in, k, n, tab, (const uint32_t*)offs, (const uint32_t*)lens,
+         q, status);
   if (status_out) launch(k_rans_status, dim3(1), dim3(1), st, (const int32_t*)status, status_out);
   return hipGetLastError();
 }

@@ -219,7 +219,7 @@ def ncodec_destroy(ctx) -> None:
 def _capacity(n: int) -> int:
     """Worst-case container bytes for n symbols (the ABI's bound)."""
     ns = (n + 8191) // 8192
-    return 20 + 4 * ((ns + 1) // 2) + ns * (128 + 7 * 8192) * 2
+    return 20 + 4 * ((ns + 1) // 2) + ns * (128 + 2 * 8192) * 2
 
 
 # ---------------------------------------------------------------- convenience

@@ -120,11 +120,12 @@ def test_null_context_calls(lib):
 
 def test_stream_capacity_is_the_worst_case_bound():
     # 20-byte header, 2 bytes per stream length (padded to 4), and per stream of
-    # 8192 symbols 64 two-word final states plus at most 7 words per symbol
+    # 8192 symbols 64 two-word final states plus at most 2 words per symbol (one
+    # per sub-symbol: the table entry and, for an escape, the 16-bit field)
     for H, W, C in [(64, 64, 64), (480, 832, 128), (1088, 1920, 256)]:
         n = (H // 16) * (W // 16) * C
         ns = -(-n // 8192)
-        want = 20 + 4 * ((ns + 1) // 2) + ns * (128 + 7 * 8192) * 2
+        want = 20 + 4 * ((ns + 1) // 2) + ns * (128 + 2 * 8192) * 2
         assert nc.ncodec_stream_capacity(nc.make_config(H, W, C, 1, 1, "fp16")) == want
         assert nc._capacity(n) == want
     assert nc.ncodec_stream_capacity(nc.make_config(63, 64, 64, 1, 1, "fp16")) == 0

@@ -33,7 +33,7 @@ def test_scale_index_is_the_smallest_covering_scale():
 def test_tables_are_valid_quantised_gaussians(j):
     R, f, c = E.table(j)
     sigma = float(E.scale_table()[j])
-    assert R == int(np.ceil(8.0 * sigma))
+    assert R == max(int(np.ceil(8.0 * sigma)), 32)
     n = 2 * R + 2
     assert len(f) == n and np.all(f >= 1) and int(f.sum()) == E.M
     assert np.array_equal(c, np.concatenate([[0], np.cumsum(f)[:-1]]))
@@ -50,16 +50,45 @@ def test_tables_are_valid_quantised_gaussians(j):
 
 
 def test_worked_example_one_symbol():
-    # Scale 0 has R = 1 and frequencies [1, 65533, 1, 1] for q = -1, 0, 1, ESC (starts 0, 1, 65534, 65535).
+    # Scale 0 (sigma 0.11) has R = 32: every symbol but q = 0 has probability
+    # below 2^-17, so f = 1 for q = -32 .. -1, 1 .. 32 and ESC, and
+    # f(0) = 65536 - 65 = 65471 with start 32.
     R, f, c = E.table(0)
-    assert R == 1 and list(f) == [1, 65533, 1, 1]
-    # Encoding q = 0 from x = 65536: no renormalisation (65536 < 65533 * 65536);
-    # x = (65536 div 65533) * 65536 + (65536 mod 65533) + 1 = 65536 + 3 + 1 = 65540.
-    # Lane 0 ends at 65540 -> words (1, 4); the other 63 lanes stay at 65536 -> (1, 0).
+    assert R == 32 and f[R] == 65471 and c[R] == 32 and np.all(np.delete(f, R) == 1)
+    # Encoding q = 0 from x = 65536: no renormalisation (65536 < 65471 * 65536);
+    # x = (65536 div 65471) * 65536 + (65536 mod 65471) + 32 = 65536 + 65 + 32 = 65633.
+    # Lane 0 ends at 65633 -> words (1, 97); the other 63 lanes stay at 65536 -> (1, 0).
     words = E.encode_stream(np.array([0]), np.array([0]))
-    assert words == [1, 4] + [1, 0] * 63
+    assert words == [1, 97] + [1, 0] * 63
     q, ok = E.decode_stream(words, np.array([0]))
     assert ok and list(q) == [0]
+
+
+def test_worked_example_escape():
+    # q = -40 at scale 0 escapes (|q| > R = 32): ESC (start 65535, f 1), then the
+    # field 32768 + (40 - 33) = 32775 with f = 1.  From x = 65536: the field
+    # needs renormalisation (65536 >= 1 * 65536): word 0, x = 1, then
+    # x = 1 * 65536 + 0 + 32775 = 98311; ESC: again 98311 >= 65536: word
+    # 98311 mod 65536 = 32775, x = 1, then x = 65536 + 65535 = 131071.
+    # Decoding order: states (131071 -> 1, 65535), then the words of ESC's
+    # renormalisation (32775), then the field's (0).
+    words = E.encode_stream(np.array([-40]), np.array([0]))
+    assert words == [1, 65535] + [1, 0] * 63 + [32775, 0]
+    q, ok = E.decode_stream(words, np.array([0]))
+    assert ok and list(q) == [-40]
+
+
+def test_all_escape_stream_meets_the_two_word_bound():
+    # Every symbol escapes at the smallest scale: each sub-symbol moves at most
+    # one word, so a full stream holds at most 128 + 2 * 8192 words; with
+    # frequency 1 the field always moves one, so the bound is nearly reached.
+    rng = np.random.default_rng(9)
+    q = rng.integers(33, 32768, E.STREAM) * rng.choice([-1, 1], E.STREAM)
+    k = np.zeros(E.STREAM, dtype=np.int64)
+    words = E.encode_stream(q, k)
+    assert 128 + 2 * E.STREAM - 64 <= len(words) <= 128 + 2 * E.STREAM
+    out, ok = E.decode_stream(words, k)
+    assert ok and np.array_equal(out, q)
 
 
 def _symbols(n, seed, esc_every=0):
