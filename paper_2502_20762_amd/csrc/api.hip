@@ -299,7 +299,7 @@ struct Layout {
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
   // entropy coder: scale indices, symbols, per-stream scratch, lengths,
   // offsets, status words, byte count
-  size_t kmap, qtmp, rscratch, rlens, roffs, rstatus, rbytes;
+  size_t kmap, qtmp, rscratch, rlens, rerrs, rcount;
   int64_t n_sym, n_streams;
   int n_partials;
   size_t total;
@@ -333,13 +333,19 @@ void build_coder_tables(Image& img, Layout& L, bool is_int, std::string* err) {
       sum += f[i];
     }
     f[R] += 65536 - sum;
-    tab[j] = (uint16_t)R;
-    tab[NS + j] = (uint16_t)(tab.size() - kTabStarts);
+    int T = 0, U = 0;
+    while (T < n && f[T] == 1) ++T;
+    while (U < n && f[n - 1 - U] == 1) ++U;
+    tab[4 * j] = (uint16_t)R;
+    tab[4 * j + 1] = (uint16_t)(tab.size() - kTabStarts);
+    tab[4 * j + 2] = (uint16_t)T;
+    tab[4 * j + 3] = (uint16_t)U;
     uint32_t start = 0;
     int b = 0;
     for (int i = 0; i < n; ++i) {
       tab.push_back((uint16_t)start);
-      while (b < 256 && (uint32_t)(256 * b) < start + (uint32_t)f[i]) bkt[(size_t)j * 257 + b++] = (uint16_t)i;
+      while (b < 256 && std::max<uint32_t>(256u * b, (uint32_t)T) < start + (uint32_t)f[i])
+        bkt[(size_t)j * 257 + b++] = (uint16_t)i;
       start += (uint32_t)f[i];
     }
     tab.push_back(0);  // closing start, 2^16 mod 2^16
@@ -442,9 +448,8 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.qtmp = alloc((size_t)L.n_sym * 2);
   L.rscratch = alloc((size_t)L.n_streams * kRansMaxWords * 2);
   L.rlens = alloc((size_t)L.n_streams * 4);
-  L.roffs = alloc((size_t)L.n_streams * 4);
-  L.rstatus = alloc(8);
-  L.rbytes = alloc(8);
+  L.rerrs = alloc((size_t)L.n_streams * 4);
+  L.rcount = alloc(4);  // decoder ticket counter: zeroed at create, left at zero by every decode
   L.total = off;
   return pk.ok;
 }
@@ -972,8 +977,7 @@ ncodec_status ncodec_rans_encode(ncodec_ctx* ctx, const int16_t* d_q, const uint
   const Layout& L = ctx->L;
   NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
            return launch_rans_encode(d_q, d_k, n, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch), kRansMaxWords,
-                                     ctx->p<uint32_t>(L.rlens), ctx->p<uint32_t>(L.roffs), (uint8_t*)d_stream,
-                                     d_stream_bytes, ctx->stream);
+                                     ctx->p<uint32_t>(L.rlens), (uint8_t*)d_stream, d_stream_bytes, ctx->stream);
          }),
          "rans encode");
   return NCODEC_OK;
@@ -990,8 +994,7 @@ ncodec_status ncodec_rans_decode(ncodec_ctx* ctx, const void* d_stream, size_t s
   const Layout& L = ctx->L;
   NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
            return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, d_k, n, rans_tab(ctx),
-                                     ctx->p<uint32_t>(L.roffs), ctx->p<uint32_t>(L.rlens), d_q,
-                                     ctx->p<int32_t>(L.rstatus), d_status, ctx->stream);
+                                     ctx->p<uint32_t>(L.rerrs), ctx->p<uint32_t>(L.rcount), d_q, d_status, ctx->stream);
          }),
          "rans decode");
   return NCODEC_OK;
@@ -1012,8 +1015,8 @@ ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, in
   if (st) return st;
   NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
            return launch_rans_encode(q, ctx->p<uint8_t>(L.kmap), L.n_sym, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch),
-                                     kRansMaxWords, ctx->p<uint32_t>(L.rlens), ctx->p<uint32_t>(L.roffs),
-                                     (uint8_t*)d_stream, d_stream_bytes, ctx->stream);
+                                     kRansMaxWords, ctx->p<uint32_t>(L.rlens), (uint8_t*)d_stream, d_stream_bytes,
+                                     ctx->stream);
          }),
          "rans encode");
   ctx->cur = 1 - ctx->cur;
@@ -1032,8 +1035,8 @@ ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, s
   if (st) return st;
   NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
            return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, ctx->p<uint8_t>(L.kmap), L.n_sym,
-                                     rans_tab(ctx), ctx->p<uint32_t>(L.roffs), ctx->p<uint32_t>(L.rlens),
-                                     ctx->p<int16_t>(L.qtmp), ctx->p<int32_t>(L.rstatus), d_status, ctx->stream);
+                                     rans_tab(ctx), ctx->p<uint32_t>(L.rerrs), ctx->p<uint32_t>(L.rcount),
+                                     ctx->p<int16_t>(L.qtmp), d_status, ctx->stream);
          }),
          "rans decode");
   st = enqueue_decode(ctx, ctx->p<int16_t>(L.qtmp), d_frame_out);

@@ -111,25 +111,27 @@ __host__ __device__ constexpr int rans_payload_offset(int ns) { return kRansHead
 
 // Coder tables: one block of uint16 in the weights image (16-byte aligned),
 // staged whole into LDS by the coder kernels.
-//   [0, 64)              R_j
-//   [64, 128)            first start of scale j (index into the starts)
-//   [128, 128 + STARTS)  starts: per scale the 2 R_j + 2 entry starts
+//   [4 j .. 4 j + 3]     scale j: R_j, index of its first start, T_j and U_j,
+//                        the numbers of leading and trailing entries of
+//                        frequency 1 (entry i < T_j covers slot i alone, the
+//                        last U_j entries the last U_j slots)
+//   [256, 256 + STARTS)  starts: per scale the 2 R_j + 2 entry starts
 //                        (q = -R .. R, then the escape) and a closing 0
 //                        (standing for 2^16), so f_i = (start_{i+1} - start_i) mod 2^16
-//   then [NS][257]       buckets: entry holding slot 256 b (b < 256); [256] = last entry
+//   then [NS][257]       buckets: entry holding slot max(256 b, T_j) (b < 256);
+//                        [256] = last entry
 constexpr int kCoderStarts = 36976;  // sum over j of 2 R_j + 3
-constexpr int kTabStarts = 128;
+constexpr int kTabStarts = 4 * kCoderScales;
 constexpr int kTabBuckets = kTabStarts + kCoderStarts;
 constexpr int kTabEncU16 = kTabBuckets;                       // what the encoder stages
 constexpr int kTabU16 = kTabBuckets + kCoderScales * 257;     // what the decoder stages
 static_assert(kTabEncU16 % 8 == 0 && kTabU16 % 8 == 0, "coder table block must be whole 16-byte chunks");
 
 hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, const uint16_t* tab, uint16_t* scratch,
-                              int64_t max_words, uint32_t* lens, uint32_t* offs, uint8_t* out, uint64_t* nbytes,
-                              hipStream_t st);
+                              int64_t max_words, uint32_t* lens, uint8_t* out, uint64_t* nbytes, hipStream_t st);
+// errs: one word per stream; count: a zero-initialised ticket counter, left at zero
 hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const uint16_t* tab,
-                              uint32_t* offs, uint32_t* lens, int16_t* q, int32_t* status, int32_t* status_out,
-                              hipStream_t st);
+                              uint32_t* errs, uint32_t* count, int16_t* q, int32_t* status_out, hipStream_t st);
 
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
