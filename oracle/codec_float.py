@@ -23,7 +23,7 @@ import numpy as np
 
 from . import bits as _bits
 from .ops import (conv1x1, conv2x2s2, dwconv3x3, leaky_relu, pixel_shuffle,
-                  pixel_unshuffle)
+                  pixel_unshuffle, wsilu)
 from .params import Params
 
 
@@ -40,10 +40,16 @@ def zero_state(p: Params, height: int, width: int) -> State:
 
 
 def dc_block(z: np.ndarray, blk) -> np.ndarray:
-    """z + pw2(LeakyReLU_0.1(pw1(dw3x3(z))))."""
+    """LeakyReLU block: z + pw2(LeakyReLU_0.1(pw1(dw3x3(z)))).
+    Gated block (Supp. B.1: WSiLU, Chunk): h = pw1(dw3x3(z)) is chunked on
+    channels into (h1, h2) and z + pw2(WSiLU(h1) * h2)."""
     a = dwconv3x3(z, blk.dw.w, blk.dw.b)
     h = conv1x1(a, blk.pw1.w, blk.pw1.b)
-    g = leaky_relu(h, 0.1)
+    if blk.kind == "gated":
+        C = z.shape[0]
+        g = wsilu(h[:C]) * h[C:]
+    else:
+        g = leaky_relu(h, 0.1)
     return z + conv1x1(g, blk.pw2.w, blk.pw2.b)
 
 

@@ -25,6 +25,7 @@ from __future__ import annotations
 import dataclasses
 
 import numpy as np
+from scipy.special import expit
 
 from . import bits as _bits
 from .ops import pixel_shuffle, pixel_unshuffle
@@ -124,11 +125,38 @@ def int_leaky_relu(h: np.ndarray) -> np.ndarray:
     return np.where(h >= 0, h, rhe_shift(LRELU_SLOPE_I * h, K2_SHIFT))
 
 
+_SIGMOID = None
+
+
+def sigmoid_table() -> np.ndarray:
+    """The int16 -> int16 sigmoid table of the integer WSiLU (Sec. 4.5: a
+    precomputed lookup table handles the sigmoid): entry v + 32768 is
+    round(K1 * sigmoid(4 v / K1)), the sigmoid of the K1-scaled input with the
+    WSiLU weight alpha = 4 (Supp. B.1), itself K1-scaled (0 .. 512)."""
+    global _SIGMOID
+    if _SIGMOID is None:
+        v = np.arange(-32768, 32768, dtype=np.float64)
+        _SIGMOID = np.rint(K1 * expit(4.0 * v / K1)).astype(np.int64)
+    return _SIGMOID
+
+
+def int_wsilu(h: np.ndarray) -> np.ndarray:
+    """round(h * S[h] / K1): |h S[h]| <= 2^24, the result is within int16."""
+    return rhe_shift(h * sigmoid_table()[h + 32768], 9)
+
+
+def int_gate(h1: np.ndarray, h2: np.ndarray) -> np.ndarray:
+    """clip(round(WSiLU(h1) * h2 / K1)): the product of two K1-scaled values
+    rescaled by K1 (|product| < 2^30)."""
+    return clip16(rhe_shift(int_wsilu(h1) * h2, 9))
+
+
 @dataclasses.dataclass
 class IBlock:
     dw: IConv
     pw1: IConv
     pw2: IConv
+    kind: str = "lrelu"
 
 
 @dataclasses.dataclass
@@ -146,7 +174,7 @@ class IParams:
 
 
 def integerize(p: Params) -> IParams:
-    blk = lambda b: IBlock(iconv(b.dw), iconv(b.pw1), iconv(b.pw2))  # noqa: E731
+    blk = lambda b: IBlock(iconv(b.dw), iconv(b.pw1), iconv(b.pw2), b.kind)  # noqa: E731
     return IParams(p.C, iconv(p.pe), iconv(p.fuse_enc), [blk(b) for b in p.enc],
                    iconv(p.down), iconv(p.head), iconv(p.up), iconv(p.fuse_dec),
                    [blk(b) for b in p.dec], iconv(p.rec))
@@ -167,7 +195,11 @@ def zero_state(ip: IParams, height: int, width: int) -> State:
 def dc_block(z: np.ndarray, b: IBlock) -> np.ndarray:
     a = int_dwconv3x3(z, b.dw)
     h = int_conv1x1(a, b.pw1, "pw1")
-    g = int_leaky_relu(h)
+    if b.kind == "gated":
+        C = z.shape[0]
+        g = int_gate(h[:C], h[C:])
+    else:
+        g = int_leaky_relu(h)
     p = int_conv1x1(g, b.pw2, "pw2")
     return clip16(z + p)
 

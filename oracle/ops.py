@@ -6,6 +6,7 @@ Each is the textbook definition; pins live in ``tests/test_oracle_ops.py``
 from __future__ import annotations
 
 import numpy as np
+from scipy.special import expit
 
 
 def pixel_unshuffle(x: np.ndarray, r: int) -> np.ndarray:
@@ -69,3 +70,8 @@ def conv2x2s2(x: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
 
 def leaky_relu(h: np.ndarray, slope: float = 0.1) -> np.ndarray:
     return np.where(h >= 0.0, h, slope * h)
+
+
+def wsilu(x: np.ndarray, alpha: float = 4.0) -> np.ndarray:
+    """Weighted SiLU of Supp. B.1: x * sigmoid(alpha x), alpha = 4 by default."""
+    return x * expit(alpha * x)

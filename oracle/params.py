@@ -3,7 +3,8 @@
 Order (each weight row-major, each followed by its bias):
   pe        W(C,192)   b(C)
   fuse_enc  W(C,2C)    b(C)      input channels [e ; f_prev]
-  enc[k]    dw W(C,3,3) b(C); pw1 W(2C,C) b(2C); pw2 W(C,2C) b(C)   k < N_e
+  enc[k]    dw W(C,3,3) b(C); pw1 W(2C,C) b(2C); pw2 W(C,H) b(C)    k < N_e
+            (H = 2C for the LeakyReLU block, C for the gated block)
   down      W(C,C,2,2) b(C)
   head      W(2C,C)    b(2C)     rows [mu ; s]
   up        W(4C,C)    b(4C)     row 4c+2i+j -> pixel-shuffle position (c,i,j)
@@ -29,6 +30,7 @@ class Block:
     dw: Conv
     pw1: Conv
     pw2: Conv
+    kind: str = "lrelu"   # "lrelu" or "gated"
 
 
 @dataclasses.dataclass
@@ -43,19 +45,26 @@ class Params:
     fuse_dec: Conv
     dec: list
     rec: Conv
+    block: str = "lrelu"
 
 
-def count(C: int, n_enc: int, n_dec: int) -> int:
-    blk = C * 9 + C + 2 * C * C + 2 * C + C * 2 * C + C
+def _hidden(C: int, block: str) -> int:
+    if block not in ("lrelu", "gated"):
+        raise ValueError(f"unknown block form {block!r}")
+    return 2 * C if block == "lrelu" else C
+
+
+def count(C: int, n_enc: int, n_dec: int, block: str = "lrelu") -> int:
+    blk = C * 9 + C + 2 * C * C + 2 * C + C * _hidden(C, block) + C
     return (C * 192 + C + C * 2 * C + C + n_enc * blk + C * C * 4 + C
             + 2 * C * C + 2 * C + 4 * C * C + 4 * C + C * 2 * C + C
             + n_dec * blk + 192 * C + 192)
 
 
-def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int) -> Params:
+def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu") -> Params:
     flat = np.asarray(flat, dtype=np.float64).reshape(-1)
-    if flat.size != count(C, n_enc, n_dec):
-        raise ValueError(f"expected {count(C, n_enc, n_dec)} parameters, got {flat.size}")
+    if flat.size != count(C, n_enc, n_dec, block):
+        raise ValueError(f"expected {count(C, n_enc, n_dec, block)} parameters, got {flat.size}")
     pos = 0
 
     def take(shape):
@@ -70,17 +79,17 @@ def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int) -> Params:
         b = take((wshape[0],))
         return Conv(w, b)
 
-    def block():
-        return Block(conv((C, 3, 3)), conv((2 * C, C)), conv((C, 2 * C)))
+    def blk():
+        return Block(conv((C, 3, 3)), conv((2 * C, C)), conv((C, _hidden(C, block))), block)
 
     pe = conv((C, 192))
     fuse_enc = conv((C, 2 * C))
-    enc = [block() for _ in range(n_enc)]
+    enc = [blk() for _ in range(n_enc)]
     down = conv((C, C, 2, 2))
     head = conv((2 * C, C))
     up = conv((4 * C, C))
     fuse_dec = conv((C, 2 * C))
-    dec = [block() for _ in range(n_dec)]
+    dec = [blk() for _ in range(n_dec)]
     rec = conv((192, C))
     assert pos == flat.size
-    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec)
+    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec, block)

@@ -61,36 +61,42 @@ PRESETS = {
 }
 
 
-def param_list(channels: int, n_enc: int, n_dec: int):
-    """(name, shape, fan_in, kind) in canonical order; kind is 'w', 'w_res' or 'b'."""
+def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu"):
+    """(name, shape, fan_in, kind) in canonical order; kind is 'w', 'w_res' or 'b'.
+
+    ``block`` is the DC-block form: "lrelu" (pw2 is C x 2C) or "gated" (the
+    hidden 2C channels are chunked into two halves and gated, pw2 is C x C)."""
     C = channels
     out = []
+    if block not in ("lrelu", "gated"):
+        raise ValueError(f"unknown block form {block!r}")
+    hid = 2 * C if block == "lrelu" else C
 
     def conv(name, wshape, fan_in, kind="w"):
         out.append((name + ".w", wshape, fan_in, kind))
         out.append((name + ".b", (wshape[0],), fan_in, "b"))
 
-    def block(prefix):
+    def block_params(prefix):
         conv(prefix + ".dw", (C, 3, 3), 9)
         conv(prefix + ".pw1", (2 * C, C), C)
-        conv(prefix + ".pw2", (C, 2 * C), 2 * C, "w_res")
+        conv(prefix + ".pw2", (C, hid), hid, "w_res")
 
     conv("pe", (C, 192), 192)
     conv("fuse_enc", (C, 2 * C), 2 * C)
     for k in range(n_enc):
-        block(f"enc{k}")
+        block_params(f"enc{k}")
     conv("down", (C, C, 2, 2), 4 * C)
     conv("head", (2 * C, C), C)
     conv("up", (4 * C, C), C)
     conv("fuse_dec", (C, 2 * C), 2 * C)
     for k in range(n_dec):
-        block(f"dec{k}")
+        block_params(f"dec{k}")
     conv("rec", (192, C), C)
     return out
 
 
 def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
-                 resid_gain: float = RESID_GAIN) -> np.ndarray:
+                 resid_gain: float = RESID_GAIN, block: str = "lrelu") -> np.ndarray:
     """Flat float32 parameter vector; every value is exactly fp16-representable.
 
     Weights ~ N(0, 1/fan_in) (the residual projection times ``resid_gain``),
@@ -98,7 +104,7 @@ def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
     """
     rng = np.random.default_rng(seed)
     chunks = []
-    for _name, shape, fan_in, kind in param_list(channels, n_enc, n_dec):
+    for _name, shape, fan_in, kind in param_list(channels, n_enc, n_dec, block):
         if kind == "b":
             v = rng.uniform(-0.1, 0.1, size=shape)
         else:
