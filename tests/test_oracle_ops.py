@@ -182,6 +182,7 @@ def test_dc_block_matches_torch_composition():
 
     blk = P()
     blk.dw, blk.pw1, blk.pw2 = P(), P(), P()
+    blk.kind = "lrelu"
     blk.dw.w, blk.dw.b = r.standard_normal((C, 3, 3)), r.standard_normal(C)
     blk.pw1.w, blk.pw1.b = r.standard_normal((2 * C, C)), r.standard_normal(2 * C)
     blk.pw2.w, blk.pw2.b = r.standard_normal((C, 2 * C)), r.standard_normal(C)
