@@ -65,6 +65,14 @@ typedef enum {
 
 typedef enum { NCODEC_PATH_FP16 = 0, NCODEC_PATH_INT16 = 1 } ncodec_path;
 
+/* Form of the DC block (Supp. B.1).  LRELU: z + pw2(LeakyReLU_0.1(pw1(dw(z))))
+ * with pw2 2C -> C.  GATED: h = pw1(dw(z)) is chunked on channels into
+ * (h1, h2) and the block returns z + pw2(WSiLU(h1) * h2), WSiLU(x) =
+ * x sigmoid(4x), pw2 C -> C; on the int path the sigmoid is the int16 table
+ * S[v] = round(512 sigmoid(4 v / 512)) (Sec. 4.5), WSiLU_i = round(h1 S[h1] / 512)
+ * and the gate clip(round(WSiLU_i h2 / 512)). */
+typedef enum { NCODEC_BLOCK_LRELU = 0, NCODEC_BLOCK_GATED = 1 } ncodec_block;
+
 typedef struct {
   int32_t height;        /* H, multiple of 16, 16..8192 (caller pads 1080 -> 1088) */
   int32_t width;         /* W, multiple of 16, 16..8192                             */
@@ -72,13 +80,15 @@ typedef struct {
   int32_t n_enc_blocks;  /* N_e, 0..32                                              */
   int32_t n_dec_blocks;  /* N_d, 0..32                                              */
   int32_t path;          /* ncodec_path                                             */
+  int32_t block;         /* ncodec_block (0 = LRELU)                                */
 } ncodec_config;
 
 /* Number of float32 values in the canonical parameter list for cfg, or 0 if
  * cfg is invalid.  Canonical order (each weight row-major, followed by its
  * bias): pe W(C,192) b(C); fuse_enc W(C,2C) b(C) with input channels
  * [e ; f_prev]; N_e blocks of {dw W(C,3,3) b(C); pw1 W(2C,C) b(2C);
- * pw2 W(C,2C) b(C)}; down W(C,C,2,2) b(C); head W(2C,C) b(2C) with rows
+ * pw2 W(C,2C) b(C), or W(C,C) b(C) for the GATED block, whose pw1 rows are
+ * [h1 ; h2]}; down W(C,C,2,2) b(C); head W(2C,C) b(2C) with rows
  * [mu ; s]; up W(4C,C) b(4C), row 4c+2i+j -> pixel-shuffle position (c,i,j);
  * fuse_dec W(C,2C) b(C) with input channels [d ; f_prev]; N_d blocks;
  * rec W(192,C) b(192), row 64c+8i+j -> colour c at pixel (8y+i, 8x+j).

@@ -45,12 +45,17 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "path must be NCODEC_PATH_FP16 or NCODEC_PATH_INT16";
     return false;
   }
+  if (c->block != NCODEC_BLOCK_LRELU && c->block != NCODEC_BLOCK_GATED) {
+    if (why) *why = "block must be NCODEC_BLOCK_LRELU or NCODEC_BLOCK_GATED";
+    return false;
+  }
   return true;
 }
 
 size_t weight_count(const ncodec_config& c) {
   const size_t C = (size_t)c.channels;
-  const size_t blk = C * 9 + C + 2 * C * C + 2 * C + 2 * C * C + C;
+  const size_t hid = c.block == NCODEC_BLOCK_GATED ? C : 2 * C;  // pw2 input channels
+  const size_t blk = C * 9 + C + 2 * C * C + 2 * C + C * hid + C;
   return C * 192 + C + 2 * C * C + C + c.n_enc_blocks * blk + 4 * C * C + C + 2 * C * C + 2 * C + 4 * C * C + 4 * C +
          2 * C * C + C + c.n_dec_blocks * blk + 192 * C + 192;
 }
@@ -146,12 +151,13 @@ struct Packer {
 
   BlockDev block(const float*& cur) {
     const int C = cfg.channels;
+    const bool gated = cfg.block == NCODEC_BLOCK_GATED;
     BlockDev d;
     const float* dw = cur; cur += (size_t)C * 9;
     const float* dwb = cur; cur += C;
     const float* w1 = cur; cur += (size_t)2 * C * C;
     const float* b1 = cur; cur += 2 * C;
-    const float* w2 = cur; cur += (size_t)2 * C * C;
+    const float* w2 = cur; cur += (size_t)C * (gated ? C : 2 * C);
     const float* b2 = cur; cur += C;
     if (!is_int) {
       // fp16: 48 bytes per channel pair (c, c+1): 9 taps as (w_c, w_c+1) fp16
@@ -196,6 +202,17 @@ struct Packer {
         }
         o[22] = o[23] = 0;
       }
+    }
+    if (gated) {
+      // Gated block: pw1 as a pointwise GEMM whose packed rows come in passes
+      // of 64, the 32 h1 rows of channels 32 t .. 32 t + 31 then their 32 h2
+      // rows (so one pass holds both halves of the chunk for the gate
+      // epilogue); pw2 is a plain C x C GEMM.
+      d.pw1 = gemm(w1, b1, 2 * C, C, C,
+                   [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
+                   [](int k) { return k; });
+      d.pw2 = plain(w2, b2, C, C);
+      return d;
     }
     if (!is_int) {
       // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1
@@ -292,6 +309,8 @@ struct Layout {
   ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
   std::vector<BlockDev> enc, dec;
   size_t sigma_tab = 0;
+  size_t sig_tab = 0;  // int path, gated block: int16 sigmoid table
+  size_t zC = 0;       // gated block: hidden buffer
   // entropy coder tables
   size_t c_scales = 0, c_tab = 0, c_ktab = 0;
   size_t image_bytes = 0;
@@ -411,6 +430,16 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
     if (err) *err = "internal: parameter walk mismatch";
     return false;
   }
+  if (is_int && cfg.block == NCODEC_BLOCK_GATED) {
+    // S[v] = RHE(512 sigmoid(4 v / 512)) for every int16 v (the WSiLU's
+    // sigmoid, K1-scaled in and out); no entry lies within 1e-6 of a rounding tie
+    L.sig_tab = img.add(65536 * 2);
+    int16_t* st = img.at<int16_t>(L.sig_tab);
+    for (int i = 0; i < 65536; ++i) {
+      const double v = (double)(i - 32768);
+      st[i] = (int16_t)std::nearbyint(512.0 / (1.0 + std::exp(-4.0 * v / 512.0)));
+    }
+  }
   if (is_int) {
     L.sigma_tab = img.add(65536 * 4);
     float* tab = img.at<float>(L.sigma_tab);
@@ -436,6 +465,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.feat[0] = alloc(fb); L.feat[1] = alloc(fb);
   L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
+  if (cfg.block == NCODEC_BLOCK_GATED) L.zC = alloc(fb);
   L.y = alloc(lb);
   const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
@@ -578,6 +608,35 @@ PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
   return a;
 }
 
+// One gated DC block (Supp. B.1 with WSiLU and Chunk) as three launches:
+// depthwise z -> ed, pw1 with the gate epilogue ed -> zC, pw2 with the
+// residual epilogue (zC, z) -> dst.  ed and zC are free while the blocks run.
+hipError_t gated_block(ncodec_ctx* ctx, const BlockDev& b, const void* z, void* dst) {
+  const int C = ctx->cfg.channels;
+  const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
+  const Layout& L = ctx->L;
+  hipError_t e = timed(ctx, "dw", [&] {
+    return ctx->is_int() ? launch_dw_i16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream)
+                         : launch_dw_f16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream);
+  });
+  if (e != hipSuccess) return e;
+  PwArgs a = conv_args(ctx, b.pw1, C, 2 * C, h8 * w8);
+  a.src0 = ctx->p(L.ed);
+  a.C0 = C;
+  a.dst = ctx->p(L.zC);
+  a.Cdst = C;
+  a.sig_tab = ctx->is_int() ? ctx->p<int16_t>(L.sig_tab) : nullptr;
+  e = pw(ctx, "gate", LD_NHWC, EP_GATE, a);
+  if (e != hipSuccess) return e;
+  a = conv_args(ctx, b.pw2, C, C, h8 * w8);
+  a.src0 = ctx->p(L.zC);
+  a.C0 = C;
+  a.y = z;
+  a.dst = dst;
+  a.Cdst = C;
+  return pw(ctx, "res", LD_NHWC, EP_RES, a);
+}
+
 // Runs the decoder-side transform from yhat_new (already written) into feat[nxt].
 ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   const ncodec_config& c = ctx->cfg;
@@ -608,6 +667,11 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   for (int k = 0; k < c.n_dec_blocks; ++k) {
     void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
     const BlockDev& b = L.dec[k];
+    if (c.block == NCODEC_BLOCK_GATED) {
+      NC_HIP(ctx, gated_block(ctx, b, z, dst), "decoder block");
+      z = dst;
+      continue;
+    }
     BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                  ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
                  ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
@@ -647,6 +711,11 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   for (int k = 0; k < c.n_enc_blocks; ++k) {
     void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
     const BlockDev& b = L.enc[k];
+    if (c.block == NCODEC_BLOCK_GATED) {
+      NC_HIP(ctx, gated_block(ctx, b, z, dst), "encoder block");
+      z = dst;
+      continue;
+    }
     BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                  ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
                  ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};

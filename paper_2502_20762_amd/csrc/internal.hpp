@@ -38,6 +38,8 @@ enum Epi : int {
   EP_PRIOR = 3,      // rows (32 mu, 32 s) per pass: quantise y, write q, yhat, bit partials
   EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
   EP_SCALES = 5,     // same rows: only the scale index of every symbol (entropy decoding)
+  EP_GATE = 6,       // rows (32 h1, 32 h2) per pass: dst = WSiLU(h1) * h2 (gated block, C channels)
+  EP_RES = 7,        // dst[p*Cdst + n] = result + y[p*Cdst + n] (residual add; int: saturating)
 };
 
 struct PwArgs {
@@ -64,6 +66,7 @@ struct PwArgs {
   uint8_t* k_out;          // planar scale indices of the entropy coder (nullable for EP_PRIOR)
   const float* scales;     // fp16 path: the NS coder scales sigma_j (fp32)
   const uint8_t* k_tab;    // int path: scale index for s_i + 32768
+  const int16_t* sig_tab;  // int path, EP_GATE: sigmoid table, entry v + 32768
 };
 
 struct BlockArgs {
@@ -133,6 +136,10 @@ hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, con
 hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const uint16_t* tab,
                               uint32_t* errs, uint32_t* count, int16_t* q, int32_t* status_out, hipStream_t st);
 
+// Depthwise 3x3 + bias of the gated block, NHWC (C channels, h x w pixels),
+// weights in the block's packed depthwise image.
+hipError_t launch_dw_f16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st);
+hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st);
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st);

@@ -283,6 +283,19 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
     }
+  } else if constexpr (EPI == EP_GATE) {
+    // gated block: a pass holds hidden rows h1 of channels c0 .. c0+31 then h2
+    // of the same channels; thread = (pixel px, 8 channels g8)
+    static_assert(NT == 64, "gate passes are 64 rows");
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    if (gp < a.P) {
+      const floatx16 u = parked(px, g8), v = parked(px, 4 + g8);
+      half8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (f16)(u[e] / (1.f + __expf(-4.f * u[e])) * v[e]);
+      *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = o;
+    }
   } else if constexpr (EPI == EP_REC) {
     // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
     // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
@@ -312,10 +325,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       if (gp < a.P) {
         const floatx16 r = parked(px, nl8);
         half8 o;
+        if constexpr (EPI == EP_RES) {
+          const half8 res = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + n0 + 8 * nl8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
+          for (int e = 0; e < 8; ++e) o[e] = (f16)(r[e] + (float)res[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
+        }
         size_t off;
-        if constexpr (EPI == EP_NHWC) {
+        if constexpr (EPI == EP_NHWC || EPI == EP_RES) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {  // EP_UP: pass rows n = sp * C + c, all in one sub-position sp
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -752,8 +771,58 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_NHWC, EP_PRIOR)
   NC_PW(LD_NHWC, EP_PRIOR_DEC)
   NC_PW(LD_NHWC, EP_SCALES)
+  NC_PW(LD_NHWC, EP_GATE)
+  NC_PW(LD_NHWC, EP_RES)
 #undef NC_PW
   return hipErrorInvalidValue;
+}
+
+// Depthwise 3x3 + bias of the gated block (Supp. B.1), NHWC fp16 with fp32
+// accumulation.  Thread = (pixel, 8 channels), consecutive threads walk the
+// channels of a pixel, so the nine neighbour reads of a wave are contiguous
+// 16-byte vectors (the halo comes from the caches).  The weights of the
+// thread's 4 channel pairs come from the block's packed depthwise image (48
+// bytes per pair: the 9 taps as half2, the two biases as fp32, a pad word).
+__global__ __launch_bounds__(256) void k_dw_f16(const f16* z, const uint32_t* dww, f16* out, int h8, int w8, int C) {
+  const int C8 = C >> 3;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)h8 * w8 * C8) return;
+  const int c8 = (int)(t % C8), p = (int)(t / C8);
+  const int y = p / w8, x = p - y * w8;
+  const intx4* wq = (const intx4*)(dww + 48 * c8);
+  intx4 wv[12];
+#pragma unroll
+  for (int i = 0; i < 12; ++i) wv[i] = wq[i];
+  auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[3 * j + (k >> 2)][k & 3]; };
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = __uint_as_float(word(e >> 1, 9 + (e & 1)));
+#pragma unroll
+  for (int dy = -1; dy <= 1; ++dy)
+#pragma unroll
+    for (int dx = -1; dx <= 1; ++dx) {
+      const int yy = y + dy, xx = x + dx;
+      if (yy < 0 || yy >= h8 || xx < 0 || xx >= w8) continue;
+      const half8 v = *(const half8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
+      const int tap = 3 * (dy + 1) + (dx + 1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint16_t hb = (uint16_t)(word(e >> 1, tap) >> (16 * (e & 1)));
+        acc[e] = fmaf((float)__builtin_bit_cast(f16, hb), (float)v[e], acc[e]);
+      }
+    }
+  half8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
+  *(half8*)(out + (size_t)p * C + 8 * c8) = o;
+}
+
+hipError_t launch_dw_f16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
+  if (C % 8) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)h * w * (C / 8);
+  launch(k_dw_f16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const f16*)z, (const uint32_t*)dww, (f16*)out,
+         h, w, C);
+  return hipGetLastError();
 }
 
 // 64 rows per workgroup pass: two workgroups fit a CU, and the passes over one

@@ -308,6 +308,25 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
     }
+  } else if constexpr (EPI == EP_GATE) {
+    // gated block: a pass holds h1 of channels c0 .. c0+31 then h2 of the same
+    // channels; WSiLU_i = RHE(h1 S[h1] / 512) with the int16 sigmoid table S,
+    // g = clip(RHE(WSiLU_i h2 / 512)) (|h1 S| <= 2^24, |WSiLU_i h2| <= 2^30)
+    static_assert(NT == 64, "gate passes are 64 rows");
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    if (gp < a.P) {
+      int u[8], v[8];
+      parked(px, g8, u);
+      parked(px, 4 + g8, v);
+      shortx8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int ws = rhe_shift(u[e] * (int)a.sig_tab[u[e] + 32768], 9);
+        o[e] = (short)clip16(rhe_shift(ws * v[e], 9));
+      }
+      *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = o;
+    }
   } else if constexpr (EPI == EP_REC) {
 #pragma unroll
     for (int it = 0; it < UNITS / 512; ++it) {
@@ -335,10 +354,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         int v[8];
         parked(px, nl8, v);
         shortx8 o;
+        if constexpr (EPI == EP_RES) {
+          const shortx8 res = *(const shortx8*)((const int16_t*)a.y + (size_t)gp * a.Cdst + n0 + 8 * nl8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
+          for (int e = 0; e < 8; ++e) o[e] = (short)clip16(v[e] + (int)res[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
+        }
         size_t off;
-        if constexpr (EPI == EP_NHWC) {
+        if constexpr (EPI == EP_NHWC || EPI == EP_RES) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -791,8 +816,59 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_NHWC, EP_PRIOR)
   NC_PW(LD_NHWC, EP_PRIOR_DEC)
   NC_PW(LD_NHWC, EP_SCALES)
+  NC_PW(LD_NHWC, EP_GATE)
+  NC_PW(LD_NHWC, EP_RES)
 #undef NC_PW
   return hipErrorInvalidValue;
+}
+
+// Depthwise 3x3 of the gated block on the integer path (Alg. 1):
+// a = clip(RHE((sum z_i w_i + 512 b_i) / 8192)) in wrapping int32.  Thread =
+// (pixel, 8 channels); the weights of its 2 channel quads come from the
+// block's packed depthwise image (96 bytes per quad: per tap the int16 pairs
+// (w_c, w_c+1), (w_c+2, w_c+3); then the four 512 b_i; two pad words).
+__global__ __launch_bounds__(256) void k_dw_i16(const int16_t* z, const uint32_t* dww, int16_t* out, int h8, int w8,
+                                              int C) {
+  const int C8 = C >> 3;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)h8 * w8 * C8) return;
+  const int c8 = (int)(t % C8), p = (int)(t / C8);
+  const int y = p / w8, x = p - y * w8;
+  const intx4* wq = (const intx4*)(dww + 48 * c8);
+  intx4 wv[12];
+#pragma unroll
+  for (int i = 0; i < 12; ++i) wv[i] = wq[i];
+  // word k of quad j (j = 0, 1)
+  auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[6 * j + (k >> 2)][k & 3]; };
+  uint32_t acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = word(e >> 2, 18 + (e & 3));
+#pragma unroll
+  for (int dy = -1; dy <= 1; ++dy)
+#pragma unroll
+    for (int dx = -1; dx <= 1; ++dx) {
+      const int yy = y + dy, xx = x + dx;
+      if (yy < 0 || yy >= h8 || xx < 0 || xx >= w8) continue;
+      const shortx8 v = *(const shortx8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
+      const int tap = 3 * (dy + 1) + (dx + 1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int wgt = (int)(int16_t)(uint16_t)(word(e >> 2, 2 * tap + ((e >> 1) & 1)) >> (16 * (e & 1)));
+        acc[e] += (uint32_t)(wgt * (int)v[e]);
+      }
+    }
+  shortx8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (short)rescale13((int)acc[e]);
+  *(shortx8*)(out + (size_t)p * C + 8 * c8) = o;
+}
+
+hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
+  if (C % 8) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)h * w * (C / 8);
+  launch(k_dw_i16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const int16_t*)z, (const uint32_t*)dww,
+         (int16_t*)out, h, w, C);
+  return hipGetLastError();
 }
 
 // 64 rows per workgroup pass: two workgroups fit a CU, and the passes over one

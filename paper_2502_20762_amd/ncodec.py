@@ -27,6 +27,8 @@ NCODEC_PATH_FP16 = 0
 NCODEC_PATH_INT16 = 1
 
 PATHS = {"fp16": NCODEC_PATH_FP16, "int16": NCODEC_PATH_INT16}
+NCODEC_BLOCK_LRELU, NCODEC_BLOCK_GATED = 0, 1
+BLOCKS = {"lrelu": NCODEC_BLOCK_LRELU, "gated": NCODEC_BLOCK_GATED}
 
 
 class ncodec_config(ctypes.Structure):
@@ -37,6 +39,7 @@ class ncodec_config(ctypes.Structure):
         ("n_enc_blocks", ctypes.c_int32),
         ("n_dec_blocks", ctypes.c_int32),
         ("path", ctypes.c_int32),
+        ("block", ctypes.c_int32),
     ]
 
 
@@ -97,10 +100,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
-def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path) -> ncodec_config:
+def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block="lrelu") -> ncodec_config:
     if isinstance(path, str):
         path = PATHS[path]
-    return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path)
+    if isinstance(block, str):
+        block = BLOCKS[block]
+    return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block)
 
 
 def _p(v: int):
@@ -230,11 +235,11 @@ class Codec:
     """
 
     def __init__(self, height, width, channels, n_enc_blocks, n_dec_blocks, path, weights,
-                 device="cuda:0", stream=None):
+                 device="cuda:0", stream=None, block="lrelu"):
         import torch
 
         self.torch = torch
-        self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path)
+        self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block)
         self.device = torch.device(device)
         self.path = self.cfg.path
         nbytes = ncodec_workspace_bytes(self.cfg)

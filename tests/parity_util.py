@@ -30,9 +30,9 @@ def q_band(y, mu, tol=FP16_TOL):
     return np.abs(frac - 0.5) <= tol * np.maximum(1.0, np.abs(np.asarray(y, np.float64)))
 
 
-def params_for(C, ne, nd):
-    flat = synth.make_weights(C, ne, nd)
-    p = oracle.unpack(flat, C, ne, nd)
+def params_for(C, ne, nd, block="lrelu"):
+    flat = synth.make_weights(C, ne, nd, block=block)
+    p = oracle.unpack(flat, C, ne, nd, block=block)
     return flat, p
 
 

@@ -41,10 +41,10 @@ def host_state(codec):
         host(y).astype(np.float64 if y.dtype == torch.float16 else np.int64)
 
 
-def run_fp16_sequence(H, W, C, ne, nd, frames, what):
-    flat, p = params_for(C, ne, nd)
-    enc = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV)
-    dec = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV)
+def run_fp16_sequence(H, W, C, ne, nd, frames, what, block="lrelu"):
+    flat, p = params_for(C, ne, nd, block)
+    enc = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block)
+    dec = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block)
     worst = 0.0
     for t, x in enumerate(frames):
         say(what, "frame", t, (H, W, C, ne, nd))
@@ -62,11 +62,11 @@ def run_fp16_sequence(H, W, C, ne, nd, frames, what):
     return worst
 
 
-def run_int_sequence(H, W, C, ne, nd, frames, what):
-    flat, p = params_for(C, ne, nd)
+def run_int_sequence(H, W, C, ne, nd, frames, what, block="lrelu"):
+    flat, p = params_for(C, ne, nd, block)
     ip = ci.integerize(p)
-    enc = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
-    dec = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
+    enc = Codec(H, W, C, ne, nd, "int16", flat, device=DEV, block=block)
+    dec = Codec(H, W, C, ne, nd, "int16", flat, device=DEV, block=block)
     st = ci.zero_state(ip, H, W)
     for t, x in enumerate(frames):
         say(what, "frame", t, (H, W, C, ne, nd))
