@@ -259,6 +259,46 @@ def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
     return r
 
 
+def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
+    """The gated DC-block form (Supp. B.1, WSiLU + Chunk) on the same frames:
+    frames/s and the per-kernel event times of its launches."""
+    import synth
+    H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
+    weights = synth.make_weights(C, ne, nd, block="gated")
+    enc = Codec(H, W, C, ne, nd, path, weights, block="gated")
+    dec = Codec(H, W, C, ne, nd, path, weights, block="gated")
+    odt = torch.int16 if path == "int16" else torch.float16
+    qbuf = [torch.empty(enc.q_shape, dtype=torch.int16, device="cuda") for _ in range(steps)]
+    bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
+    xout = torch.empty(enc.frame_shape, dtype=odt, device="cuda")
+    nfr = len(gframes)
+    for i in range(warmup):
+        q, _ = enc.encode(gframes[i % nfr])
+        dec.decode(q, out=xout)
+    enc.reset()
+    dec.reset()
+    torch.cuda.synchronize()
+    r = timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch)
+    enc.reset()
+    dec.reset()
+    enc.timing(True)
+    dec.timing(True)
+    for k in range(steps):
+        enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
+        dec.decode(qbuf[k], out=xout)
+    kern = {}
+    for src in (enc.timing_read(), dec.timing_read()):
+        for kind, (n, ms) in src.items():
+            a = kern.setdefault(kind, [0, 0.0])
+            a[0] += n
+            a[1] += ms
+    K = steps
+    return {"value": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3), "encode_fps": K / (r["enc_ms"] * 1e-3),
+            "decode_fps": K / (r["dec_ms"] * 1e-3),
+            "kernels_us": {k: round(1e3 * ms / n, 2) for k, (n, ms) in kern.items()},
+            "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +306,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--paths", default="fp16,int16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gated", action="store_true", help="skip the gated DC-block form")
     ap.add_argument("--cpu-strip-rows", type=int, default=1088)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (3 times), as the reference "
@@ -362,6 +403,9 @@ def main():
     })
     if "int16" in res and main_path != "int16":
         out["int16"] = summary("int16", res["int16"], MFMA_I8_PEAK_TOPS, 4, "TOP/s")
+    if not args.no_gated:
+        out["gated_block"] = {p: run_gated(p, pre, gframes, args.steps, args.warmup, torch, Codec)
+                              for p in args.paths.split(",")}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(pre, weights, args.cpu_strip_rows, main_path)
         if "int16" in out:

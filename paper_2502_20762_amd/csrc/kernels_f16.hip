@@ -778,48 +778,72 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
 }
 
 // Depthwise 3x3 + bias of the gated block (Supp. B.1), NHWC fp16 with fp32
-// accumulation.  Thread = (pixel, 8 channels), consecutive threads walk the
-// channels of a pixel, so the nine neighbour reads of a wave are contiguous
-// 16-byte vectors (the halo comes from the caches).  The weights of the
-// thread's 4 channel pairs come from the block's packed depthwise image (48
-// bytes per pair: the 9 taps as half2, the two biases as fp32, a pad word).
+// accumulation.  Thread = (8 channels, one column, 8 rows): it slides a 3 x 3
+// window of 16-byte vectors down the column, loading one new row of three
+// vectors per output (out-of-frame vectors are zero).  Consecutive threads
+// walk the channels of a pixel, so a wave's loads are contiguous.  The weights
+// of the thread's 4 channel pairs come once from the block's packed depthwise
+// image (48 bytes per pair: the 9 taps as half2, the two biases as fp32, a pad
+// word).
+constexpr int kDwRows = 8;
+
 __global__ __launch_bounds__(256) void k_dw_f16(const f16* z, const uint32_t* dww, f16* out, int h8, int w8, int C) {
   const int C8 = C >> 3;
+  const int nyb = (h8 + kDwRows - 1) / kDwRows;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)h8 * w8 * C8) return;
-  const int c8 = (int)(t % C8), p = (int)(t / C8);
-  const int y = p / w8, x = p - y * w8;
+  if (t >= (int64_t)nyb * w8 * C8) return;
+  const int c8 = (int)(t % C8);
+  const int64_t r = t / C8;
+  const int x = (int)(r % w8), y0 = (int)(r / w8) * kDwRows;
   const intx4* wq = (const intx4*)(dww + 48 * c8);
   intx4 wv[12];
 #pragma unroll
   for (int i = 0; i < 12; ++i) wv[i] = wq[i];
   auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[3 * j + (k >> 2)][k & 3]; };
-  float acc[8];
+  auto ld = [&](int yy, int xx) -> half8 {
+    half8 v = {};
+    if (yy >= 0 && yy < h8 && xx >= 0 && xx < w8) v = *(const half8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
+    return v;
+  };
+  half8 win[3][3];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = __uint_as_float(word(e >> 1, 9 + (e & 1)));
+  for (int dx = 0; dx < 3; ++dx) {
+    win[0][dx] = ld(y0 - 1, x + dx - 1);
+    win[1][dx] = ld(y0, x + dx - 1);
+  }
 #pragma unroll
-  for (int dy = -1; dy <= 1; ++dy)
+  for (int i = 0; i < kDwRows; ++i) {
+    const int y = y0 + i;
+    if (y >= h8) break;
 #pragma unroll
-    for (int dx = -1; dx <= 1; ++dx) {
-      const int yy = y + dy, xx = x + dx;
-      if (yy < 0 || yy >= h8 || xx < 0 || xx >= w8) continue;
-      const half8 v = *(const half8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
-      const int tap = 3 * (dy + 1) + (dx + 1);
+    for (int dx = 0; dx < 3; ++dx) win[2][dx] = ld(y + 1, x + dx - 1);
+    float acc[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint16_t hb = (uint16_t)(word(e >> 1, tap) >> (16 * (e & 1)));
-        acc[e] = fmaf((float)__builtin_bit_cast(f16, hb), (float)v[e], acc[e]);
-      }
+    for (int e = 0; e < 8; ++e) acc[e] = __uint_as_float(word(e >> 1, 9 + (e & 1)));
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < 3; ++kx)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint16_t hb = (uint16_t)(word(e >> 1, 3 * ky + kx) >> (16 * (e & 1)));
+          acc[e] = fmaf((float)__builtin_bit_cast(f16, hb), (float)win[ky][kx][e], acc[e]);
+        }
+    half8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
+    *(half8*)(out + (size_t)(y * w8 + x) * C + 8 * c8) = o;
+#pragma unroll
+    for (int dx = 0; dx < 3; ++dx) {
+      win[0][dx] = win[1][dx];
+      win[1][dx] = win[2][dx];
     }
-  half8 o;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
-  *(half8*)(out + (size_t)p * C + 8 * c8) = o;
+  }
 }
 
 hipError_t launch_dw_f16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
   if (C % 8) return hipErrorInvalidValue;
-  const int64_t n = (int64_t)h * w * (C / 8);
+  const int64_t n = (int64_t)((h + kDwRows - 1) / kDwRows) * w * (C / 8);
   launch(k_dw_f16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const f16*)z, (const uint32_t*)dww, (f16*)out,
          h, w, C);
   return hipGetLastError();

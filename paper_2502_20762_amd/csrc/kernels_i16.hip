@@ -824,48 +824,73 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
 
 // Depthwise 3x3 of the gated block on the integer path (Alg. 1):
 // a = clip(RHE((sum z_i w_i + 512 b_i) / 8192)) in wrapping int32.  Thread =
-// (pixel, 8 channels); the weights of its 2 channel quads come from the
-// block's packed depthwise image (96 bytes per quad: per tap the int16 pairs
-// (w_c, w_c+1), (w_c+2, w_c+3); then the four 512 b_i; two pad words).
+// (8 channels, one column, 8 rows) sliding a 3 x 3 window of 16-byte vectors
+// down the column (out-of-frame vectors are zero); the weights of its 2
+// channel quads come once from the block's packed depthwise image (96 bytes
+// per quad: per tap the int16 pairs (w_c, w_c+1), (w_c+2, w_c+3); then the
+// four 512 b_i; two pad words).
+constexpr int kDwRowsI = 8;
+
 __global__ __launch_bounds__(256) void k_dw_i16(const int16_t* z, const uint32_t* dww, int16_t* out, int h8, int w8,
                                               int C) {
   const int C8 = C >> 3;
+  const int nyb = (h8 + kDwRowsI - 1) / kDwRowsI;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)h8 * w8 * C8) return;
-  const int c8 = (int)(t % C8), p = (int)(t / C8);
-  const int y = p / w8, x = p - y * w8;
+  if (t >= (int64_t)nyb * w8 * C8) return;
+  const int c8 = (int)(t % C8);
+  const int64_t r = t / C8;
+  const int x = (int)(r % w8), y0 = (int)(r / w8) * kDwRowsI;
   const intx4* wq = (const intx4*)(dww + 48 * c8);
   intx4 wv[12];
 #pragma unroll
   for (int i = 0; i < 12; ++i) wv[i] = wq[i];
   // word k of quad j (j = 0, 1)
   auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[6 * j + (k >> 2)][k & 3]; };
-  uint32_t acc[8];
+  auto ld = [&](int yy, int xx) -> shortx8 {
+    shortx8 v = {};
+    if (yy >= 0 && yy < h8 && xx >= 0 && xx < w8) v = *(const shortx8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
+    return v;
+  };
+  shortx8 win[3][3];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = word(e >> 2, 18 + (e & 3));
+  for (int dx = 0; dx < 3; ++dx) {
+    win[0][dx] = ld(y0 - 1, x + dx - 1);
+    win[1][dx] = ld(y0, x + dx - 1);
+  }
 #pragma unroll
-  for (int dy = -1; dy <= 1; ++dy)
+  for (int i = 0; i < kDwRowsI; ++i) {
+    const int y = y0 + i;
+    if (y >= h8) break;
 #pragma unroll
-    for (int dx = -1; dx <= 1; ++dx) {
-      const int yy = y + dy, xx = x + dx;
-      if (yy < 0 || yy >= h8 || xx < 0 || xx >= w8) continue;
-      const shortx8 v = *(const shortx8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
-      const int tap = 3 * (dy + 1) + (dx + 1);
+    for (int dx = 0; dx < 3; ++dx) win[2][dx] = ld(y + 1, x + dx - 1);
+    uint32_t acc[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int wgt = (int)(int16_t)(uint16_t)(word(e >> 2, 2 * tap + ((e >> 1) & 1)) >> (16 * (e & 1)));
-        acc[e] += (uint32_t)(wgt * (int)v[e]);
-      }
+    for (int e = 0; e < 8; ++e) acc[e] = word(e >> 2, 18 + (e & 3));
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < 3; ++kx)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int tap = 3 * ky + kx;
+          const int wgt = (int)(int16_t)(uint16_t)(word(e >> 2, 2 * tap + ((e >> 1) & 1)) >> (16 * (e & 1)));
+          acc[e] += (uint32_t)(wgt * (int)win[ky][kx][e]);
+        }
+    shortx8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (short)rescale13((int)acc[e]);
+    *(shortx8*)(out + (size_t)(y * w8 + x) * C + 8 * c8) = o;
+#pragma unroll
+    for (int dx = 0; dx < 3; ++dx) {
+      win[0][dx] = win[1][dx];
+      win[1][dx] = win[2][dx];
     }
-  shortx8 o;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = (short)rescale13((int)acc[e]);
-  *(shortx8*)(out + (size_t)p * C + 8 * c8) = o;
+  }
 }
 
 hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
   if (C % 8) return hipErrorInvalidValue;
-  const int64_t n = (int64_t)h * w * (C / 8);
+  const int64_t n = (int64_t)((h + kDwRowsI - 1) / kDwRowsI) * w * (C / 8);
   launch(k_dw_i16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const int16_t*)z, (const uint32_t*)dww,
          (int16_t*)out, h, w, C);
   return hipGetLastError();
