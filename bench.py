@@ -299,6 +299,59 @@ def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
             "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)]}
 
 
+SWEEP = [  # (label, H, W, C, N_e, N_d): resolution, width and depth
+    ("720p", 720, 1280, 256, 8, 8),
+    ("1080p C=64", 1088, 1920, 64, 8, 8),
+    ("1080p C=128", 1088, 1920, 128, 8, 8),
+    ("1080p", 1088, 1920, 256, 8, 8),
+    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16),
+    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32),
+    ("4K", 2176, 3840, 256, 8, 8),
+]
+
+
+def sweep(paths, steps, warmup, torch, Codec):
+    """Frames/s and the DC block's MFMA fraction across resolutions, widths and
+    depths (random-init weights, seeded random frames); one JSON line each."""
+    import synth
+    for label, H, W, C, ne, nd in SWEEP:
+        frames = [torch.from_numpy(synth.random_frame(H, W, seed=90 + i)).to("cuda") for i in range(4)]
+        weights = synth.make_weights(C, ne, nd)
+        kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd)
+        for path in paths:
+            enc = Codec(H, W, C, ne, nd, path, weights)
+            dec = Codec(H, W, C, ne, nd, path, weights)
+            odt = torch.int16 if path == "int16" else torch.float16
+            qbuf = [torch.empty(enc.q_shape, dtype=torch.int16, device="cuda") for _ in range(steps)]
+            bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
+            xout = torch.empty(enc.frame_shape, dtype=odt, device="cuda")
+            for i in range(warmup):
+                q, _ = enc.encode(frames[i % 4])
+                dec.decode(q, out=xout)
+            enc.reset()
+            dec.reset()
+            torch.cuda.synchronize()
+            r = timed_loop(enc, dec, frames, qbuf, bits, xout, steps, warmup, torch)
+            enc.reset()
+            enc.timing(True)
+            for k in range(min(steps, 4)):
+                enc.encode(frames[k % 4], q_out=qbuf[k], bits_out=bits[k])
+            t = enc.timing_read()
+            n, ms = t.get("dcblock", (0, 0.0))
+            peak, scale = (MFMA_F16_PEAK_TFLOPS, 1) if path == "fp16" else (MFMA_I8_PEAK_TOPS, 4)
+            frac = scale * kinds["dcblock"][0] / (ms * 1e-3 / n) / 1e12 / peak if n else None
+            t_roof = roofline_seconds(kinds, enc_list + dec_list, peak * 1e12 / scale)
+            value = steps / ((r["enc_ms"] + r["dec_ms"]) * 1e-3)
+            print(json.dumps({"sweep": label, "path": path, "height": H, "width": W, "channels": C,
+                              "n_enc_blocks": ne, "n_dec_blocks": nd, "frames_per_s": value,
+                              "encode_fps": steps / (r["enc_ms"] * 1e-3), "decode_fps": steps / (r["dec_ms"] * 1e-3),
+                              "dcblock_us": 1e3 * ms / n if n else None, "dcblock_mfma_frac": frac,
+                              "frame_roofline_fps": 1.0 / t_roof, "frac_of_frame_roofline": value * t_roof}),
+                  flush=True)
+            del enc, dec, qbuf, xout
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -307,6 +360,8 @@ def main():
     ap.add_argument("--paths", default="fp16,int16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gated", action="store_true", help="skip the gated DC-block form")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the 1080p line: one line per resolution / width / depth of the sweep table")
     ap.add_argument("--cpu-strip-rows", type=int, default=1088)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (3 times), as the reference "
@@ -321,6 +376,10 @@ def main():
 
     import synth
     from paper_2502_20762_amd.ncodec import Codec
+
+    if args.sweep:
+        sweep(args.paths.split(","), args.steps, args.warmup, torch, Codec)
+        return
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 20
