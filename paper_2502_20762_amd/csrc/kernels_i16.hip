@@ -813,11 +813,13 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
-  NC_PW(LD_NHWC, EP_PRIOR)
-  NC_PW(LD_NHWC, EP_PRIOR_DEC)
-  NC_PW(LD_NHWC, EP_SCALES)
-  NC_PW(LD_NHWC, EP_GATE)
   NC_PW(LD_NHWC, EP_RES)
+  if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
+    NC_PW(LD_NHWC, EP_PRIOR)
+    NC_PW(LD_NHWC, EP_PRIOR_DEC)
+    NC_PW(LD_NHWC, EP_SCALES)
+    NC_PW(LD_NHWC, EP_GATE)
+  }
 #undef NC_PW
   return hipErrorInvalidValue;
 }
@@ -901,6 +903,11 @@ hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w
 // 128, 256; 192 for the patch embed) and N a multiple of 64.
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   if (a.K % 64 || a.N % 64) return hipErrorInvalidValue;
+  // 128 rows per pass for the patch embed and the 2C -> C fuse: their activation
+  // tiles are the widest (K = 192 frame values or 2C channels), so halving the
+  // passes that re-stage them pays, and they still have two passes per tile.
+  if (a.N % 128 == 0 && epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512)))
+    return pw_dispatch<128>(loader, epi, a, st);
   return pw_dispatch<64>(loader, epi, a, st);
 }
 
