@@ -175,6 +175,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   const int c0 = n0 / 2;
   int16_t* qt = (int16_t*)st2;
   uint8_t* kt = (uint8_t*)(st2 + 8192);  // scale indices, [channel][pixel]
+  float* sct = (float*)(st2 + 12288);    // the coder scales, for the scale-index search
+  if constexpr (EPI == EP_SCALES || EPI == EP_PRIOR) {
+    if (threadIdx.x < kCoderScales && a.k_out) sct[threadIdx.x] = a.scales[threadIdx.x];
+  }
   // planar store of the staged scale indices (after a barrier)
   auto store_k = [&]() __attribute__((always_inline)) {
     const int ch = threadIdx.x >> 4, k = threadIdx.x & 15;
@@ -219,7 +223,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
     const floatx16 sg = parked(px, 4 + g8);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), a.scales);
+    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), sct);
     lds_barrier();
     store_k();
   } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
@@ -233,7 +237,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       if (a.k_out) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), a.scales);
+          kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), sct);
       }
       half8 yv = {};
       if (gp < a.P) yv = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + c);
