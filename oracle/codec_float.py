@@ -53,11 +53,20 @@ def dc_block(z: np.ndarray, blk) -> np.ndarray:
     return z + conv1x1(g, blk.pw2.w, blk.pw2.b)
 
 
+def context(p: Params, f_prev: np.ndarray) -> np.ndarray:
+    """Temporal context F_{t-1}: the feature extractor's blocks on f_{t-1}
+    (f_{t-1} itself without a feature extractor)."""
+    z = f_prev
+    for blk in p.fe:
+        z = dc_block(z, blk)
+    return z
+
+
 def encoder_feature(p: Params, x: np.ndarray, f_prev: np.ndarray) -> np.ndarray:
     """Patch embed, concatenate context, fuse, N_e blocks (the analysis transform at 1/8)."""
     u = pixel_unshuffle(np.asarray(x, dtype=np.float64), 8)
     e = conv1x1(u, p.pe.w, p.pe.b)
-    z = conv1x1(np.concatenate([e, f_prev], axis=0), p.fuse_enc.w, p.fuse_enc.b)
+    z = conv1x1(np.concatenate([e, context(p, f_prev)], axis=0), p.fuse_enc.w, p.fuse_enc.b)
     for blk in p.enc:
         z = dc_block(z, blk)
     return z
@@ -78,13 +87,16 @@ def prior(p: Params, yhat_prev: np.ndarray):
 def decoder_feature(p: Params, yhat: np.ndarray, f_prev: np.ndarray) -> np.ndarray:
     """Upsample to 1/8, concatenate context, fuse, N_d blocks -> f_t."""
     d = pixel_shuffle(conv1x1(yhat, p.up.w, p.up.b), 2)
-    z = conv1x1(np.concatenate([d, f_prev], axis=0), p.fuse_dec.w, p.fuse_dec.b)
+    z = conv1x1(np.concatenate([d, context(p, f_prev)], axis=0), p.fuse_dec.w, p.fuse_dec.b)
     for blk in p.dec:
         z = dc_block(z, blk)
     return z
 
 
 def reconstruct(p: Params, f: np.ndarray) -> np.ndarray:
+    """Reconstruction generation blocks on f_t, then the reconstruction conv."""
+    for blk in p.rg:
+        f = dc_block(f, blk)
     r = conv1x1(f, p.rec.w, p.rec.b)
     return np.clip(pixel_shuffle(r, 8), 0.0, 1.0)
 

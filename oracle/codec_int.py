@@ -171,13 +171,16 @@ class IParams:
     fuse_dec: IConv
     dec: list
     rec: IConv
+    fe: list = dataclasses.field(default_factory=list)
+    rg: list = dataclasses.field(default_factory=list)
 
 
 def integerize(p: Params) -> IParams:
+    """Integer weights of p (fold the vector banks first: integerize(fold_qp(p, qp)))."""
     blk = lambda b: IBlock(iconv(b.dw), iconv(b.pw1), iconv(b.pw2), b.kind)  # noqa: E731
     return IParams(p.C, iconv(p.pe), iconv(p.fuse_enc), [blk(b) for b in p.enc],
                    iconv(p.down), iconv(p.head), iconv(p.up), iconv(p.fuse_dec),
-                   [blk(b) for b in p.dec], iconv(p.rec))
+                   [blk(b) for b in p.dec], iconv(p.rec), [blk(b) for b in p.fe], [blk(b) for b in p.rg])
 
 
 @dataclasses.dataclass
@@ -204,10 +207,17 @@ def dc_block(z: np.ndarray, b: IBlock) -> np.ndarray:
     return clip16(z + p)
 
 
+def context(ip: IParams, f_prev: np.ndarray) -> np.ndarray:
+    z = f_prev
+    for b in ip.fe:
+        z = dc_block(z, b)
+    return z
+
+
 def encoder_feature(ip: IParams, x: np.ndarray, f_prev: np.ndarray) -> np.ndarray:
     u = pixel_unshuffle(frame_to_int(x), 8)
     e = int_conv1x1(u, ip.pe, "patch embed")
-    z = int_conv1x1(np.concatenate([e, f_prev], axis=0), ip.fuse_enc, "fuse_enc")
+    z = int_conv1x1(np.concatenate([e, context(ip, f_prev)], axis=0), ip.fuse_enc, "fuse_enc")
     for b in ip.enc:
         z = dc_block(z, b)
     return z
@@ -233,13 +243,15 @@ def sigma_int(s: np.ndarray) -> np.ndarray:
 
 def decoder_feature(ip: IParams, yhat: np.ndarray, f_prev: np.ndarray) -> np.ndarray:
     d = pixel_shuffle(int_conv1x1(yhat, ip.up, "up"), 2)
-    z = int_conv1x1(np.concatenate([d, f_prev], axis=0), ip.fuse_dec, "fuse_dec")
+    z = int_conv1x1(np.concatenate([d, context(ip, f_prev)], axis=0), ip.fuse_dec, "fuse_dec")
     for b in ip.dec:
         z = dc_block(z, b)
     return z
 
 
 def reconstruct(ip: IParams, f: np.ndarray) -> np.ndarray:
+    for b in ip.rg:
+        f = dc_block(f, b)
     r = int_conv1x1(f, ip.rec, "rec")
     return np.clip(pixel_shuffle(r, 8), 0, K1).astype(np.int64)
 

@@ -11,6 +11,17 @@ Order (each weight row-major, each followed by its bias):
   fuse_dec  W(C,2C)    b(C)      input channels [d ; f_prev]
   dec[k]    as enc[k]                                                k < N_d
   rec       W(192,C)   b(192)    row 64c+8i+j -> colour c at (8y+i, 8x+j)
+  fe[k]     as enc[k]                                                k < N_f
+  rg[k]     as enc[k]                                                k < N_r
+  q_e, q_d, q_f, q_r   (64, C) each, only with vector banks
+
+The conditional-coding modules (Fig. 4; Sec. 4.3, 4.4): the feature extractor
+fe turns f_{t-1} into the temporal context F_{t-1} that both fuse convs take
+in place of f_{t-1}; the reconstruction generation rg runs on f_t before the
+reconstruction conv; the vector banks (Sec. 4.4) hold one per-channel scale
+vector per rate point qp for the encoder output (q_e), the decoder input
+(q_d), the extracted context (q_f) and the reconstruction input (q_r).
+:func:`fold_qp` applies row qp of the banks to the adjacent convolutions.
 """
 from __future__ import annotations
 
@@ -46,6 +57,12 @@ class Params:
     dec: list
     rec: Conv
     block: str = "lrelu"
+    fe: list = dataclasses.field(default_factory=list)
+    rg: list = dataclasses.field(default_factory=list)
+    banks: dict = None    # name -> (64, C) array, or None
+
+
+NUM_QP = 64
 
 
 def _hidden(C: int, block: str) -> int:
@@ -54,17 +71,21 @@ def _hidden(C: int, block: str) -> int:
     return 2 * C if block == "lrelu" else C
 
 
-def count(C: int, n_enc: int, n_dec: int, block: str = "lrelu") -> int:
+def count(C: int, n_enc: int, n_dec: int, block: str = "lrelu", n_fe: int = 0, n_rg: int = 0,
+          banks: bool = False) -> int:
     blk = C * 9 + C + 2 * C * C + 2 * C + C * _hidden(C, block) + C
     return (C * 192 + C + C * 2 * C + C + n_enc * blk + C * C * 4 + C
             + 2 * C * C + 2 * C + 4 * C * C + 4 * C + C * 2 * C + C
-            + n_dec * blk + 192 * C + 192)
+            + n_dec * blk + 192 * C + 192
+            + (n_fe + n_rg) * blk + (4 * NUM_QP * C if banks else 0))
 
 
-def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu") -> Params:
+def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu", n_fe: int = 0,
+           n_rg: int = 0, banks: bool = False) -> Params:
     flat = np.asarray(flat, dtype=np.float64).reshape(-1)
-    if flat.size != count(C, n_enc, n_dec, block):
-        raise ValueError(f"expected {count(C, n_enc, n_dec, block)} parameters, got {flat.size}")
+    want = count(C, n_enc, n_dec, block, n_fe, n_rg, banks)
+    if flat.size != want:
+        raise ValueError(f"expected {want} parameters, got {flat.size}")
     pos = 0
 
     def take(shape):
@@ -91,5 +112,40 @@ def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu
     fuse_dec = conv((C, 2 * C))
     dec = [blk() for _ in range(n_dec)]
     rec = conv((192, C))
+    fe = [blk() for _ in range(n_fe)]
+    rg = [blk() for _ in range(n_rg)]
+    bk = {name: take((NUM_QP, C)) for name in ("q_e", "q_d", "q_f", "q_r")} if banks else None
     assert pos == flat.size
-    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec, block)
+    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec, block, fe, rg, bk)
+
+
+def _f16(v: np.ndarray) -> np.ndarray:
+    return np.asarray(v, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
+def fold_qp(p: Params, qp: int) -> Params:
+    """Params with row qp of the vector banks folded into the convolutions
+    next to them, each folded value rounded to fp16 once (the precision of
+    every weight):
+      q_e scales y:           down rows and bias,  W'[o] = q_e[o] W[o]
+      q_d scales yhat:        up columns,          W'[:, c] = W[:, c] q_d[c]
+      q_f scales the context: fuse columns C..2C,  W'[:, C + c] = W[:, C + c] q_f[c]
+      q_r scales the rg output: rec columns,       W'[:, c] = W[:, c] q_r[c]
+    Without banks, p itself."""
+    if p.banks is None:
+        return p
+    if not 0 <= qp < NUM_QP:
+        raise ValueError(f"qp must be in [0, {NUM_QP})")
+    C = p.C
+    qe, qd, qf, qr = (p.banks[n][qp] for n in ("q_e", "q_d", "q_f", "q_r"))
+    down = Conv(_f16(p.down.w * qe[:, None, None, None]), _f16(p.down.b * qe))
+    up = Conv(_f16(p.up.w * qd[None, :]), p.up.b)
+
+    def ctx_cols(c: Conv) -> Conv:
+        w = np.array(c.w)
+        w[:, C:] = _f16(w[:, C:] * qf[None, :])
+        return Conv(w, c.b)
+
+    rec = Conv(_f16(p.rec.w * qr[None, :]), p.rec.b)
+    return dataclasses.replace(p, down=down, up=up, fuse_enc=ctx_cols(p.fuse_enc),
+                               fuse_dec=ctx_cols(p.fuse_dec), rec=rec)

@@ -61,11 +61,16 @@ PRESETS = {
 }
 
 
-def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu"):
-    """(name, shape, fan_in, kind) in canonical order; kind is 'w', 'w_res' or 'b'.
+def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu",
+               n_fe: int = 0, n_rg: int = 0, banks: bool = False):
+    """(name, shape, fan_in, kind) in canonical order; kind is 'w', 'w_res', 'b'
+    or 'bank'.
 
     ``block`` is the DC-block form: "lrelu" (pw2 is C x 2C) or "gated" (the
-    hidden 2C channels are chunked into two halves and gated, pw2 is C x C)."""
+    hidden 2C channels are chunked into two halves and gated, pw2 is C x C).
+    After the transform come ``n_fe`` feature-extractor blocks, ``n_rg``
+    reconstruction-generation blocks and, with ``banks``, the four qp-indexed
+    vector banks q_e, q_d, q_f, q_r (64 rate points x C each)."""
     C = channels
     out = []
     if block not in ("lrelu", "gated"):
@@ -92,11 +97,36 @@ def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu"):
     for k in range(n_dec):
         block_params(f"dec{k}")
     conv("rec", (192, C), C)
+    for k in range(n_fe):
+        block_params(f"fe{k}")
+    for k in range(n_rg):
+        block_params(f"rg{k}")
+    if banks:
+        for name in ("q_e", "q_d", "q_f", "q_r"):
+            out.append((name, (NUM_QP, C), 0, "bank"))
     return out
 
 
+NUM_QP = 64  # rate points of the vector banks
+
+
+def bank_values(rng: np.random.Generator, name: str, channels: int) -> np.ndarray:
+    """Synthetic vector banks: row qp scales the encoder output by about
+    2^(-qp / 32) (coarser quantisation at higher qp) and the decoder input by the
+    inverse; the context and reconstruction banks stay near 1; every entry
+    carries a +-10 % per-channel jitter."""
+    qp = np.arange(NUM_QP, dtype=np.float64)[:, None]
+    jit = np.exp(rng.uniform(-0.1, 0.1, size=(NUM_QP, channels)))
+    if name == "q_e":
+        return 2.0 ** (-qp / 32.0) * jit
+    if name == "q_d":
+        return 2.0 ** (qp / 32.0) * jit
+    return jit
+
+
 def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
-                 resid_gain: float = RESID_GAIN, block: str = "lrelu") -> np.ndarray:
+                 resid_gain: float = RESID_GAIN, block: str = "lrelu",
+                 n_fe: int = 0, n_rg: int = 0, banks: bool = False) -> np.ndarray:
     """Flat float32 parameter vector; every value is exactly fp16-representable.
 
     Weights ~ N(0, 1/fan_in) (the residual projection times ``resid_gain``),
@@ -104,7 +134,10 @@ def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
     """
     rng = np.random.default_rng(seed)
     chunks = []
-    for _name, shape, fan_in, kind in param_list(channels, n_enc, n_dec, block):
+    for name, shape, fan_in, kind in param_list(channels, n_enc, n_dec, block, n_fe, n_rg, banks):
+        if kind == "bank":
+            chunks.append(bank_values(rng, name, channels).reshape(-1))
+            continue
         if kind == "b":
             v = rng.uniform(-0.1, 0.1, size=shape)
         else:
