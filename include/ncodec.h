@@ -81,6 +81,13 @@ typedef struct {
   int32_t n_dec_blocks;  /* N_d, 0..32                                              */
   int32_t path;          /* ncodec_path                                             */
   int32_t block;         /* ncodec_block (0 = LRELU)                                */
+  int32_t n_fe_blocks;   /* N_f, 0..32: feature extractor (Fig. 4; Sec. 4.3): DC
+                            blocks on f_{t-1}, whose output replaces f_{t-1} as the
+                            temporal context in both fuse convs                     */
+  int32_t n_rg_blocks;   /* N_r, 0..32: reconstruction generation: DC blocks on f_t
+                            before the reconstruction conv (decode only)            */
+  int32_t qp_banks;      /* 1: the weights end with the vector banks (Sec. 4.4), see
+                            ncodec_set_qp; 0: none                                  */
 } ncodec_config;
 
 /* Number of float32 values in the canonical parameter list for cfg, or 0 if
@@ -91,7 +98,10 @@ typedef struct {
  * [h1 ; h2]}; down W(C,C,2,2) b(C); head W(2C,C) b(2C) with rows
  * [mu ; s]; up W(4C,C) b(4C), row 4c+2i+j -> pixel-shuffle position (c,i,j);
  * fuse_dec W(C,2C) b(C) with input channels [d ; f_prev]; N_d blocks;
- * rec W(192,C) b(192), row 64c+8i+j -> colour c at pixel (8y+i, 8x+j).
+ * rec W(192,C) b(192), row 64c+8i+j -> colour c at pixel (8y+i, 8x+j);
+ * then N_f feature-extractor blocks and N_r reconstruction-generation blocks
+ * (each as the encoder's blocks); then, with qp_banks, the four vector banks
+ * q_e, q_d, q_f, q_r, each 64 x C (row = rate point qp).
  * Pure host function. */
 size_t ncodec_weight_count(const ncodec_config* cfg);
 
@@ -114,6 +124,18 @@ ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights,
 
 /* Make the next frame an I-frame: zero f_{t-1} and yhat_{t-1} (enqueued). */
 ncodec_status ncodec_reset(ncodec_ctx* ctx);
+
+/* Select rate point qp in [0, 64) of the vector banks (Sec. 4.4; the context
+ * starts at qp 0).  Row qp scales per channel the latent y (q_e), the decoder
+ * input yhat (q_d), the temporal context (q_f) and the generated feature
+ * before the reconstruction conv (q_r); the scales are folded into the
+ * adjacent convolutions (down rows, up columns, the fuse convs' context
+ * columns, rec columns), each folded weight rounded to fp16, and the weights
+ * are re-uploaded.  Synchronises the context's stream; the state is kept
+ * (encoder and decoder must switch at the same frame).  EINVAL if the context
+ * has no banks, qp is out of range, or (int path) a folded weight exceeds the
+ * integer range. */
+ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp);
 
 /* Encode one frame (Sec. 4.1, Fig. 4 encoder side, Supp. B.3 encoding).
  *  d_frame: 3 x H x W planar fp16 (IEEE binary16), values in [0, 1]; the int

@@ -25,6 +25,7 @@ namespace {
 thread_local std::string g_create_error;
 
 constexpr size_t kAlign = 256;
+constexpr int kNumQp = 64;  // rate points of the vector banks
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 bool cfg_valid(const ncodec_config* c, std::string* why) {
@@ -49,6 +50,14 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "block must be NCODEC_BLOCK_LRELU or NCODEC_BLOCK_GATED";
     return false;
   }
+  if (c->n_fe_blocks < 0 || c->n_fe_blocks > 32 || c->n_rg_blocks < 0 || c->n_rg_blocks > 32) {
+    if (why) *why = "feature-extractor and reconstruction-generation block counts must be in [0, 32]";
+    return false;
+  }
+  if (c->qp_banks != 0 && c->qp_banks != 1) {
+    if (why) *why = "qp_banks must be 0 or 1";
+    return false;
+  }
   return true;
 }
 
@@ -57,8 +66,12 @@ size_t weight_count(const ncodec_config& c) {
   const size_t hid = c.block == NCODEC_BLOCK_GATED ? C : 2 * C;  // pw2 input channels
   const size_t blk = C * 9 + C + 2 * C * C + 2 * C + C * hid + C;
   return C * 192 + C + 2 * C * C + C + c.n_enc_blocks * blk + 4 * C * C + C + 2 * C * C + 2 * C + 4 * C * C + 4 * C +
-         2 * C * C + C + c.n_dec_blocks * blk + 192 * C + 192;
+         2 * C * C + C + c.n_dec_blocks * blk + 192 * C + 192 + (size_t)(c.n_fe_blocks + c.n_rg_blocks) * blk +
+         (c.qp_banks ? 4 * (size_t)kNumQp * C : 0);
 }
+
+// fp16(w q) with one rounding: the precision of every weight of the image.
+float fold16(float w, float q) { return (float)(f16)((double)w * (double)q); }
 
 // ---------------------------------------------------------------- weight image
 struct ConvDev {
@@ -307,10 +320,11 @@ struct Packer {
 
 struct Layout {
   ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
-  std::vector<BlockDev> enc, dec;
+  std::vector<BlockDev> enc, dec, fe, rg;
   size_t sigma_tab = 0;
   size_t sig_tab = 0;  // int path, gated block: int16 sigmoid table
   size_t zC = 0;       // gated block: hidden buffer
+  size_t ctxF = 0;     // feature extractor output (the temporal context)
   // entropy coder tables
   size_t c_scales = 0, c_tab = 0, c_ktab = 0;
   size_t image_bytes = 0;
@@ -394,7 +408,7 @@ void build_coder_tables(Image& img, Layout& L, bool is_int, std::string* err) {
   }
 }
 
-bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err) {
+bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err, int qp = 0) {
   const int C = cfg.channels;
   const bool is_int = cfg.path == NCODEC_PATH_INT16;
   std::vector<float> zeros;
@@ -405,12 +419,37 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   Packer pk{cfg, img, is_int, err};
   const float* cur = w;
   auto take = [&](size_t n) { const float* p = cur; cur += n; return p; };
+  // vector banks (Sec. 4.4): row qp of q_e, q_d, q_f, q_r, at the end of the list
+  const size_t nb = (size_t)kNumQp * C;
+  const float* bank = cfg.qp_banks ? w + weight_count(cfg) - 4 * nb : nullptr;
+  auto brow = [&](int b) { return bank + b * nb + (size_t)qp * C; };
+  std::vector<float> fdown, fdown_b, fup, ffe, ffd, frec;
+  // fuse conv with its context columns C .. 2C scaled by q_f
+  auto fuse_fold = [&](const float* W, std::vector<float>& out) -> const float* {
+    if (!bank) return W;
+    out.assign(W, W + (size_t)2 * C * C);
+    const float* qf = brow(2);
+    for (int n = 0; n < C; ++n)
+      for (int c = 0; c < C; ++c) out[(size_t)n * 2 * C + C + c] = fold16(out[(size_t)n * 2 * C + C + c], qf[c]);
+    return out.data();
+  };
   const float* pe_w = take((size_t)C * 192); const float* pe_b = take(C);
   L.pe = pk.plain(pe_w, pe_b, C, 192);
   const float* fe_w = take((size_t)2 * C * C); const float* fe_b = take(C);
-  L.fuse_enc = pk.plain(fe_w, fe_b, C, 2 * C);
+  L.fuse_enc = pk.plain(fuse_fold(fe_w, ffe), fe_b, C, 2 * C);
   for (int k = 0; k < cfg.n_enc_blocks; ++k) L.enc.push_back(pk.block(cur));
   const float* dn_w = take((size_t)4 * C * C); const float* dn_b = take(C);
+  if (bank) {  // q_e scales the rows of the downsample (y)
+    const float* qe = brow(0);
+    fdown.assign(dn_w, dn_w + (size_t)4 * C * C);
+    fdown_b.assign(dn_b, dn_b + C);
+    for (int o = 0; o < C; ++o) {
+      for (size_t k = 0; k < (size_t)4 * C; ++k) fdown[(size_t)o * 4 * C + k] = fold16(fdown[(size_t)o * 4 * C + k], qe[o]);
+      fdown_b[o] = fold16(fdown_b[o], qe[o]);
+    }
+    dn_w = fdown.data();
+    dn_b = fdown_b.data();
+  }
   // packed k' = (2i + j) * C + c  <-  source column c * 4 + 2i + j
   L.down = pk.gemm(dn_w, dn_b, C, 4 * C, 4 * C, [](int n) { return n; }, [C](int k) { return (k % C) * 4 + k / C; });
   const float* hd_w = take((size_t)2 * C * C); const float* hd_b = take(2 * C);
@@ -419,13 +458,30 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
                    [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
                    [](int k) { return k; });
   const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
+  if (bank) {  // q_d scales the columns of the upsample (its input yhat)
+    const float* qd = brow(1);
+    fup.assign(up_w, up_w + (size_t)4 * C * C);
+    for (size_t n = 0; n < (size_t)4 * C; ++n)
+      for (int c = 0; c < C; ++c) fup[n * C + c] = fold16(fup[n * C + c], qd[c]);
+    up_w = fup.data();
+  }
   // packed row n' = sp * C + c  <-  source row 4c + sp
   L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });
   const float* fd_w = take((size_t)2 * C * C); const float* fd_b = take(C);
-  L.fuse_dec = pk.plain(fd_w, fd_b, C, 2 * C);
+  L.fuse_dec = pk.plain(fuse_fold(fd_w, ffd), fd_b, C, 2 * C);
   for (int k = 0; k < cfg.n_dec_blocks; ++k) L.dec.push_back(pk.block(cur));
   const float* rc_w = take((size_t)192 * C); const float* rc_b = take(192);
+  if (bank) {  // q_r scales the columns of the reconstruction (the generated feature)
+    const float* qr = brow(3);
+    frec.assign(rc_w, rc_w + (size_t)192 * C);
+    for (int n = 0; n < 192; ++n)
+      for (int c = 0; c < C; ++c) frec[(size_t)n * C + c] = fold16(frec[(size_t)n * C + c], qr[c]);
+    rc_w = frec.data();
+  }
   L.rec = pk.plain(rc_w, rc_b, 192, C);
+  for (int k = 0; k < cfg.n_fe_blocks; ++k) L.fe.push_back(pk.block(cur));
+  for (int k = 0; k < cfg.n_rg_blocks; ++k) L.rg.push_back(pk.block(cur));
+  if (bank) cur += 4 * nb;
   if ((size_t)(cur - w) != weight_count(cfg)) {
     if (err) *err = "internal: parameter walk mismatch";
     return false;
@@ -465,6 +521,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.feat[0] = alloc(fb); L.feat[1] = alloc(fb);
   L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
+  if (cfg.n_fe_blocks > 0) L.ctxF = alloc(fb);
   if (cfg.block == NCODEC_BLOCK_GATED) L.zC = alloc(fb);
   L.y = alloc(lb);
   const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
@@ -488,6 +545,8 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
 
 struct ncodec_ctx {
   ncodec_config cfg;
+  std::vector<float> host_w;  // canonical weights, kept to refold the vector banks (qp_banks only)
+  int qp = 0;
   int device;
   hipStream_t stream;
   char* ws;
@@ -637,6 +696,43 @@ hipError_t gated_block(ncodec_ctx* ctx, const BlockDev& b, const void* z, void* 
   return pw(ctx, "res", LD_NHWC, EP_RES, a);
 }
 
+// One DC block of either form, src -> dst.
+hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* dst) {
+  if (ctx->cfg.block == NCODEC_BLOCK_GATED) return gated_block(ctx, b, src, dst);
+  const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
+  BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
+               ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
+               ctx->p(b.dww), ctx->p(b.dwb), src, dst, h8, w8, ctx->p(ctx->L.zpad)};
+  return dcblock(ctx, ba);
+}
+
+// A chain of DC blocks from src, ping-ponging through zA / zB, the last one
+// writing `last`; returns the buffer that holds the result (src if empty).
+// src and last must not be zA or zB.
+hipError_t run_chain(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, const void* src, void* last,
+                     const void** result) {
+  const void* z = src;
+  for (size_t k = 0; k < blocks.size(); ++k) {
+    void* dst = k + 1 == blocks.size() ? last : (z == ctx->p(ctx->L.zA) ? ctx->p(ctx->L.zB) : ctx->p(ctx->L.zA));
+    const hipError_t e = run_block(ctx, blocks[k], z, dst);
+    if (e != hipSuccess) return e;
+    z = dst;
+  }
+  *result = z;
+  return hipSuccess;
+}
+
+// The temporal context of this frame: the feature extractor's blocks on
+// f_{t-1} into ctxF, or f_{t-1} itself without a feature extractor.
+hipError_t temporal_context(ncodec_ctx* ctx, const void** out) {
+  const void* f_prev = ctx->p(ctx->L.feat[ctx->cur]);
+  if (ctx->L.fe.empty()) {
+    *out = f_prev;
+    return hipSuccess;
+  }
+  return run_chain(ctx, ctx->L.fe, f_prev, ctx->p(ctx->L.ctxF), out);
+}
+
 // Runs the decoder-side transform from yhat_new (already written) into feat[nxt].
 ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   const ncodec_config& c = ctx->cfg;
@@ -644,7 +740,7 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   const int h8 = c.height / 8, w8 = c.width / 8;
   const int P8 = h8 * w8, P16 = P8 / 4;
   const Layout& L = ctx->L;
-  void* f_prev = ctx->p(L.feat[1 - nxt]);
+  const void* f_prev = L.fe.empty() ? ctx->p(L.feat[1 - nxt]) : ctx->p(L.ctxF);  // the temporal context
   void* f_new = ctx->p(L.feat[nxt]);
 
   PwArgs a = conv_args(ctx, L.up, C, 4 * C, P16);
@@ -692,6 +788,9 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   const Layout& L = ctx->L;
   const int cur = ctx->cur, nxt = 1 - cur;
 
+  const void* context = nullptr;  // F_{t-1}, also used by the decoder part below
+  NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
+
   PwArgs a = conv_args(ctx, L.pe, 192, C, P8);
   a.src0 = d_frame;
   a.dst = ctx->p(L.ed);
@@ -702,7 +801,7 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
   a.src0 = ctx->p(L.ed);
   a.C0 = C;
-  a.src1 = ctx->p(L.feat[cur]);
+  a.src1 = context;
   a.C1 = C;
   a.dst = z;
   a.Cdst = C;
@@ -776,12 +875,17 @@ ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_
   pa.C = C;
   pa.P = P16;
   pa.decode = 1;
+  const void* context = nullptr;
+  NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
   NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
   st = run_decoder(ctx, nxt);
   if (st) return st;
 
+  // reconstruction generation on f_t (into ed, free after the decoder), then the reconstruction conv
+  const void* rsrc = nullptr;
+  NC_HIP(ctx, run_chain(ctx, L.rg, ctx->p(L.feat[nxt]), ctx->p(L.ed), &rsrc), "reconstruction generation");
   PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
-  a.src0 = ctx->p(L.feat[nxt]);
+  a.src0 = rsrc;
   a.C0 = C;
   a.dst = d_frame_out;
   NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
@@ -952,6 +1056,7 @@ ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights,
 
   ncodec_ctx* ctx = new ncodec_ctx();
   ctx->cfg = *cfg;
+  if (cfg->qp_banks) ctx->host_w.assign(host_weights, host_weights + n_weights);
   ctx->stream = (hipStream_t)hip_stream;
   ctx->ws = (char*)d_workspace;
   ctx->L = std::move(L);
@@ -965,6 +1070,24 @@ ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights,
     return NCODEC_EHIP;
   }
   *out = ctx;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!ctx->cfg.qp_banks) return fail(ctx, NCODEC_EINVAL, "the context has no vector banks (qp_banks = 0)");
+  if (qp < 0 || qp >= kNumQp) return fail(ctx, NCODEC_EINVAL, "qp must be in [0, 64)");
+  if (qp == ctx->qp) return NCODEC_OK;
+  Image img;
+  Layout L;
+  std::string why;
+  if (!build_layout(ctx->cfg, ctx->host_w.data(), img, L, &why, qp)) return fail(ctx, NCODEC_EINVAL, why);
+  if (L.image_bytes != ctx->L.image_bytes) return fail(ctx, NCODEC_EINVAL, "internal: image size depends on qp");
+  NC_HIP(ctx, hipMemcpyAsync(ctx->ws, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, ctx->stream),
+         "set_qp upload");
+  NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "set_qp");
+  ctx->qp = qp;
   return NCODEC_OK;
 }
 

@@ -40,6 +40,9 @@ class ncodec_config(ctypes.Structure):
         ("n_dec_blocks", ctypes.c_int32),
         ("path", ctypes.c_int32),
         ("block", ctypes.c_int32),
+        ("n_fe_blocks", ctypes.c_int32),
+        ("n_rg_blocks", ctypes.c_int32),
+        ("qp_banks", ctypes.c_int32),
     ]
 
 
@@ -60,6 +63,7 @@ _SIGNATURES = {
     "ncodec_create": (ctypes.c_int, [ctypes.POINTER(ncodec_config), _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P,
                                      ctypes.POINTER(_P)]),
     "ncodec_reset": (ctypes.c_int, [_P]),
+    "ncodec_set_qp": (ctypes.c_int, [_P, ctypes.c_int32]),
     "ncodec_encode_frame": (ctypes.c_int, [_P, _P, _P, _P]),
     "ncodec_decode_frame": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_estimate_bits": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P]),
@@ -100,12 +104,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
-def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block="lrelu") -> ncodec_config:
+def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block="lrelu", n_fe_blocks=0,
+                n_rg_blocks=0, qp_banks=False) -> ncodec_config:
     if isinstance(path, str):
         path = PATHS[path]
     if isinstance(block, str):
         block = BLOCKS[block]
-    return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block)
+    return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block, n_fe_blocks,
+                         n_rg_blocks, int(bool(qp_banks)))
 
 
 def _p(v: int):
@@ -140,6 +146,10 @@ def ncodec_create(cfg: ncodec_config, host_weights: np.ndarray, d_workspace: int
 
 def ncodec_reset(ctx) -> None:
     _check(load_library().ncodec_reset(ctx), ctx)
+
+
+def ncodec_set_qp(ctx, qp: int) -> None:
+    _check(load_library().ncodec_set_qp(ctx, int(qp)), ctx)
 
 
 def ncodec_encode_frame(ctx, d_frame: int, d_q: int, d_bits: int = 0) -> None:
@@ -235,11 +245,12 @@ class Codec:
     """
 
     def __init__(self, height, width, channels, n_enc_blocks, n_dec_blocks, path, weights,
-                 device="cuda:0", stream=None, block="lrelu"):
+                 device="cuda:0", stream=None, block="lrelu", n_fe_blocks=0, n_rg_blocks=0, qp_banks=False):
         import torch
 
         self.torch = torch
-        self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block)
+        self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block, n_fe_blocks,
+                               n_rg_blocks, qp_banks)
         self.device = torch.device(device)
         self.path = self.cfg.path
         nbytes = ncodec_workspace_bytes(self.cfg)
@@ -343,6 +354,9 @@ class Codec:
 
     def reset(self):
         ncodec_reset(self.ctx)
+
+    def set_qp(self, qp: int):
+        ncodec_set_qp(self.ctx, qp)
 
     def kernels_per_frame(self, decode=False):
         return ncodec_kernels_per_frame(self.ctx, decode)
