@@ -299,14 +299,16 @@ def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
             "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)]}
 
 
-SWEEP = [  # (label, H, W, C, N_e, N_d): resolution, width and depth
-    ("720p", 720, 1280, 256, 8, 8),
-    ("1080p C=64", 1088, 1920, 64, 8, 8),
-    ("1080p C=128", 1088, 1920, 128, 8, 8),
-    ("1080p", 1088, 1920, 256, 8, 8),
-    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16),
-    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32),
-    ("4K", 2176, 3840, 256, 8, 8),
+SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r): resolution, width, depth, modules
+    ("720p", 720, 1280, 256, 8, 8, 0, 0),
+    ("1080p C=64", 1088, 1920, 64, 8, 8, 0, 0),
+    ("1080p C=128", 1088, 1920, 128, 8, 8, 0, 0),
+    ("1080p", 1088, 1920, 256, 8, 8, 0, 0),
+    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16, 0, 0),
+    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32, 0, 0),
+    ("1080p + feature extractor (2 blocks), reconstruction generation (2 blocks), qp banks",
+     1088, 1920, 256, 8, 8, 2, 2),
+    ("4K", 2176, 3840, 256, 8, 8, 0, 0),
 ]
 
 
@@ -314,13 +316,17 @@ def sweep(paths, steps, warmup, torch, Codec):
     """Frames/s and the DC block's MFMA fraction across resolutions, widths and
     depths (random-init weights, seeded random frames); one JSON line each."""
     import synth
-    for label, H, W, C, ne, nd in SWEEP:
+    for label, H, W, C, ne, nd, nfe, nrg in SWEEP:
         frames = [torch.from_numpy(synth.random_frame(H, W, seed=90 + i)).to("cuda") for i in range(4)]
-        weights = synth.make_weights(C, ne, nd)
+        banks = nfe + nrg > 0
+        weights = synth.make_weights(C, ne, nd, n_fe=nfe, n_rg=nrg, banks=banks)
         kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd)
+        enc_list = ["dcblock"] * nfe + enc_list
+        dec_list = ["dcblock"] * (nfe + nrg) + dec_list
         for path in paths:
-            enc = Codec(H, W, C, ne, nd, path, weights)
-            dec = Codec(H, W, C, ne, nd, path, weights)
+            kw = dict(n_fe_blocks=nfe, n_rg_blocks=nrg, qp_banks=banks)
+            enc = Codec(H, W, C, ne, nd, path, weights, **kw)
+            dec = Codec(H, W, C, ne, nd, path, weights, **kw)
             odt = torch.int16 if path == "int16" else torch.float16
             qbuf = [torch.empty(enc.q_shape, dtype=torch.int16, device="cuda") for _ in range(steps)]
             bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
@@ -343,7 +349,8 @@ def sweep(paths, steps, warmup, torch, Codec):
             t_roof = roofline_seconds(kinds, enc_list + dec_list, peak * 1e12 / scale)
             value = steps / ((r["enc_ms"] + r["dec_ms"]) * 1e-3)
             print(json.dumps({"sweep": label, "path": path, "height": H, "width": W, "channels": C,
-                              "n_enc_blocks": ne, "n_dec_blocks": nd, "frames_per_s": value,
+                              "n_enc_blocks": ne, "n_dec_blocks": nd, "n_fe_blocks": nfe, "n_rg_blocks": nrg,
+                              "frames_per_s": value,
                               "encode_fps": steps / (r["enc_ms"] * 1e-3), "decode_fps": steps / (r["dec_ms"] * 1e-3),
                               "dcblock_us": 1e3 * ms / n if n else None, "dcblock_mfma_frac": frac,
                               "frame_roofline_fps": 1.0 / t_roof, "frac_of_frame_roofline": value * t_roof}),
