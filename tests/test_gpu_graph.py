@@ -15,8 +15,6 @@ import torch
 import synth
 from paper_2502_20762_amd.ncodec import Codec
 
-from parity_util import params_for
-
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
@@ -31,16 +29,25 @@ def host(t):
     return t.cpu().numpy()
 
 
-@pytest.mark.parametrize("path,H,W,C,ne,nd", [("int16", 64, 64, 64, 2, 2), ("fp16", 112, 208, 128, 2, 1),
-                                             ("int16", 48, 80, 128, 1, 2)])
-def test_graph_replay_matches_eager(path, H, W, C, ne, nd):
-    flat, _ = params_for(C, ne, nd)
-    enc_g = Codec(H, W, C, ne, nd, path, flat, device=DEV)
-    enc_e = Codec(H, W, C, ne, nd, path, flat, device=DEV)
-    dec_g = Codec(H, W, C, ne, nd, path, flat, device=DEV)
-    dec_e = Codec(H, W, C, ne, nd, path, flat, device=DEV)
+GATED = dict(block="gated")
+MODULES = dict(n_fe_blocks=1, n_rg_blocks=1, qp_banks=True)
+
+
+@pytest.mark.parametrize("path,H,W,C,ne,nd,extra", [
+    ("int16", 64, 64, 64, 2, 2, {}), ("fp16", 112, 208, 128, 2, 1, {}), ("int16", 48, 80, 128, 1, 2, {}),
+    ("int16", 64, 96, 64, 1, 1, GATED), ("fp16", 64, 96, 64, 1, 1, MODULES),
+    ("int16", 48, 80, 128, 1, 1, dict(GATED, **MODULES))])
+def test_graph_replay_matches_eager(path, H, W, C, ne, nd, extra):
+    block = extra.get("block", "lrelu")
+    flat = synth.make_weights(C, ne, nd, block=block, n_fe=extra.get("n_fe_blocks", 0),
+                              n_rg=extra.get("n_rg_blocks", 0), banks=extra.get("qp_banks", False))
+    enc_g = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
+    enc_e = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
+    dec_g = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
+    dec_e = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
     enc_g.graphs(True)
     dec_g.graphs(True)
+    banks = extra.get("qp_banks", False)
     frames = [torch.from_numpy(synth.random_frame(H, W, seed=40 + s)).to(DEV) for s in range(6)]
     # two alternating sets of caller buffers, so the graph nodes are re-pointed
     qbuf = [torch.empty(enc_g.q_shape, dtype=torch.int16, device=DEV) for _ in range(2)]
@@ -48,7 +55,10 @@ def test_graph_replay_matches_eager(path, H, W, C, ne, nd):
     odt = torch.int16 if path == "int16" else torch.float16
     obuf = [torch.empty(enc_g.frame_shape, dtype=odt, device=DEV) for _ in range(3)]
     for t, x in enumerate(frames):
-        say(path, (H, W, C, ne, nd), "frame", t)
+        say(path, (H, W, C, ne, nd), extra, "frame", t)
+        if banks and t == 3:  # a new rate point between replays: the weights change under the graphs
+            for c in (enc_g, enc_e, dec_g, dec_e):
+                c.set_qp(45)
         want_bits = t % 3 != 2
         qg, bg = enc_g.encode(x, q_out=qbuf[t % 2], bits_out=bbuf[t % 2] if want_bits else None,
                               want_bits=want_bits)
