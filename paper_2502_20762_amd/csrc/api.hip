@@ -216,7 +216,7 @@ struct Packer {
         o[22] = o[23] = 0;
       }
     }
-    if (gated) {
+    if (gated && is_int) {
       // Gated block: pw1 as a pointwise GEMM whose packed rows come in passes
       // of 64, the 32 h1 rows of channels 32 t .. 32 t + 31 then their 32 h2
       // rows (so one pass holds both halves of the chunk for the gate
@@ -241,21 +241,29 @@ struct Packer {
       d.pw2.bias = img.add((size_t)C * 4);
       f16* cp = img.at<f16>(d.pw1.w);
       auto kmap = [](int k) { return 8 * ((k % 8) / 4) + 4 * ((k / 8) % 2) + (k % 4); };  // within 16
+      // Gated form: entry 2p carries h1 rows 32 p .. +31 (pw1 rows 32 p ..), entry
+      // 2p + 1 the matching h2 rows (pw1 rows C + 32 p ..) and the pw2 fragments
+      // of gated channels 32 p .. +31; entry 2p's pw2 part is unused (zero).
+      auto row1 = [&](int j) { return gated ? (j & 1 ? C : 0) + 32 * (j >> 1) : 32 * j; };
+      auto hid0 = [&](int j) { return gated ? 32 * (j >> 1) : 32 * j; };
+      const int ld2 = gated ? C : 2 * C;
       for (int j = 0; j < NCH; ++j)
         for (int f = 0; f < FR; ++f)
           for (int l = 0; l < 64; ++l)
             for (int e = 0; e < 8; ++e) {
               float v;
               if (f < KS) {
-                const int n = 32 * j + (l & 31), k = 16 * f + 8 * (l >> 5) + e;
+                const int n = row1(j) + (l & 31), k = 16 * f + 8 * (l >> 5) + e;
                 v = w1[(size_t)n * C + k];
               } else if (f == KS) {
-                v = (l < 32 && e == 0) ? b1[32 * j + l] : 0.f;
+                v = (l < 32 && e == 0) ? b1[row1(j) + l] : 0.f;
+              } else if (gated && !(j & 1)) {
+                v = 0.f;
               } else {
                 const int t = (f - KS - 1) / 2, u = (f - KS - 1) % 2;
                 const int n = 32 * t + (l & 31);
-                const int hidden = 32 * j + 16 * u + kmap(8 * (l >> 5) + e);
-                v = w2[(size_t)n * 2 * C + hidden];
+                const int hidden = hid0(j) + 16 * u + kmap(8 * (l >> 5) + e);
+                v = w2[(size_t)n * ld2 + hidden];
               }
               cp[(((size_t)j * FR + f) * 64 + l) * 8 + e] = (f16)v;
             }
@@ -323,7 +331,7 @@ struct Layout {
   std::vector<BlockDev> enc, dec, fe, rg;
   size_t sigma_tab = 0;
   size_t sig_tab = 0;  // int path, gated block: int16 sigmoid table
-  size_t zC = 0;       // gated block: hidden buffer
+  size_t zC = 0;       // int path, gated block: hidden buffer
   size_t ctxF = 0;     // feature extractor output (the temporal context)
   // entropy coder tables
   size_t c_scales = 0, c_tab = 0, c_ktab = 0;
@@ -522,7 +530,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
   if (cfg.n_fe_blocks > 0) L.ctxF = alloc(fb);
-  if (cfg.block == NCODEC_BLOCK_GATED) L.zC = alloc(fb);
+  if (cfg.block == NCODEC_BLOCK_GATED && is_int) L.zC = alloc(fb);
   L.y = alloc(lb);
   const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
@@ -642,7 +650,8 @@ hipError_t pw(ncodec_ctx* ctx, const char* kind, int loader, int epi, const PwAr
 hipError_t dcblock(ncodec_ctx* ctx, const BlockArgs& ba) {
   const int C = ctx->cfg.channels;
   return timed(ctx, "dcblock", [&] {
-    return ctx->is_int() ? launch_dcblock_i16(C, ba, ctx->stream) : launch_dcblock_f16(C, ba, ctx->stream);
+    return ctx->is_int() ? launch_dcblock_i16(C, ba, ctx->stream)
+                         : launch_dcblock_f16(C, ctx->cfg.block == NCODEC_BLOCK_GATED, ba, ctx->stream);
   });
 }
 
@@ -667,24 +676,22 @@ PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
   return a;
 }
 
-// One gated DC block (Supp. B.1 with WSiLU and Chunk) as three launches:
-// depthwise z -> ed, pw1 with the gate epilogue ed -> zC, pw2 with the
-// residual epilogue (zC, z) -> dst.  ed and zC are free while the blocks run.
+// One gated DC block (Supp. B.1 with WSiLU and Chunk) on the int path, as
+// three launches: depthwise z -> ed, pw1 with the gate epilogue ed -> zC, pw2
+// with the residual epilogue (zC, z) -> dst.  ed and zC are free while the
+// blocks run.  (The fp16 path runs the gated block fused, in one launch.)
 hipError_t gated_block(ncodec_ctx* ctx, const BlockDev& b, const void* z, void* dst) {
   const int C = ctx->cfg.channels;
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   const Layout& L = ctx->L;
-  hipError_t e = timed(ctx, "dw", [&] {
-    return ctx->is_int() ? launch_dw_i16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream)
-                         : launch_dw_f16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream);
-  });
+  hipError_t e = timed(ctx, "dw", [&] { return launch_dw_i16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream); });
   if (e != hipSuccess) return e;
   PwArgs a = conv_args(ctx, b.pw1, C, 2 * C, h8 * w8);
   a.src0 = ctx->p(L.ed);
   a.C0 = C;
   a.dst = ctx->p(L.zC);
   a.Cdst = C;
-  a.sig_tab = ctx->is_int() ? ctx->p<int16_t>(L.sig_tab) : nullptr;
+  a.sig_tab = ctx->p<int16_t>(L.sig_tab);
   e = pw(ctx, "gate", LD_NHWC, EP_GATE, a);
   if (e != hipSuccess) return e;
   a = conv_args(ctx, b.pw2, C, C, h8 * w8);
@@ -698,7 +705,8 @@ hipError_t gated_block(ncodec_ctx* ctx, const BlockDev& b, const void* z, void* 
 
 // One DC block of either form, src -> dst.
 hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* dst) {
-  if (ctx->cfg.block == NCODEC_BLOCK_GATED) return gated_block(ctx, b, src, dst);
+  // the gated form is fused on the fp16 path; the int path runs it as three launches
+  if (ctx->cfg.block == NCODEC_BLOCK_GATED && ctx->is_int()) return gated_block(ctx, b, src, dst);
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
@@ -763,7 +771,7 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   for (int k = 0; k < c.n_dec_blocks; ++k) {
     void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
     const BlockDev& b = L.dec[k];
-    if (c.block == NCODEC_BLOCK_GATED) {
+    if (c.block == NCODEC_BLOCK_GATED && ctx->is_int()) {
       NC_HIP(ctx, gated_block(ctx, b, z, dst), "decoder block");
       z = dst;
       continue;
@@ -810,7 +818,7 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   for (int k = 0; k < c.n_enc_blocks; ++k) {
     void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
     const BlockDev& b = L.enc[k];
-    if (c.block == NCODEC_BLOCK_GATED) {
+    if (c.block == NCODEC_BLOCK_GATED && ctx->is_int()) {
       NC_HIP(ctx, gated_block(ctx, b, z, dst), "encoder block");
       z = dst;
       continue;

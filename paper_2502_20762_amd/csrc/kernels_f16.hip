@@ -6,7 +6,8 @@
 //               the bit partial sums as its epilogue (Fig. 4 "Q", Supp. B.2).
 // k_dcblock_f16 one whole DC block (Supp. B.1): depthwise 3x3, pw C->2C +
 //               LeakyReLU chained into pw 2C->C through registers 32 hidden
-//               channels at a time, residual add.
+//               channels at a time, residual add; or the gated form (WSiLU
+//               and Chunk, pw C->C) with the same pipeline.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -287,19 +288,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
     }
-  } else if constexpr (EPI == EP_GATE) {
-    // gated block: a pass holds hidden rows h1 of channels c0 .. c0+31 then h2
-    // of the same channels; thread = (pixel px, 8 channels g8)
-    static_assert(NT == 64, "gate passes are 64 rows");
-    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
-    const int gp = tile * 128 + px;
-    if (gp < a.P) {
-      const floatx16 u = parked(px, g8), v = parked(px, 4 + g8);
-      half8 o;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (f16)(u[e] / (1.f + __expf(-4.f * u[e])) * v[e]);
-      *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = o;
-    }
+
   } else if constexpr (EPI == EP_REC) {
     // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
     // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
@@ -329,16 +318,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       if (gp < a.P) {
         const floatx16 r = parked(px, nl8);
         half8 o;
-        if constexpr (EPI == EP_RES) {
-          const half8 res = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + n0 + 8 * nl8);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = (f16)(r[e] + (float)res[e]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
-        }
+        for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
         size_t off;
-        if constexpr (EPI == EP_NHWC || EPI == EP_RES) {
+        if constexpr (EPI == EP_NHWC) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {  // EP_UP: pass rows n = sp * C + c, all in one sub-position sp
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -428,6 +411,35 @@ __device__ __forceinline__ void dc_hidden_store(const floatx16& hacc, int lane, 
   gx[64 + lane] = g1;
 }
 
+// Gated form.  WSiLU(h1) = h1 sigmoid(4 h1) of the h1 chain, kept as fp16 (8
+// registers) until the pair's h2 chain is done; then g = WSiLU(h1) * h2 for
+// the same elements, fp16, stored like dc_hidden_store.
+struct Wsilu16 {
+  half8 v[2];
+};
+__device__ __forceinline__ Wsilu16 dc_wsilu(const floatx16& h1) {
+  Wsilu16 w;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float u = h1[r];
+    w.v[r >> 3][r & 7] = (f16)(u / (1.f + __expf(-4.f * u)));
+  }
+  return w;
+}
+__device__ __forceinline__ void dc_gate_store(const Wsilu16& s1, const floatx16& h2, int lane, half8* gx) {
+  half8 g0, g1;
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 4 * g + e;
+      const f16 v = (f16)((float)s1.v[r >> 3][r & 7] * h2[r]);
+      if (g < 2) g0[4 * g + e] = v; else g1[4 * (g - 2) + e] = v;
+    }
+  gx[lane] = g0;
+  gx[64 + lane] = g1;
+}
+
 // Second pointwise conv, hidden chunk j, this wave's MT/2 output tiles.
 template <int C>
 __device__ __forceinline__ void dc_project(const char* wb, const half8* gx, int hf, int lane, floatx16* out) {
@@ -472,7 +484,14 @@ struct DcDw {
 
 __device__ __forceinline__ int dw_pos(int hp) { return hp ^ ((hp >> 2) & 1); }
 
-template <int C>
+// GATED: the gated form (Supp. B.1, WSiLU and Chunk).  The weight entries
+// alternate: entry 2p holds the pw1 fragments and bias of h1 rows 32 p .. +31,
+// entry 2p + 1 those of the matching h2 rows and the pw2 fragments of gated
+// channels 32 p .. +31.  One wave produces both chains of pair p (wave p % 2
+// of its SIMD pair), keeps h1 in registers, and gates when h2 is done; the
+// pair is projected in the next iteration (odd entries), so even iterations
+// run no pw2.
+template <int C, bool GATED>
 __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   using G = DcDw<C>;
   constexpr int KS = DcSmem<C>::KS;
@@ -637,9 +656,11 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + FR / 8) : "memory");
   lds_barrier();  // chunks 0 and 1 staged
+  Wsilu16 sw1 = {};  // gated: WSiLU of the h1 chain of the pair being produced
   if (hf == 0) {
     dc_load_w1<C>(wb0, lane, wf);
-    dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0 + 128 * pg);
+    if constexpr (GATED) sw1 = dc_wsilu(dc_hidden<C>(wf, wb0, av, ones, lane));
+    else dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0 + 128 * pg);
   }
   floatx16 out[MT / 2];  // pw2 accumulators, starting from the bias
 #pragma unroll
@@ -652,7 +673,7 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
       for (int e = 0; e < 4; ++e) out[t][4 * g + e] = bv[e];
     }
   }
-  if (hf == 1) dc_load_w1<C>(wb1, lane, wf);  // chunk 1, for its chain in iteration 0
+  if (hf == (GATED ? 0 : 1)) dc_load_w1<C>(wb1, lane, wf);  // chunk 1, for its chain in iteration 0
   lds_barrier();  // hidden chunk 0 visible
 
   // The residual tile (128 pixels x C fp16; 16-byte unit u of pixel px holds
@@ -674,17 +695,26 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
                   __attribute__((always_inline)) {
     const bool dma = j + 3 < NCH;
     if (dma) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
-    const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
-    const bool prefetch = j >= 1 && j + 2 < NCH && hf == (j & 1);
+    // producer of chunk c: wave c % 2 of the pair, or in the gated form (c / 2) % 2
+    const int pj1 = GATED ? ((j + 1) >> 1) & 1 : (j + 1) & 1, pj2 = GATED ? ((j + 2) >> 1) & 1 : j & 1;
+    const bool produce = j + 1 < NCH && hf == pj1;
+    const bool prefetch = j >= 1 && j + 2 < NCH && hf == pj2;
     floatx16 hacc;
     if (produce) {
       if (j == 1) dc_load_w1<C>(wnxt, lane, wf);  // iteration 0 had no prefetch
       hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
     }
     if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
-    dc_project<C>(wcur, gcur, hf, lane, out);
+    if (!GATED || (j & 1)) dc_project<C>(wcur, gcur, hf, lane, out);
     if (prefetch) dc_load_w1<C>(wpre, lane, wf);
-    if (produce) dc_hidden_store(hacc, lane, gnxt);
+    if (produce) {
+      if constexpr (GATED) {
+        if ((j + 1) & 1) dc_gate_store(sw1, hacc, lane, gnxt);  // h2 of the pair: gate it
+        else sw1 = dc_wsilu(hacc);
+      } else {
+        dc_hidden_store(hacc, lane, gnxt);
+      }
+    }
     // chunk j+3 (in iteration 0 also chunk 2), or the residual in the last step
     if (dma || j == NCH - 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
@@ -772,87 +802,13 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
-  NC_PW(LD_NHWC, EP_RES)
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
     NC_PW(LD_NHWC, EP_SCALES)
-    NC_PW(LD_NHWC, EP_GATE)
   }
 #undef NC_PW
   return hipErrorInvalidValue;
-}
-
-// Depthwise 3x3 + bias of the gated block (Supp. B.1), NHWC fp16 with fp32
-// accumulation.  Thread = (8 channels, one column, 8 rows): it slides a 3 x 3
-// window of 16-byte vectors down the column, loading one new row of three
-// vectors per output (out-of-frame vectors are zero).  Consecutive threads
-// walk the channels of a pixel, so a wave's loads are contiguous.  The weights
-// of the thread's 4 channel pairs come once from the block's packed depthwise
-// image (48 bytes per pair: the 9 taps as half2, the two biases as fp32, a pad
-// word).
-constexpr int kDwRows = 8;
-
-__global__ __launch_bounds__(256) void k_dw_f16(const f16* z, const uint32_t* dww, f16* out, int h8, int w8, int C) {
-  const int C8 = C >> 3;
-  const int nyb = (h8 + kDwRows - 1) / kDwRows;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)nyb * w8 * C8) return;
-  const int c8 = (int)(t % C8);
-  const int64_t r = t / C8;
-  const int x = (int)(r % w8), y0 = (int)(r / w8) * kDwRows;
-  const intx4* wq = (const intx4*)(dww + 48 * c8);
-  intx4 wv[12];
-#pragma unroll
-  for (int i = 0; i < 12; ++i) wv[i] = wq[i];
-  auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[3 * j + (k >> 2)][k & 3]; };
-  auto ld = [&](int yy, int xx) -> half8 {
-    half8 v = {};
-    if (yy >= 0 && yy < h8 && xx >= 0 && xx < w8) v = *(const half8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
-    return v;
-  };
-  half8 win[3][3];
-#pragma unroll
-  for (int dx = 0; dx < 3; ++dx) {
-    win[0][dx] = ld(y0 - 1, x + dx - 1);
-    win[1][dx] = ld(y0, x + dx - 1);
-  }
-#pragma unroll
-  for (int i = 0; i < kDwRows; ++i) {
-    const int y = y0 + i;
-    if (y >= h8) break;
-#pragma unroll
-    for (int dx = 0; dx < 3; ++dx) win[2][dx] = ld(y + 1, x + dx - 1);
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = __uint_as_float(word(e >> 1, 9 + (e & 1)));
-#pragma unroll
-    for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-      for (int kx = 0; kx < 3; ++kx)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint16_t hb = (uint16_t)(word(e >> 1, 3 * ky + kx) >> (16 * (e & 1)));
-          acc[e] = fmaf((float)__builtin_bit_cast(f16, hb), (float)win[ky][kx][e], acc[e]);
-        }
-    half8 o;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (f16)acc[e];
-    *(half8*)(out + (size_t)(y * w8 + x) * C + 8 * c8) = o;
-#pragma unroll
-    for (int dx = 0; dx < 3; ++dx) {
-      win[0][dx] = win[1][dx];
-      win[1][dx] = win[2][dx];
-    }
-  }
-}
-
-hipError_t launch_dw_f16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
-  if (C % 8) return hipErrorInvalidValue;
-  const int64_t n = (int64_t)((h + kDwRows - 1) / kDwRows) * w * (C / 8);
-  launch(k_dw_f16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const f16*)z, (const uint32_t*)dww, (f16*)out,
-         h, w, C);
-  return hipGetLastError();
 }
 
 // 64 rows per workgroup pass: two workgroups fit a CU, and the passes over one
@@ -868,12 +824,15 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   return pw_dispatch<64>(loader, epi, a, st);
 }
 
-hipError_t launch_dcblock_f16(int C, const BlockArgs& a, hipStream_t st) {
+hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t st) {
   dim3 grid(dc_grid(a.h, a.w)), block(512);
-  switch (C) {
-    case 64: launch(k_dcblock_f16<64>, grid, block, st, a); break;
-    case 128: launch(k_dcblock_f16<128>, grid, block, st, a); break;
-    case 256: launch(k_dcblock_f16<256>, grid, block, st, a); break;
+  switch (C * 2 + (gated ? 1 : 0)) {
+    case 128: launch(k_dcblock_f16<64, false>, grid, block, st, a); break;
+    case 256: launch(k_dcblock_f16<128, false>, grid, block, st, a); break;
+    case 512: launch(k_dcblock_f16<256, false>, grid, block, st, a); break;
+    case 129: launch(k_dcblock_f16<64, true>, grid, block, st, a); break;
+    case 257: launch(k_dcblock_f16<128, true>, grid, block, st, a); break;
+    case 513: launch(k_dcblock_f16<256, true>, grid, block, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

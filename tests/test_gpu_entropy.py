@@ -152,3 +152,25 @@ def test_int_scale_indices_and_cross_decode_with_oracle():
         assert ok
         np.testing.assert_array_equal(q_or.reshape(r.q.shape), r.q)
         st = r.state
+
+
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_coded_round_trip_with_gated_blocks_and_modules(path):
+    # the coder takes the symbols and scale indices of any model form
+    H, W, C, ne, nd = 112, 208, 128, 1, 1
+    kw = dict(block="gated", n_fe_blocks=1, n_rg_blocks=1, qp_banks=True)
+    flat = synth.make_weights(C, ne, nd, block="gated", n_fe=1, n_rg=1, banks=True)
+    enc, dec, ref = (Codec(H, W, C, ne, nd, path, flat, device=DEV, **kw) for _ in range(3))
+    odt = torch.int16 if path == "int16" else torch.float16
+    for t, qp in enumerate([5, 5, 50]):
+        say("coded gated + modules", path, "frame", t, "qp", qp)
+        for c in (enc, dec, ref):
+            c.set_qp(qp)
+        x = gpu(synth.random_frame(H, W, seed=70 + t))
+        q = torch.empty(enc.q_shape, dtype=torch.int16, device=DEV)
+        buf, nb = enc.encode_coded(x, q_out=q)
+        xo, st = dec.decode_coded(buf, int(host(nb)))
+        xr = ref.decode(q, out=torch.empty(enc.frame_shape, dtype=odt, device=DEV))
+        assert int(host(st)) == 0
+        np.testing.assert_array_equal(host(xo), host(xr))
+        np.testing.assert_array_equal(host(dec.get_state()[0]), host(enc.get_state()[0]))
