@@ -216,17 +216,13 @@ struct Packer {
         o[22] = o[23] = 0;
       }
     }
-    if (gated && is_int) {
-      // Gated block: pw1 as a pointwise GEMM whose packed rows come in passes
-      // of 64, the 32 h1 rows of channels 32 t .. 32 t + 31 then their 32 h2
-      // rows (so one pass holds both halves of the chunk for the gate
-      // epilogue); pw2 is a plain C x C GEMM.
-      d.pw1 = gemm(w1, b1, 2 * C, C, C,
-                   [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
-                   [](int k) { return k; });
-      d.pw2 = plain(w2, b2, C, C);
-      return d;
-    }
+    // Gated form (both paths): entry 2p carries h1 rows 32 p .. +31 (pw1 rows
+    // 32 p ..), entry 2p + 1 the matching h2 rows (pw1 rows C + 32 p ..) and
+    // the pw2 fragments of gated channels 32 p .. +31; entry 2p's pw2 part is
+    // unused (zero).  The LeakyReLU form takes hidden rows 32 j .. in entry j.
+    auto row1 = [&](int j) { return gated ? (j & 1 ? C : 0) + 32 * (j >> 1) : 32 * j; };
+    auto hid0 = [&](int j) { return gated ? 32 * (j >> 1) : 32 * j; };
+    const int ld2 = gated ? C : 2 * C;
     if (!is_int) {
       // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1
       // fragments (rows 32j..32j+31, all C inputs), one bias fragment (column
@@ -241,12 +237,6 @@ struct Packer {
       d.pw2.bias = img.add((size_t)C * 4);
       f16* cp = img.at<f16>(d.pw1.w);
       auto kmap = [](int k) { return 8 * ((k % 8) / 4) + 4 * ((k / 8) % 2) + (k % 4); };  // within 16
-      // Gated form: entry 2p carries h1 rows 32 p .. +31 (pw1 rows 32 p ..), entry
-      // 2p + 1 the matching h2 rows (pw1 rows C + 32 p ..) and the pw2 fragments
-      // of gated channels 32 p .. +31; entry 2p's pw2 part is unused (zero).
-      auto row1 = [&](int j) { return gated ? (j & 1 ? C : 0) + 32 * (j >> 1) : 32 * j; };
-      auto hid0 = [&](int j) { return gated ? 32 * (j >> 1) : 32 * j; };
-      const int ld2 = gated ? C : 2 * C;
       for (int j = 0; j < NCH; ++j)
         for (int f = 0; f < FR; ++f)
           for (int l = 0; l < 64; ++l)
@@ -300,26 +290,27 @@ struct Packer {
             if (f < 2 * KSI) {
               const int sstep = f % KSI;
               hi = f < KSI;
-              const int n = 32 * j + (l & 31), k = 32 * sstep + 16 * (l >> 5) + e;
+              const int n = row1(j) + (l & 31), k = 32 * sstep + 16 * (l >> 5) + e;
               wi = q16(w1[(size_t)n * C + k]);
             } else {
               const int t = (f - 2 * KSI) % MT;
               hi = f < 2 * KSI + MT;
               const int n = 32 * t + (l & 31);
-              wi = q16(w2[(size_t)n * 2 * C + 32 * j + kmap(16 * (l >> 5) + e)]);
+              wi = gated && !(j & 1) ? 0 : q16(w2[(size_t)n * ld2 + hid0(j) + kmap(16 * (l >> 5) + e)]);
             }
             cp[(((size_t)j * FR + f) * 64 + l) * 16 + e] = digit(wi, hi);
           }
     int32_t* c1 = img.at<int32_t>(d.pw1.bias);
     int32_t* c2 = img.at<int32_t>(d.pw2.bias);
-    for (int n = 0; n < 2 * C; ++n) {
+    for (int i = 0; i < 2 * C; ++i) {  // in entry order: position 32 j + r is row row1(j) + r
+      const int n = row1(i / 32) + i % 32;
       int64_t sum = 0;
       for (int k = 0; k < C; ++k) sum += q16(w1[(size_t)n * C + k]);
-      c1[n] = (int32_t)(uint32_t)(uint64_t)(512 * (int64_t)q16(b1[n]) + 128 * sum);
+      c1[i] = (int32_t)(uint32_t)(uint64_t)(512 * (int64_t)q16(b1[n]) + 128 * sum);
     }
     for (int n = 0; n < C; ++n) {
       int64_t sum = 0;
-      for (int k = 0; k < 2 * C; ++k) sum += q16(w2[(size_t)n * 2 * C + k]);
+      for (int k = 0; k < ld2; ++k) sum += q16(w2[(size_t)n * ld2 + k]);
       c2[n] = (int32_t)(uint32_t)(uint64_t)(512 * (int64_t)q16(b2[n]) + 128 * sum);
     }
     return d;
@@ -330,8 +321,7 @@ struct Layout {
   ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
   std::vector<BlockDev> enc, dec, fe, rg;
   size_t sigma_tab = 0;
-  size_t sig_tab = 0;  // int path, gated block: int16 sigmoid table
-  size_t zC = 0;       // int path, gated block: hidden buffer
+  size_t sig8 = 0;     // int path, gated block: compact sigmoid table
   size_t ctxF = 0;     // feature extractor output (the temporal context)
   // entropy coder tables
   size_t c_scales = 0, c_tab = 0, c_ktab = 0;
@@ -496,12 +486,28 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   }
   if (is_int && cfg.block == NCODEC_BLOCK_GATED) {
     // S[v] = RHE(512 sigmoid(4 v / 512)) for every int16 v (the WSiLU's
-    // sigmoid, K1-scaled in and out); no entry lies within 1e-6 of a rounding tie
-    L.sig_tab = img.add(65536 * 2);
-    int16_t* st = img.at<int16_t>(L.sig_tab);
-    for (int i = 0; i < 65536; ++i) {
-      const double v = (double)(i - 32768);
-      st[i] = (int16_t)std::nearbyint(512.0 / (1.0 + std::exp(-4.0 * v / 512.0)));
+    // sigmoid, K1-scaled in and out; no entry lies within 1e-6 of a rounding
+    // tie).  The kernel reads it from a compact form: s8[a] = S[a] - 256 for
+    // 0 <= a < 888, S[a] = 512 above, S[-a] = 512 - S[a].  That form is
+    // checked against the full table here.
+    constexpr int kSat = 888, kBytes = 896;
+    auto S = [](int v) { return (int)std::nearbyint(512.0 / (1.0 + std::exp(-4.0 * (double)v / 512.0))); };
+    L.sig8 = img.add(kBytes);
+    uint8_t* s8 = img.at<uint8_t>(L.sig8);
+    bool shape_ok = S(-32768) == 0;
+    for (int a = 0; a < 32768; ++a) {
+      const int sa = S(a);
+      if (a < kSat) {
+        shape_ok = shape_ok && sa >= 256 && sa <= 511;
+        s8[a] = (uint8_t)(sa - 256);
+      } else {
+        shape_ok = shape_ok && sa == 512;
+      }
+      shape_ok = shape_ok && S(-a) == 512 - sa;
+    }
+    if (!shape_ok) {
+      if (err) *err = "internal: sigmoid table does not have the compact form";
+      return false;
     }
   }
   if (is_int) {
@@ -530,7 +536,6 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
   if (cfg.n_fe_blocks > 0) L.ctxF = alloc(fb);
-  if (cfg.block == NCODEC_BLOCK_GATED && is_int) L.zC = alloc(fb);
   L.y = alloc(lb);
   const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
@@ -647,11 +652,13 @@ hipError_t pw(ncodec_ctx* ctx, const char* kind, int loader, int epi, const PwAr
   });
 }
 
-hipError_t dcblock(ncodec_ctx* ctx, const BlockArgs& ba) {
+hipError_t dcblock(ncodec_ctx* ctx, BlockArgs ba) {
   const int C = ctx->cfg.channels;
+  const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
+  if (gated && ctx->is_int()) ba.sig8 = ctx->p(ctx->L.sig8);
   return timed(ctx, "dcblock", [&] {
-    return ctx->is_int() ? launch_dcblock_i16(C, ba, ctx->stream)
-                         : launch_dcblock_f16(C, ctx->cfg.block == NCODEC_BLOCK_GATED, ba, ctx->stream);
+    return ctx->is_int() ? launch_dcblock_i16(C, gated, ba, ctx->stream)
+                         : launch_dcblock_f16(C, gated, ba, ctx->stream);
   });
 }
 
@@ -676,37 +683,8 @@ PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
   return a;
 }
 
-// One gated DC block (Supp. B.1 with WSiLU and Chunk) on the int path, as
-// three launches: depthwise z -> ed, pw1 with the gate epilogue ed -> zC, pw2
-// with the residual epilogue (zC, z) -> dst.  ed and zC are free while the
-// blocks run.  (The fp16 path runs the gated block fused, in one launch.)
-hipError_t gated_block(ncodec_ctx* ctx, const BlockDev& b, const void* z, void* dst) {
-  const int C = ctx->cfg.channels;
-  const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
-  const Layout& L = ctx->L;
-  hipError_t e = timed(ctx, "dw", [&] { return launch_dw_i16(z, ctx->p(b.dww), ctx->p(L.ed), h8, w8, C, ctx->stream); });
-  if (e != hipSuccess) return e;
-  PwArgs a = conv_args(ctx, b.pw1, C, 2 * C, h8 * w8);
-  a.src0 = ctx->p(L.ed);
-  a.C0 = C;
-  a.dst = ctx->p(L.zC);
-  a.Cdst = C;
-  a.sig_tab = ctx->p<int16_t>(L.sig_tab);
-  e = pw(ctx, "gate", LD_NHWC, EP_GATE, a);
-  if (e != hipSuccess) return e;
-  a = conv_args(ctx, b.pw2, C, C, h8 * w8);
-  a.src0 = ctx->p(L.zC);
-  a.C0 = C;
-  a.y = z;
-  a.dst = dst;
-  a.Cdst = C;
-  return pw(ctx, "res", LD_NHWC, EP_RES, a);
-}
-
 // One DC block of either form, src -> dst.
 hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* dst) {
-  // the gated form is fused on the fp16 path; the int path runs it as three launches
-  if (ctx->cfg.block == NCODEC_BLOCK_GATED && ctx->is_int()) return gated_block(ctx, b, src, dst);
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
@@ -771,15 +749,7 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   for (int k = 0; k < c.n_dec_blocks; ++k) {
     void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
     const BlockDev& b = L.dec[k];
-    if (c.block == NCODEC_BLOCK_GATED && ctx->is_int()) {
-      NC_HIP(ctx, gated_block(ctx, b, z, dst), "decoder block");
-      z = dst;
-      continue;
-    }
-    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
-                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
-                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
-    NC_HIP(ctx, dcblock(ctx, ba), "decoder block");
+    NC_HIP(ctx, run_block(ctx, b, z, dst), "decoder block");
     z = dst;
   }
   return NCODEC_OK;
@@ -818,15 +788,7 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   for (int k = 0; k < c.n_enc_blocks; ++k) {
     void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
     const BlockDev& b = L.enc[k];
-    if (c.block == NCODEC_BLOCK_GATED && ctx->is_int()) {
-      NC_HIP(ctx, gated_block(ctx, b, z, dst), "encoder block");
-      z = dst;
-      continue;
-    }
-    BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
-                 ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
-                 ctx->p(b.dww), ctx->p(b.dwb), z, dst, h8, w8, ctx->p(L.zpad)};
-    NC_HIP(ctx, dcblock(ctx, ba), "encoder block");
+    NC_HIP(ctx, run_block(ctx, b, z, dst), "encoder block");
     z = dst;
   }
 

@@ -38,8 +38,6 @@ enum Epi : int {
   EP_PRIOR = 3,      // rows (32 mu, 32 s) per pass: quantise y, write q, yhat, bit partials
   EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
   EP_SCALES = 5,     // same rows: only the scale index of every symbol (entropy decoding)
-  EP_GATE = 6,       // int path: rows (32 h1, 32 h2) per pass: dst = WSiLU(h1) * h2 (gated block, C channels)
-  EP_RES = 7,        // int path: dst[p*Cdst + n] = sat16(result + y[p*Cdst + n]) (residual add)
 };
 
 struct PwArgs {
@@ -66,7 +64,6 @@ struct PwArgs {
   uint8_t* k_out;          // planar scale indices of the entropy coder (nullable for EP_PRIOR)
   const float* scales;     // fp16 path: the NS coder scales sigma_j (fp32)
   const uint8_t* k_tab;    // int path: scale index for s_i + 32768
-  const int16_t* sig_tab;  // int path, EP_GATE: sigmoid table, entry v + 32768
 };
 
 struct BlockArgs {
@@ -82,6 +79,7 @@ struct BlockArgs {
   void* dst;         // z' (NHWC), must not alias src
   int h, w;
   const void* zpad;  // C zero elements: the depthwise taps outside the image read these
+  const void* sig8 = nullptr;  // int path, gated form: compact sigmoid table (896 bytes)
 };
 
 struct PriorArgs {
@@ -138,11 +136,10 @@ hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_
 
 // Depthwise 3x3 + bias of the gated block, NHWC (C channels, h x w pixels),
 // weights in the block's packed depthwise image.
-hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st);
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t st);
-hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st);
+hipError_t launch_dcblock_i16(int C, bool gated, const BlockArgs& a, hipStream_t st);
 hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials);
 hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials);
 int prior_partials_f16(int C, int P);

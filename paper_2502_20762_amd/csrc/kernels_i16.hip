@@ -308,25 +308,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
     }
-  } else if constexpr (EPI == EP_GATE) {
-    // gated block: a pass holds h1 of channels c0 .. c0+31 then h2 of the same
-    // channels; WSiLU_i = RHE(h1 S[h1] / 512) with the int16 sigmoid table S,
-    // g = clip(RHE(WSiLU_i h2 / 512)) (|h1 S| <= 2^24, |WSiLU_i h2| <= 2^30)
-    static_assert(NT == 64, "gate passes are 64 rows");
-    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
-    const int gp = tile * 128 + px;
-    if (gp < a.P) {
-      int u[8], v[8];
-      parked(px, g8, u);
-      parked(px, 4 + g8, v);
-      shortx8 o;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int ws = rhe_shift(u[e] * (int)a.sig_tab[u[e] + 32768], 9);
-        o[e] = (short)clip16(rhe_shift(ws * v[e], 9));
-      }
-      *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = o;
-    }
   } else if constexpr (EPI == EP_REC) {
 #pragma unroll
     for (int it = 0; it < UNITS / 512; ++it) {
@@ -354,16 +335,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         int v[8];
         parked(px, nl8, v);
         shortx8 o;
-        if constexpr (EPI == EP_RES) {
-          const shortx8 res = *(const shortx8*)((const int16_t*)a.y + (size_t)gp * a.Cdst + n0 + 8 * nl8);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = (short)clip16(v[e] + (int)res[e]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
-        }
+        for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
         size_t off;
-        if constexpr (EPI == EP_NHWC || EPI == EP_RES) {
+        if constexpr (EPI == EP_NHWC) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -464,6 +439,52 @@ __device__ __forceinline__ void dci_hidden_store(const I16Acc& acc, int lane, in
   gx[64 + lane] = gl;
 }
 
+// Gated form (Supp. B.1, WSiLU and Chunk; Sec. 4.5, the sigmoid table).  With
+// h = rescale(pw1 sum) on the int16 scale, WSiLU(h1) = RHE(h1 S[h1] / 512) and
+// g = clip(RHE(WSiLU(h1) h2 / 512)), S[v] = RHE(512 sigmoid(4 v / 512)).  S is
+// read from the compact LDS table s8: S[v] = 256 + s8[v] for 0 <= v < 888,
+// 512 for v >= 888, and 512 - S[-v] for v < 0 (the table is odd about 256).
+constexpr int kSigSat = 888;   // S[v] = 512 from here on
+constexpr int kSigBytes = 896; // s8, padded to 16-byte units
+__device__ __forceinline__ int dci_sigmoid(int v, const uint8_t* s8) {
+  const int a = v < 0 ? -v : v;
+  const int sa = a >= kSigSat ? 512 : 256 + (int)s8[min(a, kSigSat - 1)];  // index kept in the table
+  return v < 0 ? 512 - sa : sa;
+}
+// RHE(m / 512) for |m| <= 2^30
+__device__ __forceinline__ int rhe9(int m) { return (m + 255 + ((m >> 9) & 1)) >> 9; }
+
+// WSiLU of the rescaled h1 chain, as 8 packed int16 pairs.
+__device__ __forceinline__ void dci_wsilu(const I16Acc& acc, const uint8_t* s8, uint32_t* ws) {
+  int wv[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int hv = rescale13(combine_i16(acc.hh[r], acc.mid[r], acc.ll[r], 0));
+    wv[r] = rhe9(hv * dci_sigmoid(hv, s8));  // |h S| <= 2^24, |WSiLU| <= |h|
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ws[e] = pack2(wv[2 * e], wv[2 * e + 1]);
+}
+
+// g = clip(RHE(WSiLU(h1) h2 / 512)) from the h2 chain, split into int8 digits
+// and stored as the pw2 operand fragments (as dci_hidden_store).
+__device__ __forceinline__ void dci_gate_store(const uint32_t* ws, const I16Acc& acc, int lane, intx4* gx) {
+  int gv[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int h2 = rescale13(combine_i16(acc.hh[r], acc.mid[r], acc.ll[r], 0));
+    const int w1 = (int)(short)(ws[r >> 1] >> (16 * (r & 1)));
+    gv[r] = clip16(rhe9(w1 * h2));  // |product| <= 2^30
+  }
+  uint32_t d[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[e] = pack2(gv[2 * e], gv[2 * e + 1]);
+  intx4 gh, gl;
+  split16(d, gh, gl);
+  gx[lane] = gh;
+  gx[64 + lane] = gl;
+}
+
 template <int C>
 __device__ __forceinline__ void dci_project(const char* wb, const intx4* gx, int hf, int lane, intx16* out) {
   constexpr int KSI = DcSmemI<C>::KSI, MT = DcSmemI<C>::MT;
@@ -513,7 +534,12 @@ struct DcDwI {
   static_assert(2 * SPW * (NRW / 2) * XF <= RB, "the exchange fits the band's region");
 };
 
-template <int C>
+// GATED: the gated form, scheduled like the fp16 kernel's: the weight entries
+// alternate between the h1 rows and the h2 rows (plus the pw2 fragments) of
+// one 32-channel pair, one wave of each SIMD pair produces both chains of a
+// pair, keeps WSiLU(h1) in registers and gates when h2 is done; pw2 runs in odd
+// iterations only.  The compact sigmoid table sits after the corrections.
+template <int C, bool GATED>
 __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   using G = DcDwI<C>;
   constexpr int KSI = DcSmemI<C>::KSI;
@@ -534,7 +560,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   constexpr int O1 = BUF, O2 = 2 * BUF, O3 = 3 * BUF, OGX = 4 * BUF;
   constexpr int OR = BUF + 2 * KSI * 1024;  // first band region
   constexpr int OC = (OR + 8 * G::RB > OGX + 16384 ? OR + 8 * G::RB : OGX + 16384);
-  constexpr int SMEM = OC + 3 * C * 4;      // c1s: 2 C ints, c2s: C ints
+  constexpr int SMEM = OC + 3 * C * 4 + (GATED ? kSigBytes : 0);  // c1s: 2 C ints, c2s: C ints, s8
   static_assert(SMEM <= 160 * 1024, "fits the LDS of a CU");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   char* const wb0 = smem;
@@ -545,6 +571,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   intx4* const gx1 = (intx4*)(smem + OGX + 8192);  // odd chunks
   int* const c1s = (int*)(smem + OC);              // pw1 corrections 512 b + 128 sum w
   int* const c2s = c1s + 2 * C;                    // pw2 corrections
+  const uint8_t* const s8 = (const uint8_t*)(c2s + C);  // gated: compact sigmoid table
 
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -568,6 +595,8 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     for (int i = 0; i < (2 * C / 4 + 63) / 64; ++i)
       if (64 * i + lane < n16) dma16(src + 4 * (64 * i + lane), dstl + 4 * 64 * i);
   }
+  if constexpr (GATED)  // wave 2, likewise
+    if (wave == 2 && lane < kSigBytes / 16) dma16((const char*)a.sig8 + 16 * lane, (char*)(c2s + C));
 
   // Depthwise role.
   const int cbk = wave % G::NCB, rbk = wave / G::NCB;
@@ -713,7 +742,11 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
   // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + LDS_PER_WAVE) : "memory");
   lds_barrier();
-  if (hf == 0) dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0 + 128 * pg);
+  uint32_t ws[8];  // gated: WSiLU of the h1 chain of the pair being produced
+  if (hf == 0) {
+    if constexpr (GATED) dci_wsilu(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), s8, ws);
+    else dci_hidden_store(dci_hidden_mfma<C>(wb0, ah, al, c1s, 0, h, lane), lane, gx0 + 128 * pg);
+  }
   lds_barrier();  // hidden chunk 0 visible
 
   // The residual tile (128 pixels x C int16, pixel px at byte 2 C px of
@@ -736,12 +769,20 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
                   __attribute__((always_inline)) {
     const bool more = j + 3 < NCH;
     if (more) dci_issue<C>(wchunks, j + 3, wiss, wave, lane);
-    const bool produce = j + 1 < NCH && hf == ((j + 1) & 1);
+    // producer of chunk c: wave c % 2 of the pair, or in the gated form (c / 2) % 2
+    const bool produce = j + 1 < NCH && hf == (GATED ? ((j + 1) >> 1) & 1 : (j + 1) & 1);
     I16Acc hacc;
     if (produce) hacc = dci_hidden_mfma<C>(wnxt, ah, al, c1s, j + 1, h, lane);
     if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
-    dci_project<C>(wcur, gcur, hf, lane, out);
-    if (produce) dci_hidden_store(hacc, lane, gnxt);
+    if (!GATED || (j & 1)) dci_project<C>(wcur, gcur, hf, lane, out);
+    if (produce) {
+      if constexpr (GATED) {
+        if ((j + 1) & 1) dci_gate_store(ws, hacc, lane, gnxt);  // h2 of the pair: gate it
+        else dci_wsilu(hacc, s8, ws);
+      } else {
+        dci_hidden_store(hacc, lane, gnxt);
+      }
+    }
     if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
@@ -813,89 +854,13 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
-  NC_PW(LD_NHWC, EP_RES)
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
     NC_PW(LD_NHWC, EP_SCALES)
-    NC_PW(LD_NHWC, EP_GATE)
   }
 #undef NC_PW
   return hipErrorInvalidValue;
-}
-
-// Depthwise 3x3 of the gated block on the integer path (Alg. 1):
-// a = clip(RHE((sum z_i w_i + 512 b_i) / 8192)) in wrapping int32.  Thread =
-// (8 channels, one column, 8 rows) sliding a 3 x 3 window of 16-byte vectors
-// down the column (out-of-frame vectors are zero); the weights of its 2
-// channel quads come once from the block's packed depthwise image (96 bytes
-// per quad: per tap the int16 pairs (w_c, w_c+1), (w_c+2, w_c+3); then the
-// four 512 b_i; two pad words).
-constexpr int kDwRowsI = 8;
-
-__global__ __launch_bounds__(256) void k_dw_i16(const int16_t* z, const uint32_t* dww, int16_t* out, int h8, int w8,
-                                              int C) {
-  const int C8 = C >> 3;
-  const int nyb = (h8 + kDwRowsI - 1) / kDwRowsI;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)nyb * w8 * C8) return;
-  const int c8 = (int)(t % C8);
-  const int64_t r = t / C8;
-  const int x = (int)(r % w8), y0 = (int)(r / w8) * kDwRowsI;
-  const intx4* wq = (const intx4*)(dww + 48 * c8);
-  intx4 wv[12];
-#pragma unroll
-  for (int i = 0; i < 12; ++i) wv[i] = wq[i];
-  // word k of quad j (j = 0, 1)
-  auto word = [&](int j, int k) -> uint32_t { return (uint32_t)wv[6 * j + (k >> 2)][k & 3]; };
-  auto ld = [&](int yy, int xx) -> shortx8 {
-    shortx8 v = {};
-    if (yy >= 0 && yy < h8 && xx >= 0 && xx < w8) v = *(const shortx8*)(z + (size_t)(yy * w8 + xx) * C + 8 * c8);
-    return v;
-  };
-  shortx8 win[3][3];
-#pragma unroll
-  for (int dx = 0; dx < 3; ++dx) {
-    win[0][dx] = ld(y0 - 1, x + dx - 1);
-    win[1][dx] = ld(y0, x + dx - 1);
-  }
-#pragma unroll
-  for (int i = 0; i < kDwRowsI; ++i) {
-    const int y = y0 + i;
-    if (y >= h8) break;
-#pragma unroll
-    for (int dx = 0; dx < 3; ++dx) win[2][dx] = ld(y + 1, x + dx - 1);
-    uint32_t acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = word(e >> 2, 18 + (e & 3));
-#pragma unroll
-    for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-      for (int kx = 0; kx < 3; ++kx)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int tap = 3 * ky + kx;
-          const int wgt = (int)(int16_t)(uint16_t)(word(e >> 2, 2 * tap + ((e >> 1) & 1)) >> (16 * (e & 1)));
-          acc[e] += (uint32_t)(wgt * (int)win[ky][kx][e]);
-        }
-    shortx8 o;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (short)rescale13((int)acc[e]);
-    *(shortx8*)(out + (size_t)(y * w8 + x) * C + 8 * c8) = o;
-#pragma unroll
-    for (int dx = 0; dx < 3; ++dx) {
-      win[0][dx] = win[1][dx];
-      win[1][dx] = win[2][dx];
-    }
-  }
-}
-
-hipError_t launch_dw_i16(const void* z, const void* dww, void* out, int h, int w, int C, hipStream_t st) {
-  if (C % 8) return hipErrorInvalidValue;
-  const int64_t n = (int64_t)((h + kDwRowsI - 1) / kDwRowsI) * w * (C / 8);
-  launch(k_dw_i16, dim3((unsigned)((n + 255) / 256)), dim3(256), st, (const int16_t*)z, (const uint32_t*)dww,
-         (int16_t*)out, h, w, C);
-  return hipGetLastError();
 }
 
 // 64 rows per workgroup pass: two workgroups fit a CU, and the passes over one
@@ -911,12 +876,16 @@ hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   return pw_dispatch<64>(loader, epi, a, st);
 }
 
-hipError_t launch_dcblock_i16(int C, const BlockArgs& a, hipStream_t st) {
+hipError_t launch_dcblock_i16(int C, bool gated, const BlockArgs& a, hipStream_t st) {
   dim3 grid(dc_grid(a.h, a.w)), block(512);
-  switch (C) {
-    case 64: launch(k_dcblock_i16<64>, grid, block, st, a); break;
-    case 128: launch(k_dcblock_i16<128>, grid, block, st, a); break;
-    case 256: launch(k_dcblock_i16<256>, grid, block, st, a); break;
+  if (gated && !a.sig8) return hipErrorInvalidValue;
+  switch (C * 2 + (gated ? 1 : 0)) {
+    case 128: launch(k_dcblock_i16<64, false>, grid, block, st, a); break;
+    case 256: launch(k_dcblock_i16<128, false>, grid, block, st, a); break;
+    case 512: launch(k_dcblock_i16<256, false>, grid, block, st, a); break;
+    case 129: launch(k_dcblock_i16<64, true>, grid, block, st, a); break;
+    case 257: launch(k_dcblock_i16<128, true>, grid, block, st, a); break;
+    case 513: launch(k_dcblock_i16<256, true>, grid, block, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
