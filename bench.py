@@ -104,8 +104,8 @@ def cpu_baseline(pre, weights, strip_rows, path="fp16"):
 
 TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "dcblock_hd1080_hbm_traffic.md")
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2502_20762_amd", "csrc")
-SOURCES = {"k_dcblock_f16<256>": ["kernels_f16.hip", "common.hpp", "internal.hpp"],
-           "k_dcblock_i16<256>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
+SOURCES = {"k_dcblock_f16<256, false>": ["kernels_f16.hip", "common.hpp", "internal.hpp"],
+           "k_dcblock_i16<256, false>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
 
 
 def counted_traffic(kernel):
@@ -122,7 +122,7 @@ def counted_traffic(kernel):
         return None
     for line in text.splitlines():
         parts = line.split()
-        if len(parts) == 4 and parts[0] == "traffic" and parts[1] == kernel:
+        if len(parts) == 4 and parts[0] == "traffic" and parts[1] == kernel.replace(" ", ""):
             fields = dict(p.split("=", 1) for p in parts[2:])
             if fields.get("sources_sha256") == h.hexdigest():
                 return int(fields["bytes_per_launch"])
@@ -411,7 +411,7 @@ def main():
         res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
 
     def summary(path, r, peak_tflops, op_scale, unit):
-        traffic = counted_traffic("k_dcblock_f16<256>" if path == "fp16" else "k_dcblock_i16<256>")
+        traffic = counted_traffic("k_dcblock_f16<256, false>" if path == "fp16" else "k_dcblock_i16<256, false>")
         K = args.steps
         fl, by = kinds["dcblock"]
         kd = r["kernels"]["dcblock"]

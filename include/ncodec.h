@@ -137,6 +137,16 @@ ncodec_status ncodec_reset(ncodec_ctx* ctx);
  * integer range. */
 ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp);
 
+/* Select a rate between the rate points (supplementary material, rate
+ * adjustment: linear interpolation in the bank for rates between two learned
+ * points).  qp is a real number in [0, 63]; with i = min(floor(qp), 62) and
+ * t = qp - i, each bank vector is (1 - t) row i + t row i+1, computed in
+ * double, then folded as in ncodec_set_qp.  An integer qp gives exactly row
+ * qp (ncodec_set_qp(ctx, q) is ncodec_set_rate(ctx, q)).  Same
+ * synchronisation, state and error behaviour as ncodec_set_qp; EINVAL for qp
+ * outside [0, 63] or NaN. */
+ncodec_status ncodec_set_rate(ncodec_ctx* ctx, double qp);
+
 /* Encode one frame (Sec. 4.1, Fig. 4 encoder side, Supp. B.3 encoding).
  *  d_frame: 3 x H x W planar fp16 (IEEE binary16), values in [0, 1]; the int
  *           path converts it with x_i = round(512 x) (Alg. 1).

@@ -123,10 +123,24 @@ def _f16(v: np.ndarray) -> np.ndarray:
     return np.asarray(v, dtype=np.float64).astype(np.float16).astype(np.float64)
 
 
-def fold_qp(p: Params, qp: int) -> Params:
-    """Params with row qp of the vector banks folded into the convolutions
-    next to them, each folded value rounded to fp16 once (the precision of
-    every weight):
+def bank_vectors(p: Params, qp) -> tuple:
+    """The four bank vectors (q_e, q_d, q_f, q_r) at rate point qp in [0, 63].
+    Integer qp: row qp.  Between two rate points the supplementary
+    rate-adjustment section interpolates the vectors linearly; with
+    i = min(floor(qp), 62) and t = qp - i the vector is (1 - t) row i +
+    t row i+1 (float64; exactly row qp when qp is an integer)."""
+    qp = float(qp)
+    if not 0.0 <= qp <= NUM_QP - 1:
+        raise ValueError(f"qp must be in [0, {NUM_QP - 1}]")
+    i = min(int(np.floor(qp)), NUM_QP - 2)
+    t = qp - i
+    return tuple((1.0 - t) * p.banks[n][i] + t * p.banks[n][i + 1] for n in ("q_e", "q_d", "q_f", "q_r"))
+
+
+def fold_qp(p: Params, qp) -> Params:
+    """Params with the vector banks at rate point qp (:func:`bank_vectors`)
+    folded into the convolutions next to them, each folded value rounded to
+    fp16 once (the precision of every weight):
       q_e scales y:           down rows and bias,  W'[o] = q_e[o] W[o]
       q_d scales yhat:        up columns,          W'[:, c] = W[:, c] q_d[c]
       q_f scales the context: fuse columns C..2C,  W'[:, C + c] = W[:, C + c] q_f[c]
@@ -134,10 +148,8 @@ def fold_qp(p: Params, qp: int) -> Params:
     Without banks, p itself."""
     if p.banks is None:
         return p
-    if not 0 <= qp < NUM_QP:
-        raise ValueError(f"qp must be in [0, {NUM_QP})")
     C = p.C
-    qe, qd, qf, qr = (p.banks[n][qp] for n in ("q_e", "q_d", "q_f", "q_r"))
+    qe, qd, qf, qr = bank_vectors(p, qp)
     down = Conv(_f16(p.down.w * qe[:, None, None, None]), _f16(p.down.b * qe))
     up = Conv(_f16(p.up.w * qd[None, :]), p.up.b)
 

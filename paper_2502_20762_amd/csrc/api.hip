@@ -5,6 +5,7 @@
 // prior/quantiser/bits -> decoder (upsample -> fuse -> blocks) and keeps the
 // decoder output f_t as the next context without reconstructing the frame;
 // decoding runs prior -> decoder -> reconstruction.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -71,7 +72,7 @@ size_t weight_count(const ncodec_config& c) {
 }
 
 // fp16(w q) with one rounding: the precision of every weight of the image.
-float fold16(float w, float q) { return (float)(f16)((double)w * (double)q); }
+float fold16(float w, double q) { return (float)(f16)((double)w * q); }
 
 // ---------------------------------------------------------------- weight image
 struct ConvDev {
@@ -406,7 +407,7 @@ void build_coder_tables(Image& img, Layout& L, bool is_int, std::string* err) {
   }
 }
 
-bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err, int qp = 0) {
+bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& L, std::string* err, double qp = 0) {
   const int C = cfg.channels;
   const bool is_int = cfg.path == NCODEC_PATH_INT16;
   std::vector<float> zeros;
@@ -417,16 +418,30 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   Packer pk{cfg, img, is_int, err};
   const float* cur = w;
   auto take = [&](size_t n) { const float* p = cur; cur += n; return p; };
-  // vector banks (Sec. 4.4): row qp of q_e, q_d, q_f, q_r, at the end of the list
+  // vector banks (Sec. 4.4): q_e, q_d, q_f, q_r at the end of the list, 64
+  // rate points each.  Rate qp in [0, 63] takes (1 - t) row i + t row i+1 with
+  // i = min(floor(qp), 62), t = qp - i (in double): the row itself at an
+  // integer qp, the linear interpolation of the supplementary rate-adjustment
+  // section between two rate points otherwise.
   const size_t nb = (size_t)kNumQp * C;
   const float* bank = cfg.qp_banks ? w + weight_count(cfg) - 4 * nb : nullptr;
-  auto brow = [&](int b) { return bank + b * nb + (size_t)qp * C; };
+  std::vector<double> rows[4];
+  if (bank) {
+    const int i = std::min((int)std::floor(qp), kNumQp - 2);
+    const double t = qp - i;
+    for (int b = 0; b < 4; ++b) {
+      rows[b].resize(C);
+      const float* r0 = bank + b * nb + (size_t)i * C;
+      for (int c = 0; c < C; ++c) rows[b][c] = (1.0 - t) * (double)r0[c] + t * (double)r0[C + c];
+    }
+  }
+  auto brow = [&](int b) { return rows[b].data(); };
   std::vector<float> fdown, fdown_b, fup, ffe, ffd, frec;
   // fuse conv with its context columns C .. 2C scaled by q_f
   auto fuse_fold = [&](const float* W, std::vector<float>& out) -> const float* {
     if (!bank) return W;
     out.assign(W, W + (size_t)2 * C * C);
-    const float* qf = brow(2);
+    const double* qf = brow(2);
     for (int n = 0; n < C; ++n)
       for (int c = 0; c < C; ++c) out[(size_t)n * 2 * C + C + c] = fold16(out[(size_t)n * 2 * C + C + c], qf[c]);
     return out.data();
@@ -438,7 +453,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   for (int k = 0; k < cfg.n_enc_blocks; ++k) L.enc.push_back(pk.block(cur));
   const float* dn_w = take((size_t)4 * C * C); const float* dn_b = take(C);
   if (bank) {  // q_e scales the rows of the downsample (y)
-    const float* qe = brow(0);
+    const double* qe = brow(0);
     fdown.assign(dn_w, dn_w + (size_t)4 * C * C);
     fdown_b.assign(dn_b, dn_b + C);
     for (int o = 0; o < C; ++o) {
@@ -457,7 +472,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
                    [](int k) { return k; });
   const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
   if (bank) {  // q_d scales the columns of the upsample (its input yhat)
-    const float* qd = brow(1);
+    const double* qd = brow(1);
     fup.assign(up_w, up_w + (size_t)4 * C * C);
     for (size_t n = 0; n < (size_t)4 * C; ++n)
       for (int c = 0; c < C; ++c) fup[n * C + c] = fold16(fup[n * C + c], qd[c]);
@@ -470,7 +485,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   for (int k = 0; k < cfg.n_dec_blocks; ++k) L.dec.push_back(pk.block(cur));
   const float* rc_w = take((size_t)192 * C); const float* rc_b = take(192);
   if (bank) {  // q_r scales the columns of the reconstruction (the generated feature)
-    const float* qr = brow(3);
+    const double* qr = brow(3);
     frec.assign(rc_w, rc_w + (size_t)192 * C);
     for (int n = 0; n < 192; ++n)
       for (int c = 0; c < C; ++c) frec[(size_t)n * C + c] = fold16(frec[(size_t)n * C + c], qr[c]);
@@ -559,7 +574,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
 struct ncodec_ctx {
   ncodec_config cfg;
   std::vector<float> host_w;  // canonical weights, kept to refold the vector banks (qp_banks only)
-  int qp = 0;
+  double qp = 0;  // rate point of the folded banks
   int device;
   hipStream_t stream;
   char* ws;
@@ -1044,10 +1059,15 @@ ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights,
 }
 
 ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp) {
+  if (ctx && (qp < 0 || qp >= kNumQp)) return fail(ctx, NCODEC_EINVAL, "qp must be in [0, 64)");
+  return ncodec_set_rate(ctx, (double)qp);
+}
+
+ncodec_status ncodec_set_rate(ncodec_ctx* ctx, double qp) {
   ncodec_status st = enter(ctx);
   if (st) return st;
   if (!ctx->cfg.qp_banks) return fail(ctx, NCODEC_EINVAL, "the context has no vector banks (qp_banks = 0)");
-  if (qp < 0 || qp >= kNumQp) return fail(ctx, NCODEC_EINVAL, "qp must be in [0, 64)");
+  if (!(qp >= 0.0 && qp <= kNumQp - 1)) return fail(ctx, NCODEC_EINVAL, "qp must be in [0, 63]");
   if (qp == ctx->qp) return NCODEC_OK;
   Image img;
   Layout L;
@@ -1055,8 +1075,8 @@ ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp) {
   if (!build_layout(ctx->cfg, ctx->host_w.data(), img, L, &why, qp)) return fail(ctx, NCODEC_EINVAL, why);
   if (L.image_bytes != ctx->L.image_bytes) return fail(ctx, NCODEC_EINVAL, "internal: image size depends on qp");
   NC_HIP(ctx, hipMemcpyAsync(ctx->ws, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, ctx->stream),
-         "set_qp upload");
-  NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "set_qp");
+         "set_rate upload");
+  NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "set_rate");
   ctx->qp = qp;
   return NCODEC_OK;
 }

@@ -64,6 +64,7 @@ _SIGNATURES = {
                                      ctypes.POINTER(_P)]),
     "ncodec_reset": (ctypes.c_int, [_P]),
     "ncodec_set_qp": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "ncodec_set_rate": (ctypes.c_int, [_P, ctypes.c_double]),
     "ncodec_encode_frame": (ctypes.c_int, [_P, _P, _P, _P]),
     "ncodec_decode_frame": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_estimate_bits": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P]),
@@ -150,6 +151,10 @@ def ncodec_reset(ctx) -> None:
 
 def ncodec_set_qp(ctx, qp: int) -> None:
     _check(load_library().ncodec_set_qp(ctx, int(qp)), ctx)
+
+
+def ncodec_set_rate(ctx, qp: float) -> None:
+    _check(load_library().ncodec_set_rate(ctx, float(qp)), ctx)
 
 
 def ncodec_encode_frame(ctx, d_frame: int, d_q: int, d_bits: int = 0) -> None:
@@ -357,6 +362,9 @@ class Codec:
 
     def set_qp(self, qp: int):
         ncodec_set_qp(self.ctx, qp)
+
+    def set_rate(self, qp: float):
+        ncodec_set_rate(self.ctx, qp)
 
     def kernels_per_frame(self, decode=False):
         return ncodec_kernels_per_frame(self.ctx, decode)

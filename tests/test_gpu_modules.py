@@ -117,3 +117,41 @@ def test_set_qp_errors_and_bits_fall_with_qp():
         bits.append(float(host(b)))
     say("bits at qp 0, 32, 63:", bits)
     assert bits[0] > bits[1] > bits[2]
+
+
+@pytest.mark.parametrize("path", ["int16", "fp16"])
+def test_interpolated_rates_match_the_oracle(path):
+    # rates between the learned points: linearly interpolated bank vectors
+    H, W, C, ne, nd, nfe, nrg = 64, 96, 64, 1, 1, 1, 1
+    p, enc, dec = setup(H, W, C, ne, nd, nfe, nrg, path)
+    rates = [12.5, 12.5, 40.25, 62.75, 63.0]
+    st = None
+    for t, qp in enumerate(rates):
+        say("interpolated rate", path, "frame", t, "qp", qp)
+        enc.set_rate(qp)
+        dec.set_rate(qp)
+        x = synth.random_frame(H, W, seed=50 + t)
+        if path == "int16":
+            ip = ci.integerize(fold_qp(p, qp))
+            if st is None:
+                st = ci.zero_state(ip, H, W)
+            r = ci.encode_frame(ip, x, st)
+            q, bits = enc.encode(gpu(x))
+            np.testing.assert_array_equal(host(q), r.q, err_msg=f"qp={qp} q")
+            f, y = (host(v).astype(np.int64) for v in enc.get_state())
+            np.testing.assert_array_equal(f, r.state.feat, err_msg=f"qp={qp} f_t")
+            np.testing.assert_array_equal(y, r.state.yhat, err_msg=f"qp={qp} yhat")
+            xr, _ = ci.decode_frame(ip, r.q, st)
+            np.testing.assert_array_equal(host(dec.decode(q)), xr, err_msg=f"qp={qp} xhat")
+            st = r.state
+        else:
+            pq = fold_qp(p, qp)
+            f0, y0 = (host(v).astype(np.float64) for v in enc.get_state())
+            q, bits = enc.encode(gpu(x))
+            f1, y1 = (host(v).astype(np.float64) for v in enc.get_state())
+            f_ref, _ = check_fp16_encode(pq, x, f0, y0, host(q), float(host(bits)), f1, y1, f"rate {qp}")
+            xhat = host(dec.decode(q)).astype(np.float64)
+            assert_close_fp16(xhat, cf.reconstruct(pq, f_ref), f"rate {qp} xhat")
+    for bad in (-0.5, 63.01, float("nan")):
+        with pytest.raises(NcodecError):
+            enc.set_rate(bad)

@@ -138,3 +138,36 @@ def test_bits_fall_as_qp_rises():
         r = cf.encode_frame(pq, x, cf.zero_state(pq, 64, 64))
         bits.append(r.bits)
     assert bits[0] > bits[1] > bits[2], bits
+
+
+def test_bank_vectors_between_rate_points():
+    _, p = modular(C=64, ne=1, nd=1, nfe=0, nrg=0)
+    names = ("q_e", "q_d", "q_f", "q_r")
+    for qp in range(64):  # the learned points themselves, exactly
+        for v, n in zip(P.bank_vectors(p, qp), names):
+            np.testing.assert_array_equal(v, p.banks[n][qp])
+    for i in (0, 17, 62):
+        lo, hi = p.banks["q_d"][i], p.banks["q_d"][i + 1]
+        mid = P.bank_vectors(p, i + 0.5)[1]
+        np.testing.assert_allclose(mid, 0.5 * (lo + hi), rtol=0, atol=1e-15)
+        # on the segment between the two points, at a quarter of the way
+        q1 = P.bank_vectors(p, i + 0.25)[1]
+        np.testing.assert_allclose(q1 - lo, 0.25 * (hi - lo), rtol=0, atol=1e-15)
+        assert np.all(np.minimum(lo, hi) - 1e-15 <= q1) and np.all(q1 <= np.maximum(lo, hi) + 1e-15)
+    for bad in (-0.25, 63.5, float("nan")):
+        with pytest.raises(ValueError):
+            P.bank_vectors(p, bad)
+    # the fold at an interpolated rate differs from both neighbours
+    f = P.fold_qp(p, 20.5)
+    assert not np.array_equal(f.up.w, P.fold_qp(p, 20).up.w)
+    assert not np.array_equal(f.up.w, P.fold_qp(p, 21).up.w)
+
+
+def test_bits_at_an_interpolated_rate_lie_between():
+    _, p = modular(nfe=1, nrg=0)
+    x = synth.random_frame(64, 64, seed=8)
+    bits = []
+    for qp in (0, 31.5, 63):
+        pq = P.fold_qp(p, qp)
+        bits.append(cf.encode_frame(pq, x, cf.zero_state(pq, 64, 64)).bits)
+    assert bits[0] > bits[1] > bits[2], bits
