@@ -701,6 +701,9 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     const bool prefetch = j >= 1 && j + 2 < NCH && hf == pj2;
     floatx16 hacc;
     if (produce) {
+      // the producer's chain is the iteration's critical path: its MFMAs go
+      // first on the SIMD, the partner's projection fills the gaps
+      __builtin_amdgcn_s_setprio(2);
       if (j == 1) dc_load_w1<C>(wnxt, lane, wf);  // iteration 0 had no prefetch
       hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
     }
@@ -717,6 +720,7 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     }
     // chunk j+3 (in iteration 0 also chunk 2), or the residual in the last step
     if (dma || j == NCH - 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_setprio(0);
     lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {

@@ -772,7 +772,10 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     // producer of chunk c: wave c % 2 of the pair, or in the gated form (c / 2) % 2
     const bool produce = j + 1 < NCH && hf == (GATED ? ((j + 1) >> 1) & 1 : (j + 1) & 1);
     I16Acc hacc;
-    if (produce) hacc = dci_hidden_mfma<C>(wnxt, ah, al, c1s, j + 1, h, lane);
+    if (produce) {
+      __builtin_amdgcn_s_setprio(2);  // the producer's chain first on the SIMD
+      hacc = dci_hidden_mfma<C>(wnxt, ah, al, c1s, j + 1, h, lane);
+    }
     if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
     if (!GATED || (j & 1)) dci_project<C>(wcur, gcur, hf, lane, out);
     if (produce) {
@@ -785,6 +788,7 @@ __global__ __launch_bounds__(512) void k_dcblock_i16(BlockArgs a) {
     }
     if (more) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LDS_PER_WAVE) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_setprio(0);
     lds_barrier();
   };
   for (int j = 0; j < NCH; j += 4) {
