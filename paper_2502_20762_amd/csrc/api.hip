@@ -226,9 +226,9 @@ struct Packer {
     const int ld2 = gated ? C : 2 * C;
     if (!is_int) {
       // Chunk-major image: for each 32-channel hidden chunk j, the KS pw1
-      // fragments (rows 32j..32j+31, all C inputs), one bias fragment (column
-      // C of the pw1 matrix extended by its bias, contracted with a constant
-      // one), then the 2*MT pw2 fragments that consume that chunk.  The pw2
+      // fragments (rows 32j..32j+31, all C inputs), one bias fragment (the 32
+      // biases as fp32 at its start, the rest zero), then the 2*MT pw2
+      // fragments that consume that chunk.  The pw2
       // contraction index is permuted inside the chunk so that the pw1
       // accumulator registers are directly the pw2 operand.  One chunk is one
       // contiguous copy into LDS.
@@ -247,7 +247,7 @@ struct Packer {
                 const int n = row1(j) + (l & 31), k = 16 * f + 8 * (l >> 5) + e;
                 v = w1[(size_t)n * C + k];
               } else if (f == KS) {
-                v = (l < 32 && e == 0) ? b1[row1(j) + l] : 0.f;
+                v = 0.f;  // the bias, written below
               } else if (gated && !(j & 1)) {
                 v = 0.f;
               } else {
@@ -258,6 +258,12 @@ struct Packer {
               }
               cp[(((size_t)j * FR + f) * 64 + l) * 8 + e] = (f16)v;
             }
+      // fragment KS of chunk j: the 32 pw1 biases of its rows as fp32 (fp16 values),
+      // the chain's initial accumulator
+      for (int j = 0; j < NCH; ++j) {
+        float* fb = (float*)(cp + ((size_t)j * FR + KS) * 64 * 8);
+        for (int r = 0; r < 32; ++r) fb[r] = (float)(f16)b1[row1(j) + r];
+      }
       float* b1p = img.at<float>(d.pw1.bias);
       float* b2p = img.at<float>(d.pw2.bias);
       for (int n = 0; n < 2 * C; ++n) b1p[n] = (float)(f16)b1[n];

@@ -345,8 +345,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
 // goes to LDS in MFMA operand order so both waves of the pair consume it.
 //
 // The weights of one block are streamed in NCH = 2C/32 chunks: chunk j holds
-// the KS = C/16 pw1 fragments of hidden channels 32 j .. +31, their bias as
-// one more fragment (contracted with a constant-one B fragment), then the 2 MT
+// the KS = C/16 pw1 fragments of hidden channels 32 j .. +31, their bias in
+// one more fragment (32 fp32 values that start the chain), then the 2 MT
 // pw2 fragments that consume them (one 1 KiB MFMA A fragment each), into a
 // ring of four LDS buffers with direct global->LDS loads (the loop is unrolled
 // by four, so every buffer address is static).  The residual is added from
@@ -376,24 +376,33 @@ __device__ __forceinline__ void dc_load_w1(const char* wb, int lane, half8* wf) 
   for (int s = 0; s < DcSmem<C>::KS / 2; ++s) wf[s] = w[s * 64];
 }
 
-// pw1 chain of one hidden chunk (bias included): the first half of the
-// fragments comes from registers (loaded an iteration earlier), the second
-// half and the bias fragment are read from the chunk's buffer while the first
-// half runs.
+// pw1 chain of one hidden chunk, starting from its bias: the first half of
+// the fragments comes from registers (loaded an iteration earlier), the second
+// half and the bias are read from the chunk's buffer while the first half runs.
 template <int C>
-__device__ __forceinline__ floatx16 dc_hidden(const half8* wf, const char* wb, const half8* av, half8 ones, int lane) {
+__device__ __forceinline__ floatx16 dc_hidden(const half8* wf, const char* wb, const half8* av, int lane) {
   constexpr int KS = DcSmem<C>::KS;
   const half8* w = (const half8*)wb + lane;
-  half8 w2[KS / 2 + 1];
+  half8 w2[KS / 2];
 #pragma unroll
-  for (int s = 0; s <= KS / 2; ++s) w2[s] = w[(KS / 2 + s) * 64];
+  for (int s = 0; s < KS / 2; ++s) w2[s] = w[(KS / 2 + s) * 64];
+  // the bias: 32 fp32 values at the start of fragment KS; row 8 g + 4 h + e of
+  // the accumulator is element 4 g + e of lane half h
+  const int h = lane >> 5;
+  floatx4 bv[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) bv[g] = *(const floatx4*)(wb + KS * 1024 + (8 * g + 4 * h) * 4);
   __builtin_amdgcn_sched_barrier(0);
-  floatx16 hacc = {};
+  floatx16 hacc;
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) hacc[4 * g + e] = bv[g][e];
 #pragma unroll
   for (int s = 0; s < KS / 2; ++s) hacc = mfma_f16(wf[s], av[s], hacc);
 #pragma unroll
   for (int s = 0; s < KS / 2; ++s) hacc = mfma_f16(w2[s], av[KS / 2 + s], hacc);
-  return mfma_f16(w2[KS / 2], ones, hacc);
+  return hacc;
 }
 
 // LeakyReLU, fp16; stored to `gx` as two B fragments (k = hidden in the
@@ -650,8 +659,6 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     if ((2 * MT) % 8 == 0 || f < FR) dma16(wchunks + ((size_t)FR + f) * 1024 + lane * 16, wb1 + f * 1024);
   }
   dc_issue<C>(wchunks, 2, wb2, wave, lane);
-  half8 ones = {};  // B fragment of the bias step: k = 0 is one for every pixel
-  if (lane < 32) ones[0] = (f16)1.f;
   half8 wf[KS / 2];  // first half of the next chain's pw1 fragments
   // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + FR / 8) : "memory");
@@ -659,8 +666,8 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   Wsilu16 sw1 = {};  // gated: WSiLU of the h1 chain of the pair being produced
   if (hf == 0) {
     dc_load_w1<C>(wb0, lane, wf);
-    if constexpr (GATED) sw1 = dc_wsilu(dc_hidden<C>(wf, wb0, av, ones, lane));
-    else dc_hidden_store(dc_hidden<C>(wf, wb0, av, ones, lane), lane, gx0 + 128 * pg);
+    if constexpr (GATED) sw1 = dc_wsilu(dc_hidden<C>(wf, wb0, av, lane));
+    else dc_hidden_store(dc_hidden<C>(wf, wb0, av, lane), lane, gx0 + 128 * pg);
   }
   floatx16 out[MT / 2];  // pw2 accumulators, starting from the bias
 #pragma unroll
@@ -705,7 +712,7 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
       // first on the SIMD, the partner's projection fills the gaps
       __builtin_amdgcn_s_setprio(2);
       if (j == 1) dc_load_w1<C>(wnxt, lane, wf);  // iteration 0 had no prefetch
-      hacc = dc_hidden<C>(wf, wnxt, av, ones, lane);
+      hacc = dc_hidden<C>(wf, wnxt, av, lane);
     }
     if (j == NCH - 2) issue_residual();  // buffers 0 and 1 are free from here on
     if (!GATED || (j & 1)) dc_project<C>(wcur, gcur, hf, lane, out);
