@@ -125,17 +125,45 @@ __device__ __forceinline__ void lds_barrier() {
 // form for every v (0.1 v <= v exactly when v >= 0), two VALU operations.
 __device__ __forceinline__ float leaky(float v) { return fmaxf(v, 0.1f * v); }
 
-// Gaussian rate of one symbol, -log2(max(L, 1e-9)),
-// L = 1/2 [erfc((|q| - 1/2) / (sigma sqrt2)) - erfc((|q| + 1/2) / (sigma sqrt2))].
-__device__ __forceinline__ float symbol_bits(float q, float sigma) {
-  const float a = fabsf(q);
-  const float inv = 0.70710678118654752f / sigma;
-  const float L = 0.5f * (erfcf((a - 0.5f) * inv) - erfcf((a + 0.5f) * inv));
-  return -log2f(fmaxf(L, 1e-9f));
+// erfc(x) for x >= 0 without branches: the Chebyshev fit of Numerical Recipes
+// (Press et al., 2nd ed., sec. 6.2; fractional error below 1.2e-7),
+// erfc(x) = t exp(-x^2 + P(t)), t = 1 / (1 + x / 2), P of degree 9.
+__device__ __forceinline__ float erfc_pos(float x) {
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.5f, x, 1.f));
+  float p = 0.17087277f;
+  p = fmaf(p, t, -0.82215223f);
+  p = fmaf(p, t, 1.48851587f);
+  p = fmaf(p, t, -1.13520398f);
+  p = fmaf(p, t, 0.27886807f);
+  p = fmaf(p, t, -0.18628806f);
+  p = fmaf(p, t, 0.09678418f);
+  p = fmaf(p, t, 0.37409196f);
+  p = fmaf(p, t, 1.00002368f);
+  p = fmaf(p, t, -1.26551223f);
+  return t * __expf(fmaf(-x, x, p));
 }
 
+// Gaussian rate of one symbol, -log2(max(L, 1e-9)),
+// L = 1/2 [erfc((|q| - 1/2) / (sigma sqrt2)) - erfc((|q| + 1/2) / (sigma sqrt2))].
+// For q = 0, L = 1 - erfc(u) with u = 1 / (2 sigma sqrt2), and the rate is
+// -log1p(-erfc(u)) / ln 2, with log1p(v) = log(1 + v) v / ((1 + v) - 1)
+// (Goldberg 1991), accurate where L is close to one.  No branches.
+__device__ __forceinline__ float symbol_bits(float q, float sigma) {
+  const float a = fabsf(q);
+  const float inv = 0.70710678118654752f * __builtin_amdgcn_rcpf(sigma);
+  const float e1 = erfc_pos(fabsf(a - 0.5f) * inv), e2 = erfc_pos((a + 0.5f) * inv);
+  const float L = 0.5f * (e1 - e2);
+  const float b1 = -__log2f(fmaxf(L, 1e-9f));
+  const float y = 1.f - e2, d = y - 1.f;  // log1p(-e2) = ln(y) (-e2) / d, or -e2 when y rounds to 1
+  const float l1p = d == 0.f ? -e2 : __logf(y) * (-e2 / d);
+  const float b0 = fminf(-1.44269504088896341f * l1p, 29.8973529f);  // -log2(1e-9)
+  return a == 0.f ? b0 : b1;
+}
+
+// sigma = max(softplus(s), 0.11).  Where softplus(s) >= 0.11, exp(s) > 0.11,
+// so log(1 + exp(s)) loses nothing to the rounding of 1 + exp(s) at fp32.
 __device__ __forceinline__ float softplus_sigma(float s) {
-  const float sp = s > 20.f ? s : log1pf(expf(s));
+  const float sp = s > 20.f ? s : __logf(1.f + __expf(s));
   return fmaxf(sp, 0.11f);
 }
 
