@@ -32,8 +32,10 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 MFMA_I8_PEAK_TOPS = 5000.0
 
 
-def workload_model(H, W, C, ne, nd):
-    """Algorithmic flops and HBM bytes per launch of each kernel kind (weights excluded)."""
+def workload_model(H, W, C, ne, nd, block="lrelu"):
+    """Algorithmic flops and HBM bytes per launch of each kernel kind (weights excluded).
+    The DC block's pointwise pair is C -> 2C -> C (LeakyReLU form) or C -> 2C, C -> C
+    (gated form: 6 C^2 flops per pixel instead of 8 C^2)."""
     P8 = (H // 8) * (W // 8)
     P16 = P8 // 4
     fmap = P8 * C * 2
@@ -42,7 +44,7 @@ def workload_model(H, W, C, ne, nd):
     k = {
         "embed": (2 * P8 * C * 192, frame + fmap),
         "fuse": (2 * P8 * C * 2 * C, 3 * fmap),
-        "dcblock": (P8 * (8 * C * C + 18 * C), 2 * fmap),
+        "dcblock": (P8 * ((8 if block == "lrelu" else 6) * C * C + 18 * C), 2 * fmap),
         "down": (2 * P16 * C * 4 * C, fmap + lat),
         "prior_enc": (2 * P16 * 2 * C * C, 4 * lat),
         "prior_dec": (2 * P16 * C * C, 3 * lat),
@@ -299,16 +301,17 @@ def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
             "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)]}
 
 
-SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r): resolution, width, depth, modules
-    ("720p", 720, 1280, 256, 8, 8, 0, 0),
-    ("1080p C=64", 1088, 1920, 64, 8, 8, 0, 0),
-    ("1080p C=128", 1088, 1920, 128, 8, 8, 0, 0),
-    ("1080p", 1088, 1920, 256, 8, 8, 0, 0),
-    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16, 0, 0),
-    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32, 0, 0),
+SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r, block): resolution, width, depth, modules, form
+    ("720p", 720, 1280, 256, 8, 8, 0, 0, "lrelu"),
+    ("1080p C=64", 1088, 1920, 64, 8, 8, 0, 0, "lrelu"),
+    ("1080p C=128", 1088, 1920, 128, 8, 8, 0, 0, "lrelu"),
+    ("1080p", 1088, 1920, 256, 8, 8, 0, 0, "lrelu"),
+    ("1080p gated blocks", 1088, 1920, 256, 8, 8, 0, 0, "gated"),
+    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16, 0, 0, "lrelu"),
+    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32, 0, 0, "lrelu"),
     ("1080p + feature extractor (2 blocks), reconstruction generation (2 blocks), qp banks",
-     1088, 1920, 256, 8, 8, 2, 2),
-    ("4K", 2176, 3840, 256, 8, 8, 0, 0),
+     1088, 1920, 256, 8, 8, 2, 2, "lrelu"),
+    ("4K", 2176, 3840, 256, 8, 8, 0, 0, "lrelu"),
 ]
 
 
@@ -316,15 +319,15 @@ def sweep(paths, steps, warmup, torch, Codec):
     """Frames/s and the DC block's MFMA fraction across resolutions, widths and
     depths (random-init weights, seeded random frames); one JSON line each."""
     import synth
-    for label, H, W, C, ne, nd, nfe, nrg in SWEEP:
+    for label, H, W, C, ne, nd, nfe, nrg, block in SWEEP:
         frames = [torch.from_numpy(synth.random_frame(H, W, seed=90 + i)).to("cuda") for i in range(4)]
         banks = nfe + nrg > 0
-        weights = synth.make_weights(C, ne, nd, n_fe=nfe, n_rg=nrg, banks=banks)
-        kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd)
+        weights = synth.make_weights(C, ne, nd, block=block, n_fe=nfe, n_rg=nrg, banks=banks)
+        kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd, block)
         enc_list = ["dcblock"] * nfe + enc_list
         dec_list = ["dcblock"] * (nfe + nrg) + dec_list
         for path in paths:
-            kw = dict(n_fe_blocks=nfe, n_rg_blocks=nrg, qp_banks=banks)
+            kw = dict(block=block, n_fe_blocks=nfe, n_rg_blocks=nrg, qp_banks=banks)
             enc = Codec(H, W, C, ne, nd, path, weights, **kw)
             dec = Codec(H, W, C, ne, nd, path, weights, **kw)
             odt = torch.int16 if path == "int16" else torch.float16
@@ -350,6 +353,7 @@ def sweep(paths, steps, warmup, torch, Codec):
             value = steps / ((r["enc_ms"] + r["dec_ms"]) * 1e-3)
             print(json.dumps({"sweep": label, "path": path, "height": H, "width": W, "channels": C,
                               "n_enc_blocks": ne, "n_dec_blocks": nd, "n_fe_blocks": nfe, "n_rg_blocks": nrg,
+                              "block": block,
                               "frames_per_s": value,
                               "encode_fps": steps / (r["enc_ms"] * 1e-3), "decode_fps": steps / (r["dec_ms"] * 1e-3),
                               "dcblock_us": 1e3 * ms / n if n else None, "dcblock_mfma_frac": frac,
