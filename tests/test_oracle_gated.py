@@ -210,3 +210,15 @@ def test_gated_activations_stay_in_int16_range(name):
         r = ci.encode_frame(ip, x, st)   # raises OverflowError on any int32 overflow
         st = r.state
         assert np.max(np.abs(st.feat)) < 16 * 512
+
+
+def test_sigmoid_table_compact_form():
+    # the integer gated block keeps S in a compact exact form: S[v] - 256 for
+    # 0 <= v < 888 (one byte each), S[v] = 512 from 888 on, S[-v] = 512 - S[v]
+    S = ci.sigmoid_table()
+    v = np.arange(0, 32768)
+    pos = S[v + 32768]
+    assert np.all(pos[888:] == 512) and pos[887] == 511
+    assert np.all((pos[:888] >= 256) & (pos[:888] <= 511))
+    np.testing.assert_array_equal(S[32768 - v[1:]], 512 - pos[1:])
+    assert S[0] == 0  # v = -32768
