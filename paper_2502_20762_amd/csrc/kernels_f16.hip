@@ -356,15 +356,16 @@ struct DcSmem {
   static constexpr int KS = C / 16, MT = C / 32, FR = KS + 1 + 2 * MT, CHUNK = FR * 1024;
 };
 
-// Chunk j -> buf; fragment f is loaded by wave f % 8, so every wave issues at
-// least FR / 8 loads.
+// Fragments 0 .. n-1 of chunk j -> buf (n = FR, or KS + 1 for a gated h1
+// entry, whose pw2 slots are unused); fragment f is loaded by wave f % 8, so
+// every wave issues at least n / 8 loads.
 template <int C>
-__device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, int wave, int lane) {
+__device__ __forceinline__ void dc_issue(const char* wchunks, int j, char* buf, int wave, int lane, int n) {
   constexpr int FR = DcSmem<C>::FR;
 #pragma unroll
   for (int i = 0; i < (FR + 7) / 8; ++i) {
     const int f = wave + 8 * i;
-    if (FR % 8 == 0 || f < FR) dma16(wchunks + ((size_t)j * FR + f) * 1024 + lane * 16, buf + f * 1024);
+    if (f < n) dma16(wchunks + ((size_t)j * FR + f) * 1024 + lane * 16, buf + f * 1024);
   }
 }
 
@@ -658,10 +659,10 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
     const int f = KS + 1 + wave + 8 * i;
     if ((2 * MT) % 8 == 0 || f < FR) dma16(wchunks + ((size_t)FR + f) * 1024 + lane * 16, wb1 + f * 1024);
   }
-  dc_issue<C>(wchunks, 2, wb2, wave, lane);
+  dc_issue<C>(wchunks, 2, wb2, wave, lane, GATED ? KS + 1 : FR);  // gated: chunk 2 is an h1 entry
   half8 wf[KS / 2];  // first half of the next chain's pw1 fragments
   // chunk 0 and the pw1 part of chunk 1 (the rest of chunk 1 and chunk 2 in flight)
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + FR / 8) : "memory");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * MT / 8 + (GATED ? KS + 1 : FR) / 8) : "memory");
   lds_barrier();  // chunks 0 and 1 staged
   Wsilu16 sw1 = {};  // gated: WSiLU of the h1 chain of the pair being produced
   if (hf == 0) {
@@ -701,7 +702,7 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   auto step = [&](int j, const char* wcur, const char* wnxt, const char* wpre, char* wiss, half8* gcur, half8* gnxt)
                   __attribute__((always_inline)) {
     const bool dma = j + 3 < NCH;
-    if (dma) dc_issue<C>(wchunks, j + 3, wiss, wave, lane);
+    if (dma) dc_issue<C>(wchunks, j + 3, wiss, wave, lane, GATED && !((j + 3) & 1) ? KS + 1 : FR);
     // producer of chunk c: wave c % 2 of the pair, or in the gated form (c / 2) % 2
     const int pj1 = GATED ? ((j + 1) >> 1) & 1 : (j + 1) & 1, pj2 = GATED ? ((j + 2) >> 1) & 1 : j & 1;
     const bool produce = j + 1 < NCH && hf == pj1;
