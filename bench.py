@@ -244,6 +244,8 @@ def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
         enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
         dec.decode(qbuf[k], out=xout)
     te, td = enc.timing_read(), dec.timing_read()
+    enc.timing(False)
+    dec.timing(False)
     kern = {}
     for src in (te, td):
         for kind, (n, ms) in src.items():
@@ -289,7 +291,10 @@ def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
         enc.encode(gframes[(warmup + k) % nfr], q_out=qbuf[k], bits_out=bits[k])
         dec.decode(qbuf[k], out=xout)
     kern = {}
-    for src in (enc.timing_read(), dec.timing_read()):
+    te, td = enc.timing_read(), dec.timing_read()
+    enc.timing(False)
+    dec.timing(False)
+    for src in (te, td):
         for kind, (n, ms) in src.items():
             a = kern.setdefault(kind, [0, 0.0])
             a[0] += n
@@ -346,6 +351,7 @@ def sweep(paths, steps, warmup, torch, Codec):
             for k in range(min(steps, 4)):
                 enc.encode(frames[k % 4], q_out=qbuf[k], bits_out=bits[k])
             t = enc.timing_read()
+            enc.timing(False)
             n, ms = t.get("dcblock", (0, 0.0))
             peak, scale = (MFMA_F16_PEAK_TFLOPS, 1) if path == "fp16" else (MFMA_I8_PEAK_TOPS, 4)
             frac = scale * kinds["dcblock"][0] / (ms * 1e-3 / n) / 1e12 / peak if n else None

@@ -109,7 +109,10 @@ size_t ncodec_weight_count(const ncodec_config* cfg);
  * state, intermediates), or 0 if cfg is invalid.  Pure host function. */
 size_t ncodec_workspace_bytes(const ncodec_config* cfg);
 
-/* Create a context.  host_weights: n_weights float32 values in canonical
+/* Create a context: the state of one encoder or one decoder of the low-delay
+ * P-frame setting (Sec. 4.1, Fig. 4; Sec. 5.1 "Test Details"), holding the
+ * weights of Fig. 4's transform and the temporal state (f_{t-1}, yhat_{t-1}),
+ * Sec. 4.3.  host_weights: n_weights float32 values in canonical
  * order (host memory, copied; the fp16 path rounds them to fp16, the int
  * path converts them to round(8192 w) and rejects any weight of the
  * pointwise / 2x2 convolutions whose integer value exceeds 32639 in magnitude
@@ -122,7 +125,11 @@ size_t ncodec_workspace_bytes(const ncodec_config* cfg);
 ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights, size_t n_weights,
                             void* d_workspace, size_t ws_bytes, void* hip_stream, ncodec_ctx** out);
 
-/* Make the next frame an I-frame: zero f_{t-1} and yhat_{t-1} (enqueued). */
+/* Make the next frame an I-frame: zero f_{t-1} and yhat_{t-1} (enqueued), so
+ * the frame is coded without temporal context.  The paper's low-delay tests
+ * (Sec. 5.1 "Test Details") use an intra period of -1: one I-frame starts the
+ * sequence and every later frame is a P-frame, which is what a context does
+ * from creation until the next reset.  Errors: EINVAL (NULL ctx), EHIP. */
 ncodec_status ncodec_reset(ncodec_ctx* ctx);
 
 /* Select rate point qp in [0, 64) of the vector banks (Sec. 4.4; the context
@@ -164,10 +171,18 @@ ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_f
 
 /* Rate of n symbols under zero-mean Gaussians (Supp. B.2; likelihood
  * L = Phi((|q|+1/2)/sigma) - Phi((|q|-1/2)/sigma), bits = sum -log2 max(L, 1e-9)).
- *  d_q: n int16 symbols; d_sigma: n float32 scales (> 0); d_bits: device
- *  double output.  The sum is formed in a fixed order (deterministic).
- * n must be in [0, 2^31); n = 0 writes 0. */
-ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const float* d_sigma,
+ *  d_q:     n int16 symbols.
+ *  d_scale: n scales in the form the context's path produces them: on an
+ *           fp16 context float32 sigma (> 0); on an int16 context the prior's
+ *           int16 scale outputs s_i (K1 = 512 units), each mapped to
+ *           sigma = max(softplus(s_i / 512), 0.11) through the context's table
+ *           of all 65,536 values (Sec. 4.5: table lookups keep the integer path
+ *           identical across devices).
+ *  d_bits:  device double output.
+ * The sum is formed in a fixed order (deterministic).  n must be in
+ * [0, 2^31); n = 0 writes 0.  Uses the context's workspace as scratch, so
+ * calls on one context are ordered by its stream. */
+ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const void* d_scale,
                                    int64_t n, double* d_bits);
 
 /* ---- Entropy coding (Fig. 4 "AE" / "AD", Fig. 6; Supp. B.2) ----------------
@@ -232,13 +247,23 @@ ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, in
 ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes,
                                         void* d_frame_out, int32_t* d_status);
 
-/* Copy the state out of / into the context (enqueued).  d_feat: C x H/8 x W/8
- * planar, d_yhat: C x H/16 x W/16 planar; fp16 (fp16 path) or int16 (int
- * path).  Either pointer may be NULL to skip that tensor. */
+/* Copy the state out of / into the context (enqueued): the temporal context
+ * f_{t-1} (the decoder feature before reconstruction, Sec. 4.3; Supp. B.3) and
+ * the previous latent yhat_{t-1} that the prior reads.  Encoder and decoder
+ * hold the same state after every frame (Sec. 4.5: on the int path bitwise,
+ * on any device), so a state copied from one context continues the stream in
+ * another.  d_feat: C x H/8 x W/8 planar, d_yhat: C x H/16 x W/16 planar; fp16
+ * (fp16 path) or int16 (int path), caller-owned device memory, 16-byte
+ * aligned.  Either pointer may be NULL to skip that tensor.  Errors: EINVAL
+ * (NULL ctx), EHIP. */
 ncodec_status ncodec_get_state(ncodec_ctx* ctx, void* d_feat, void* d_yhat);
 ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* d_yhat);
 
-/* Kernel launches one ncodec_encode_frame / ncodec_decode_frame enqueues. */
+/* Kernel launches one ncodec_encode_frame (decode = 0, with a non-NULL
+ * d_bits; one fewer without) or ncodec_decode_frame (decode = 1) enqueues,
+ * counting the feature-extractor and reconstruction-generation blocks
+ * (Sec. 3: the number of modules called per frame is one of the costs the
+ * design minimises).  0 for a NULL ctx. */
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
 
 /* Graph replay of the per-frame launch sequence (Sec. 3: at this size the

@@ -17,13 +17,20 @@
 
 using namespace nc;
 
-namespace nc {
-thread_local LaunchEvents g_launch_events;
+namespace {
+thread_local std::string g_create_error;
 }
 
-namespace {
+namespace nc {
+thread_local LaunchEvents g_launch_events;
 
-thread_local std::string g_create_error;
+ncodec_status set_error(ncodec_status st, const std::string& msg) {
+  g_create_error = msg;
+  return st;
+}
+}  // namespace nc
+
+namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kNumQp = 64;  // rate points of the vector banks
@@ -1128,14 +1135,15 @@ ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_f
   return NCODEC_OK;
 }
 
-ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const float* d_sigma, int64_t n,
+ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const void* d_scale, int64_t n,
                                    double* d_bits) {
   ncodec_status st = enter(ctx);
   if (st) return st;
   if (!d_bits) return fail(ctx, NCODEC_EINVAL, "d_bits is NULL");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(ctx, NCODEC_EINVAL, "n out of range");
-  if (n > 0 && (!d_q || !d_sigma)) return fail(ctx, NCODEC_EINVAL, "d_q and d_sigma must be non-NULL");
-  NC_HIP(ctx, launch_estimate_bits(d_q, d_sigma, n, ctx->p<double>(ctx->L.partials), d_bits, ctx->stream),
+  if (n > 0 && (!d_q || !d_scale)) return fail(ctx, NCODEC_EINVAL, "d_q and d_scale must be non-NULL");
+  const float* tab = ctx->is_int() ? ctx->p<float>(ctx->L.sigma_tab) : nullptr;
+  NC_HIP(ctx, launch_estimate_bits(d_q, d_scale, tab, n, ctx->p<double>(ctx->L.partials), d_bits, ctx->stream),
          "estimate_bits");
   return NCODEC_OK;
 }
@@ -1255,8 +1263,11 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
 
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   if (!ctx) return 0;
-  if (decode) return 4 + ctx->cfg.n_dec_blocks;
-  return 7 + ctx->cfg.n_enc_blocks + ctx->cfg.n_dec_blocks;
+  const ncodec_config& c = ctx->cfg;
+  // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
+  if (decode) return 4 + c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks;
+  // feature extractor, embed, fuse, encoder blocks, downsample, prior, bit sum, upsample, fuse, decoder blocks
+  return 7 + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
 }
 
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {

@@ -6,7 +6,15 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <string>
+
+#include "../../include/ncodec.h"
+
 namespace nc {
+
+// Records msg as the error that ncodec_last_error(NULL) reports (this thread)
+// and returns st.
+ncodec_status set_error(ncodec_status st, const std::string& msg);
 
 // Events attached to the next kernel dispatch (timing mode of the C ABI): when
 // set, launches go through hipExtLaunchKernelGGL, whose start / stop events
@@ -134,8 +142,6 @@ hipError_t launch_rans_encode(const int16_t* q, const uint8_t* k, int64_t n, con
 hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_t* k, int64_t n, const uint16_t* tab,
                               uint32_t* errs, uint32_t* count, int16_t* q, int32_t* status_out, hipStream_t st);
 
-// Depthwise 3x3 + bias of the gated block, NHWC (C channels, h x w pixels),
-// weights in the block's packed depthwise image.
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t st);
@@ -147,8 +153,10 @@ int prior_partials_i16(int C, int P);
 
 hipError_t launch_reduce(const double* partials, int n, double* out, hipStream_t st);
 constexpr int kBitsBlocks = 1024;
-hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n, double* partials,
-                                double* out, hipStream_t st);
+// sigma_tab == nullptr: scale is float32 sigma; else scale is int16 s and
+// sigma = sigma_tab[s + 32768].  partials: kBitsBlocks doubles of scratch.
+hipError_t launch_estimate_bits(const int16_t* q, const void* scale, const float* sigma_tab, int64_t n,
+                                double* partials, double* out, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);

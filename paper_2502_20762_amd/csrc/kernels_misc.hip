@@ -21,12 +21,21 @@ __global__ __launch_bounds__(256) void k_reduce(const double* part, int n, doubl
 }
 
 // Block b owns elements [b*chunk, min(n, (b+1)*chunk)); chunk depends only on n.
-__global__ __launch_bounds__(256) void k_bits(const int16_t* q, const float* sigma, int64_t n, int64_t chunk,
-                                              double* part) {
+// The scale of element i is sigma[i] (float32), or on the integer path
+// sigma_tab[s[i] + 32768] for the prior's int16 scale output s (a table of
+// max(softplus(s / 512), 0.11) over every int16 value).
+template <bool INT_SCALE>
+__global__ __launch_bounds__(256) void k_bits(const int16_t* q, const void* scale, const float* sigma_tab, int64_t n,
+                                              int64_t chunk, double* part) {
   const int64_t lo = (int64_t)blockIdx.x * chunk;
   const int64_t hi = min(n, lo + chunk);
   double v = 0.0;
-  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) v += (double)symbol_bits((float)q[i], sigma[i]);
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
+    float sg;
+    if constexpr (INT_SCALE) sg = sigma_tab[(int)((const int16_t*)scale)[i] + 32768];
+    else sg = ((const float*)scale)[i];
+    v += (double)symbol_bits((float)q[i], sg);
+  }
   __shared__ double red[4];
   v = wave_sum(v);
   const int wave = threadIdx.x >> 6;
@@ -61,10 +70,13 @@ hipError_t launch_reduce(const double* partials, int n, double* out, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_estimate_bits(const int16_t* q, const float* sigma, int64_t n, double* partials, double* out,
-                                hipStream_t st) {
+hipError_t launch_estimate_bits(const int16_t* q, const void* scale, const float* sigma_tab, int64_t n,
+                                double* partials, double* out, hipStream_t st) {
   const int64_t chunk = n > 0 ? (n + kBitsBlocks - 1) / kBitsBlocks : 1;
-  launch(k_bits, dim3(kBitsBlocks), dim3(256), st, q, sigma, n, chunk, partials);
+  if (sigma_tab)
+    launch(k_bits<true>, dim3(kBitsBlocks), dim3(256), st, q, scale, sigma_tab, n, chunk, partials);
+  else
+    launch(k_bits<false>, dim3(kBitsBlocks), dim3(256), st, q, scale, sigma_tab, n, chunk, partials);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_reduce(partials, kBitsBlocks, out, st);

@@ -165,8 +165,8 @@ def ncodec_decode_frame(ctx, d_q: int, d_frame_out: int) -> None:
     _check(load_library().ncodec_decode_frame(ctx, d_q, d_frame_out), ctx)
 
 
-def ncodec_estimate_bits(ctx, d_q: int, d_sigma: int, n: int, d_bits: int) -> None:
-    _check(load_library().ncodec_estimate_bits(ctx, d_q or None, d_sigma or None, n, d_bits), ctx)
+def ncodec_estimate_bits(ctx, d_q: int, d_scale: int, n: int, d_bits: int) -> None:
+    _check(load_library().ncodec_estimate_bits(ctx, d_q or None, d_scale or None, n, d_bits), ctx)
 
 
 def ncodec_stream_capacity(cfg: ncodec_config) -> int:
@@ -290,11 +290,15 @@ class Codec:
         ncodec_decode_frame(self.ctx, q.data_ptr(), x.data_ptr())
         return x
 
-    def estimate_bits(self, q, sigma, bits_out=None):
+    def estimate_bits(self, q, scale, bits_out=None):
+        """Bits of q under scales `scale`: float32 sigma on an fp16 context, the
+        prior's int16 scale outputs s_i on an int16 context."""
         torch = self.torch
-        assert q.dtype == torch.int16 and sigma.dtype == torch.float32 and q.numel() == sigma.numel()
+        sdt = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float32
+        assert q.dtype == torch.int16 and scale.dtype == sdt and q.numel() == scale.numel()
+        assert q.is_contiguous() and scale.is_contiguous()
         bits = bits_out if bits_out is not None else self._empty((), torch.float64)
-        ncodec_estimate_bits(self.ctx, q.data_ptr(), sigma.data_ptr(), q.numel(), bits.data_ptr())
+        ncodec_estimate_bits(self.ctx, q.data_ptr(), scale.data_ptr(), q.numel(), bits.data_ptr())
         return bits
 
     # ---- entropy coding

@@ -52,6 +52,8 @@ def check_fp16_encode(p, x, feat_prev, yhat_prev, q_gpu, bits_gpu, feat_new, yha
     sl16, sl8 = valid if valid is not None else (np.s_[:, :, :], np.s_[:, :, :])
     mism = (q != q_ref) & ~band
     assert not mism[sl16].any(), f"{what}: q differs outside the rounding band at {int(mism[sl16].sum())} elements"
+    far = np.abs(q - q_ref) > 1
+    assert not far[sl16].any(), f"{what}: q off by more than 1 inside the rounding band at {int(far[sl16].sum())} elements"
     agree = float(np.mean((q == q_ref)[sl16]))
     assert agree > 0.99, f"{what}: q agreement {agree}"
     yhat_ref = q + mu

@@ -182,3 +182,78 @@ def test_determinism_reset_and_state_round_trip(path):
     np.testing.assert_array_equal(host(c.encode(frames[0])[0]), qa[0])
     fz, yz = Codec(H, W, C, 2, 2, path, flat, device=DEV).get_state()
     assert not host(fz).any() and not host(yz).any()
+
+
+def test_estimate_bits_int_scales_match_oracle():
+    # the int path's table-driven rate: int16 scale outputs s_i (K1 = 512 units),
+    # sigma = max(softplus(s_i / 512), 0.11) (Sec. 4.5; Supp. B.2), against the
+    # oracle's float64 sigma of the same s_i
+    flat, _ = params_for(64, 1, 1)
+    c = Codec(16, 16, 64, 1, 1, "int16", flat, device=DEV)
+    rng = np.random.default_rng(6)
+    for n in (0, 1, 4097, 2088960):
+        say("estimate_bits int16 scales, n =", n)
+        q = rng.integers(-60, 61, size=n).astype(np.int16)
+        s = rng.integers(-4000, 6000, size=n).astype(np.int16)
+        if n > 10:
+            s[:3] = (-32768, 32767, 0)
+        b = float(host(c.estimate_bits(gpu(q), gpu(s))))
+        ref = oracle.estimate_bits(q, ci.sigma_int(s.astype(np.int64)))
+        assert abs(b - ref) <= 1e-5 * max(abs(ref), 1e-30), (n, b, ref)
+
+
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_kernels_per_frame_counts_launches(path):
+    # with the feature extractor and reconstruction generation the count covers their blocks
+    H, W, C, ne, nd, nfe, nrg = 64, 64, 64, 2, 1, 2, 3
+    flat = synth.make_weights(C, ne, nd, n_fe=nfe, n_rg=nrg)
+    enc = Codec(H, W, C, ne, nd, path, flat, device=DEV, n_fe_blocks=nfe, n_rg_blocks=nrg)
+    dec = Codec(H, W, C, ne, nd, path, flat, device=DEV, n_fe_blocks=nfe, n_rg_blocks=nrg)
+    enc.timing(True)
+    dec.timing(True)
+    q, _ = enc.encode(gpu(synth.random_frame(H, W, seed=40)))
+    dec.decode(q)
+    ne_l = sum(n for n, _ in enc.timing_read().values())
+    nd_l = sum(n for n, _ in dec.timing_read().values())
+    enc.timing(False)
+    dec.timing(False)
+    assert enc.kernels_per_frame(False) == ne_l == 7 + nfe + ne + nd
+    assert dec.kernels_per_frame(True) == nd_l == 4 + nfe + nd + nrg
+
+
+def test_int_saturation_c256_bit_exact():
+    # Alg. 1's clip at C = 256: the fuse conv's context columns are scaled by 4
+    # and the injected context f_{t-1} is large, so the fuse output clips to the
+    # int16 range (|a| / 8192 > 32767 with |a| < 2^31) and the first block's
+    # residual add saturates; the oracle raises on any int32 overflow, so the
+    # case stays inside the accumulator contract.  Free-running, two frames.
+    C, ne, nd, H, W = 256, 2, 1, 128, 128
+    flat = synth.make_weights(C, ne, nd).copy()
+    off, n = C * 192 + C, C * 2 * C
+    flat[off:off + n] *= 4
+    p = oracle.unpack(flat, C, ne, nd)
+    ip = ci.integerize(p)
+    rng = np.random.default_rng(7)
+    fprev = rng.integers(-16000, 16001, size=(C, H // 8, W // 8)).astype(np.int64)
+    st = ci.State(fprev, np.zeros((C, H // 16, W // 16), np.int64))
+    enc = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
+    dec = Codec(H, W, C, ne, nd, "int16", flat, device=DEV)
+    for cdc in (enc, dec):
+        cdc.set_state(gpu(fprev.astype(np.int16)), gpu(np.zeros((C, H // 16, W // 16), np.int16)))
+    from oracle.ops import pixel_unshuffle
+    for t, x in enumerate(synth.random_frame(H, W, seed=s) for s in (30, 31)):
+        say("int saturation C=256 frame", t)
+        e = ci.int_conv1x1(pixel_unshuffle(ci.frame_to_int(x), 8), ip.pe)
+        acc = ci.int_matmul(ip.fuse_enc.w, np.concatenate([e, st.feat]).reshape(2 * C, -1)) \
+            + 512 * ip.fuse_enc.b[:, None]
+        assert (np.abs(ci.rhe_shift(acc, 13)) > 32767).sum() > 1000   # the fuse conv clips
+        r = ci.encode_frame(ip, x, st)
+        xr, _ = ci.decode_frame(ip, r.q, st)
+        assert np.abs(r.state.feat).max() >= 32767                      # saturated features
+        q, bits = enc.encode(gpu(x))
+        np.testing.assert_array_equal(host(q), r.q, err_msg=f"t={t} q")
+        f, y = host_state(enc)
+        np.testing.assert_array_equal(f, r.state.feat, err_msg=f"t={t} f_t")
+        np.testing.assert_array_equal(y, r.state.yhat, err_msg=f"t={t} yhat")
+        np.testing.assert_array_equal(host(dec.decode(q)), xr, err_msg=f"t={t} xhat")
+        st = r.state

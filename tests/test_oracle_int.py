@@ -113,3 +113,90 @@ def test_int_leaky_relu():
 
 def test_residual_saturates():
     assert list(ci.clip16(np.array([30000 + 5000, -30000 - 5000]))) == [32767, -32768]
+
+
+def brute_int_lrelu_block(z, dw_w, dw_b, w1, b1, w2, b2):
+    """The LeakyReLU DC block (reading A1) evaluated element by element with
+    Python integers, every rescale an exact Fraction rounded half-to-even
+    (Alg. 1: a = sum x_i w_i + b_i K1, y_i = clip(round(a / K2))), the negative
+    branch of the LeakyReLU round(819 h / 8192), the residual a saturating
+    int16 add of the block input and the clipped pw2 output."""
+    C, H, W = z.shape
+
+    def rq(num, den):
+        return round(Fraction(int(num), int(den)))
+
+    def c16(v):
+        return max(-32768, min(32767, v))
+
+    out = np.zeros_like(z)
+    for y in range(H):
+        for x in range(W):
+            a = []
+            for c in range(C):
+                acc = 512 * int(dw_b[c])
+                for dy in (-1, 0, 1):
+                    for dx in (-1, 0, 1):
+                        if 0 <= y + dy < H and 0 <= x + dx < W:
+                            acc += int(dw_w[c, dy + 1, dx + 1]) * int(z[c, y + dy, x + dx])
+                assert abs(acc) < 2 ** 31
+                a.append(c16(rq(acc, 8192)))
+            g = []
+            for n in range(2 * C):
+                acc = 512 * int(b1[n]) + sum(int(w1[n, k]) * a[k] for k in range(C))
+                assert abs(acc) < 2 ** 31
+                h = c16(rq(acc, 8192))
+                g.append(h if h >= 0 else rq(819 * h, 8192))
+            for n in range(C):
+                acc = 512 * int(b2[n]) + sum(int(w2[n, k]) * g[k] for k in range(2 * C))
+                assert abs(acc) < 2 ** 31
+                p = c16(rq(acc, 8192))
+                out[n, y, x] = c16(int(z[n, y, x]) + p)
+    return out
+
+
+def _int_block(dw_w, dw_b, w1, b1, w2, b2):
+    return ci.IBlock(ci.IConv(dw_w, dw_b), ci.IConv(w1, b1), ci.IConv(w2, b2), "lrelu")
+
+
+def test_int_lrelu_block_matches_brute_force():
+    # the random-init block of the tiny configuration on a random int16 feature map
+    import oracle
+    import synth
+    C = 8
+    p = oracle.unpack(synth.make_weights(C, 1, 1), C, 1, 1)
+    ib = ci.integerize(p).enc[0]
+    rng = np.random.default_rng(11)
+    z = rng.integers(-3000, 3000, size=(C, 5, 6), dtype=np.int64)
+    got = ci.dc_block(z, ib)
+    ref = brute_int_lrelu_block(z, ib.dw.w, ib.dw.b, ib.pw1.w, ib.pw1.b, ib.pw2.w, ib.pw2.b)
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_int_lrelu_block_saturation_matches_brute_force():
+    # Large weights and inputs near the int16 limits: the pw1 and pw2 rescales
+    # clip (|a| / 8192 > 32767 while |a| < 2^31) and the residual add saturates
+    # in both directions.  A clip placed before the residual add instead of
+    # after it, or a missing clip of p, changes the result.
+    C = 8
+    rng = np.random.default_rng(12)
+    dw_w = rng.integers(-4000, 4000, size=(C, 3, 3), dtype=np.int64)
+    dw_b = rng.integers(-800, 800, size=C, dtype=np.int64)
+    w1 = rng.integers(-16000, 16000, size=(2 * C, C), dtype=np.int64)
+    b1 = rng.integers(-800, 800, size=2 * C, dtype=np.int64)
+    w2 = rng.integers(-4000, 4000, size=(C, 2 * C), dtype=np.int64)
+    b2 = rng.integers(-800, 800, size=C, dtype=np.int64)
+    z = rng.integers(-32768, 32768, size=(C, 4, 5), dtype=np.int64)
+    z[:, 0, :] = 32767
+    z[:, 1, :] = -32768
+    ib = _int_block(dw_w, dw_b, w1, b1, w2, b2)
+    got = ci.dc_block(z, ib)
+    ref = brute_int_lrelu_block(z, dw_w, dw_b, w1, b1, w2, b2)
+    np.testing.assert_array_equal(got, ref)
+    # the case is saturating: some pw1 / pw2 outputs and residual sums leave int16
+    a = ci.int_dwconv3x3(z, ib.dw)
+    h_acc = ci.int_matmul(w1, a.reshape(C, -1)) + 512 * b1[:, None]
+    assert np.abs(ci.rhe_shift(h_acc, 13)).max() > 32767
+    p = ci.int_conv1x1(ci.int_leaky_relu(ci.int_conv1x1(a, ib.pw1)), ib.pw2)
+    assert (z + p > 32767).any() and (z + p < -32768).any()
+    assert (np.abs(p) == 32767).any() or (p == -32768).any()
