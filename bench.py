@@ -155,11 +155,15 @@ def timed_loop(enc, dec, gframes, qbuf, bits, xout, steps, warmup, torch):
             "enc_median_ms": statistics.median(fe), "dec_median_ms": statistics.median(fd)}
 
 
-def coded_loop(enc, dec, gframes, steps, warmup, xout, torch):
+def coded_loop(enc, dec, gframes, steps, warmup, xout, torch, parallel=False):
     """Encode each frame into a container and decode it from the container
     (Fig. 4 "AE" / "AD" on the GPU); per-frame event stamps; the decoder is given
-    the buffer capacity as the container size (the header holds the lengths)."""
+    the buffer capacity as the container size (the header holds the lengths).
+    parallel: the coder overlaps the decoder part of the encode on a second
+    stream (Fig. 6, supplementary "Parallel Coding")."""
     stream = torch.cuda.current_stream()
+    enc.parallel_coding(parallel)
+    dec.parallel_coding(parallel)
     nfr = len(gframes)
     cap = enc.stream_capacity()
     sbuf = [torch.empty(cap, dtype=torch.uint8, device="cuda") for _ in range(2)]
@@ -183,6 +187,25 @@ def coded_loop(enc, dec, gframes, steps, warmup, xout, torch):
     torch.cuda.synchronize()
     enc_ms = [e[0].elapsed_time(e[1]) for e in ev]
     dec_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    # the same loop without the coder (encode with bits, decode from the symbols),
+    # for the coder's share at equal loop structure
+    qk = torch.empty(enc.q_shape, dtype=torch.int16, device="cuda")
+    enc.reset()
+    dec.reset()
+    for i in range(warmup):
+        enc.encode(gframes[i % nfr], q_out=qk, bits_out=bits[0])
+        dec.decode(qk, out=xout)
+    pv = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        pv[k][0].record(stream)
+        enc.encode(gframes[(warmup + k) % nfr], q_out=qk, bits_out=bits[k])
+        pv[k][1].record(stream)
+        dec.decode(qk, out=xout)
+        pv[k][2].record(stream)
+    torch.cuda.synchronize()
+    plain_enc = sum(e[0].elapsed_time(e[1]) for e in pv)
+    plain_dec = sum(e[1].elapsed_time(e[2]) for e in pv)
     # the coder alone, on the last frame's symbols: container in, container out
     q = torch.empty(enc.q_shape, dtype=torch.int16, device="cuda")
     k_idx = enc.scale_indices()
@@ -198,9 +221,12 @@ def coded_loop(enc, dec, gframes, steps, warmup, xout, torch):
         enc.rans_decode(sbuf[0], cap, k_idx, out=out_q, status_out=status[0])
     e2.record(stream)
     torch.cuda.synchronize()
+    enc.parallel_coding(False)
+    dec.parallel_coding(False)
     ok = bool((status == 0).all().item()) and bool(torch.equal(out_q, q))
     return {"encode_fps": steps / (sum(enc_ms) * 1e-3), "decode_fps": steps / (sum(dec_ms) * 1e-3),
             "value": steps / ((sum(enc_ms) + sum(dec_ms)) * 1e-3),
+            "uncoded_same_loop": {"encode_fps": steps / (plain_enc * 1e-3), "decode_fps": steps / (plain_dec * 1e-3)},
             "bytes_per_frame": float(nbytes[1:].double().mean().item()) if steps > 1 else float(nbytes[0].item()),
             "estimated_bytes_per_frame": float(bits[1:].mean().item()) / 8.0 if steps > 1 else float(bits[0].item()) / 8.0,
             "rans_encode_us": 1e3 * e0.elapsed_time(e1) / reps, "rans_decode_us": 1e3 * e1.elapsed_time(e2) / reps,
@@ -253,6 +279,9 @@ def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
             a[0] += n
             a[1] += ms
     coded = coded_loop(enc, dec, gframes, steps, warmup, xout, torch)
+    coded["parallel_coding"] = {k: v for k, v in coded_loop(enc, dec, gframes, steps, warmup, xout, torch,
+                                                            parallel=True).items()
+                                if k in ("encode_fps", "decode_fps", "value", "decoded_ok", "uncoded_same_loop")}
     r.update({
         "graph": graph,
         "coded": coded,

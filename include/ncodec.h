@@ -247,6 +247,18 @@ ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, in
 ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes,
                                         void* d_frame_out, int32_t* d_status);
 
+/* Parallel coding (Fig. 6; supplementary "Parallel Coding"): with enable != 0
+ * the coded calls overlap entropy coding with the network parts that do not
+ * depend on it.  ncodec_encode_frame_coded runs the rANS coder on a second
+ * HIP stream (default priority, created on first use) as soon as the symbols
+ * and their scale indices exist, while the decoder part of the encode runs on
+ * the context's stream; ncodec_decode_frame_coded runs the feature extractor
+ * (n_fe_blocks > 0) on the second stream while the symbols are decoded.  Both
+ * join the context's stream with an event before its last launches, so
+ * results are valid, as always, once the context's stream has synchronised,
+ * and are identical to the serial order (the default, enable = 0). */
+ncodec_status ncodec_parallel_coding(ncodec_ctx* ctx, int32_t enable);
+
 /* Copy the state out of / into the context (enqueued): the temporal context
  * f_{t-1} (the decoder feature before reconstruction, Sec. 4.3; Supp. B.3) and
  * the previous latent yhat_{t-1} that the prior reads.  Encoder and decoder

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/ncodec.h"
@@ -345,6 +346,7 @@ struct Layout {
   // entropy coder: scale indices, symbols, per-stream scratch, lengths,
   // offsets, status words, byte count
   size_t kmap, qtmp, rscratch, rlens, rerrs, rcount;
+  size_t mu;  // coded decode: the prior's mu (fp32 or int16, NHWC) between scale indices and symbols
   int64_t n_sym, n_streams;
   int n_partials;
   size_t total;
@@ -578,6 +580,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.rlens = alloc((size_t)L.n_streams * 4);
   L.rerrs = alloc((size_t)L.n_streams * 4);
   L.rcount = alloc(4);  // decoder ticket counter: zeroed at create, left at zero by every decode
+  L.mu = alloc(P16 * C * 4);
   L.total = off;
   return pk.ok;
 }
@@ -614,6 +617,13 @@ struct ncodec_ctx {
   };
   bool use_graphs = false;
   GraphSlot graphs[2][2];  // [decode][cur]
+  // Parallel coding (Fig. 6; supplementary "Parallel Coding"): the coded
+  // calls run the entropy coder (encode) or the feature extractor (decode) on
+  // a second stream of default priority, joined by events before the call's
+  // last launch on the context's stream.
+  bool overlap = false;
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipStream_t cap_stream = nullptr;
   std::vector<CapturedNode>* capturing = nullptr;
   bool is_int() const { return cfg.path == NCODEC_PATH_INT16; }
@@ -784,8 +794,11 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
 }
 
 // Enqueues one encode on ctx->stream (or records it under capture).
+// after_prior (optional) runs once q and the scale indices are enqueued,
+// before the decoder part.
+template <class Hook = std::nullptr_t>
 ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits,
-                             uint8_t* d_k = nullptr) {
+                             uint8_t* d_k = nullptr, Hook after_prior = nullptr) {
   ncodec_status st;
   const ncodec_config& c = ctx->cfg;
   const int C = c.channels;
@@ -848,14 +861,37 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
   if (d_bits)
     NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(pa.partials, np, d_bits, ctx->stream); }), "bits reduce");
+  if constexpr (!std::is_same<Hook, std::nullptr_t>::value) {
+    st = after_prior();
+    if (st) return st;
+  }
 
   st = run_decoder(ctx, nxt);
   return st;
 }
 
+// The decode after yhat_t is in place: decoder transform, reconstruction
+// generation on f_t (into ed, free after the decoder), reconstruction conv.
+ncodec_status decode_tail(ncodec_ctx* ctx, void* d_frame_out) {
+  const ncodec_config& c = ctx->cfg;
+  const int C = c.channels;
+  const int P8 = (c.height / 8) * (c.width / 8);
+  const Layout& L = ctx->L;
+  const int nxt = 1 - ctx->cur;
+  ncodec_status st = run_decoder(ctx, nxt);
+  if (st) return st;
+  const void* rsrc = nullptr;
+  NC_HIP(ctx, run_chain(ctx, L.rg, ctx->p(L.feat[nxt]), ctx->p(L.ed), &rsrc), "reconstruction generation");
+  PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
+  a.src0 = rsrc;
+  a.C0 = C;
+  a.dst = d_frame_out;
+  NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
+  return NCODEC_OK;
+}
+
 // Enqueues one decode on ctx->stream (or records it under capture).
 ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_out) {
-  ncodec_status st;
   const ncodec_config& c = ctx->cfg;
   const int C = c.channels;
   const int P8 = (c.height / 8) * (c.width / 8), P16 = P8 / 4;
@@ -876,25 +912,14 @@ ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_
   const void* context = nullptr;
   NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
   NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
-  st = run_decoder(ctx, nxt);
-  if (st) return st;
-
-  // reconstruction generation on f_t (into ed, free after the decoder), then the reconstruction conv
-  const void* rsrc = nullptr;
-  NC_HIP(ctx, run_chain(ctx, L.rg, ctx->p(L.feat[nxt]), ctx->p(L.ed), &rsrc), "reconstruction generation");
-  PwArgs a = conv_args(ctx, L.rec, C, 192, P8);
-  a.src0 = rsrc;
-  a.C0 = C;
-  a.dst = d_frame_out;
-  NC_HIP(ctx, pw(ctx, "recon", LD_NHWC, EP_REC, a), "reconstruction");
-  return NCODEC_OK;
+  return decode_tail(ctx, d_frame_out);
 }
 
 const uint16_t* rans_tab(const ncodec_ctx* ctx) { return ctx->p<uint16_t>(ctx->L.c_tab); }
 
 // Scale indices of the next frame's symbols, from the current state (the
 // prior head on yhat_{t-1}, Supp. B.2), into d_k (planar, C x h16 x w16).
-ncodec_status enqueue_scales(ncodec_ctx* ctx, uint8_t* d_k) {
+ncodec_status enqueue_scales(ncodec_ctx* ctx, uint8_t* d_k, void* mu_out = nullptr) {
   const int C = ctx->cfg.channels;
   const int P16 = (ctx->cfg.height / 16) * (ctx->cfg.width / 16);
   const Layout& L = ctx->L;
@@ -907,6 +932,7 @@ ncodec_status enqueue_scales(ncodec_ctx* ctx, uint8_t* d_k) {
   pa.k_out = d_k;
   pa.scales = ctx->p<float>(L.c_scales);
   pa.k_tab = ctx->is_int() ? ctx->p<uint8_t>(L.c_ktab) : nullptr;
+  pa.mu_out = mu_out;
   pa.C = C;
   pa.P = P16;
   pa.decode = 2;
@@ -1009,6 +1035,14 @@ ncodec_status run_graph(ncodec_ctx* ctx, bool decode, const void* p0, const void
     NC_HIP(ctx, retarget(ctx, gs, decode, ptr), "graph update");
   }
   NC_HIP(ctx, hipGraphLaunch(gs.exec, ctx->stream), "graph launch");
+  return NCODEC_OK;
+}
+
+// The second stream and its two events, created on first use.
+ncodec_status ensure_aux(ncodec_ctx* ctx) {
+  if (!ctx->aux) NC_HIP(ctx, hipStreamCreateWithFlags(&ctx->aux, hipStreamNonBlocking), "aux stream");
+  if (!ctx->ev_fork) NC_HIP(ctx, hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming), "fork event");
+  if (!ctx->ev_join) NC_HIP(ctx, hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming), "join event");
   return NCODEC_OK;
 }
 
@@ -1206,15 +1240,38 @@ ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, in
   const Layout& L = ctx->L;
   if (capacity < stream_capacity(L.n_sym))
     return fail(ctx, NCODEC_EINVAL, "capacity below ncodec_stream_capacity()");
+  const bool par = ctx->overlap;
+  if (par && (st = ensure_aux(ctx))) return st;
   int16_t* q = d_q ? d_q : ctx->p<int16_t>(L.qtmp);
-  st = enqueue_encode(ctx, d_frame, q, d_bits, ctx->p<uint8_t>(L.kmap));
-  if (st) return st;
-  NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
-           return launch_rans_encode(q, ctx->p<uint8_t>(L.kmap), L.n_sym, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch),
-                                     kRansMaxWords, ctx->p<uint32_t>(L.rlens), (uint8_t*)d_stream, d_stream_bytes,
-                                     ctx->stream);
-         }),
-         "rans encode");
+  // the coder: on the context's stream after the decoder, or (parallel coding)
+  // on the second stream as soon as q and the scale indices exist, while the
+  // decoder part of the encode runs (Fig. 6)
+  auto coder = [&](hipStream_t s) -> ncodec_status {
+    NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
+             return launch_rans_encode(q, ctx->p<uint8_t>(L.kmap), L.n_sym, rans_tab(ctx),
+                                       ctx->p<uint16_t>(L.rscratch), kRansMaxWords, ctx->p<uint32_t>(L.rlens),
+                                       (uint8_t*)d_stream, d_stream_bytes, s);
+           }),
+           "rans encode");
+    return NCODEC_OK;
+  };
+  if (par) {
+    st = enqueue_encode(ctx, d_frame, q, d_bits, ctx->p<uint8_t>(L.kmap), [&]() -> ncodec_status {
+      NC_HIP(ctx, hipEventRecord(ctx->ev_fork, ctx->stream), "fork");
+      NC_HIP(ctx, hipStreamWaitEvent(ctx->aux, ctx->ev_fork, 0), "fork");
+      ncodec_status s2 = coder(ctx->aux);
+      if (s2) return s2;
+      NC_HIP(ctx, hipEventRecord(ctx->ev_join, ctx->aux), "join");
+      return NCODEC_OK;
+    });
+    if (st) return st;
+    NC_HIP(ctx, hipStreamWaitEvent(ctx->stream, ctx->ev_join, 0), "join");
+  } else {
+    st = enqueue_encode(ctx, d_frame, q, d_bits, ctx->p<uint8_t>(L.kmap));
+    if (st) return st;
+    st = coder(ctx->stream);
+    if (st) return st;
+  }
   ctx->cur = 1 - ctx->cur;
   return NCODEC_OK;
 }
@@ -1227,7 +1284,27 @@ ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, s
   if ((uintptr_t)d_frame_out % 16) return fail(ctx, NCODEC_EINVAL, "d_frame_out must be 16-byte aligned");
   if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
   const Layout& L = ctx->L;
-  st = enqueue_scales(ctx, ctx->p<uint8_t>(L.kmap));
+  const int C = ctx->cfg.channels;
+  const int P16 = (ctx->cfg.height / 16) * (ctx->cfg.width / 16);
+  // the feature extractor does not depend on the symbols: with parallel coding
+  // it runs on the second stream while the symbols are decoded (Fig. 6)
+  const bool par = ctx->overlap && !L.fe.empty();
+  if (par && (st = ensure_aux(ctx))) return st;
+  const void* context = nullptr;
+  if (par) {
+    NC_HIP(ctx, hipEventRecord(ctx->ev_fork, ctx->stream), "fork");
+    NC_HIP(ctx, hipStreamWaitEvent(ctx->aux, ctx->ev_fork, 0), "fork");
+    const hipStream_t user = ctx->stream;
+    ctx->stream = ctx->aux;
+    const hipError_t e = temporal_context(ctx, &context);
+    ctx->stream = user;
+    NC_HIP(ctx, e, "feature extractor");
+    NC_HIP(ctx, hipEventRecord(ctx->ev_join, ctx->aux), "join");
+  } else {
+    NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
+  }
+  // one prior pass: the scale indices for the coder and mu for yhat = q + mu
+  st = enqueue_scales(ctx, ctx->p<uint8_t>(L.kmap), ctx->p(L.mu));
   if (st) return st;
   NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
            return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, ctx->p<uint8_t>(L.kmap), L.n_sym,
@@ -1235,9 +1312,22 @@ ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, s
                                      ctx->p<int16_t>(L.qtmp), d_status, ctx->stream);
          }),
          "rans decode");
-  st = enqueue_decode(ctx, ctx->p<int16_t>(L.qtmp), d_frame_out);
+  NC_HIP(ctx, timed(ctx, "yhat", [&] {
+           return launch_yhat_from_q(ctx->p<int16_t>(L.qtmp), ctx->p(L.mu), ctx->p(L.yhat[1 - ctx->cur]), C, P16,
+                                     ctx->is_int(), ctx->stream);
+         }),
+         "yhat");
+  if (par) NC_HIP(ctx, hipStreamWaitEvent(ctx->stream, ctx->ev_join, 0), "join");
+  st = decode_tail(ctx, d_frame_out);
   if (st) return st;
   ctx->cur = 1 - ctx->cur;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_parallel_coding(ncodec_ctx* ctx, int32_t enable) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  ctx->overlap = enable != 0;
   return NCODEC_OK;
 }
 
@@ -1345,6 +1435,12 @@ void ncodec_destroy(ncodec_ctx* ctx) {
       if (gs.graph) (void)hipGraphDestroy(gs.graph);
     }
   if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
+  if (ctx->aux) {
+    (void)hipStreamSynchronize(ctx->aux);
+    (void)hipStreamDestroy(ctx->aux);
+  }
+  if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
+  if (ctx->ev_join) (void)hipEventDestroy(ctx->ev_join);
   delete ctx;
 }
 

@@ -102,6 +102,7 @@ struct PriorArgs {
   double* partials;       // one per (tile, channel slice) (encode)
   const float* sigma_tab; // int path: sigma for s_i + 32768
   uint8_t* k_out;         // planar scale indices (nullable; required when scales_only)
+  void* mu_out;           // scale indices only: mu (NHWC; fp32 on the fp16 path, int16 on the int path), nullable
   const float* scales;    // fp16 path: coder scales
   const uint8_t* k_tab;   // int path: scale index for s_i + 32768
   int C;
@@ -158,6 +159,11 @@ constexpr int kBitsBlocks = 1024;
 hipError_t launch_estimate_bits(const int16_t* q, const void* scale, const float* sigma_tab, int64_t n,
                                 double* partials, double* out, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+// yhat (NHWC, C channels, P pixels) = q (planar int16) + mu (NHWC): fp16 path
+// (f16)(q + mu) with fp32 mu, int path clip(512 q + mu_i) with int16 mu_i --
+// the same operations as the quantiser of the prior epilogue.
+hipError_t launch_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int C, int P, bool is_int,
+                              hipStream_t st);
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);
 

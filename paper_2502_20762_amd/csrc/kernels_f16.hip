@@ -225,6 +225,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     const floatx16 sg = parked(px, 4 + g8);
 #pragma unroll
     for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), sct);
+    // mu as fp32 (NHWC), for yhat = q + mu once the symbols are decoded
+    const int gp = tile * 128 + px;
+    if (a.dst && gp < a.P) {
+      const floatx16 mu = parked(px, g8);
+      float* dm = (float*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8;
+      *(floatx4*)dm = floatx4{mu[0], mu[1], mu[2], mu[3]};
+      *(floatx4*)(dm + 4) = floatx4{mu[4], mu[5], mu[6], mu[7]};
+    }
     lds_barrier();
     store_k();
   } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
@@ -870,7 +878,7 @@ hipError_t launch_prior_f16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.P = pa.P;
   a.src0 = pa.yhat_prev;
   a.C0 = pa.C;
-  a.dst = pa.yhat_new;
+  a.dst = pa.decode == 2 ? pa.mu_out : pa.yhat_new;
   a.Cdst = pa.C;
   a.y = pa.y;
   a.q_in = pa.q_in;

@@ -248,6 +248,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     parked(px, 4 + g8, sv);
 #pragma unroll
     for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = a.k_tab[sv[e] + 32768];
+    // mu_i (int16, NHWC), for yhat_i = clip(512 q + mu_i) once the symbols are decoded
+    const int gp = tile * 128 + px;
+    if (a.dst && gp < a.P) {
+      int mu[8];
+      parked(px, g8, mu);
+      shortx8 m;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m[e] = (short)mu[e];
+      *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = m;
+    }
     lds_barrier();
     store_k();
   } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
@@ -914,7 +924,7 @@ hipError_t launch_prior_i16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.P = pa.P;
   a.src0 = pa.yhat_prev;
   a.C0 = pa.C;
-  a.dst = pa.yhat_new;
+  a.dst = pa.decode == 2 ? pa.mu_out : pa.yhat_new;
   a.Cdst = pa.C;
   a.y = pa.y;
   a.q_in = pa.q_in;

@@ -74,6 +74,7 @@ _SIGNATURES = {
     "ncodec_rans_decode": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P, ctypes.c_int64, _P, _P]),
     "ncodec_encode_frame_coded": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "ncodec_decode_frame_coded": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P, _P]),
+    "ncodec_parallel_coding": (ctypes.c_int, [_P, ctypes.c_int32]),
     "ncodec_get_state": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_set_state": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_kernels_per_frame": (ctypes.c_int32, [_P, ctypes.c_int32]),
@@ -194,6 +195,10 @@ def ncodec_encode_frame_coded(ctx, d_frame: int, d_q: int, d_bits: int, d_stream
 def ncodec_decode_frame_coded(ctx, d_stream: int, stream_bytes: int, d_frame_out: int, d_status: int = 0) -> None:
     _check(load_library().ncodec_decode_frame_coded(ctx, _p(d_stream), stream_bytes, _p(d_frame_out), _p(d_status)),
            ctx)
+
+
+def ncodec_parallel_coding(ctx, enable: bool) -> None:
+    _check(load_library().ncodec_parallel_coding(ctx, 1 if enable else 0), ctx)
 
 
 def ncodec_get_state(ctx, d_feat: int, d_yhat: int) -> None:
@@ -369,6 +374,9 @@ class Codec:
 
     def set_rate(self, qp: float):
         ncodec_set_rate(self.ctx, qp)
+
+    def parallel_coding(self, enable: bool):
+        ncodec_parallel_coding(self.ctx, enable)
 
     def kernels_per_frame(self, decode=False):
         return ncodec_kernels_per_frame(self.ctx, decode)

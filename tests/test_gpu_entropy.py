@@ -174,3 +174,36 @@ def test_coded_round_trip_with_gated_blocks_and_modules(path):
         assert int(host(st)) == 0
         np.testing.assert_array_equal(host(xo), host(xr))
         np.testing.assert_array_equal(host(dec.get_state()[0]), host(enc.get_state()[0]))
+
+
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_parallel_coding_matches_serial(path):
+    # Fig. 6 / supplementary "Parallel Coding": the coder on a second stream
+    # beside the decoder part of the encode, the feature extractor beside the
+    # symbol decoding; containers, symbols, frames and states equal the serial
+    # order bit for bit
+    H, W, C, ne, nd = 112, 208, 128, 2, 2
+    kw = dict(n_fe_blocks=2, n_rg_blocks=1)
+    flat = synth.make_weights(C, ne, nd, n_fe=2, n_rg=1)
+    se, sd, pe, pd = (Codec(H, W, C, ne, nd, path, flat, device=DEV, **kw) for _ in range(4))
+    pe.parallel_coding(True)
+    pd.parallel_coding(True)
+    for t in range(3):
+        say("parallel coding", path, "frame", t)
+        x = gpu(synth.random_frame(H, W, seed=90 + t))
+        qs = torch.empty(se.q_shape, dtype=torch.int16, device=DEV)
+        qp = torch.empty(se.q_shape, dtype=torch.int16, device=DEV)
+        bs, ns = se.encode_coded(x, q_out=qs)
+        bp, npb = pe.encode_coded(x, q_out=qp)
+        n1, n2 = int(host(ns)), int(host(npb))
+        assert n1 == n2
+        np.testing.assert_array_equal(host(bs)[:n1], host(bp)[:n2])
+        np.testing.assert_array_equal(host(qs), host(qp))
+        xs, st1 = sd.decode_coded(bs, n1)
+        xp, st2 = pd.decode_coded(bp, n2)
+        assert int(host(st1)) == 0 and int(host(st2)) == 0
+        np.testing.assert_array_equal(host(xs), host(xp))
+        for a, b in ((se, pe), (sd, pd), (pe, pd)):
+            fa, ya = a.get_state()
+            fb, yb = b.get_state()
+            assert torch.equal(fa, fb) and torch.equal(ya, yb)

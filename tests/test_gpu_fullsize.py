@@ -186,3 +186,43 @@ def test_hd1080_int_frame_bits_whole_frame():
         b = float(host(bits))
         say(f"int frame {t}: bits {b:.1f} (oracle {ref:.1f})")
         assert abs(b - ref) <= 1e-5 * ref, (t, b, ref)
+
+
+def test_hd720_both_paths():
+    # 1280x720 (Tab. 3d's resolution), C = 256, 8 + 8 blocks: fp16 whole frame
+    # teacher-forced (two frames), int path two frames free-running compared on
+    # three sampled regions (ragged tiles: 90 x 160 at 1/8, 45 x 80 latent)
+    H, W, C, NE, ND = 720, 1280, 256, 8, 8
+    flat, p = params_for(C, NE, ND)
+    xs = [synth.random_frame(H, W, seed=s) for s in (50, 51)]
+    enc = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
+    dec = Codec(H, W, C, NE, ND, "fp16", flat, device=DEV)
+    for t, x in enumerate(xs):
+        say("720p fp16 frame", t)
+        f0, y0 = (host(v).astype(np.float64) for v in enc.get_state())
+        q, bits = enc.encode(torch.from_numpy(x).to(DEV))
+        xhat = host(dec.decode(q)).astype(np.float64)
+        f1, y1 = (host(v).astype(np.float64) for v in enc.get_state())
+        f_ref, _ = check_fp16_encode(p, x, f0, y0, host(q), float(host(bits)), f1, y1, what=f"720p t={t}")
+        assert_close_fp16(xhat, cf.reconstruct(p, f_ref), f"720p t={t} xhat")
+    ip = ci.integerize(p)
+    enc = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
+    dec = Codec(H, W, C, NE, ND, "int16", flat, device=DEV)
+    H16, W16 = H // 16, W // 16
+    for t, x in enumerate(xs):
+        say("720p int frame", t)
+        f0, y0 = (host(v).astype(np.int64) for v in enc.get_state())
+        q, _ = enc.encode(torch.from_numpy(x).to(DEV))
+        xhat = host(dec.decode(q))
+        f1, y1 = (host(v).astype(np.int64) for v in enc.get_state())
+        qh = host(q).astype(np.int64)
+        for (Y0, X0) in [(0, 0), (H16 - S, W16 - S), (H16 // 3, W16 // 2 - 14)]:
+            full, valid = crop_views(Y0, X0, H16, W16)
+            st = ci.State(f0[(slice(None),) + full["f"]], y0[(slice(None),) + full["l"]])
+            r = ci.encode_frame(ip, x[(slice(None),) + full["x"]], st)
+            xr, _ = ci.decode_frame(ip, r.q, st)
+            sl, sf, sx = ((slice(None),) + valid[k] for k in ("l", "f", "x"))
+            np.testing.assert_array_equal(qh[(slice(None),) + full["l"]][sl], r.q[sl])
+            np.testing.assert_array_equal(y1[(slice(None),) + full["l"]][sl], r.state.yhat[sl])
+            np.testing.assert_array_equal(f1[(slice(None),) + full["f"]][sf], r.state.feat[sf])
+            np.testing.assert_array_equal(xhat[(slice(None),) + full["x"]][sx], xr[sx])

@@ -121,6 +121,15 @@ def test_edge_shapes_int(H, W, C, ne, nd):
     run_int_sequence(H, W, C, ne, nd, frames, "edge int")
 
 
+@pytest.mark.parametrize("C", [128, 256])
+def test_deep_16_16_blocks_both_paths(C):
+    # the depth axis of the scaling sweep (supplementary, larger model): 16 + 16 DC blocks
+    H, W = 64, 128
+    frames = [synth.random_frame(H, W, seed=s) for s in (60, 61)]
+    run_fp16_sequence(H, W, C, 16, 16, frames, "16+16 fp16")
+    run_int_sequence(H, W, C, 16, 16, frames, "16+16 int")
+
+
 def test_extreme_frames_int():
     # all-zero, all-one and saturated-out-of-range inputs
     H = W = 32
