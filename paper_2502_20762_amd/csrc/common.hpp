@@ -99,6 +99,15 @@ __device__ __forceinline__ void dma16(const void* g, const void* lds_wave_base) 
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m) : "memory", "m0");
 }
 
+// The same with a wave-uniform 64-bit base in SGPRs and a per-lane 32-bit
+// byte offset (one VGPR shared by every such load of a kernel, instead of a
+// 64-bit address per load).
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, const void* lds_wave_base) {
+  const uint32_t m = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_wave_base;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(m)
+               : "memory", "m0");
+}
+
 // Read-only kernel data seen through the constant address space: loads at
 // wave-uniform addresses become scalar loads.
 typedef const __attribute__((address_space(4))) float cfloat;
