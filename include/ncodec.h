@@ -185,6 +185,23 @@ ncodec_status ncodec_decode_frame(ncodec_ctx* ctx, const int16_t* d_q, void* d_f
 ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const void* d_scale,
                                    int64_t n, double* d_bits);
 
+/* ncodec_estimate_bits without a context, for callers that cannot allocate
+ * device memory (code under graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same rate, same fixed summation order and the same
+ * result bit for bit as ncodec_estimate_bits on an fp16 context: d_q n int16
+ * symbols, d_sigma n float32 scales, *d_bits (device double) the total.
+ * Enqueued on hip_stream (a hipStream_t; NULL = default stream) on the
+ * current device.  Allocates nothing: its partial sums live in a static
+ * device array of 1,024 doubles (8 KiB) that each GPU the library runs on
+ * holds until the process ends.  All calls on one GPU share that array, so
+ * calls that overlap on one GPU (different streams, or threads without
+ * ordering) race; calls ordered on one stream do not.  n must be in
+ * [0, 2^31) (any n uses the same 1,024 partials); NCODEC_EINVAL otherwise or
+ * for a NULL d_bits (or NULL d_q / d_sigma with n > 0), NCODEC_EHIP for a
+ * HIP failure; ncodec_last_error(NULL) gives the message. */
+ncodec_status ncodec_estimate_bits_noalloc(const int16_t* d_q, const float* d_sigma, int64_t n,
+                                           double* d_bits, void* hip_stream);
+
 /* ---- Entropy coding (Fig. 4 "AE" / "AD", Fig. 6; Supp. B.2) ----------------
  * The symbols are coded with rANS (Duda 2013; 32-bit state in [2^16, 2^32),
  * 16-bit words, 16-bit frequencies) under quantised-scale Gaussian tables:

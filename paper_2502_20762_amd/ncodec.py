@@ -68,6 +68,7 @@ _SIGNATURES = {
     "ncodec_encode_frame": (ctypes.c_int, [_P, _P, _P, _P]),
     "ncodec_decode_frame": (ctypes.c_int, [_P, _P, _P]),
     "ncodec_estimate_bits": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P]),
+    "ncodec_estimate_bits_noalloc": (ctypes.c_int, [_P, _P, ctypes.c_int64, _P, _P]),
     "ncodec_stream_capacity": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
     "ncodec_scale_indices": (ctypes.c_int, [_P, _P]),
     "ncodec_rans_encode": (ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P, ctypes.c_size_t, _P]),
@@ -168,6 +169,11 @@ def ncodec_decode_frame(ctx, d_q: int, d_frame_out: int) -> None:
 
 def ncodec_estimate_bits(ctx, d_q: int, d_scale: int, n: int, d_bits: int) -> None:
     _check(load_library().ncodec_estimate_bits(ctx, d_q or None, d_scale or None, n, d_bits), ctx)
+
+
+def ncodec_estimate_bits_noalloc(d_q: int, d_sigma: int, n: int, d_bits: int, stream: int = 0) -> None:
+    _check(load_library().ncodec_estimate_bits_noalloc(d_q or None, d_sigma or None, n, d_bits or None,
+                                                       stream or None), None)
 
 
 def ncodec_stream_capacity(cfg: ncodec_config) -> int:
