@@ -15,12 +15,14 @@ CVPR 2025):
 * ``bits``         -- the Gaussian likelihood / bit estimate.
 * ``entropy``      -- the coder: quantised-scale Gaussian tables and
                       interleaved rANS streams (Fig. 4 "AE"/"AD", Fig. 6).
+* ``hyperprior``   -- the two-step entropy model with the hyper latent z
+                      (Sec. 4.4; supplementary "Entropy model").
 * ``params``       -- its own reading of the canonical flat parameter list.
 
 Parity status of each function is stated in its docstring; every function is
 pinned by ``tests/test_oracle_*.py`` against closed forms, brute force or
 library routines (none is "parity unpinned").
 """
-from . import bits, codec_float, codec_int, entropy, ops, params  # noqa: F401
+from . import bits, codec_float, codec_int, entropy, hyperprior, ops, params  # noqa: F401
 from .bits import estimate_bits, likelihood, sigma_from_s  # noqa: F401
 from .params import Params, unpack  # noqa: F401

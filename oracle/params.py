@@ -14,6 +14,13 @@ Order (each weight row-major, each followed by its bias):
   fe[k]     as enc[k]                                                k < N_f
   rg[k]     as enc[k]                                                k < N_r
   q_e, q_d, q_f, q_r   (64, C) each, only with vector banks
+  then, only with the two-step entropy model (``hyper``):
+  zana      W(CZ,C,2,2) b(CZ)    hyper-analysis y -> z at 1/32
+  zsyn      W(8C,CZ)    b(8C)    hyper-synthesis, row 4m+2i+j -> pixel-shuffle
+                                 position (m,i,j) of the 2C hyper channels [mu ; s]
+  step2     W(C,C/2)    b(C)     second step: rows [dmu ; ds] for the last C/2
+                                 channels, from the first C/2 channels of yhat
+  zbank     (64, CZ)             scale of z per channel at each rate point (> 0)
 
 The conditional-coding modules (Fig. 4; Sec. 4.3, 4.4): the feature extractor
 fe turns f_{t-1} into the temporal context F_{t-1} that both fuse convs take
@@ -44,6 +51,17 @@ class Block:
     kind: str = "lrelu"   # "lrelu" or "gated"
 
 
+CZ = 64  # channels of the hyper latent z
+
+
+@dataclasses.dataclass
+class Hyper:
+    zana: Conv
+    zsyn: Conv
+    step2: Conv
+    zbank: np.ndarray   # (64, CZ)
+
+
 @dataclasses.dataclass
 class Params:
     C: int
@@ -60,6 +78,7 @@ class Params:
     fe: list = dataclasses.field(default_factory=list)
     rg: list = dataclasses.field(default_factory=list)
     banks: dict = None    # name -> (64, C) array, or None
+    hyper: Hyper = None   # the two-step entropy model with hyperprior, or None
 
 
 NUM_QP = 64
@@ -71,19 +90,24 @@ def _hidden(C: int, block: str) -> int:
     return 2 * C if block == "lrelu" else C
 
 
+def hyper_count(C: int) -> int:
+    return CZ * C * 4 + CZ + 8 * C * CZ + 8 * C + C * (C // 2) + C + NUM_QP * CZ
+
+
 def count(C: int, n_enc: int, n_dec: int, block: str = "lrelu", n_fe: int = 0, n_rg: int = 0,
-          banks: bool = False) -> int:
+          banks: bool = False, hyper: bool = False) -> int:
     blk = C * 9 + C + 2 * C * C + 2 * C + C * _hidden(C, block) + C
     return (C * 192 + C + C * 2 * C + C + n_enc * blk + C * C * 4 + C
             + 2 * C * C + 2 * C + 4 * C * C + 4 * C + C * 2 * C + C
             + n_dec * blk + 192 * C + 192
-            + (n_fe + n_rg) * blk + (4 * NUM_QP * C if banks else 0))
+            + (n_fe + n_rg) * blk + (4 * NUM_QP * C if banks else 0)
+            + (hyper_count(C) if hyper else 0))
 
 
 def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu", n_fe: int = 0,
-           n_rg: int = 0, banks: bool = False) -> Params:
+           n_rg: int = 0, banks: bool = False, hyper: bool = False) -> Params:
     flat = np.asarray(flat, dtype=np.float64).reshape(-1)
-    want = count(C, n_enc, n_dec, block, n_fe, n_rg, banks)
+    want = count(C, n_enc, n_dec, block, n_fe, n_rg, banks, hyper)
     if flat.size != want:
         raise ValueError(f"expected {want} parameters, got {flat.size}")
     pos = 0
@@ -115,8 +139,14 @@ def unpack(flat: np.ndarray, C: int, n_enc: int, n_dec: int, block: str = "lrelu
     fe = [blk() for _ in range(n_fe)]
     rg = [blk() for _ in range(n_rg)]
     bk = {name: take((NUM_QP, C)) for name in ("q_e", "q_d", "q_f", "q_r")} if banks else None
+    hy = None
+    if hyper:
+        zana = conv((CZ, C, 2, 2))
+        zsyn = conv((8 * C, CZ))
+        step2 = conv((C, C // 2))
+        hy = Hyper(zana, zsyn, step2, take((NUM_QP, CZ)))
     assert pos == flat.size
-    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec, block, fe, rg, bk)
+    return Params(C, pe, fuse_enc, enc, down, head, up, fuse_dec, dec, rec, block, fe, rg, bk, hy)
 
 
 def _f16(v: np.ndarray) -> np.ndarray:

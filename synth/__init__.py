@@ -61,8 +61,11 @@ PRESETS = {
 }
 
 
+CZ = 64  # channels of the hyper latent z (two-step entropy model)
+
+
 def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu",
-               n_fe: int = 0, n_rg: int = 0, banks: bool = False):
+               n_fe: int = 0, n_rg: int = 0, banks: bool = False, hyper: bool = False):
     """(name, shape, fan_in, kind) in canonical order; kind is 'w', 'w_res', 'b'
     or 'bank'.
 
@@ -70,7 +73,10 @@ def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu",
     hidden 2C channels are chunked into two halves and gated, pw2 is C x C).
     After the transform come ``n_fe`` feature-extractor blocks, ``n_rg``
     reconstruction-generation blocks and, with ``banks``, the four qp-indexed
-    vector banks q_e, q_d, q_f, q_r (64 rate points x C each)."""
+    vector banks q_e, q_d, q_f, q_r (64 rate points x C each) and, with
+    ``hyper``, the two-step entropy model: hyper-analysis zana (CZ x C x 2 x 2),
+    hyper-synthesis zsyn (8C x CZ), second-step head step2 (C x C/2) and the
+    bank of z scales zbank (64 rate points x CZ)."""
     C = channels
     out = []
     if block not in ("lrelu", "gated"):
@@ -104,6 +110,11 @@ def param_list(channels: int, n_enc: int, n_dec: int, block: str = "lrelu",
     if banks:
         for name in ("q_e", "q_d", "q_f", "q_r"):
             out.append((name, (NUM_QP, C), 0, "bank"))
+    if hyper:
+        conv("zana", (CZ, C, 2, 2), 4 * C)
+        conv("zsyn", (8 * C, CZ), CZ)
+        conv("step2", (C, C // 2), C // 2)
+        out.append(("zbank", (NUM_QP, CZ), 0, "zbank"))
     return out
 
 
@@ -119,6 +130,8 @@ def bank_values(rng: np.random.Generator, name: str, channels: int) -> np.ndarra
     jit = np.exp(rng.uniform(-0.1, 0.1, size=(NUM_QP, channels)))
     if name == "q_e":
         return 2.0 ** (-qp / 32.0) * jit
+    if name == "zbank":  # scale of z: about 2 at qp 0, falling with the rate
+        return 2.0 * 2.0 ** (-qp / 32.0) * jit
     if name == "q_d":
         return 2.0 ** (qp / 32.0) * jit
     return jit
@@ -126,7 +139,7 @@ def bank_values(rng: np.random.Generator, name: str, channels: int) -> np.ndarra
 
 def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
                  resid_gain: float = RESID_GAIN, block: str = "lrelu",
-                 n_fe: int = 0, n_rg: int = 0, banks: bool = False) -> np.ndarray:
+                 n_fe: int = 0, n_rg: int = 0, banks: bool = False, hyper: bool = False) -> np.ndarray:
     """Flat float32 parameter vector; every value is exactly fp16-representable.
 
     Weights ~ N(0, 1/fan_in) (the residual projection times ``resid_gain``),
@@ -134,9 +147,12 @@ def make_weights(channels: int, n_enc: int, n_dec: int, seed: int = SEED_W,
     """
     rng = np.random.default_rng(seed)
     chunks = []
-    for name, shape, fan_in, kind in param_list(channels, n_enc, n_dec, block, n_fe, n_rg, banks):
+    for name, shape, fan_in, kind in param_list(channels, n_enc, n_dec, block, n_fe, n_rg, banks, hyper):
         if kind == "bank":
             chunks.append(bank_values(rng, name, channels).reshape(-1))
+            continue
+        if kind == "zbank":
+            chunks.append(bank_values(rng, name, shape[1]).reshape(-1))
             continue
         if kind == "b":
             v = rng.uniform(-0.1, 0.1, size=shape)
