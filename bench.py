@@ -167,8 +167,11 @@ def coded_loop(enc, dec, gframes, steps, warmup, xout, torch, parallel=False):
     nfr = len(gframes)
     cap = enc.stream_capacity()
     sbuf = [torch.empty(cap, dtype=torch.uint8, device="cuda") for _ in range(2)]
-    nbytes = torch.zeros(steps, dtype=torch.int64, device="cuda")
-    status = torch.zeros(steps, dtype=torch.int32, device="cuda")
+    # one byte count and status per container: three (z, y^1, y^2) with the
+    # two-step entropy model
+    nsec = (3,) if enc.hyperprior else ()
+    nbytes = torch.zeros((steps,) + nsec, dtype=torch.int64, device="cuda")
+    status = torch.zeros((steps,) + nsec, dtype=torch.int32, device="cuda")
     bits = torch.zeros(steps, dtype=torch.float64, device="cuda")
     enc.reset()
     dec.reset()
@@ -206,6 +209,18 @@ def coded_loop(enc, dec, gframes, steps, warmup, xout, torch, parallel=False):
     torch.cuda.synchronize()
     plain_enc = sum(e[0].elapsed_time(e[1]) for e in pv)
     plain_dec = sum(e[1].elapsed_time(e[2]) for e in pv)
+    per_frame = nbytes.reshape(steps, -1).sum(dim=1).double()
+    res = {"encode_fps": steps / (sum(enc_ms) * 1e-3), "decode_fps": steps / (sum(dec_ms) * 1e-3),
+           "value": steps / ((sum(enc_ms) + sum(dec_ms)) * 1e-3),
+           "uncoded_same_loop": {"encode_fps": steps / (plain_enc * 1e-3), "decode_fps": steps / (plain_dec * 1e-3)},
+           "bytes_per_frame": float(per_frame[1:].mean().item()) if steps > 1 else float(per_frame[0].item()),
+           "estimated_bytes_per_frame": float(bits[1:].mean().item()) / 8.0 if steps > 1 else float(bits[0].item()) / 8.0}
+    if enc.hyperprior:
+        # the scale indices of y depend on the frame's z and y^1: no coder-alone timing
+        enc.parallel_coding(False)
+        dec.parallel_coding(False)
+        res["decoded_ok"] = bool((status == 0).all().item())
+        return res
     # the coder alone, on the last frame's symbols: container in, container out
     q = torch.empty(enc.q_shape, dtype=torch.int16, device="cuda")
     k_idx = enc.scale_indices()
@@ -224,13 +239,9 @@ def coded_loop(enc, dec, gframes, steps, warmup, xout, torch, parallel=False):
     enc.parallel_coding(False)
     dec.parallel_coding(False)
     ok = bool((status == 0).all().item()) and bool(torch.equal(out_q, q))
-    return {"encode_fps": steps / (sum(enc_ms) * 1e-3), "decode_fps": steps / (sum(dec_ms) * 1e-3),
-            "value": steps / ((sum(enc_ms) + sum(dec_ms)) * 1e-3),
-            "uncoded_same_loop": {"encode_fps": steps / (plain_enc * 1e-3), "decode_fps": steps / (plain_dec * 1e-3)},
-            "bytes_per_frame": float(nbytes[1:].double().mean().item()) if steps > 1 else float(nbytes[0].item()),
-            "estimated_bytes_per_frame": float(bits[1:].mean().item()) / 8.0 if steps > 1 else float(bits[0].item()) / 8.0,
-            "rans_encode_us": 1e3 * e0.elapsed_time(e1) / reps, "rans_decode_us": 1e3 * e1.elapsed_time(e2) / reps,
-            "decoded_ok": ok}
+    res.update({"rans_encode_us": 1e3 * e0.elapsed_time(e1) / reps, "rans_decode_us": 1e3 * e1.elapsed_time(e2) / reps,
+                "decoded_ok": ok})
+    return res
 
 
 def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
@@ -335,33 +346,39 @@ def run_gated(path, pre, gframes, steps, warmup, torch, Codec):
             "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)]}
 
 
-SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r, block): resolution, width, depth, modules, form
-    ("720p", 720, 1280, 256, 8, 8, 0, 0, "lrelu"),
-    ("1080p C=64", 1088, 1920, 64, 8, 8, 0, 0, "lrelu"),
-    ("1080p C=128", 1088, 1920, 128, 8, 8, 0, 0, "lrelu"),
-    ("1080p", 1088, 1920, 256, 8, 8, 0, 0, "lrelu"),
-    ("1080p gated blocks", 1088, 1920, 256, 8, 8, 0, 0, "gated"),
-    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16, 0, 0, "lrelu"),
-    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32, 0, 0, "lrelu"),
+SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r, block, two-step entropy model):
+    # resolution, width, depth, modules, form
+    ("720p", 720, 1280, 256, 8, 8, 0, 0, "lrelu", False),
+    ("1080p C=64", 1088, 1920, 64, 8, 8, 0, 0, "lrelu", False),
+    ("1080p C=128", 1088, 1920, 128, 8, 8, 0, 0, "lrelu", False),
+    ("1080p", 1088, 1920, 256, 8, 8, 0, 0, "lrelu", False),
+    ("1080p gated blocks", 1088, 1920, 256, 8, 8, 0, 0, "gated", False),
+    ("1080p 16+16 blocks", 1088, 1920, 256, 16, 16, 0, 0, "lrelu", False),
+    ("1080p 32+32 blocks", 1088, 1920, 256, 32, 32, 0, 0, "lrelu", False),
     ("1080p + feature extractor (2 blocks), reconstruction generation (2 blocks), qp banks",
-     1088, 1920, 256, 8, 8, 2, 2, "lrelu"),
-    ("4K", 2176, 3840, 256, 8, 8, 0, 0, "lrelu"),
+     1088, 1920, 256, 8, 8, 2, 2, "lrelu", False),
+    ("1080p + two-step entropy model with hyperprior", 1088, 1920, 256, 8, 8, 0, 0, "lrelu", True),
+    ("1080p, all modules: feature extractor, reconstruction generation, qp banks, two-step entropy model",
+     1088, 1920, 256, 8, 8, 2, 2, "lrelu", True),
+    ("4K", 2176, 3840, 256, 8, 8, 0, 0, "lrelu", False),
 ]
 
 
-def sweep(paths, steps, warmup, torch, Codec):
+def sweep(paths, steps, warmup, torch, Codec, match=""):
     """Frames/s and the DC block's MFMA fraction across resolutions, widths and
     depths (random-init weights, seeded random frames); one JSON line each."""
     import synth
-    for label, H, W, C, ne, nd, nfe, nrg, block in SWEEP:
+    for label, H, W, C, ne, nd, nfe, nrg, block, hyper in SWEEP:
+        if match not in label:
+            continue
         frames = [torch.from_numpy(synth.random_frame(H, W, seed=90 + i)).to("cuda") for i in range(4)]
         banks = nfe + nrg > 0
-        weights = synth.make_weights(C, ne, nd, block=block, n_fe=nfe, n_rg=nrg, banks=banks)
+        weights = synth.make_weights(C, ne, nd, block=block, n_fe=nfe, n_rg=nrg, banks=banks, hyper=hyper)
         kinds, enc_list, dec_list = workload_model(H, W, C, ne, nd, block)
         enc_list = ["dcblock"] * nfe + enc_list
         dec_list = ["dcblock"] * (nfe + nrg) + dec_list
         for path in paths:
-            kw = dict(block=block, n_fe_blocks=nfe, n_rg_blocks=nrg, qp_banks=banks)
+            kw = dict(block=block, n_fe_blocks=nfe, n_rg_blocks=nrg, qp_banks=banks, hyperprior=hyper)
             enc = Codec(H, W, C, ne, nd, path, weights, **kw)
             dec = Codec(H, W, C, ne, nd, path, weights, **kw)
             odt = torch.int16 if path == "int16" else torch.float16
@@ -386,12 +403,18 @@ def sweep(paths, steps, warmup, torch, Codec):
             frac = scale * kinds["dcblock"][0] / (ms * 1e-3 / n) / 1e12 / peak if n else None
             t_roof = roofline_seconds(kinds, enc_list + dec_list, peak * 1e12 / scale)
             value = steps / ((r["enc_ms"] + r["dec_ms"]) * 1e-3)
+            coded = None
+            if hyper:  # three containers per frame (z, y^1, y^2)
+                c = coded_loop(enc, dec, frames, steps, warmup, xout, torch)
+                coded = {k: c[k] for k in ("encode_fps", "decode_fps", "value", "bytes_per_frame",
+                                           "estimated_bytes_per_frame", "decoded_ok")}
             print(json.dumps({"sweep": label, "path": path, "height": H, "width": W, "channels": C,
                               "n_enc_blocks": ne, "n_dec_blocks": nd, "n_fe_blocks": nfe, "n_rg_blocks": nrg,
-                              "block": block,
+                              "block": block, "two_step_entropy_model": hyper, "coded": coded,
                               "frames_per_s": value,
                               "encode_fps": steps / (r["enc_ms"] * 1e-3), "decode_fps": steps / (r["dec_ms"] * 1e-3),
                               "dcblock_us": 1e3 * ms / n if n else None, "dcblock_mfma_frac": frac,
+                              "encode_kernels_us": {k: round(1e3 * v[1] / v[0], 2) for k, v in t.items()},
                               "frame_roofline_fps": 1.0 / t_roof, "frac_of_frame_roofline": value * t_roof}),
                   flush=True)
             del enc, dec, qbuf, xout
@@ -408,6 +431,7 @@ def main():
     ap.add_argument("--no-gated", action="store_true", help="skip the gated DC-block form")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the 1080p line: one line per resolution / width / depth of the sweep table")
+    ap.add_argument("--sweep-match", default="", help="only the sweep rows whose label contains this text")
     ap.add_argument("--cpu-strip-rows", type=int, default=1088)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (3 times), as the reference "
@@ -424,7 +448,7 @@ def main():
     from paper_2502_20762_amd.ncodec import Codec
 
     if args.sweep:
-        sweep(args.paths.split(","), args.steps, args.warmup, torch, Codec)
+        sweep(args.paths.split(","), args.steps, args.warmup, torch, Codec, args.sweep_match)
         return
 
     if args.calib_copy_mib > 0:

@@ -88,7 +88,34 @@ typedef struct {
                             before the reconstruction conv (decode only)            */
   int32_t qp_banks;      /* 1: the weights end with the vector banks (Sec. 4.4), see
                             ncodec_set_qp; 0: none                                  */
+  int32_t hyperprior;    /* 1: the two-step entropy model with the hyper latent z
+                            (Sec. 4.4; supplementary "Entropy model"), see below;
+                            needs C in {128, 256} and H, W multiples of 32.
+                            0: the one-step prior on yhat_{t-1}                     */
 } ncodec_config;
+
+/* The two-step entropy model (hyperprior = 1).  The paper codes a hyper
+ * latent z with a bank of factorized modules (one per rate point; the nearest
+ * one between points, Sec. 4.4 and the supplementary rate adjustment) and
+ * estimates y's distribution in two steps, decoding z, then y^1, then y^2
+ * (supplementary "Entropy model" and "Parallel Coding").  This library reads
+ * it as:
+ *   z      = conv2x2/s2(y) + b            (CZ = 64 channels at H/32 x W/32)
+ *   q_z    = round(z)  (int: round(z_i / 512)), zhat = q_z (int: clip(512 q_z)),
+ *            coded under a zero-mean Gaussian of scale max(zbank[qp'][c], 0.11)
+ *            per channel c, qp' the nearest rate point
+ *   [mu_h ; s_h] = shuffle2(W_zs zhat + b)  (2C channels at 1/16)
+ *   [mu ; s] = prior(yhat_{t-1}) + [mu_h ; s_h]  (int: saturating)
+ *   y^1 = channels 0 .. C/2-1, quantised with (mu, s) of those channels
+ *   [dmu ; ds] = W_2 yhat^1 + b  (C/2 -> C)
+ *   y^2 = channels C/2 .. C-1, quantised with mu + dmu, s + ds
+ *   bits = bits(z) + bits(y^1) + bits(y^2)
+ * The frame's symbols (d_q of encode / decode) are then the C x H/16 x W/16
+ * planar y symbols followed by the CZ x H/32 x W/32 planar z symbols
+ * (ncodec_symbol_count values).  Weights: after the vector banks, zana
+ * W(CZ,C,2,2) b(CZ); zsyn W(8C,CZ) b(8C), row 4m+2i+j -> pixel-shuffle
+ * position (m,i,j) of the 2C channels [mu_h ; s_h]; step2 W(C,C/2) b(C),
+ * rows [dmu ; ds]; zbank (64, CZ). */
 
 /* Number of float32 values in the canonical parameter list for cfg, or 0 if
  * cfg is invalid.  Canonical order (each weight row-major, followed by its
@@ -108,6 +135,10 @@ size_t ncodec_weight_count(const ncodec_config* cfg);
 /* Bytes of device workspace a context needs (weights in kernel-ready form,
  * state, intermediates), or 0 if cfg is invalid.  Pure host function. */
 size_t ncodec_workspace_bytes(const ncodec_config* cfg);
+
+/* int16 symbols of one frame: C (H/16) (W/16), plus 64 (H/32) (W/32) with
+ * the two-step entropy model.  0 if cfg is invalid.  Pure host function. */
+size_t ncodec_symbol_count(const ncodec_config* cfg);
 
 /* Create a context: the state of one encoder or one decoder of the low-delay
  * P-frame setting (Sec. 4.1, Fig. 4; Sec. 5.1 "Test Details"), holding the
@@ -157,13 +188,14 @@ ncodec_status ncodec_set_rate(ncodec_ctx* ctx, double qp);
 /* Encode one frame (Sec. 4.1, Fig. 4 encoder side, Supp. B.3 encoding).
  *  d_frame: 3 x H x W planar fp16 (IEEE binary16), values in [0, 1]; the int
  *           path converts it with x_i = round(512 x) (Alg. 1).
- *  d_q:     C x H/16 x W/16 planar int16 output symbols q.
+ *  d_q:     C x H/16 x W/16 planar int16 output symbols q (with the
+ *           two-step model followed by the z symbols: ncodec_symbol_count).
  *  d_bits:  device double receiving the frame's estimated bits, or NULL.
  * Updates the context state to (f_t, yhat_t).  d_frame must not alias d_q. */
 ncodec_status ncodec_encode_frame(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits);
 
 /* Decode one frame from its symbols (Fig. 4 decoder side, Supp. B.3).
- *  d_q:         C x H/16 x W/16 planar int16 symbols from ncodec_encode_frame.
+ *  d_q:         the symbols from ncodec_encode_frame (ncodec_symbol_count).
  *  d_frame_out: 3 x H x W planar; fp16 in [0,1] (fp16 path) or int16 in
  *               [0, 512] (int path).
  * Updates the context state to (f_t, yhat_t). */
@@ -227,11 +259,16 @@ ncodec_status ncodec_estimate_bits_noalloc(const int16_t* d_q, const float* d_si
  * 16-byte aligned.  A stream holds at most 128 + 2 * 8192 words. */
 
 /* Worst-case container size in bytes for one frame of cfg (what d_stream
- * must hold for ncodec_encode_frame_coded).  0 for an invalid cfg. */
+ * must hold for ncodec_encode_frame_coded).  0 for an invalid cfg.  With the
+ * two-step entropy model a frame is three containers, z, y^1 and y^2, each
+ * at a fixed offset: 0, cap(nz), cap(nz) + cap(n1), with cap(n) the
+ * worst case of n symbols (nz = 64 (H/32) (W/32), n1 = n2 = C/2 (H/16) (W/16)),
+ * and the capacity is their sum. */
 size_t ncodec_stream_capacity(const ncodec_config* cfg);
 
 /* Scale indices (uint8, C x H/16 x W/16 planar) of the symbols of the next
- * frame, from the current state (the prior head on yhat_{t-1}). */
+ * frame, from the current state (the prior head on yhat_{t-1}).  ESTATE with
+ * the two-step model (its indices depend on the frame's z and y^1). */
 ncodec_status ncodec_scale_indices(ncodec_ctx* ctx, uint8_t* d_k);
 
 /* Code n symbols d_q (int16) with scale indices d_k (uint8, values >= 64 are
@@ -253,14 +290,18 @@ ncodec_status ncodec_rans_decode(ncodec_ctx* ctx, const void* d_stream, size_t s
 
 /* ncodec_encode_frame, then the frame's symbols coded into d_stream
  * (capacity >= ncodec_stream_capacity(cfg)); *d_stream_bytes (device u64)
- * receives the container size.  d_q (symbols) and d_bits (estimate) may be
- * NULL. */
+ * receives the container size (two-step model: d_stream_bytes[0 .. 2], the
+ * sizes of the z, y^1 and y^2 containers).  d_q (symbols) and d_bits
+ * (estimate) may be NULL. */
 ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q, double* d_bits,
                                         void* d_stream, size_t capacity, uint64_t* d_stream_bytes);
 
 /* Decode one frame from its container: scale indices from the state, symbols
  * from the container, then ncodec_decode_frame.  *d_status as for
- * ncodec_rans_decode (may be NULL); the state advances even on error. */
+ * ncodec_rans_decode (may be NULL; two-step model: d_status[0 .. 2] for the
+ * z, y^1 and y^2 containers, decoded in that order, each with the
+ * distribution that the previous ones determine); the state advances even on
+ * error.  stream_bytes bounds every read. */
 ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, size_t stream_bytes,
                                         void* d_frame_out, int32_t* d_status);
 
@@ -289,7 +330,8 @@ ncodec_status ncodec_get_state(ncodec_ctx* ctx, void* d_feat, void* d_yhat);
 ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* d_yhat);
 
 /* Kernel launches one ncodec_encode_frame (decode = 0, with a non-NULL
- * d_bits; one fewer without) or ncodec_decode_frame (decode = 1) enqueues,
+ * d_bits; one fewer without) or ncodec_decode_frame (decode = 1) enqueues
+ * (three more each with the two-step model),
  * counting the feature-extractor and reconstruction-generation blocks
  * (Sec. 3: the number of modules called per frame is one of the costs the
  * design minimises).  0 for a NULL ctx. */
@@ -304,7 +346,8 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
  * the direct launches.  Off by default: on MI355X with ROCm 7 the replay of
  * this linear launch chain measured slightly slower than direct launches.
  * While per-kernel timing is enabled, calls launch directly.  Errors: EHIP if
- * capture, instantiation, update or launch fails. */
+ * capture, instantiation, update or launch fails; ESTATE for a context with the
+ * two-step entropy model (not supported there). */
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
 
 /* Optional per-kernel timing.  While enabled, every kernel the context

@@ -67,7 +67,21 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "qp_banks must be 0 or 1";
     return false;
   }
+  if (c->hyperprior != 0 && c->hyperprior != 1) {
+    if (why) *why = "hyperprior must be 0 or 1";
+    return false;
+  }
+  if (c->hyperprior && (c->channels < 128 || c->height % 32 || c->width % 32)) {
+    if (why) *why = "the two-step entropy model needs C in {128, 256} and H, W multiples of 32";
+    return false;
+  }
   return true;
+}
+
+constexpr int kCZ = 64;  // channels of the hyper latent z
+
+size_t hyper_count(int C) {
+  return (size_t)kCZ * C * 4 + kCZ + (size_t)8 * C * kCZ + 8 * C + (size_t)C * (C / 2) + C + (size_t)kNumQp * kCZ;
 }
 
 size_t weight_count(const ncodec_config& c) {
@@ -76,7 +90,7 @@ size_t weight_count(const ncodec_config& c) {
   const size_t blk = C * 9 + C + 2 * C * C + 2 * C + C * hid + C;
   return C * 192 + C + 2 * C * C + C + c.n_enc_blocks * blk + 4 * C * C + C + 2 * C * C + 2 * C + 4 * C * C + 4 * C +
          2 * C * C + C + c.n_dec_blocks * blk + 192 * C + 192 + (size_t)(c.n_fe_blocks + c.n_rg_blocks) * blk +
-         (c.qp_banks ? 4 * (size_t)kNumQp * C : 0);
+         (c.qp_banks ? 4 * (size_t)kNumQp * C : 0) + (c.hyperprior ? hyper_count(c.channels) : 0);
 }
 
 // fp16(w q) with one rounding: the precision of every weight of the image.
@@ -347,6 +361,12 @@ struct Layout {
   // offsets, status words, byte count
   size_t kmap, qtmp, rscratch, rlens, rerrs, rcount;
   size_t mu;  // coded decode: the prior's mu (fp32 or int16, NHWC) between scale indices and symbols
+  // two-step entropy model
+  ConvDev zana, zsyn, step2;
+  size_t zsig = 0;     // sigma of each z channel at the current rate point (fp32)
+  size_t zk = 0;       // scale index of every z symbol (uint8, CZ x P32 planar)
+  size_t zhat = 0, hp = 0, base = 0;
+  int64_t n_z = 0;     // z symbols per frame
   int64_t n_sym, n_streams;
   int n_partials;
   size_t total;
@@ -439,7 +459,8 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   // integer qp, the linear interpolation of the supplementary rate-adjustment
   // section between two rate points otherwise.
   const size_t nb = (size_t)kNumQp * C;
-  const float* bank = cfg.qp_banks ? w + weight_count(cfg) - 4 * nb : nullptr;
+  const size_t nhyper = cfg.hyperprior ? hyper_count(C) : 0;
+  const float* bank = cfg.qp_banks ? w + weight_count(cfg) - nhyper - 4 * nb : nullptr;
   std::vector<double> rows[4];
   if (bank) {
     const int i = std::min((int)std::floor(qp), kNumQp - 2);
@@ -510,6 +531,40 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   for (int k = 0; k < cfg.n_fe_blocks; ++k) L.fe.push_back(pk.block(cur));
   for (int k = 0; k < cfg.n_rg_blocks; ++k) L.rg.push_back(pk.block(cur));
   if (bank) cur += 4 * nb;
+  if (cfg.hyperprior) {
+    // hyper-analysis: like the downsample, packed k' = (2i + j) C + c <- source column 4c + 2i + j
+    const float* za_w = take((size_t)kCZ * 4 * C); const float* za_b = take(kCZ);
+    L.zana = pk.gemm(za_w, za_b, kCZ, 4 * C, 4 * C, [](int n) { return n; }, [C](int k) { return (k % C) * 4 + k / C; });
+    // hyper-synthesis: like the upsample over 2C channels, packed row n' = sp 2C + m <- source row 4m + sp
+    const float* zs_w = take((size_t)8 * C * kCZ); const float* zs_b = take(8 * C);
+    L.zsyn = pk.gemm(zs_w, zs_b, 8 * C, kCZ, kCZ, [C](int n) { return 4 * (n % (2 * C)) + n / (2 * C); },
+                     [](int k) { return k; });
+    // second step: like the prior head over C / 2 channels, packed row n' = 64 t + r:
+    // dmu row 32 t + r (r < 32), else ds row C/2 + 32 t + r - 32
+    const float* s2_w = take((size_t)C * (C / 2)); const float* s2_b = take(C);
+    L.step2 = pk.gemm(s2_w, s2_b, C, C / 2, C / 2,
+                      [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C / 2 + 32 * (n / 64) + n % 64 - 32; },
+                      [](int k) { return k; });
+    // the z bank row of the rate point (the nearest learned point), sigma floored at 0.11
+    const float* zbank = take((size_t)kNumQp * kCZ);
+    const int row = std::min((int)std::floor(qp + 0.5), kNumQp - 1);
+    L.zsig = img.add(kCZ * 4);
+    float* zs = img.at<float>(L.zsig);
+    double zsd[kCZ];
+    for (int c = 0; c < kCZ; ++c) {
+      zsd[c] = std::fmax((double)zbank[(size_t)row * kCZ + c], 0.11);
+      zs[c] = (float)zsd[c];
+    }
+    // scale index of every z symbol (the smallest coder scale >= sigma_z, in double)
+    const size_t P32 = (size_t)(cfg.height / 32) * (cfg.width / 32);
+    L.zk = img.add(kCZ * P32);
+    uint8_t* zk = img.at<uint8_t>(L.zk);
+    for (int c = 0; c < kCZ; ++c) {
+      int j = 0;
+      while (j < kCoderScales - 1 && (double)(float)(0.11 * std::pow(256.0 / 0.11, (double)j / (kCoderScales - 1))) < zsd[c]) ++j;
+      std::memset(zk + (size_t)c * P32, j, P32);
+    }
+  }
   if ((size_t)(cur - w) != weight_count(cfg)) {
     if (err) *err = "internal: parameter walk mismatch";
     return false;
@@ -567,20 +622,30 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
   if (cfg.n_fe_blocks > 0) L.ctxF = alloc(fb);
   L.y = alloc(lb);
-  const int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
+  const size_t P32 = P16 / 4;
+  // rate partial sums: the prior's (tiles x passes); with the two-step model
+  // also the z quantiser's (one per tile) and the second step's
+  int np = is_int ? prior_partials_i16(C, (int)P16) : prior_partials_f16(C, (int)P16);
+  if (cfg.hyperprior) np += (int)((P32 + 127) / 128) + (int)((P16 + 127) / 128) * (C / 64);
   L.n_partials = np > kBitsBlocks ? np : kBitsBlocks;
   L.partials = alloc((size_t)L.n_partials * 8);
   L.zpad = alloc((size_t)C * 2);  // zeroed at create and never written
   L.spare_bits = alloc(8);        // bit total of graph replays called without d_bits
+  L.n_z = cfg.hyperprior ? (int64_t)P32 * kCZ : 0;
   L.n_sym = (int64_t)P16 * C;
   L.n_streams = (L.n_sym + kRansStream - 1) / kRansStream;
   L.kmap = alloc((size_t)L.n_sym);
-  L.qtmp = alloc((size_t)L.n_sym * 2);
+  L.qtmp = alloc((size_t)(L.n_sym + L.n_z) * 2);
   L.rscratch = alloc((size_t)L.n_streams * kRansMaxWords * 2);
   L.rlens = alloc((size_t)L.n_streams * 4);
   L.rerrs = alloc((size_t)L.n_streams * 4);
   L.rcount = alloc(4);  // decoder ticket counter: zeroed at create, left at zero by every decode
   L.mu = alloc(P16 * C * 4);
+  if (cfg.hyperprior) {
+    L.zhat = alloc(P32 * kCZ * 2);
+    L.hp = alloc(P16 * 2 * C * 2);
+    L.base = alloc(P16 * C * 4);
+  }
   L.total = off;
   return pk.ok;
 }
@@ -793,6 +858,94 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   return NCODEC_OK;
 }
 
+// ---- two-step entropy model with the hyper latent z (Sec. 4.4; supplementary
+// "Entropy model", "Parallel Coding")
+int P16_of(const ncodec_ctx* ctx) { return (ctx->cfg.height / 16) * (ctx->cfg.width / 16); }
+int P32_of(const ncodec_ctx* ctx) { return (ctx->cfg.height / 32) * (ctx->cfg.width / 32); }
+
+// z = conv2x2/s2(y), quantised: symbols to qz (planar), zhat (NHWC), one rate
+// partial per 1/32 tile from *parts on.
+hipError_t z_encode(ncodec_ctx* ctx, int16_t* qz, double* parts, int* np) {
+  const Layout& L = ctx->L;
+  const int C = ctx->cfg.channels;
+  PwArgs a = conv_args(ctx, L.zana, 4 * C, kCZ, P32_of(ctx));
+  a.src0 = ctx->p(L.y);
+  a.Csrc = C;
+  a.w8 = ctx->cfg.width / 16;  // the gather reads the 1/16 grid
+  a.dst = ctx->p(L.zhat);
+  a.Cdst = kCZ;
+  a.q_out = qz;
+  a.partials = parts;
+  a.zsigma = ctx->p<float>(L.zsig);
+  return timed(ctx, "zquant", [&] {
+    return ctx->is_int() ? launch_zquant_i16(a, ctx->stream, np) : launch_zquant_f16(a, ctx->stream, np);
+  });
+}
+
+// zhat from the decoded z symbols (fp16: q_z; int: clip(512 q_z)).
+hipError_t z_from_symbols(ncodec_ctx* ctx, const int16_t* qz) {
+  return timed(ctx, "zhat", [&] {
+    return launch_yhat_from_q(qz, nullptr, ctx->p(ctx->L.zhat), kCZ, P32_of(ctx), ctx->is_int(), ctx->stream, kCZ, 0);
+  });
+}
+
+// hyper parameters [mu_h ; s_h] (NHWC, 2C channels at 1/16) = shuffle2(W_zs zhat + b).
+hipError_t hyper_synth(ncodec_ctx* ctx) {
+  const Layout& L = ctx->L;
+  const int C = ctx->cfg.channels;
+  PwArgs a = conv_args(ctx, L.zsyn, kCZ, 8 * C, P32_of(ctx));
+  a.src0 = ctx->p(L.zhat);
+  a.C0 = kCZ;
+  a.dst = ctx->p(L.hp);
+  a.Cdst = 2 * C;
+  a.w8 = ctx->cfg.width / 16;  // the shuffle writes the 1/16 grid
+  return pw(ctx, "hyper", LD_NHWC, EP_UP, a);
+}
+
+// Step 1 of the two-step model on a prior call: the hyper parameters are
+// added to (mu, s); the second half of the channels leaves (mu, s) in base.
+void step1_fields(const ncodec_ctx* ctx, PriorArgs& pa) {
+  const int C = ctx->cfg.channels;
+  pa.add = ctx->p(ctx->L.hp);
+  pa.add_ld = 2 * C;
+  pa.add_s = C;
+  pa.add_c0 = 0;
+  pa.add_f32 = 0;
+  pa.split = C / 2;
+  pa.base = ctx->p(ctx->L.base);
+}
+
+// Step 2: the second-step head on yhat^1 (the first C / 2 channels of
+// yhat_t), plus the first step's (mu, s) of the second half, for channels
+// C / 2 .. C.
+PriorArgs step2_args(const ncodec_ctx* ctx, int nxt, int decode) {
+  const int C = ctx->cfg.channels;
+  const Layout& L = ctx->L;
+  PriorArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  pa.wfrag = ctx->p(L.step2.w);
+  pa.wfrag_lo = ctx->is_int() ? ctx->p(L.step2.wlo) : nullptr;
+  pa.bias = ctx->p(L.step2.bias);
+  pa.K = C / 2;
+  pa.N = C;
+  pa.yhat_prev = ctx->p(L.yhat[nxt]);
+  pa.ld0 = C;
+  pa.yhat_new = ctx->p(L.yhat[nxt]);
+  pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
+  pa.scales = ctx->p<float>(L.c_scales);
+  pa.k_tab = ctx->is_int() ? ctx->p<uint8_t>(L.c_ktab) : nullptr;
+  pa.C = C;
+  pa.P = P16_of(ctx);
+  pa.decode = decode;
+  pa.c_off = C / 2;
+  pa.add = ctx->p(L.base);
+  pa.add_ld = C;
+  pa.add_s = C / 2;
+  pa.add_c0 = C / 2;
+  pa.add_f32 = ctx->is_int() ? 0 : 1;
+  return pa;
+}
+
 // Enqueues one encode on ctx->stream (or records it under capture).
 // after_prior (optional) runs once q and the scale indices are enqueued,
 // before the decoder part.
@@ -840,6 +993,12 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   a.Cdst = C;
   NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
 
+  double* const parts = ctx->p<double>(L.partials);
+  int np_z = 0;
+  if (c.hyperprior) {
+    NC_HIP(ctx, z_encode(ctx, d_q + (size_t)C * P16, parts, &np_z), "hyper-analysis");
+    NC_HIP(ctx, hyper_synth(ctx), "hyper-synthesis");
+  }
   PriorArgs pa;
   std::memset(&pa, 0, sizeof(pa));
   pa.wfrag = ctx->p(L.head.w);
@@ -849,7 +1008,7 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   pa.y = ctx->p(L.y);
   pa.q_out = d_q;
   pa.yhat_new = ctx->p(L.yhat[nxt]);
-  pa.partials = ctx->p<double>(L.partials);
+  pa.partials = parts + np_z;
   pa.sigma_tab = ctx->is_int() ? ctx->p<float>(L.sigma_tab) : nullptr;
   pa.k_out = d_k;
   pa.scales = ctx->p<float>(L.c_scales);
@@ -857,10 +1016,22 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   pa.C = C;
   pa.P = P16;
   pa.decode = 0;
+  if (c.hyperprior) step1_fields(ctx, pa);
   int np = 0;
   NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
+  if (c.hyperprior) {
+    PriorArgs p2 = step2_args(ctx, nxt, 0);
+    p2.y = ctx->p(L.y);
+    p2.q_out = d_q;
+    p2.k_out = d_k;
+    p2.partials = parts + np_z + np;
+    int np2 = 0;
+    NC_HIP(ctx, prior(ctx, p2, &np2), "second step");
+    np += np2;
+  }
   if (d_bits)
-    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(pa.partials, np, d_bits, ctx->stream); }), "bits reduce");
+    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(parts, np_z + np, d_bits, ctx->stream); }),
+           "bits reduce");
   if constexpr (!std::is_same<Hook, std::nullptr_t>::value) {
     st = after_prior();
     if (st) return st;
@@ -911,7 +1082,17 @@ ncodec_status enqueue_decode(ncodec_ctx* ctx, const int16_t* d_q, void* d_frame_
   pa.decode = 1;
   const void* context = nullptr;
   NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
+  if (c.hyperprior) {
+    NC_HIP(ctx, z_from_symbols(ctx, d_q + (size_t)C * P16), "zhat");
+    NC_HIP(ctx, hyper_synth(ctx), "hyper-synthesis");
+    step1_fields(ctx, pa);
+  }
   NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (decode)");
+  if (c.hyperprior) {
+    PriorArgs p2 = step2_args(ctx, nxt, 1);
+    p2.q_in = d_q;
+    NC_HIP(ctx, prior(ctx, p2, nullptr), "second step (decode)");
+  }
   return decode_tail(ctx, d_frame_out);
 }
 
@@ -1088,7 +1269,7 @@ ncodec_status ncodec_create(const ncodec_config* cfg, const float* host_weights,
 
   ncodec_ctx* ctx = new ncodec_ctx();
   ctx->cfg = *cfg;
-  if (cfg->qp_banks) ctx->host_w.assign(host_weights, host_weights + n_weights);
+  if (cfg->qp_banks || cfg->hyperprior) ctx->host_w.assign(host_weights, host_weights + n_weights);
   ctx->stream = (hipStream_t)hip_stream;
   ctx->ws = (char*)d_workspace;
   ctx->L = std::move(L);
@@ -1113,7 +1294,8 @@ ncodec_status ncodec_set_qp(ncodec_ctx* ctx, int32_t qp) {
 ncodec_status ncodec_set_rate(ncodec_ctx* ctx, double qp) {
   ncodec_status st = enter(ctx);
   if (st) return st;
-  if (!ctx->cfg.qp_banks) return fail(ctx, NCODEC_EINVAL, "the context has no vector banks (qp_banks = 0)");
+  if (!ctx->cfg.qp_banks && !ctx->cfg.hyperprior)
+    return fail(ctx, NCODEC_EINVAL, "the context has no rate banks (qp_banks = 0, hyperprior = 0)");
   if (!(qp >= 0.0 && qp <= kNumQp - 1)) return fail(ctx, NCODEC_EINVAL, "qp must be in [0, 63]");
   if (qp == ctx->qp) return NCODEC_OK;
   Image img;
@@ -1184,13 +1366,24 @@ ncodec_status ncodec_estimate_bits(ncodec_ctx* ctx, const int16_t* d_q, const vo
 
 size_t ncodec_stream_capacity(const ncodec_config* cfg) {
   if (!cfg_valid(cfg, nullptr)) return 0;
-  return stream_capacity((int64_t)(cfg->height / 16) * (cfg->width / 16) * cfg->channels);
+  const int64_t ny = (int64_t)(cfg->height / 16) * (cfg->width / 16) * cfg->channels;
+  if (!cfg->hyperprior) return stream_capacity(ny);
+  const int64_t nz = (int64_t)(cfg->height / 32) * (cfg->width / 32) * kCZ;
+  return stream_capacity(nz) + 2 * stream_capacity(ny / 2);
+}
+
+size_t ncodec_symbol_count(const ncodec_config* cfg) {
+  if (!cfg_valid(cfg, nullptr)) return 0;
+  const size_t ny = (size_t)(cfg->height / 16) * (cfg->width / 16) * cfg->channels;
+  return ny + (cfg->hyperprior ? (size_t)(cfg->height / 32) * (cfg->width / 32) * kCZ : 0);
 }
 
 ncodec_status ncodec_scale_indices(ncodec_ctx* ctx, uint8_t* d_k) {
   ncodec_status st = enter(ctx);
   if (st) return st;
   if (!d_k) return fail(ctx, NCODEC_EINVAL, "d_k is NULL");
+  if (ctx->cfg.hyperprior)
+    return fail(ctx, NCODEC_ESTATE, "scale indices depend on the frame's z and y^1 with the two-step entropy model");
   return enqueue_scales(ctx, d_k);
 }
 
@@ -1238,22 +1431,33 @@ ncodec_status ncodec_encode_frame_coded(ncodec_ctx* ctx, const void* d_frame, in
   if ((uintptr_t)d_frame % 16 || (d_q && (uintptr_t)d_q % 16)) return fail(ctx, NCODEC_EINVAL, "d_frame and d_q must be 16-byte aligned");
   if ((uintptr_t)d_stream % 4) return fail(ctx, NCODEC_EINVAL, "d_stream must be 4-byte aligned");
   const Layout& L = ctx->L;
-  if (capacity < stream_capacity(L.n_sym))
+  if (capacity < ncodec_stream_capacity(&ctx->cfg))
     return fail(ctx, NCODEC_EINVAL, "capacity below ncodec_stream_capacity()");
   const bool par = ctx->overlap;
   if (par && (st = ensure_aux(ctx))) return st;
   int16_t* q = d_q ? d_q : ctx->p<int16_t>(L.qtmp);
+  // one container: all symbols; two-step model: z, y^1, y^2 at fixed offsets
+  auto section = [&](hipStream_t s, const int16_t* sq, const uint8_t* sk, int64_t n, size_t off,
+                     uint64_t* nbytes) -> ncodec_status {
+    NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
+             return launch_rans_encode(sq, sk, n, rans_tab(ctx), ctx->p<uint16_t>(L.rscratch), kRansMaxWords,
+                                       ctx->p<uint32_t>(L.rlens), (uint8_t*)d_stream + off, nbytes, s);
+           }),
+           "rans encode");
+    return NCODEC_OK;
+  };
   // the coder: on the context's stream after the decoder, or (parallel coding)
   // on the second stream as soon as q and the scale indices exist, while the
   // decoder part of the encode runs (Fig. 6)
   auto coder = [&](hipStream_t s) -> ncodec_status {
-    NC_HIP(ctx, timed(ctx, "rans_enc", [&] {
-             return launch_rans_encode(q, ctx->p<uint8_t>(L.kmap), L.n_sym, rans_tab(ctx),
-                                       ctx->p<uint16_t>(L.rscratch), kRansMaxWords, ctx->p<uint32_t>(L.rlens),
-                                       (uint8_t*)d_stream, d_stream_bytes, s);
-           }),
-           "rans encode");
-    return NCODEC_OK;
+    const uint8_t* k = ctx->p<uint8_t>(L.kmap);
+    if (!ctx->cfg.hyperprior) return section(s, q, k, L.n_sym, 0, d_stream_bytes);
+    const int64_t nh = L.n_sym / 2;
+    const size_t c0 = stream_capacity(L.n_z), c1 = stream_capacity(nh);
+    ncodec_status s2 = section(s, q + L.n_sym, ctx->p<uint8_t>(L.zk), L.n_z, 0, d_stream_bytes);
+    if (!s2) s2 = section(s, q, k, nh, c0, d_stream_bytes + 1);
+    if (!s2) s2 = section(s, q + nh, k + nh, nh, c0 + c1, d_stream_bytes + 2);
+    return s2;
   };
   if (par) {
     st = enqueue_encode(ctx, d_frame, q, d_bits, ctx->p<uint8_t>(L.kmap), [&]() -> ncodec_status {
@@ -1303,20 +1507,60 @@ ncodec_status ncodec_decode_frame_coded(ncodec_ctx* ctx, const void* d_stream, s
   } else {
     NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
   }
-  // one prior pass: the scale indices for the coder and mu for yhat = q + mu
-  st = enqueue_scales(ctx, ctx->p<uint8_t>(L.kmap), ctx->p(L.mu));
-  if (st) return st;
-  NC_HIP(ctx, timed(ctx, "rans_dec", [&] {
-           return launch_rans_decode((const uint8_t*)d_stream, stream_bytes, ctx->p<uint8_t>(L.kmap), L.n_sym,
-                                     rans_tab(ctx), ctx->p<uint32_t>(L.rerrs), ctx->p<uint32_t>(L.rcount),
-                                     ctx->p<int16_t>(L.qtmp), d_status, ctx->stream);
-         }),
-         "rans decode");
-  NC_HIP(ctx, timed(ctx, "yhat", [&] {
-           return launch_yhat_from_q(ctx->p<int16_t>(L.qtmp), ctx->p(L.mu), ctx->p(L.yhat[1 - ctx->cur]), C, P16,
-                                     ctx->is_int(), ctx->stream);
-         }),
-         "yhat");
+  auto ad = [&](size_t off, size_t bytes, const uint8_t* k, int64_t n, int16_t* q, int32_t* status) -> hipError_t {
+    return timed(ctx, "rans_dec", [&] {
+      return launch_rans_decode((const uint8_t*)d_stream + off, bytes, k, n, rans_tab(ctx), ctx->p<uint32_t>(L.rerrs),
+                                ctx->p<uint32_t>(L.rcount), q, status, ctx->stream);
+    });
+  };
+  auto yhat = [&](const int16_t* q, int nch, int c_off) -> hipError_t {
+    return timed(ctx, "yhat", [&] {
+      return launch_yhat_from_q(q, ctx->p(L.mu), ctx->p(L.yhat[1 - ctx->cur]), nch, P16, ctx->is_int(), ctx->stream,
+                                C, c_off);
+    });
+  };
+  int16_t* const qt = ctx->p<int16_t>(L.qtmp);
+  uint8_t* const kt = ctx->p<uint8_t>(L.kmap);
+  if (!ctx->cfg.hyperprior) {
+    // one prior pass: the scale indices for the coder and mu for yhat = q + mu
+    st = enqueue_scales(ctx, kt, ctx->p(L.mu));
+    if (st) return st;
+    NC_HIP(ctx, ad(0, stream_bytes, kt, L.n_sym, qt, d_status), "rans decode");
+    NC_HIP(ctx, yhat(qt, C, 0), "yhat");
+  } else {
+    // z, then its hyper parameters and the first step's distribution, y^1,
+    // then the second step's distribution, y^2 (supplementary "Parallel Coding")
+    const int64_t nh = L.n_sym / 2;
+    const size_t c0 = stream_capacity(L.n_z), c1 = stream_capacity(nh);
+    if (stream_bytes < c0 + 2 * c1) return fail(ctx, NCODEC_EINVAL, "stream_bytes below ncodec_stream_capacity()");
+    const int nxt = 1 - ctx->cur;
+    NC_HIP(ctx, ad(0, c0, ctx->p<uint8_t>(L.zk), L.n_z, qt + L.n_sym, d_status), "rans decode (z)");
+    NC_HIP(ctx, z_from_symbols(ctx, qt + L.n_sym), "zhat");
+    NC_HIP(ctx, hyper_synth(ctx), "hyper-synthesis");
+    PriorArgs pa;
+    std::memset(&pa, 0, sizeof(pa));
+    pa.wfrag = ctx->p(L.head.w);
+    pa.wfrag_lo = ctx->is_int() ? ctx->p(L.head.wlo) : nullptr;
+    pa.bias = ctx->p(L.head.bias);
+    pa.yhat_prev = ctx->p(L.yhat[ctx->cur]);
+    pa.k_out = kt;
+    pa.mu_out = ctx->p(L.mu);
+    pa.scales = ctx->p<float>(L.c_scales);
+    pa.k_tab = ctx->is_int() ? ctx->p<uint8_t>(L.c_ktab) : nullptr;
+    pa.C = C;
+    pa.P = P16;
+    pa.decode = 2;
+    step1_fields(ctx, pa);
+    NC_HIP(ctx, prior(ctx, pa, nullptr), "prior (scale indices, step 1)");
+    NC_HIP(ctx, ad(c0, c1, kt, nh, qt, d_status ? d_status + 1 : nullptr), "rans decode (y^1)");
+    NC_HIP(ctx, yhat(qt, C / 2, 0), "yhat^1");
+    PriorArgs p2 = step2_args(ctx, nxt, 2);
+    p2.k_out = kt;
+    p2.mu_out = ctx->p(L.mu);
+    NC_HIP(ctx, prior(ctx, p2, nullptr), "prior (scale indices, step 2)");
+    NC_HIP(ctx, ad(c0 + c1, c1, kt + nh, nh, qt + nh, d_status ? d_status + 2 : nullptr), "rans decode (y^2)");
+    NC_HIP(ctx, yhat(qt + nh, C / 2, C / 2), "yhat^2");
+  }
   if (par) NC_HIP(ctx, hipStreamWaitEvent(ctx->stream, ctx->ev_join, 0), "join");
   st = decode_tail(ctx, d_frame_out);
   if (st) return st;
@@ -1355,14 +1599,18 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   if (!ctx) return 0;
   const ncodec_config& c = ctx->cfg;
   // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
-  if (decode) return 4 + c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks;
+  // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
+  const int hyper = c.hyperprior ? 3 : 0;
+  if (decode) return 4 + hyper + c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks;
   // feature extractor, embed, fuse, encoder blocks, downsample, prior, bit sum, upsample, fuse, decoder blocks
-  return 7 + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
+  return 7 + hyper + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
 }
 
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {
   ncodec_status st = enter(ctx);
   if (st) return st;
+  if (enable && ctx->cfg.hyperprior)
+    return fail(ctx, NCODEC_ESTATE, "graph replay is not supported with the two-step entropy model");
   ctx->use_graphs = enable != 0;
   return NCODEC_OK;
 }

@@ -46,6 +46,7 @@ enum Epi : int {
   EP_PRIOR = 3,      // rows (32 mu, 32 s) per pass: quantise y, write q, yhat, bit partials
   EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
   EP_SCALES = 5,     // same rows: only the scale index of every symbol (entropy decoding)
+  EP_ZQUANT = 6,     // 64 rows = the channels of z: q_z = round(z), zhat, rate partials
 };
 
 struct PwArgs {
@@ -72,6 +73,15 @@ struct PwArgs {
   uint8_t* k_out;          // planar scale indices of the entropy coder (nullable for EP_PRIOR)
   const float* scales;     // fp16 path: the NS coder scales sigma_j (fp32)
   const uint8_t* k_tab;    // int path: scale index for s_i + 32768
+  // two-step entropy model
+  int ld0;                 // LD_NHWC: row stride of src0 in elements (0: C0)
+  int c_off;               // prior epilogues: channel of the first row pair
+  const void* add;         // prior epilogues: (mu, s) added before use, NHWC; nullable
+  int add_ld, add_s, add_c0;  // its row stride, offset of s, channel subtracted
+  int add_f32;             // fp16 path: add is fp32 (else fp16); int path: int16
+  int split;               // prior epilogues: channels >= split write (mu, s) to base (0: none)
+  void* base;              // [P][2 (C - split)]: mu then s of those channels
+  const float* zsigma;     // EP_ZQUANT: scale of each z channel
 };
 
 struct BlockArgs {
@@ -108,6 +118,15 @@ struct PriorArgs {
   int C;
   int P;
   int decode;             // 0 encode, 1 decode (q given), 2 scale indices only
+  // two-step entropy model (PwArgs fields of the same names); a step-2 call
+  // has the second-step head as weights (K = C / 2, N = C) and yhat^1
+  // (stride ld0) as input
+  int K, N;               // 0: K = C, N = 2 C
+  int ld0, c_off;
+  const void* add;
+  int add_ld, add_s, add_c0, add_f32;
+  int split;
+  void* base;
 };
 
 // Entropy coder (container and stream geometry; the tables live in the
@@ -164,7 +183,11 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 // (f16)(q + mu) with fp32 mu, int path clip(512 q + mu_i) with int16 mu_i --
 // the same operations as the quantiser of the prior epilogue.
 hipError_t launch_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int C, int P, bool is_int,
-                              hipStream_t st);
+                              hipStream_t st, int ld = 0, int c_off = 0);
+// z quantiser and hyper latent (EP_ZQUANT) on the 1/16 latent y: z = W y' + b
+// (y' the 2 x 2 gather), q_z planar, zhat NHWC, one rate partial per tile
+hipError_t launch_zquant_f16(const PwArgs& a, hipStream_t st, int* n_partials);
+hipError_t launch_zquant_i16(const PwArgs& a, hipStream_t st, int* n_partials);
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);
 

@@ -41,7 +41,7 @@ template <int LOADER>
 __device__ __forceinline__ const char* pw_act_src(const PwArgs& a, int gp, int kc, int v) {
   const int k = 64 * kc + 8 * v;
   if constexpr (LOADER == LD_NHWC) {
-    if (k < a.C0) return (const char*)((const f16*)a.src0 + (size_t)gp * a.C0 + k);
+    if (k < a.C0) return (const char*)((const f16*)a.src0 + (size_t)gp * (a.ld0 ? a.ld0 : a.C0) + k);
     return (const char*)((const f16*)a.src1 + (size_t)gp * a.C1 + (k - a.C0));
   } else if constexpr (LOADER == LD_FRAME) {
     // unshuffle x8: k = 64 c + 8 i + j -> colour c = kc, frame row 8 py + i = 8 py + v, columns 8 px .. +7
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   }
   // prior head: a pass covers channels c0 .. c0+31 (rows 0-31 mu, 32-63 s);
   // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
-  const int c0 = n0 / 2;
+  const int c0 = a.c_off + n0 / 2;
   int16_t* qt = (int16_t*)st2;
   uint8_t* kt = (uint8_t*)(st2 + 8192);  // scale indices, [channel][pixel]
   float* sct = (float*)(st2 + 12288);    // the coder scales, for the scale-index search
@@ -220,29 +220,69 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { r[e] = o0[e]; r[4 + e] = o1[e]; }
     return r;
   };
+  // (mu, s) of 8 channels c .. c + 7 of pixel gp: the head's rows plus the
+  // addend of the two-step entropy model (hyper parameters, or the first
+  // step's (mu, s) for the second step)
+  auto prior_ms = [&](int px, int g8, int gp, float* mu, float* sg) __attribute__((always_inline)) {
+    const floatx16 m = parked(px, g8), sv = parked(px, 4 + g8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { mu[e] = m[e]; sg[e] = sv[e]; }
+    if (a.add && gp < a.P) {
+      const size_t at = (size_t)gp * a.add_ld + (c0 + 8 * g8 - a.add_c0);
+      if (a.add_f32) {
+        const float* am = (const float*)a.add + at;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { mu[e] += am[e]; sg[e] += am[a.add_s + e]; }
+      } else {
+        const half8 hm = *(const half8*)((const f16*)a.add + at), hs = *(const half8*)((const f16*)a.add + at + a.add_s);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { mu[e] += (float)hm[e]; sg[e] += (float)hs[e]; }
+      }
+    }
+  };
+  // channels >= split: (mu, s) go to the base buffer for the second step
+  const bool to_base = a.split && c0 >= a.split;
+  auto store_base = [&](int g8, int gp, const float* mu, const float* sg) __attribute__((always_inline)) {
+    if (gp >= a.P) return;
+    const int nb = a.Cdst - a.split;
+    float* b = (float*)a.base + (size_t)gp * 2 * nb + (c0 + 8 * g8 - a.split);
+    *(floatx4*)b = floatx4{mu[0], mu[1], mu[2], mu[3]};
+    *(floatx4*)(b + 4) = floatx4{mu[4], mu[5], mu[6], mu[7]};
+    *(floatx4*)(b + nb) = floatx4{sg[0], sg[1], sg[2], sg[3]};
+    *(floatx4*)(b + nb + 4) = floatx4{sg[4], sg[5], sg[6], sg[7]};
+  };
   if constexpr (EPI == EP_SCALES) {
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
-    const floatx16 sg = parked(px, 4 + g8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), sct);
-    // mu as fp32 (NHWC), for yhat = q + mu once the symbols are decoded
     const int gp = tile * 128 + px;
-    if (a.dst && gp < a.P) {
-      const floatx16 mu = parked(px, g8);
-      float* dm = (float*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8;
-      *(floatx4*)dm = floatx4{mu[0], mu[1], mu[2], mu[3]};
-      *(floatx4*)(dm + 4) = floatx4{mu[4], mu[5], mu[6], mu[7]};
+    float mu[8], sg[8];
+    prior_ms(px, g8, gp, mu, sg);
+    if (to_base) {
+      store_base(g8, gp, mu, sg);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = (uint8_t)coder_scale_index(softplus_sigma(sg[e]), sct);
+      // mu as fp32 (NHWC), for yhat = q + mu once the symbols are decoded
+      if (a.dst && gp < a.P) {
+        float* dm = (float*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8;
+        *(floatx4*)dm = floatx4{mu[0], mu[1], mu[2], mu[3]};
+        *(floatx4*)(dm + 4) = floatx4{mu[4], mu[5], mu[6], mu[7]};
+      }
     }
     lds_barrier();
-    store_k();
+    if (!to_base) store_k();
   } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
     // thread = (pixel px, 8 channels g8): mu and s from the park, y / q, yhat
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
     const int gp = tile * 128 + px;
     const int c = c0 + 8 * g8;
-    const floatx16 mu = parked(px, g8), sg = parked(px, 4 + g8);
+    float mu[8], sg[8];
+    prior_ms(px, g8, gp, mu, sg);
     double bsum = 0.0;
-    if constexpr (EPI == EP_PRIOR) {
+    if (to_base) {
+      store_base(g8, gp, mu, sg);
+      if constexpr (EPI == EP_PRIOR)
+        if (threadIdx.x == 0) a.partials[(size_t)tile * npass + n0 / NT] = 0.0;
+    } else if constexpr (EPI == EP_PRIOR) {
       if (a.k_out) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -297,6 +337,52 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       }
     }
 
+  } else if constexpr (EPI == EP_ZQUANT) {
+    // the 64 rows are the channels of z: q_z = round(z) (staged [channel][pixel]
+    // in stage buffer 2, 16 KiB), zhat = q_z (NHWC), rate under sigma_z[c]
+    static_assert(NT == 64, "z has 64 channels");
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    double bsum = 0.0;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int cz = 32 * half + 8 * g8;
+      const floatx16 zv = parked(px, 4 * half + g8);
+      half8 zh;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float q = rintf(zv[e]);
+        q = fminf(fmaxf(q, -32768.f), 32767.f);
+        qt[(cz + e) * 128 + px] = (int16_t)q;
+        zh[e] = (f16)q;
+        if (gp < a.P) bsum += (double)symbol_bits(q, a.zsigma[cz + e]);
+      }
+      if (gp < a.P) *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + cz) = zh;
+    }
+    __shared__ double redz[8];
+    bsum = wave_sum(bsum);
+    if ((threadIdx.x & 63) == 0) redz[threadIdx.x >> 6] = bsum;
+    lds_barrier();
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int ch = 32 * it + (threadIdx.x >> 4), k = threadIdx.x & 15;
+      const int p0 = tile * 128 + 8 * k;
+      const shortx8 v = *(const shortx8*)(qt + ch * 128 + 8 * k);
+      int16_t* dq = a.q_out + (size_t)ch * a.P + p0;
+      if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+        *(shortx8*)dq = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (p0 + e < a.P) dq[e] = v[e];
+      }
+    }
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) t += redz[w];
+      a.partials[tile] = t;
+    }
   } else if constexpr (EPI == EP_REC) {
     // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
     // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
@@ -826,6 +912,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
     NC_PW(LD_NHWC, EP_SCALES)
+    NC_PW(LD_DOWN, EP_ZQUANT)
   }
 #undef NC_PW
   return hipErrorInvalidValue;
@@ -875,11 +962,20 @@ hipError_t launch_prior_f16(const PriorArgs& pa, hipStream_t st, int* n_partials
   std::memset(&a, 0, sizeof(a));
   a.wfrag = pa.wfrag;
   a.bias = pa.bias;
-  a.K = pa.C;
-  a.N = 2 * pa.C;
+  a.K = pa.K ? pa.K : pa.C;
+  a.N = pa.N ? pa.N : 2 * pa.C;
+  a.ld0 = pa.ld0;
+  a.c_off = pa.c_off;
+  a.add = pa.add;
+  a.add_ld = pa.add_ld;
+  a.add_s = pa.add_s;
+  a.add_c0 = pa.add_c0;
+  a.add_f32 = pa.add_f32;
+  a.split = pa.split;
+  a.base = pa.base;
   a.P = pa.P;
   a.src0 = pa.yhat_prev;
-  a.C0 = pa.C;
+  a.C0 = a.K;
   a.dst = pa.decode == 2 ? pa.mu_out : pa.yhat_new;
   a.Cdst = pa.C;
   a.y = pa.y;
@@ -888,8 +984,14 @@ hipError_t launch_prior_f16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.partials = pa.partials;
   a.k_out = pa.k_out;
   a.scales = pa.scales;
-  if (n_partials) *n_partials = prior_partials_f16(pa.C, pa.P);
+  if (n_partials) *n_partials = ((pa.P + 127) / 128) * (a.N / 64);
   return pw_dispatch<64>(LD_NHWC, pa.decode == 2 ? EP_SCALES : pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
+}
+
+hipError_t launch_zquant_f16(const PwArgs& a, hipStream_t st, int* n_partials) {
+  if (a.N != 64 || a.K % 64) return hipErrorInvalidValue;
+  if (n_partials) *n_partials = (a.P + 127) / 128;
+  return pw_dispatch<64>(LD_DOWN, EP_ZQUANT, a, st);
 }
 
 }  // namespace nc

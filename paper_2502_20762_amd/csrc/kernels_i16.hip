@@ -51,7 +51,7 @@ template <int LOADER>
 __device__ __forceinline__ const char* pwi_act_src(const PwArgs& a, int gp, int kc, int v) {
   const int k = 64 * kc + 8 * v;
   if constexpr (LOADER == LD_NHWC) {
-    if (k < a.C0) return (const char*)((const int16_t*)a.src0 + (size_t)gp * a.C0 + k);
+    if (k < a.C0) return (const char*)((const int16_t*)a.src0 + (size_t)gp * (a.ld0 ? a.ld0 : a.C0) + k);
     return (const char*)((const int16_t*)a.src1 + (size_t)gp * a.C1 + (k - a.C0));
   } else if constexpr (LOADER == LD_FRAME) {
     const int py = gp / a.w8, px = gp - py * a.w8;
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   }
   // prior head: a pass covers channels c0 .. c0+31 (rows 0-31 mu_i, 32-63 s_i);
   // the tile's symbols are staged in stage buffer 2 as [channel][pixel]
-  const int c0 = n0 / 2;
+  const int c0 = a.c_off + n0 / 2;
   int16_t* qt = (int16_t*)st2;
   uint8_t* kt = (uint8_t*)(st2 + 8192);  // scale indices, [channel][pixel]
   // planar store of the staged scale indices (after a barrier)
@@ -242,24 +242,52 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     for (int e = 0; e < 4; ++e) { v[e] = o0[e]; v[4 + e] = o1[e]; }
   };
   constexpr int UNITS = 128 * (NT / 8);
+  // (mu_i, s_i) of 8 channels c .. c + 7 of pixel gp: the head's rows plus,
+  // saturating, the addend of the two-step entropy model (hyper parameters,
+  // or the first step's (mu_i, s_i) for the second step)
+  auto prior_ms = [&](int px, int g8, int gp, int* mu, int* sv) __attribute__((always_inline)) {
+    parked(px, g8, mu);
+    parked(px, 4 + g8, sv);
+    if (a.add && gp < a.P) {
+      const size_t at = (size_t)gp * a.add_ld + (c0 + 8 * g8 - a.add_c0);
+      const shortx8 hm = *(const shortx8*)((const int16_t*)a.add + at);
+      const shortx8 hs = *(const shortx8*)((const int16_t*)a.add + at + a.add_s);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { mu[e] = clip16(mu[e] + (int)hm[e]); sv[e] = clip16(sv[e] + (int)hs[e]); }
+    }
+  };
+  // channels >= split: (mu_i, s_i) go to the base buffer for the second step
+  const bool to_base = a.split && c0 >= a.split;
+  auto store_base = [&](int g8, int gp, const int* mu, const int* sv) __attribute__((always_inline)) {
+    if (gp >= a.P) return;
+    const int nb = a.Cdst - a.split;
+    int16_t* b = (int16_t*)a.base + (size_t)gp * 2 * nb + (c0 + 8 * g8 - a.split);
+    shortx8 m, v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { m[e] = (short)mu[e]; v[e] = (short)sv[e]; }
+    *(shortx8*)b = m;
+    *(shortx8*)(b + nb) = v;
+  };
   if constexpr (EPI == EP_SCALES) {
     const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
-    int sv[8];
-    parked(px, 4 + g8, sv);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = a.k_tab[sv[e] + 32768];
-    // mu_i (int16, NHWC), for yhat_i = clip(512 q + mu_i) once the symbols are decoded
     const int gp = tile * 128 + px;
-    if (a.dst && gp < a.P) {
-      int mu[8];
-      parked(px, g8, mu);
-      shortx8 m;
+    int mu[8], sv[8];
+    prior_ms(px, g8, gp, mu, sv);
+    if (to_base) {
+      store_base(g8, gp, mu, sv);
+    } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) m[e] = (short)mu[e];
-      *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = m;
+      for (int e = 0; e < 8; ++e) kt[(8 * g8 + e) * 128 + px] = a.k_tab[sv[e] + 32768];
+      // mu_i (int16, NHWC), for yhat_i = clip(512 q + mu_i) once the symbols are decoded
+      if (a.dst && gp < a.P) {
+        shortx8 m;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[e] = (short)mu[e];
+        *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c0 + 8 * g8) = m;
+      }
     }
     lds_barrier();
-    store_k();
+    if (!to_base) store_k();
   } else if constexpr (EPI == EP_PRIOR || EPI == EP_PRIOR_DEC) {
     // thread = (pixel px, 8 channels g8): q = RHE((y_i - mu_i) / 512),
     // yhat_i = clip(512 q + mu_i), sigma from the table at s_i
@@ -267,9 +295,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
     const int gp = tile * 128 + px;
     const int c = c0 + 8 * g8;
     int mu[8], sv[8];
-    parked(px, g8, mu);
-    parked(px, 4 + g8, sv);
-    if constexpr (EPI == EP_PRIOR) {
+    prior_ms(px, g8, gp, mu, sv);
+    if (to_base) {
+      store_base(g8, gp, mu, sv);
+      if constexpr (EPI == EP_PRIOR)
+        if (threadIdx.x == 0) a.partials[(size_t)tile * npass + n0 / NT] = 0.0;
+    } else if constexpr (EPI == EP_PRIOR) {
       double bsum = 0.0;
       shortx8 yv = {};
       if (gp < a.P) yv = *(const shortx8*)((const int16_t*)a.y + (size_t)gp * a.Cdst + c);
@@ -317,6 +348,53 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         for (int e = 0; e < 8; ++e) yh[e] = (short)clip16(512 * (int)qt[(8 * g8 + e) * 128 + px] + mu[e]);
         *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
+    }
+  } else if constexpr (EPI == EP_ZQUANT) {
+    // the 64 rows are the channels of z_i: q_z = RHE(z_i / 512) (staged
+    // [channel][pixel] in stage buffer 2, 16 KiB), zhat_i = clip(512 q_z)
+    // (NHWC), rate under sigma_z[c]
+    static_assert(NT == 64, "z has 64 channels");
+    const int px = threadIdx.x >> 2, g8 = threadIdx.x & 3;
+    const int gp = tile * 128 + px;
+    double bsum = 0.0;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int cz = 32 * half + 8 * g8;
+      int zv[8];
+      parked(px, 4 * half + g8, zv);
+      shortx8 zh;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int q = rhe_shift(zv[e], 9);
+        qt[(cz + e) * 128 + px] = (int16_t)q;
+        zh[e] = (short)clip16(512 * q);
+        if (gp < a.P) bsum += (double)symbol_bits((float)q, a.zsigma[cz + e]);
+      }
+      if (gp < a.P) *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + cz) = zh;
+    }
+    __shared__ double redz[8];
+    bsum = wave_sum(bsum);
+    if ((threadIdx.x & 63) == 0) redz[threadIdx.x >> 6] = bsum;
+    lds_barrier();
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int ch = 32 * it + (threadIdx.x >> 4), k = threadIdx.x & 15;
+      const int p0 = tile * 128 + 8 * k;
+      const shortx8 v = *(const shortx8*)(qt + ch * 128 + 8 * k);
+      int16_t* dq = a.q_out + (size_t)ch * a.P + p0;
+      if ((a.P & 7) == 0 && p0 + 8 <= a.P) {
+        *(shortx8*)dq = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (p0 + e < a.P) dq[e] = v[e];
+      }
+    }
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) t += redz[w];
+      a.partials[tile] = t;
     }
   } else if constexpr (EPI == EP_REC) {
 #pragma unroll
@@ -872,6 +950,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
     NC_PW(LD_NHWC, EP_SCALES)
+    NC_PW(LD_DOWN, EP_ZQUANT)
   }
 #undef NC_PW
   return hipErrorInvalidValue;
@@ -919,11 +998,19 @@ hipError_t launch_prior_i16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.wfrag = pa.wfrag;
   a.wfrag_lo = pa.wfrag_lo;
   a.bias = pa.bias;
-  a.K = pa.C;
-  a.N = 2 * pa.C;
+  a.K = pa.K ? pa.K : pa.C;
+  a.N = pa.N ? pa.N : 2 * pa.C;
+  a.ld0 = pa.ld0;
+  a.c_off = pa.c_off;
+  a.add = pa.add;
+  a.add_ld = pa.add_ld;
+  a.add_s = pa.add_s;
+  a.add_c0 = pa.add_c0;
+  a.split = pa.split;
+  a.base = pa.base;
   a.P = pa.P;
   a.src0 = pa.yhat_prev;
-  a.C0 = pa.C;
+  a.C0 = a.K;
   a.dst = pa.decode == 2 ? pa.mu_out : pa.yhat_new;
   a.Cdst = pa.C;
   a.y = pa.y;
@@ -933,8 +1020,14 @@ hipError_t launch_prior_i16(const PriorArgs& pa, hipStream_t st, int* n_partials
   a.sigma_tab = pa.sigma_tab;
   a.k_out = pa.k_out;
   a.k_tab = pa.k_tab;
-  if (n_partials) *n_partials = prior_partials_i16(pa.C, pa.P);
+  if (n_partials) *n_partials = ((pa.P + 127) / 128) * (a.N / 64);
   return pw_dispatch<64>(LD_NHWC, pa.decode == 2 ? EP_SCALES : pa.decode ? EP_PRIOR_DEC : EP_PRIOR, a, st);
+}
+
+hipError_t launch_zquant_i16(const PwArgs& a, hipStream_t st, int* n_partials) {
+  if (a.N != 64 || a.K % 64) return hipErrorInvalidValue;
+  if (n_partials) *n_partials = (a.P + 127) / 128;
+  return pw_dispatch<64>(LD_DOWN, EP_ZQUANT, a, st);
 }
 
 }  // namespace nc

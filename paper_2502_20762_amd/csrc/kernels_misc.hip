@@ -68,8 +68,11 @@ __global__ void k_planar_to_nhwc(const uint16_t* src, uint16_t* dst, int C, int 
 // One workgroup per (64-pixel, 32-channel) tile: the planar symbols of the
 // tile are staged through LDS (coalesced row reads), then each thread forms
 // 8 consecutive channels of one pixel and stores them as one 16-byte vector.
+// Channels c < C of q (planar, C x P) go to channel c_off + c of mu and yhat
+// (NHWC, row stride ld); a NULL mu is zero.
 template <bool IS_INT>
-__global__ __launch_bounds__(256) void k_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int C, int P) {
+__global__ __launch_bounds__(256) void k_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int C, int P, int ld,
+                                                     int c_off) {
   __shared__ int16_t qs[32][64 + 2];
   const int ntp = (P + 63) / 64;
   const int tp = blockIdx.x % ntp, tc = blockIdx.x / ntp;
@@ -82,15 +85,20 @@ __global__ __launch_bounds__(256) void k_yhat_from_q(const int16_t* q, const voi
   const int pp = threadIdx.x >> 2, g8 = threadIdx.x & 3;
   const int gp = p0 + pp;
   if (gp >= P) return;
-  const size_t off = (size_t)gp * C + c0 + 8 * g8;
+  const size_t off = (size_t)gp * ld + c_off + c0 + 8 * g8;
   if constexpr (IS_INT) {
-    const shortx8 m = *(const shortx8*)((const int16_t*)mu + off);
+    shortx8 m = {};
+    if (mu) m = *(const shortx8*)((const int16_t*)mu + off);
     shortx8 o;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = (short)clip16(512 * (int)qs[8 * g8 + e][pp] + (int)m[e]);
     *(shortx8*)((int16_t*)yhat + off) = o;
   } else {
-    const floatx4 m0 = *(const floatx4*)((const float*)mu + off), m1 = *(const floatx4*)((const float*)mu + off + 4);
+    floatx4 m0 = {}, m1 = {};
+    if (mu) {
+      m0 = *(const floatx4*)((const float*)mu + off);
+      m1 = *(const floatx4*)((const float*)mu + off + 4);
+    }
     half8 o;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = (f16)((float)qs[8 * g8 + e][pp] + (e < 4 ? m0[e] : m1[e - 4]));
@@ -99,11 +107,12 @@ __global__ __launch_bounds__(256) void k_yhat_from_q(const int16_t* q, const voi
 }
 
 hipError_t launch_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int C, int P, bool is_int,
-                              hipStream_t st) {
-  if (C % 32) return hipErrorInvalidValue;
+                              hipStream_t st, int ld, int c_off) {
+  if (C % 32 || c_off % 8) return hipErrorInvalidValue;
+  if (!ld) ld = C;
   const dim3 grid(((P + 63) / 64) * (C / 32));
-  if (is_int) launch(k_yhat_from_q<true>, grid, dim3(256), st, q, mu, yhat, C, P);
-  else launch(k_yhat_from_q<false>, grid, dim3(256), st, q, mu, yhat, C, P);
+  if (is_int) launch(k_yhat_from_q<true>, grid, dim3(256), st, q, mu, yhat, C, P, ld, c_off);
+  else launch(k_yhat_from_q<false>, grid, dim3(256), st, q, mu, yhat, C, P, ld, c_off);
   return hipGetLastError();
 }
 

@@ -43,6 +43,7 @@ class ncodec_config(ctypes.Structure):
         ("n_fe_blocks", ctypes.c_int32),
         ("n_rg_blocks", ctypes.c_int32),
         ("qp_banks", ctypes.c_int32),
+        ("hyperprior", ctypes.c_int32),
     ]
 
 
@@ -60,6 +61,7 @@ _P = ctypes.c_void_p
 _SIGNATURES = {
     "ncodec_weight_count": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
     "ncodec_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
+    "ncodec_symbol_count": (ctypes.c_size_t, [ctypes.POINTER(ncodec_config)]),
     "ncodec_create": (ctypes.c_int, [ctypes.POINTER(ncodec_config), _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P,
                                      ctypes.POINTER(_P)]),
     "ncodec_reset": (ctypes.c_int, [_P]),
@@ -108,13 +110,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
 
 
 def make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block="lrelu", n_fe_blocks=0,
-                n_rg_blocks=0, qp_banks=False) -> ncodec_config:
+                n_rg_blocks=0, qp_banks=False, hyperprior=False) -> ncodec_config:
     if isinstance(path, str):
         path = PATHS[path]
     if isinstance(block, str):
         block = BLOCKS[block]
     return ncodec_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block, n_fe_blocks,
-                         n_rg_blocks, int(bool(qp_banks)))
+                         n_rg_blocks, int(bool(qp_banks)), int(bool(hyperprior)))
 
 
 def _p(v: int):
@@ -135,6 +137,10 @@ def ncodec_weight_count(cfg: ncodec_config) -> int:
 
 def ncodec_workspace_bytes(cfg: ncodec_config) -> int:
     return int(load_library().ncodec_workspace_bytes(ctypes.byref(cfg)))
+
+
+def ncodec_symbol_count(cfg: ncodec_config) -> int:
+    return int(load_library().ncodec_symbol_count(ctypes.byref(cfg)))
 
 
 def ncodec_create(cfg: ncodec_config, host_weights: np.ndarray, d_workspace: int, ws_bytes: int,
@@ -261,12 +267,14 @@ class Codec:
     """
 
     def __init__(self, height, width, channels, n_enc_blocks, n_dec_blocks, path, weights,
-                 device="cuda:0", stream=None, block="lrelu", n_fe_blocks=0, n_rg_blocks=0, qp_banks=False):
+                 device="cuda:0", stream=None, block="lrelu", n_fe_blocks=0, n_rg_blocks=0, qp_banks=False,
+                 hyperprior=False):
         import torch
 
         self.torch = torch
         self.cfg = make_config(height, width, channels, n_enc_blocks, n_dec_blocks, path, block, n_fe_blocks,
-                               n_rg_blocks, qp_banks)
+                               n_rg_blocks, qp_banks, hyperprior)
+        self.hyperprior = bool(hyperprior)
         self.device = torch.device(device)
         self.path = self.cfg.path
         nbytes = ncodec_workspace_bytes(self.cfg)
@@ -278,7 +286,11 @@ class Codec:
             self.ctx = ncodec_create(self.cfg, weights, self.workspace.data_ptr(), nbytes, self.stream.cuda_stream)
         H, W, C = height, width, channels
         self.frame_shape = (3, H, W)
-        self.q_shape = (C, H // 16, W // 16)
+        # the frame's symbols: y (C x H/16 x W/16), then, with the two-step
+        # entropy model, z (64 x H/32 x W/32), as one flat array
+        self.y_shape = (C, H // 16, W // 16)
+        self.z_shape = (64, H // 32, W // 32)
+        self.q_shape = (ncodec_symbol_count(self.cfg),) if self.hyperprior else self.y_shape
         self.feat_shape = (C, H // 8, W // 8)
         self.state_dtype = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float16
 
@@ -347,7 +359,7 @@ class Codec:
         torch = self.torch
         assert frame.dtype == torch.float16 and tuple(frame.shape) == self.frame_shape and frame.is_contiguous()
         buf = stream if stream is not None else self._empty((self.stream_capacity(),), torch.uint8)
-        nb = nbytes_out if nbytes_out is not None else self._empty((), torch.int64)
+        nb = nbytes_out if nbytes_out is not None else self._empty((3,) if self.hyperprior else (), torch.int64)
         ncodec_encode_frame_coded(self.ctx, frame.data_ptr(), q_out.data_ptr() if q_out is not None else 0,
                                   bits_out.data_ptr() if bits_out is not None else 0, buf.data_ptr(), buf.numel(),
                                   nb.data_ptr())
@@ -357,13 +369,13 @@ class Codec:
         torch = self.torch
         odt = torch.int16 if self.path == NCODEC_PATH_INT16 else torch.float16
         x = out if out is not None else self._empty(self.frame_shape, odt)
-        st = status_out if status_out is not None else self._empty((), torch.int32)
+        st = status_out if status_out is not None else self._empty((3,) if self.hyperprior else (), torch.int32)
         ncodec_decode_frame_coded(self.ctx, stream.data_ptr(), int(nbytes), x.data_ptr(), st.data_ptr())
         return x, st
 
     def get_state(self):
         feat = self._empty(self.feat_shape, self.state_dtype)
-        yhat = self._empty(self.q_shape, self.state_dtype)
+        yhat = self._empty(self.y_shape, self.state_dtype)
         ncodec_get_state(self.ctx, feat.data_ptr(), yhat.data_ptr())
         return feat, yhat
 
