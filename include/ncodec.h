@@ -329,9 +329,10 @@ ncodec_status ncodec_parallel_coding(ncodec_ctx* ctx, int32_t enable);
 ncodec_status ncodec_get_state(ncodec_ctx* ctx, void* d_feat, void* d_yhat);
 ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* d_yhat);
 
-/* Kernel launches one ncodec_encode_frame (decode = 0, with a non-NULL
- * d_bits; one fewer without) or ncodec_decode_frame (decode = 1) enqueues
- * (three more each with the two-step model),
+/* Kernel launches one ncodec_encode_frame (decode = 0; one workgroup of the
+ * upsample that follows the prior sums the frame's bit total, so d_bits does
+ * not change the count) or ncodec_decode_frame (decode = 1) enqueues (three more each with
+ * the two-step model),
  * counting the feature-extractor and reconstruction-generation blocks
  * (Sec. 3: the number of modules called per frame is one of the costs the
  * design minimises).  0 for a NULL ctx. */

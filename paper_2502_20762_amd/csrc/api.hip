@@ -823,7 +823,9 @@ hipError_t temporal_context(ncodec_ctx* ctx, const void** out) {
 }
 
 // Runs the decoder-side transform from yhat_new (already written) into feat[nxt].
-ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
+// In an encode with d_bits, the upsample also sums the frame's n_parts rate
+// partials into d_bits.
+ncodec_status run_decoder(ncodec_ctx* ctx, int nxt, double* d_bits = nullptr, int n_parts = 0) {
   const ncodec_config& c = ctx->cfg;
   const int C = c.channels;
   const int h8 = c.height / 8, w8 = c.width / 8;
@@ -837,6 +839,9 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
   a.C0 = C;
   a.dst = ctx->p(L.ed);
   a.Cdst = C;
+  a.bits_out = d_bits;
+  a.sum_base = ctx->p<double>(L.partials);
+  a.n_sum = n_parts;
   NC_HIP(ctx, pw(ctx, "up", LD_NHWC, EP_UP, a), "upsample");
 
   void* z = c.n_dec_blocks == 0 ? f_new : ctx->p(L.zA);
@@ -861,6 +866,9 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt) {
 // ---- two-step entropy model with the hyper latent z (Sec. 4.4; supplementary
 // "Entropy model", "Parallel Coding")
 int P16_of(const ncodec_ctx* ctx) { return (ctx->cfg.height / 16) * (ctx->cfg.width / 16); }
+// rate partials of a prior launch over P latent pixels with N head rows: one
+// per (128-pixel tile, 64-row pass)
+int prior_parts(int P, int N) { return ((P + 127) / 128) * (N / 64); }
 int P32_of(const ncodec_ctx* ctx) { return (ctx->cfg.height / 32) * (ctx->cfg.width / 32); }
 
 // z = conv2x2/s2(y), quantised: symbols to qz (planar), zhat (NHWC), one rate
@@ -1017,27 +1025,25 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   pa.P = P16;
   pa.decode = 0;
   if (c.hyperprior) step1_fields(ctx, pa);
-  int np = 0;
-  NC_HIP(ctx, prior(ctx, pa, &np), "prior/quantise");
+  NC_HIP(ctx, prior(ctx, pa, nullptr), "prior/quantise");
+  // every rate partial of the frame: z's, then the one or two prior launches'
+  int n_parts = np_z + prior_parts(P16, 2 * C);
   if (c.hyperprior) {
     PriorArgs p2 = step2_args(ctx, nxt, 0);
     p2.y = ctx->p(L.y);
     p2.q_out = d_q;
     p2.k_out = d_k;
-    p2.partials = parts + np_z + np;
-    int np2 = 0;
-    NC_HIP(ctx, prior(ctx, p2, &np2), "second step");
-    np += np2;
+    p2.partials = parts + n_parts;
+    n_parts += prior_parts(P16, C);
+    NC_HIP(ctx, prior(ctx, p2, nullptr), "second step");
   }
-  if (d_bits)
-    NC_HIP(ctx, timed(ctx, "reduce", [&] { return launch_reduce(parts, np_z + np, d_bits, ctx->stream); }),
-           "bits reduce");
   if constexpr (!std::is_same<Hook, std::nullptr_t>::value) {
     st = after_prior();
     if (st) return st;
   }
 
-  st = run_decoder(ctx, nxt);
+  // the decoder part; its upsample adds up the partials into d_bits
+  st = run_decoder(ctx, nxt, d_bits, n_parts);
   return st;
 }
 
@@ -1142,19 +1148,6 @@ hipError_t set_struct_arg(hipGraphExec_t x, hipGraphNode_t n, F&& edit) {
   return hipGraphExecKernelNodeSetParams(x, n, &p);
 }
 
-hipError_t set_reduce_out(hipGraphExec_t x, hipGraphNode_t n, double* out) {
-  hipKernelNodeParams p;
-  hipError_t e = hipGraphKernelNodeGetParams(n, &p);
-  if (e != hipSuccess) return e;
-  if (!p.kernelParams) return hipErrorInvalidValue;
-  const double* part = *(const double* const*)p.kernelParams[0];
-  int np = *(const int*)p.kernelParams[1];
-  void* args[3] = {&part, &np, &out};
-  p.kernelParams = args;
-  p.extra = nullptr;
-  return hipGraphExecKernelNodeSetParams(x, n, &p);
-}
-
 // Points the caller-buffer nodes of a captured graph at this call's buffers:
 // encode ptr = {frame, q, bits}, decode ptr = {q, frame_out}.
 hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, const void* const* ptr) {
@@ -1165,9 +1158,15 @@ hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, con
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.src0 = ptr[0]; });
     } else if (!std::strcmp(cn.kind, "prior") && ptr[decode ? 0 : 1] != gs.ptr[decode ? 0 : 1]) {
       int16_t* q = (int16_t*)ptr[decode ? 0 : 1];
-      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (decode) v.q_in = q; else v.q_out = q; });
-    } else if (!decode && !std::strcmp(cn.kind, "reduce") && ptr[2] != gs.ptr[2]) {
-      e = set_reduce_out(gs.exec, cn.node, (double*)ptr[2]);
+      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) {
+        if (decode) {
+          v.q_in = q;
+        } else {
+          v.q_out = q;
+        }
+      });
+    } else if (!decode && !std::strcmp(cn.kind, "up") && ptr[2] != gs.ptr[2]) {
+      e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (v.bits_out) v.bits_out = (double*)ptr[2]; });
     } else if (decode && !std::strcmp(cn.kind, "recon") && ptr[1] != gs.ptr[1]) {
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.dst = (void*)ptr[1]; });
     }
@@ -1602,8 +1601,9 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
   const int hyper = c.hyperprior ? 3 : 0;
   if (decode) return 4 + hyper + c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks;
-  // feature extractor, embed, fuse, encoder blocks, downsample, prior, bit sum, upsample, fuse, decoder blocks
-  return 7 + hyper + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
+  // feature extractor, embed, fuse, encoder blocks, downsample, prior, upsample (with the bit total), fuse,
+  // decoder blocks
+  return 6 + hyper + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
 }
 
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {

@@ -198,4 +198,24 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// The frame's rate total, summed by one workgroup of the launch that follows
+// the last rate partials on the stream (the launch boundary makes them
+// visible): thread t adds elements t, t + blockDim, ... of part[0, n), then
+// the waves are added in order, so the sum has a fixed order.  Called
+// uniformly by every thread of that workgroup.
+__device__ __forceinline__ void block_sum_to(const double* part, int n, double* out) {
+  __shared__ double red[16];
+  double v = 0.0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) v += part[i];
+  v = wave_sum(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w];
+    *out = t;
+  }
+  __syncthreads();
+}
+
 }  // namespace nc

@@ -82,6 +82,11 @@ struct PwArgs {
   int split;               // prior epilogues: channels >= split write (mu, s) to base (0: none)
   void* base;              // [P][2 (C - split)]: mu then s of those channels
   const float* zsigma;     // EP_ZQUANT: scale of each z channel
+  // EP_UP: workgroup 0 first sums sum_base[0, n_sum) (the rate partials of
+  // the frame, written by the launches before) into *bits_out; NULL: no total
+  double* bits_out;
+  const double* sum_base;
+  int n_sum;
 };
 
 struct BlockArgs {

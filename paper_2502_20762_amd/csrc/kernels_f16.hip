@@ -113,6 +113,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int tile = lin / npass;
   if (tile >= ntile) return;
+  // the upsample that follows the prior in an encode: workgroup 0 first adds
+  // up the frame's rate partials
+  if constexpr (EPI == EP_UP)
+    if (a.bits_out && blockIdx.x == 0) block_sum_to(a.sum_base, a.n_sum, a.bits_out);
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pg = wave & 3, hf = wave >> 2;
@@ -148,18 +152,19 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   }
   lds_barrier();  // every wave is done reading the stages
 
-  // park acc + bias as fp32: pixel group pg in stage buffer pg, row = pixel,
-  // NT floats per row, 16-byte chunk c of a row at c ^ (row & SWZ)
+  // park acc + bias as fp32, one row of NT floats per tile pixel, 16-byte
+  // chunk c of the row of pixel px at c ^ (px & SWZ); the 128 rows fill the
+  // stage buffers in order, RPB rows per buffer
   constexpr int SWZ = (NT / 4 - 1) & 31;
-  // pixel group g parks at offset (g % GPS) * PARK of stage g / GPS
-  constexpr int PARK = 32 * NT * 4, GPS = S::STAGE / PARK;
-  static_assert(GPS >= 2, "four pixel groups fit three stage buffers");
-  auto park = [&](int g) __attribute__((always_inline)) -> char* {
-    return (g / GPS == 0 ? st0 : g / GPS == 1 ? st1 : st2) + (g % GPS) * PARK;
+  constexpr int ROW = NT * 4, RPB = S::STAGE / ROW;
+  static_assert(3 * RPB >= 128, "the tile's rows fit three stage buffers");
+  auto park_row = [&](int px) __attribute__((always_inline)) -> char* {
+    const int b = px / RPB, r = px - b * RPB;
+    return (b == 0 ? st0 : b == 1 ? st1 : st2) + r * ROW;
   };
   {
-    char* ob = park(pg);
     const int row = lane & 31;
+    char* ob = park_row(32 * pg + row);
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
@@ -168,7 +173,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         floatx4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = acc[t][4 * g + e] + bias[t][g][e];
-        *(floatx4*)(ob + row * (NT * 4) + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
+        *(floatx4*)(ob + (((nl >> 2) ^ (row & SWZ)) << 4)) = o;
       }
   }
   // prior head: a pass covers channels c0 .. c0+31 (rows 0-31 mu, 32-63 s);
@@ -211,10 +216,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   lds_barrier();
 
   auto parked = [&](int px, int nl8) {  // 8 floats: pass rows nl8 * 8 .. +7 of tile pixel px
-    const int gpx = px >> 5, row = px & 31;
-    const char* ob = park(gpx);
-    const floatx4 o0 = *(const floatx4*)(ob + row * (NT * 4) + (((2 * nl8) ^ (row & SWZ)) << 4));
-    const floatx4 o1 = *(const floatx4*)(ob + row * (NT * 4) + (((2 * nl8 + 1) ^ (row & SWZ)) << 4));
+    const int row = px & 31;
+    const char* ob = park_row(px);
+    const floatx4 o0 = *(const floatx4*)(ob + (((2 * nl8) ^ (row & SWZ)) << 4));
+    const floatx4 o1 = *(const floatx4*)(ob + (((2 * nl8 + 1) ^ (row & SWZ)) << 4));
     floatx16 r;  // only [0, 8) used
 #pragma unroll
     for (int e = 0; e < 4; ++e) { r[e] = o0[e]; r[4 + e] = o1[e]; }
@@ -336,7 +341,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       }
     }
-
   } else if constexpr (EPI == EP_ZQUANT) {
     // the 64 rows are the channels of z: q_z = round(z) (staged [channel][pixel]
     // in stage buffer 2, 16 KiB), zhat = q_z (NHWC), rate under sigma_z[c]
@@ -905,9 +909,11 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   }
   NC_PW(LD_NHWC, EP_NHWC)
   NC_PW(LD_FRAME, EP_NHWC)
-  NC_PW(LD_DOWN, EP_NHWC)
-  NC_PW(LD_NHWC, EP_UP)
-  NC_PW(LD_NHWC, EP_REC)
+  if constexpr (NT != 256) {
+    NC_PW(LD_DOWN, EP_NHWC)
+    NC_PW(LD_NHWC, EP_UP)
+    NC_PW(LD_NHWC, EP_REC)
+  }
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
@@ -923,11 +929,15 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
 // 128, 256; 192 for the patch embed) and N a multiple of 64.
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   if (a.K % 64 || a.N % 64) return hipErrorInvalidValue;
-  // 128 rows per pass for the patch embed and the 2C -> C fuse: their activation
-  // tiles are the widest (K = 192 frame values or 2C channels), so halving the
-  // passes that re-stage them pays, and they still have two passes per tile.
-  if (a.N % 128 == 0 && epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512)))
-    return pw_dispatch<128>(loader, epi, a, st);
+  // The patch embed and the 2C -> C fuse have the widest activation tiles (K =
+  // 192 frame values or 2C channels) at 1/8 scale (one tile per CU or more):
+  // all N rows in one pass (N = 256: 48 KiB stages, one workgroup per CU) or
+  // 128 rows per pass, so each tile is staged once or twice.  The 1/16-scale
+  // kernels have 4x fewer tiles and keep 64-row passes to fill the CUs.
+  if (epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512))) {
+    if (a.N == 256) return pw_dispatch<256>(loader, epi, a, st);
+    if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
+  }
   return pw_dispatch<64>(loader, epi, a, st);
 }
 

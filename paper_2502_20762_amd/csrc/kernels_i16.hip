@@ -141,6 +141,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int tile = lin / npass;
   if (tile >= ntile) return;
+  // the upsample that follows the prior in an encode: workgroup 0 first adds
+  // up the frame's rate partials
+  if constexpr (EPI == EP_UP)
+    if (a.bits_out && blockIdx.x == 0) block_sum_to(a.sum_base, a.n_sum, a.bits_out);
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pg = wave & 3, hf = wave >> 2;

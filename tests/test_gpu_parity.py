@@ -226,7 +226,7 @@ def test_kernels_per_frame_counts_launches(path):
     nd_l = sum(n for n, _ in dec.timing_read().values())
     enc.timing(False)
     dec.timing(False)
-    assert enc.kernels_per_frame(False) == ne_l == 7 + nfe + ne + nd
+    assert enc.kernels_per_frame(False) == ne_l == 6 + nfe + ne + nd
     assert dec.kernels_per_frame(True) == nd_l == 4 + nfe + nd + nrg
 
 
