@@ -361,6 +361,9 @@ SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r, block, two-step entropy model)
     ("1080p, all modules: feature extractor, reconstruction generation, qp banks, two-step entropy model",
      1088, 1920, 256, 8, 8, 2, 2, "lrelu", True),
     ("4K", 2176, 3840, 256, 8, 8, 0, 0, "lrelu", False),
+    ("1080p C=384 (wide blocks)", 1088, 1920, 384, 8, 8, 0, 0, "lrelu", False),
+    ("1080p C=512 (wide blocks, a Large model's width)", 1088, 1920, 512, 8, 8, 0, 0, "lrelu", False),
+    ("1080p C=512 16+16 blocks (a Large model's width and depth)", 1088, 1920, 512, 16, 16, 0, 0, "lrelu", False),
 ]
 
 
@@ -399,6 +402,9 @@ def sweep(paths, steps, warmup, torch, Codec, match=""):
             t = enc.timing_read()
             enc.timing(False)
             n, ms = t.get("dcblock", (0, 0.0))
+            if not n and "dcblock_dw" in t:  # a wide block (C > 256) is three launches
+                n = t["dcblock_dw"][0]
+                ms = sum(v[1] for k, v in t.items() if k.startswith("dcblock_"))
             peak, scale = (MFMA_F16_PEAK_TFLOPS, 1) if path == "fp16" else (MFMA_I8_PEAK_TOPS, 4)
             frac = scale * kinds["dcblock"][0] / (ms * 1e-3 / n) / 1e12 / peak if n else None
             t_roof = roofline_seconds(kinds, enc_list + dec_list, peak * 1e12 / scale)

@@ -76,7 +76,11 @@ typedef enum { NCODEC_BLOCK_LRELU = 0, NCODEC_BLOCK_GATED = 1 } ncodec_block;
 typedef struct {
   int32_t height;        /* H, multiple of 16, 16..8192 (caller pads 1080 -> 1088) */
   int32_t width;         /* W, multiple of 16, 16..8192                             */
-  int32_t channels;      /* C in {64, 128, 256}                                     */
+  int32_t channels;      /* C in {64, 128, 256, 384, 512}; above 256 (the widths of
+                            a Large model, Supp. "Performance for a Large Model")
+                            each DC block runs as three launches (depthwise, pw
+                            C -> 2C + LeakyReLU, pw 2C -> C + residual) and only
+                            the LRELU block form is accepted                        */
   int32_t n_enc_blocks;  /* N_e, 0..32                                              */
   int32_t n_dec_blocks;  /* N_d, 0..32                                              */
   int32_t path;          /* ncodec_path                                             */
@@ -90,7 +94,7 @@ typedef struct {
                             ncodec_set_qp; 0: none                                  */
   int32_t hyperprior;    /* 1: the two-step entropy model with the hyper latent z
                             (Sec. 4.4; supplementary "Entropy model"), see below;
-                            needs C in {128, 256} and H, W multiples of 32.
+                            needs C >= 128 and H, W multiples of 32.
                             0: the one-step prior on yhat_{t-1}                     */
 } ncodec_config;
 

@@ -43,8 +43,8 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "height and width must be multiples of 16 in [16, 8192]";
     return false;
   }
-  if (c->channels != 64 && c->channels != 128 && c->channels != 256) {
-    if (why) *why = "channels must be 64, 128 or 256";
+  if (c->channels != 64 && c->channels != 128 && c->channels != 256 && c->channels != 384 && c->channels != 512) {
+    if (why) *why = "channels must be 64, 128, 256, 384 or 512";
     return false;
   }
   if (c->n_enc_blocks < 0 || c->n_enc_blocks > 32 || c->n_dec_blocks < 0 || c->n_dec_blocks > 32) {
@@ -67,12 +67,16 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "qp_banks must be 0 or 1";
     return false;
   }
+  if (c->channels > 256 && c->block == NCODEC_BLOCK_GATED) {
+    if (why) *why = "the gated block form supports C <= 256";
+    return false;
+  }
   if (c->hyperprior != 0 && c->hyperprior != 1) {
     if (why) *why = "hyperprior must be 0 or 1";
     return false;
   }
   if (c->hyperprior && (c->channels < 128 || c->height % 32 || c->width % 32)) {
-    if (why) *why = "the two-step entropy model needs C in {128, 256} and H, W multiples of 32";
+    if (why) *why = "the two-step entropy model needs C >= 128 and H, W multiples of 32";
     return false;
   }
   return true;
@@ -239,6 +243,12 @@ struct Packer {
         o[22] = o[23] = 0;
       }
     }
+    if (C > 256) {
+      // wide block (three launches): the pointwise convs as plain GEMM images
+      d.pw1 = gemm(w1, b1, 2 * C, C, C, [](int n) { return n; }, [](int k) { return k; });
+      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) { return k; });
+      return d;
+    }
     // Gated form (both paths): entry 2p carries h1 rows 32 p .. +31 (pw1 rows
     // 32 p ..), entry 2p + 1 the matching h2 rows (pw1 rows C + 32 p ..) and
     // the pw2 fragments of gated channels 32 p .. +31; entry 2p's pw2 part is
@@ -357,6 +367,7 @@ struct Layout {
   size_t image_bytes = 0;
   // state and intermediates (offsets from the workspace base)
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
+  size_t dwa = 0, hid = 0;  // wide blocks (C > 256): depthwise output, hidden layer
   // entropy coder: scale indices, symbols, per-stream scratch, lengths,
   // offsets, status words, byte count
   size_t kmap, qtmp, rscratch, rlens, rerrs, rcount;
@@ -621,6 +632,10 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
   L.yhat[0] = alloc(lb); L.yhat[1] = alloc(lb);
   L.ed = alloc(fb); L.zA = alloc(fb); L.zB = alloc(fb);
   if (cfg.n_fe_blocks > 0) L.ctxF = alloc(fb);
+  if (C > 256) {  // wide blocks: the depthwise output and the hidden layer
+    L.dwa = alloc(fb);
+    L.hid = alloc(2 * fb);
+  }
   L.y = alloc(lb);
   const size_t P32 = P16 / 4;
   // rate partial sums: the prior's (tiles x passes); with the two-step model
@@ -789,6 +804,30 @@ PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
 // One DC block of either form, src -> dst.
 hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* dst) {
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
+  const int C = ctx->cfg.channels;
+  if (C > 256) {
+    // wide block: depthwise, pw C -> 2C + LeakyReLU, pw 2C -> C + residual
+    const Layout& L = ctx->L;
+    hipError_t e = timed(ctx, "dcblock_dw", [&] {
+      return ctx->is_int() ? launch_dw3x3_i16(src, ctx->p(b.dww), ctx->p(L.dwa), C, h8, w8, ctx->stream)
+                           : launch_dw3x3_f16(src, ctx->p(b.dww), ctx->p(L.dwa), C, h8, w8, ctx->stream);
+    });
+    if (e != hipSuccess) return e;
+    PwArgs a = conv_args(ctx, b.pw1, C, 2 * C, h8 * w8);
+    a.src0 = ctx->p(L.dwa);
+    a.C0 = C;
+    a.dst = ctx->p(L.hid);
+    a.Cdst = 2 * C;
+    e = pw(ctx, "dcblock_pw1", LD_NHWC, EP_LRELU, a);
+    if (e != hipSuccess) return e;
+    a = conv_args(ctx, b.pw2, 2 * C, C, h8 * w8);
+    a.src0 = ctx->p(L.hid);
+    a.C0 = 2 * C;
+    a.res = src;
+    a.dst = dst;
+    a.Cdst = C;
+    return pw(ctx, "dcblock_pw2", LD_NHWC, EP_RESID, a);
+  }
   BlockArgs ba{ctx->p(b.pw1.w), ctx->is_int() ? ctx->p(b.pw1.wlo) : nullptr, ctx->p(b.pw1.bias),
                ctx->p(b.pw2.w), ctx->is_int() ? ctx->p(b.pw2.wlo) : nullptr, ctx->p(b.pw2.bias),
                ctx->p(b.dww), ctx->p(b.dwb), src, dst, h8, w8, ctx->p(ctx->L.zpad)};
@@ -1600,10 +1639,11 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
   // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
   const int hyper = c.hyperprior ? 3 : 0;
-  if (decode) return 4 + hyper + c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks;
+  const int per_block = c.channels > 256 ? 3 : 1;  // a wide block is three launches
+  if (decode) return 4 + hyper + per_block * (c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks);
   // feature extractor, embed, fuse, encoder blocks, downsample, prior, upsample (with the bit total), fuse,
   // decoder blocks
-  return 6 + hyper + c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks;
+  return 6 + hyper + per_block * (c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks);
 }
 
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {

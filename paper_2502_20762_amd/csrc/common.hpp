@@ -62,6 +62,15 @@ __device__ __forceinline__ int rhe_shift(int a, int s) {
 }
 __device__ __forceinline__ int clip16(int v) { return min(max(v, -32768), 32767); }
 
+// Alg. 1's rescale of an int32 convolution sum, clip(RHE(a / 8192)), for any
+// int32 a.  |a| >= 2^28 saturates either way, so a is first clamped to
+// +-2^28; then the round-half-even bias can be added without overflow:
+// RHE(a / 2^s) = (a + 2^(s-1) - 1 + ((a >> s) & 1)) >> s.
+__device__ __forceinline__ int rescale13(int a) {
+  const int ac = min(max(a, -(1 << 28)), 1 << 28);
+  return clip16((ac + 4095 + ((ac >> 13) & 1)) >> 13);
+}
+
 // Combine the three partial products of an int16 x int16 contraction done as
 // int8 digits (x = 256 xh + xl' + 128, w = 256 wh + wl) in wrapping int32.
 __device__ __forceinline__ int combine_i16(int hh, int mid, int ll, int corr) {

@@ -47,6 +47,8 @@ enum Epi : int {
   EP_PRIOR_DEC = 4,  // same rows: yhat = q + mu from the given q
   EP_SCALES = 5,     // same rows: only the scale index of every symbol (entropy decoding)
   EP_ZQUANT = 6,     // 64 rows = the channels of z: q_z = round(z), zhat, rate partials
+  EP_LRELU = 7,      // NHWC store of LeakyReLU_0.1(acc + b) (a DC block's hidden layer)
+  EP_RESID = 8,      // NHWC store of res + acc + b (a DC block's projection and residual)
 };
 
 struct PwArgs {
@@ -82,6 +84,7 @@ struct PwArgs {
   int split;               // prior epilogues: channels >= split write (mu, s) to base (0: none)
   void* base;              // [P][2 (C - split)]: mu then s of those channels
   const float* zsigma;     // EP_ZQUANT: scale of each z channel
+  const void* res;         // EP_RESID: the residual, NHWC with Cdst channels
   // EP_UP: workgroup 0 first sums sum_base[0, n_sum) (the rate partials of
   // the frame, written by the launches before) into *bits_out; NULL: no total
   double* bits_out;
@@ -193,6 +196,14 @@ hipError_t launch_yhat_from_q(const int16_t* q, const void* mu, void* yhat, int 
 // (y' the 2 x 2 gather), q_z planar, zhat NHWC, one rate partial per tile
 hipError_t launch_zquant_f16(const PwArgs& a, hipStream_t st, int* n_partials);
 hipError_t launch_zquant_i16(const PwArgs& a, hipStream_t st, int* n_partials);
+// Depthwise 3x3 (zero padding) + bias of a DC block on an h x w NHWC map of
+// C channels (C % 8 == 0), weights in the block's packed depthwise layout
+// (fp16: per channel pair 9 tap pairs, 2 fp32 biases, a pad word; int: per
+// channel quad 9 x 2 tap pairs, 4 biases 512 b, 2 pad words).  fp16: fp32
+// accumulation from the bias, taps row by row, one rounding to fp16; int:
+// int32 sum rescaled as every other convolution of the integer path.
+hipError_t launch_dw3x3_f16(const void* src, const void* dww, void* dst, int C, int h, int w, hipStream_t st);
+hipError_t launch_dw3x3_i16(const void* src, const void* dww, void* dst, int C, int h, int w, hipStream_t st);
 hipError_t launch_nhwc_to_planar(const void* src, void* dst, int C, int P, hipStream_t st);
 hipError_t launch_planar_to_nhwc(const void* src, void* dst, int C, int P, hipStream_t st);
 

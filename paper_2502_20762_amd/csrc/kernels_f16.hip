@@ -416,10 +416,24 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       if (gp < a.P) {
         const floatx16 r = parked(px, nl8);
         half8 o;
+        if constexpr (EPI == EP_LRELU) {
+          // as the fused block: the hidden value rounded to fp16, then
+          // max(h, 0.1 h) in fp16
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
+          for (int e = 0; e < 8; ++e) {
+            const f16 hv = (f16)r[e];
+            o[e] = __builtin_fmaxf16(hv, hv * (f16)0.1f);
+          }
+        } else if constexpr (EPI == EP_RESID) {
+          const half8 zr = *(const half8*)((const f16*)a.res + (size_t)gp * a.Cdst + n0 + 8 * nl8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (f16)(r[e] + (float)zr[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (f16)r[e];
+        }
         size_t off;
-        if constexpr (EPI == EP_NHWC) {
+        if constexpr (EPI == EP_NHWC || EPI == EP_LRELU || EPI == EP_RESID) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {  // EP_UP: pass rows n = sp * C + c, all in one sub-position sp
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -913,6 +927,8 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
     NC_PW(LD_DOWN, EP_NHWC)
     NC_PW(LD_NHWC, EP_UP)
     NC_PW(LD_NHWC, EP_REC)
+    NC_PW(LD_NHWC, EP_LRELU)
+    NC_PW(LD_NHWC, EP_RESID)
   }
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
@@ -938,6 +954,8 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
     if (a.N == 256) return pw_dispatch<256>(loader, epi, a, st);
     if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
   }
+  // the two halves of a wide DC block (C > 256) at 1/8 scale: 128-row passes
+  if ((epi == EP_LRELU || epi == EP_RESID) && a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
   return pw_dispatch<64>(loader, epi, a, st);
 }
 

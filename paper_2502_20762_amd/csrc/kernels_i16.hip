@@ -18,14 +18,6 @@
 
 namespace nc {
 
-// clip(RHE(a / 8192)) for any int32 a.  |a| >= 2^28 saturates either way, so a
-// is first clamped to +-2^28; then the round-half-even bias can be added
-// without overflow: RHE(a / 2^s) = (a + 2^(s-1) - 1 + ((a >> s) & 1)) >> s.
-__device__ __forceinline__ int rescale13(int a) {
-  const int ac = min(max(a, -(1 << 28)), 1 << 28);
-  return clip16((ac + 4095 + ((ac >> 13) & 1)) >> 13);
-}
-
 __device__ __forceinline__ uint32_t pack2(int lo, int hi) {
   return ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
 }
@@ -427,10 +419,24 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
         int v[8];
         parked(px, nl8, v);
         shortx8 o;
+        if constexpr (EPI == EP_LRELU) {
+          // integer LeakyReLU, slope RHE(0.1 * 2^13) = 819: max(h, RHE(819 h / 2^13))
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
+          for (int e = 0; e < 8; ++e) {
+            const int m = 819 * v[e];
+            o[e] = (short)max(v[e], (m + 4095 + ((m >> 13) & 1)) >> 13);
+          }
+        } else if constexpr (EPI == EP_RESID) {
+          // saturating residual add
+          const shortx8 zr = *(const shortx8*)((const int16_t*)a.res + (size_t)gp * a.Cdst + n0 + 8 * nl8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (short)clip16((int)zr[e] + v[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (short)v[e];
+        }
         size_t off;
-        if constexpr (EPI == EP_NHWC) {
+        if constexpr (EPI == EP_NHWC || EPI == EP_LRELU || EPI == EP_RESID) {
           off = (size_t)gp * a.Cdst + n0 + 8 * nl8;
         } else {
           const int C = a.Cdst, n = n0 + 8 * nl8;
@@ -950,6 +956,8 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_DOWN, EP_NHWC)
   NC_PW(LD_NHWC, EP_UP)
   NC_PW(LD_NHWC, EP_REC)
+  NC_PW(LD_NHWC, EP_LRELU)
+  NC_PW(LD_NHWC, EP_RESID)
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
@@ -970,6 +978,8 @@ hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   // passes that re-stage them pays, and they still have two passes per tile.
   if (a.N % 128 == 0 && epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512)))
     return pw_dispatch<128>(loader, epi, a, st);
+  // the two halves of a wide DC block (C > 256) at 1/8 scale: 128-row passes
+  if ((epi == EP_LRELU || epi == EP_RESID) && a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
   return pw_dispatch<64>(loader, epi, a, st);
 }
 

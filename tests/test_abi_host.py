@@ -42,7 +42,7 @@ def test_config_struct_matches_header():
     assert names == [f for f, _ in nc.ncodec_config._fields_]
 
 
-@pytest.mark.parametrize("C,ne,nd", [(64, 2, 2), (128, 6, 6), (256, 8, 8), (64, 0, 0)])
+@pytest.mark.parametrize("C,ne,nd", [(64, 2, 2), (128, 6, 6), (256, 8, 8), (64, 0, 0), (384, 2, 2), (512, 8, 8)])
 def test_weight_count_matches_oracle(C, ne, nd):
     cfg = nc.make_config(64, 64, C, ne, nd, "fp16")
     assert nc.ncodec_weight_count(cfg) == oracle.params.count(C, ne, nd)
@@ -50,8 +50,9 @@ def test_weight_count_matches_oracle(C, ne, nd):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(height=1080), dict(width=8), dict(height=0), dict(width=8208), dict(channels=96), dict(channels=512),
-    dict(n_enc_blocks=-1), dict(n_dec_blocks=33), dict(path=2),
+    dict(height=1080), dict(width=8), dict(height=0), dict(width=8208), dict(channels=96), dict(channels=320),
+    dict(channels=768), dict(n_enc_blocks=-1), dict(n_dec_blocks=33), dict(path=2),
+    dict(channels=384, block=1),  # the gated form stops at C = 256
 ])
 def test_invalid_configs_rejected(bad):
     kw = dict(height=64, width=64, channels=64, n_enc_blocks=2, n_dec_blocks=2, path=0)
@@ -62,6 +63,15 @@ def test_invalid_configs_rejected(bad):
     with pytest.raises(nc.NcodecError) as e:
         nc.ncodec_create(cfg, np.zeros(10, np.float32), 0x10000, 1 << 30)
     assert e.value.status == nc.NCODEC_ESHAPE
+
+
+def test_wide_configs_accepted_with_block_buffers():
+    # above C = 256 a DC block runs as three launches through two extra 1/8-scale buffers
+    narrow = nc.ncodec_workspace_bytes(nc.make_config(64, 64, 256, 2, 2, "fp16"))
+    wide = nc.ncodec_workspace_bytes(nc.make_config(64, 64, 512, 2, 2, "fp16"))
+    # the wide context also holds the depthwise output (C) and the hidden layer (2C) at 1/8 scale
+    assert wide > 2 * narrow
+    assert nc.ncodec_workspace_bytes(nc.make_config(64, 64, 384, 2, 2, "int16")) > 0
 
 
 def test_workspace_bytes_grow_with_size():
