@@ -140,36 +140,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // chunks 0 and 1, pw1 part, into slot 0 (the depthwise does not touch it)
   issue_part(0, false, w1slot(0, 0));
   issue_part(1, false, w1slot(0, 1));
-  asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this wave's band (and the biases)
-
-  // every band value of this lane's 6 x 18 window
+  // The depthwise runs row by row as the band arrives: output row r needs band
+  // rows r .. r + 2, and band row y is complete once direct load (18 y + 17) / 4
+  // has landed (4 halo pixels per load).  The loads return in order, so
+  // "rows up to y in" is "at most 26 - (18 y + 17) / 4 band loads and the 8
+  // chunk loads still outstanding" (the biases, issued first, are in too).
   half2 v[TH / 2 + 2][TW + 2];
-#pragma unroll
-  for (int y = 0; y < TH / 2 + 2; ++y)
+  auto load_row = [&](int y) __attribute__((always_inline)) {
 #pragma unroll
     for (int x = 0; x < TW + 2; ++x) v[y][x] = *(const half2*)(own + (y * (TW + 2) + x) * 256 + cp * 4);
+  };
   // The residual of this wave's outputs (the band's interior), kept in
   // registers until the epilogue as the B operand of the identity MFMAs: for
   // output tile t, half hh, step q, lane = (pixel p = 32 hh + lane % 32,
-  // channel unit 4 t + 2 q + lane / 32 of the wave's 128 channels).
+  // channel unit 4 t + 2 q + lane / 32 of the wave's 128 channels).  Half hh
+  // lies in band rows 2 hh + 1, 2 hh + 2, read before the depthwise outputs
+  // overwrite them.
   half8 res[4][2][2];
+  auto load_res = [&](int hh) __attribute__((always_inline)) {
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         const int p = 32 * hh + (lane & 31);
         const int hp = ((p >> 4) + 1) * (TW + 2) + (p & 15) + 1;
         res[t][hh][q] = *(const half8*)(own + hp * 256 + (4 * t + 2 * q + h) * 16);
       }
+  };
   // output (row r of the group, column x) of channel pair cp goes to the B
   // fragment of half r / 2, k-step 8 hf + cp / 8: fragment index
   // 8 (r / 2) + cp / 8 of this region, lane 16 (r % 2) + x + 32 ((cp / 4) % 2),
-  // element 2 (cp % 4)
+  // element 2 (cp % 4).  Rows 0, 1 write bytes [0, 8 XF) of the region (band
+  // rows 0, 1, consumed), rows 2, 3 bytes [8 XF, 16 XF) (band rows 1 .. 3,
+  // consumed by then).
   const int xhalf = (cp >> 2) & 1;
-#pragma unroll
-  for (int r = 0; r < TH / 2; ++r)
+  auto dw_row = [&](int r) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < TW; ++k) {
       float a0 = bias0, a1 = bias1;
@@ -188,6 +193,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int px = 16 * (r & 1) + k;
       *(half2*)(own + f * XF + (px + 32 * xhalf) * 16 + (cp & 3) * 4) = o;
     }
+  };
+  static_assert(BAND_INSTR == 27 && (18 * 5 + 17) / 4 == 26, "band row -> load index");
+  asm volatile("s_waitcnt vmcnt(21)" ::: "memory");  // band rows 0 .. 2
+  load_row(0);
+  load_row(1);
+  load_row(2);
+  load_res(0);
+  dw_row(0);
+  asm volatile("s_waitcnt vmcnt(17)" ::: "memory");  // band row 3
+  load_row(3);
+  dw_row(1);
+  asm volatile("s_waitcnt vmcnt(12)" ::: "memory");  // band row 4
+  load_row(4);
+  load_res(1);
+  dw_row(2);
+  asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // band row 5
+  load_row(5);
+  dw_row(3);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // chunks 0, 1 (pw1) too
   lds_barrier();
 
