@@ -364,6 +364,7 @@ SWEEP = [  # (label, H, W, C, N_e, N_d, N_f, N_r, block, two-step entropy model)
     ("1080p C=384 (wide blocks)", 1088, 1920, 384, 8, 8, 0, 0, "lrelu", False),
     ("1080p C=512 (wide blocks, a Large model's width)", 1088, 1920, 512, 8, 8, 0, 0, "lrelu", False),
     ("1080p C=512 16+16 blocks (a Large model's width and depth)", 1088, 1920, 512, 16, 16, 0, 0, "lrelu", False),
+    ("1080p C=512 gated blocks (wide blocks, the paper's block form)", 1088, 1920, 512, 8, 8, 0, 0, "gated", False),
 ]
 
 

@@ -79,8 +79,8 @@ typedef struct {
   int32_t channels;      /* C in {64, 128, 256, 384, 512}; above 256 (the widths of
                             a Large model, Supp. "Performance for a Large Model")
                             each DC block runs as three launches (depthwise, pw
-                            C -> 2C + LeakyReLU, pw 2C -> C + residual) and only
-                            the LRELU block form is accepted                        */
+                            C -> 2C + LeakyReLU or the WSiLU gate, pw to C +
+                            residual), in either block form                         */
   int32_t n_enc_blocks;  /* N_e, 0..32                                              */
   int32_t n_dec_blocks;  /* N_d, 0..32                                              */
   int32_t path;          /* ncodec_path                                             */

@@ -67,10 +67,6 @@ bool cfg_valid(const ncodec_config* c, std::string* why) {
     if (why) *why = "qp_banks must be 0 or 1";
     return false;
   }
-  if (c->channels > 256 && c->block == NCODEC_BLOCK_GATED) {
-    if (why) *why = "the gated block form supports C <= 256";
-    return false;
-  }
   if (c->hyperprior != 0 && c->hyperprior != 1) {
     if (why) *why = "hyperprior must be 0 or 1";
     return false;
@@ -244,9 +240,17 @@ struct Packer {
       }
     }
     if (C > 256) {
-      // wide block (three launches): the pointwise convs as plain GEMM images
-      d.pw1 = gemm(w1, b1, 2 * C, C, C, [](int n) { return n; }, [](int k) { return k; });
-      d.pw2 = gemm(w2, b2, C, 2 * C, 2 * C, [](int n) { return n; }, [](int k) { return k; });
+      // wide block (three launches): the pointwise convs as plain GEMM images;
+      // gated form: pw1 packed row n' = 64 t + r holds h1 row 32 t + r (r < 32),
+      // else h2 row C + 32 t + r - 32, so every 64-row group gates 32 channels
+      if (gated)
+        d.pw1 = gemm(w1, b1, 2 * C, C, C,
+                     [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
+                     [](int k) { return k; });
+      else
+        d.pw1 = gemm(w1, b1, 2 * C, C, C, [](int n) { return n; }, [](int k) { return k; });
+      const int hid = gated ? C : 2 * C;
+      d.pw2 = gemm(w2, b2, C, hid, hid, [](int n) { return n; }, [](int k) { return k; });
       return d;
     }
     // Gated form (both paths): entry 2p carries h1 rows 32 p .. +31 (pw1 rows
@@ -806,7 +810,8 @@ hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* 
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   const int C = ctx->cfg.channels;
   if (C > 256) {
-    // wide block: depthwise, pw C -> 2C + LeakyReLU, pw 2C -> C + residual
+    // wide block: depthwise, pw C -> 2C + LeakyReLU (gated: + WSiLU gate), pw
+    // 2C (gated: C) -> C + residual
     const Layout& L = ctx->L;
     hipError_t e = timed(ctx, "dcblock_dw", [&] {
       return ctx->is_int() ? launch_dw3x3_i16(src, ctx->p(b.dww), ctx->p(L.dwa), C, h8, w8, ctx->stream)
@@ -816,13 +821,16 @@ hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* 
     PwArgs a = conv_args(ctx, b.pw1, C, 2 * C, h8 * w8);
     a.src0 = ctx->p(L.dwa);
     a.C0 = C;
+    const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
+    const int hid = gated ? C : 2 * C;  // hidden channels after the activation
     a.dst = ctx->p(L.hid);
-    a.Cdst = 2 * C;
-    e = pw(ctx, "dcblock_pw1", LD_NHWC, EP_LRELU, a);
+    a.Cdst = hid;
+    if (gated && ctx->is_int()) a.sig8 = ctx->p<uint8_t>(L.sig8);
+    e = pw(ctx, "dcblock_pw1", LD_NHWC, gated ? EP_GATE : EP_LRELU, a);
     if (e != hipSuccess) return e;
-    a = conv_args(ctx, b.pw2, 2 * C, C, h8 * w8);
+    a = conv_args(ctx, b.pw2, hid, C, h8 * w8);
     a.src0 = ctx->p(L.hid);
-    a.C0 = 2 * C;
+    a.C0 = hid;
     a.res = src;
     a.dst = dst;
     a.Cdst = C;

@@ -49,6 +49,7 @@ enum Epi : int {
   EP_ZQUANT = 6,     // 64 rows = the channels of z: q_z = round(z), zhat, rate partials
   EP_LRELU = 7,      // NHWC store of LeakyReLU_0.1(acc + b) (a DC block's hidden layer)
   EP_RESID = 8,      // NHWC store of res + acc + b (a DC block's projection and residual)
+  EP_GATE = 9,       // rows (32 h1, 32 h2) per 64: NHWC store of WSiLU(h1) * h2 (gated hidden layer)
 };
 
 struct PwArgs {
@@ -85,6 +86,7 @@ struct PwArgs {
   void* base;              // [P][2 (C - split)]: mu then s of those channels
   const float* zsigma;     // EP_ZQUANT: scale of each z channel
   const void* res;         // EP_RESID: the residual, NHWC with Cdst channels
+  const uint8_t* sig8;     // EP_GATE, int path: the compact sigmoid table
   // EP_UP: workgroup 0 first sums sum_base[0, n_sum) (the rate partials of
   // the frame, written by the launches before) into *bits_out; NULL: no total
   double* bits_out;

@@ -387,6 +387,29 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       for (int w = 0; w < 8; ++w) t += redz[w];
       a.partials[tile] = t;
     }
+  } else if constexpr (EPI == EP_GATE) {
+    // rows 64 j .. 64 j + 31 of the pass are h1 of gated channels n0 / 2 + 32 j
+    // .. + 31, rows 64 j + 32 .. + 63 the matching h2 (the packed pw1 order).
+    // As the fused gated block: WSiLU(h1) = h1 sigmoid(4 h1) rounded to fp16,
+    // then g = WSiLU(h1) h2 rounded to fp16.
+    constexpr int G = NT / 64, GU = 128 * G * 4;  // units (pixel, group, 8 channels)
+#pragma unroll
+    for (int it = 0; it < GU / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int px = idx / (4 * G), j = (idx >> 2) % G, g8 = idx & 3;
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        const floatx16 h1 = parked(px, 8 * j + g8), h2 = parked(px, 8 * j + 4 + g8);
+        half8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float u = h1[e];
+          const f16 s1 = (f16)(u / (1.f + __expf(-4.f * u)));
+          o[e] = (f16)((float)s1 * h2[e]);
+        }
+        *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + n0 / 2 + 32 * j + 8 * g8) = o;
+      }
+    }
   } else if constexpr (EPI == EP_REC) {
     // rows of the pass: global rows n0 .. n0+NT = 64 c + 8 i + j; a 16-byte store
     // covers the 8 frame pixels j of (colour c, row i) of one 1/8-scale pixel.
@@ -929,6 +952,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
     NC_PW(LD_NHWC, EP_REC)
     NC_PW(LD_NHWC, EP_LRELU)
     NC_PW(LD_NHWC, EP_RESID)
+    NC_PW(LD_NHWC, EP_GATE)
   }
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
@@ -955,7 +979,8 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
     if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
   }
   // the two halves of a wide DC block (C > 256) at 1/8 scale: 128-row passes
-  if ((epi == EP_LRELU || epi == EP_RESID) && a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
+  if ((epi == EP_LRELU || epi == EP_RESID || epi == EP_GATE) && a.N % 128 == 0)
+    return pw_dispatch<128>(loader, epi, a, st);
   return pw_dispatch<64>(loader, epi, a, st);
 }
 

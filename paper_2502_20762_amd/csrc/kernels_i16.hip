@@ -22,6 +22,18 @@ __device__ __forceinline__ uint32_t pack2(int lo, int hi) {
   return ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
 }
 
+// The integer sigmoid table S (Sec. 4.5) from its compact form s8, and RHE of
+// a / 512 (both described with the gated block below).
+constexpr int kSigSat = 888;   // S[v] = 512 from here on
+constexpr int kSigBytes = 896; // s8, padded to 16-byte units
+__device__ __forceinline__ int dci_sigmoid(int v, const uint8_t* s8) {
+  const int a = v < 0 ? -v : v;
+  const int sa = a >= kSigSat ? 512 : 256 + (int)s8[min(a, kSigSat - 1)];  // index kept in the table
+  return v < 0 ? 512 - sa : sa;
+}
+// RHE(m / 512) for |m| <= 2^30
+__device__ __forceinline__ int rhe9(int m) { return (m + 255 + ((m >> 9) & 1)) >> 9; }
+
 // ---------------------------------------------------------------- pointwise
 // Same tiling and LDS pipeline as the fp16 pointwise kernel: 8 waves per tile
 // of 128 output pixels, K consumed 64 at a time through three LDS stages.  A
@@ -392,6 +404,29 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       for (int w = 0; w < 8; ++w) t += redz[w];
       a.partials[tile] = t;
     }
+  } else if constexpr (EPI == EP_GATE) {
+    // rows 64 j .. + 31 of the pass: h1 of gated channels n0 / 2 + 32 j .. + 31,
+    // rows 64 j + 32 .. + 63: the matching h2.  As the fused gated block:
+    // WSiLU_i = RHE(h1 S[h1] / 512), g = clip(RHE(WSiLU_i h2 / 512)).
+    constexpr int G = NT / 64, GU = 128 * G * 4;  // units (pixel, group, 8 channels)
+#pragma unroll
+    for (int it = 0; it < GU / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int px = idx / (4 * G), j = (idx >> 2) % G, g8 = idx & 3;
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        int h1[8], h2[8];
+        parked(px, 8 * j + g8, h1);
+        parked(px, 8 * j + 4 + g8, h2);
+        shortx8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int w1 = rhe9(h1[e] * dci_sigmoid(h1[e], a.sig8));  // |h S| <= 2^24
+          o[e] = (short)clip16(rhe9(w1 * h2[e]));                    // |product| <= 2^30
+        }
+        *(shortx8*)((int16_t*)a.dst + (size_t)gp * a.Cdst + n0 / 2 + 32 * j + 8 * g8) = o;
+      }
+    }
   } else if constexpr (EPI == EP_REC) {
 #pragma unroll
     for (int it = 0; it < UNITS / 512; ++it) {
@@ -542,16 +577,6 @@ __device__ __forceinline__ void dci_hidden_store(const I16Acc& acc, int lane, in
 // g = clip(RHE(WSiLU(h1) h2 / 512)), S[v] = RHE(512 sigmoid(4 v / 512)).  S is
 // read from the compact LDS table s8: S[v] = 256 + s8[v] for 0 <= v < 888,
 // 512 for v >= 888, and 512 - S[-v] for v < 0 (the table is odd about 256).
-constexpr int kSigSat = 888;   // S[v] = 512 from here on
-constexpr int kSigBytes = 896; // s8, padded to 16-byte units
-__device__ __forceinline__ int dci_sigmoid(int v, const uint8_t* s8) {
-  const int a = v < 0 ? -v : v;
-  const int sa = a >= kSigSat ? 512 : 256 + (int)s8[min(a, kSigSat - 1)];  // index kept in the table
-  return v < 0 ? 512 - sa : sa;
-}
-// RHE(m / 512) for |m| <= 2^30
-__device__ __forceinline__ int rhe9(int m) { return (m + 255 + ((m >> 9) & 1)) >> 9; }
-
 // WSiLU of the rescaled h1 chain, as 8 packed int16 pairs.
 __device__ __forceinline__ void dci_wsilu(const I16Acc& acc, const uint8_t* s8, uint32_t* ws) {
   int wv[16];
@@ -958,6 +983,7 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   NC_PW(LD_NHWC, EP_REC)
   NC_PW(LD_NHWC, EP_LRELU)
   NC_PW(LD_NHWC, EP_RESID)
+  NC_PW(LD_NHWC, EP_GATE)
   if constexpr (NT == 64) {  // epilogues that pair two 32-row halves of a pass
     NC_PW(LD_NHWC, EP_PRIOR)
     NC_PW(LD_NHWC, EP_PRIOR_DEC)
@@ -979,7 +1005,8 @@ hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   if (a.N % 128 == 0 && epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512)))
     return pw_dispatch<128>(loader, epi, a, st);
   // the two halves of a wide DC block (C > 256) at 1/8 scale: 128-row passes
-  if ((epi == EP_LRELU || epi == EP_RESID) && a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
+  if ((epi == EP_LRELU || epi == EP_RESID || epi == EP_GATE) && a.N % 128 == 0)
+    return pw_dispatch<128>(loader, epi, a, st);
   return pw_dispatch<64>(loader, epi, a, st);
 }
 

@@ -51,8 +51,7 @@ def test_weight_count_matches_oracle(C, ne, nd):
 
 @pytest.mark.parametrize("bad", [
     dict(height=1080), dict(width=8), dict(height=0), dict(width=8208), dict(channels=96), dict(channels=320),
-    dict(channels=768), dict(n_enc_blocks=-1), dict(n_dec_blocks=33), dict(path=2),
-    dict(channels=384, block=1),  # the gated form stops at C = 256
+    dict(channels=768), dict(n_enc_blocks=-1), dict(n_dec_blocks=33), dict(path=2), dict(block=2),
 ])
 def test_invalid_configs_rejected(bad):
     kw = dict(height=64, width=64, channels=64, n_enc_blocks=2, n_dec_blocks=2, path=0)

@@ -1,6 +1,7 @@
 """GPU parity of the wide DC blocks (C = 384, 512: the widths of a Large model,
 supplementary "Performance for a Large Model", Tab. 8), which run as three
-launches per block (depthwise; pw C -> 2C + LeakyReLU; pw 2C -> C + residual).
+launches per block (depthwise; pw C -> 2C + LeakyReLU or the WSiLU gate of the
+gated form; pw to C + residual).
 Same bars as the other parity tests: int path free-running and bit-exact
 (Alg. 1 for every convolution), fp16 teacher-forced within 2e-2 max(1, |ref|).
 """
@@ -37,6 +38,15 @@ def test_wide_blocks_fp16(C, H, W, ne, nd):
 def test_wide_blocks_int_bit_exact(C, H, W, ne, nd):
     frames = [synth.random_frame(H, W, seed=s) for s in (142, 143)]
     run_int_sequence(H, W, C, ne, nd, frames, f"wide int C={C}")
+
+
+@pytest.mark.parametrize("C", [384, 512])
+def test_wide_gated_blocks_both_paths(C):
+    # the gated form (Supp. B.1: WSiLU and Chunk; the int16 sigmoid table of Sec. 4.5)
+    H, W, ne, nd = 48, 80, 1, 2
+    frames = [synth.random_frame(H, W, seed=s) for s in (146, 147)]
+    run_fp16_sequence(H, W, C, ne, nd, frames, f"wide gated fp16 C={C}", block="gated")
+    run_int_sequence(H, W, C, ne, nd, frames, f"wide gated int C={C}", block="gated")
 
 
 @pytest.mark.parametrize("path", ["fp16", "int16"])
