@@ -351,8 +351,7 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
  * the direct launches.  Off by default: on MI355X with ROCm 7 the replay of
  * this linear launch chain measured slightly slower than direct launches.
  * While per-kernel timing is enabled, calls launch directly.  Errors: EHIP if
- * capture, instantiation, update or launch fails; ESTATE for a context with the
- * two-step entropy model (not supported there). */
+ * capture, instantiation, update or launch fails. */
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
 
 /* Optional per-kernel timing.  While enabled, every kernel the context

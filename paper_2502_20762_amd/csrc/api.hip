@@ -1195,8 +1195,26 @@ hipError_t set_struct_arg(hipGraphExec_t x, hipGraphNode_t n, F&& edit) {
   return hipGraphExecKernelNodeSetParams(x, n, &p);
 }
 
+// Replaces the first (pointer) argument of a captured kernel node whose
+// arguments are not a struct (the zhat kernel of the two-step model).
+hipError_t set_first_ptr_arg(hipGraphExec_t x, hipGraphNode_t n, const void* ptr) {
+  hipKernelNodeParams p;
+  hipError_t e = hipGraphKernelNodeGetParams(n, &p);
+  if (e != hipSuccess) return e;
+  if (!p.kernelParams) return hipErrorInvalidValue;
+  // the zhat kernel takes 7 arguments: q, mu, yhat, C, P, ld, c_off
+  void* args[7];
+  for (int i = 0; i < 7; ++i) args[i] = p.kernelParams[i];
+  args[0] = &ptr;
+  p.kernelParams = args;
+  p.extra = nullptr;
+  return hipGraphExecKernelNodeSetParams(x, n, &p);
+}
+
 // Points the caller-buffer nodes of a captured graph at this call's buffers:
-// encode ptr = {frame, q, bits}, decode ptr = {q, frame_out}.
+// encode ptr = {frame, q, bits}, decode ptr = {q, frame_out}.  With the
+// two-step model the z symbols follow y's in q: the z quantiser (encode) and
+// the zhat kernel (decode) take q + C H/16 W/16.
 hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, const void* const* ptr) {
   hipError_t e = hipSuccess;
   for (const auto& cn : gs.nodes) {
@@ -1212,6 +1230,10 @@ hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, con
           v.q_out = q;
         }
       });
+    } else if (!std::strcmp(cn.kind, decode ? "zhat" : "zquant") && ptr[decode ? 0 : 1] != gs.ptr[decode ? 0 : 1]) {
+      int16_t* qz = (int16_t*)ptr[decode ? 0 : 1] + (size_t)ctx->cfg.channels * P16_of(ctx);
+      e = decode ? set_first_ptr_arg(gs.exec, cn.node, qz)
+                 : set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.q_out = qz; });
     } else if (!decode && !std::strcmp(cn.kind, "up") && ptr[2] != gs.ptr[2]) {
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (v.bits_out) v.bits_out = (double*)ptr[2]; });
     } else if (decode && !std::strcmp(cn.kind, "recon") && ptr[1] != gs.ptr[1]) {
@@ -1657,8 +1679,6 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {
   ncodec_status st = enter(ctx);
   if (st) return st;
-  if (enable && ctx->cfg.hyperprior)
-    return fail(ctx, NCODEC_ESTATE, "graph replay is not supported with the two-step entropy model");
   ctx->use_graphs = enable != 0;
   return NCODEC_OK;
 }

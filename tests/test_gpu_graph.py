@@ -31,16 +31,19 @@ def host(t):
 
 GATED = dict(block="gated")
 MODULES = dict(n_fe_blocks=1, n_rg_blocks=1, qp_banks=True)
+HYPER = dict(hyperprior=True)  # the two-step entropy model: z symbols follow y's in q
 
 
 @pytest.mark.parametrize("path,H,W,C,ne,nd,extra", [
     ("int16", 64, 64, 64, 2, 2, {}), ("fp16", 112, 208, 128, 2, 1, {}), ("int16", 48, 80, 128, 1, 2, {}),
     ("int16", 64, 96, 64, 1, 1, GATED), ("fp16", 64, 96, 64, 1, 1, MODULES),
-    ("int16", 48, 80, 128, 1, 1, dict(GATED, **MODULES))])
+    ("int16", 48, 80, 128, 1, 1, dict(GATED, **MODULES)), ("int16", 64, 96, 128, 1, 1, HYPER),
+    ("fp16", 64, 96, 128, 1, 1, dict(HYPER, **MODULES))])
 def test_graph_replay_matches_eager(path, H, W, C, ne, nd, extra):
     block = extra.get("block", "lrelu")
     flat = synth.make_weights(C, ne, nd, block=block, n_fe=extra.get("n_fe_blocks", 0),
-                              n_rg=extra.get("n_rg_blocks", 0), banks=extra.get("qp_banks", False))
+                              n_rg=extra.get("n_rg_blocks", 0), banks=extra.get("qp_banks", False),
+                              hyper=extra.get("hyperprior", False))
     enc_g = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
     enc_e = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
     dec_g = Codec(H, W, C, ne, nd, path, flat, device=DEV, **extra)
