@@ -145,11 +145,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // has landed (4 halo pixels per load).  The loads return in order, so
   // "rows up to y in" is "at most 26 - (18 y + 17) / 4 band loads and the 8
   // chunk loads still outstanding" (the biases, issued first, are in too).
-  half2 v[TH / 2 + 2][TW + 2];
+  // Band rows as tap pairs of one channel, P0[y][x] = (z[y][x], z[y][x + 1]) of
+  // channel c0 and P1 of channel c1 (x = 0 .. 16, one byte permute each), so
+  // that every v_dot2_f32_f16 takes two taps of a row: (w0, w1) . (z[k],
+  // z[k + 1]) and (0, w2) . (z[k + 1], z[k + 2]), accumulated in fp32.
+  half2 P0[TH / 2 + 2][TW + 1], P1[TH / 2 + 2][TW + 1];
   auto load_row = [&](int y) __attribute__((always_inline)) {
+    uint32_t vr[TW + 2];
 #pragma unroll
-    for (int x = 0; x < TW + 2; ++x) v[y][x] = *(const half2*)(own + (y * (TW + 2) + x) * 256 + cp * 4);
+    for (int x = 0; x < TW + 2; ++x) vr[x] = *(const uint32_t*)(own + (y * (TW + 2) + x) * 256 + cp * 4);
+#pragma unroll
+    for (int x = 0; x < TW + 1; ++x) {
+      P0[y][x] = __builtin_bit_cast(half2, __builtin_amdgcn_perm(vr[x + 1], vr[x], 0x05040100u));
+      P1[y][x] = __builtin_bit_cast(half2, __builtin_amdgcn_perm(vr[x + 1], vr[x], 0x07060302u));
+    }
   };
+  half2 W0a[3], W0b[3], W1a[3], W1b[3];
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    W0a[ky] = half2{wt[3 * ky][0], wt[3 * ky + 1][0]};
+    W0b[ky] = half2{(f16)0.f, wt[3 * ky + 2][0]};
+    W1a[ky] = half2{wt[3 * ky][1], wt[3 * ky + 1][1]};
+    W1b[ky] = half2{(f16)0.f, wt[3 * ky + 2][1]};
+  }
   // The residual of this wave's outputs (the band's interior), kept in
   // registers until the epilogue as the B operand of the identity MFMAs: for
   // output tile t, half hh, step q, lane = (pixel p = 32 hh + lane % 32,
@@ -179,13 +197,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int k = 0; k < TW; ++k) {
       float a0 = bias0, a1 = bias1;
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const half2 zz = v[r + ky][k + kx], ww = wt[3 * ky + kx];
-          a0 = fmaf((float)ww[0], (float)zz[0], a0);
-          a1 = fmaf((float)ww[1], (float)zz[1], a1);
-        }
+      for (int ky = 0; ky < 3; ++ky) {
+        a0 = __builtin_amdgcn_fdot2(W0a[ky], P0[r + ky][k], a0, false);
+        a0 = __builtin_amdgcn_fdot2(W0b[ky], P0[r + ky][k + 1], a0, false);
+        a1 = __builtin_amdgcn_fdot2(W1a[ky], P1[r + ky][k], a1, false);
+        a1 = __builtin_amdgcn_fdot2(W1b[ky], P1[r + ky][k + 1], a1, false);
+      }
       half2 o;
       o[0] = (f16)a0;
       o[1] = (f16)a1;
