@@ -354,14 +354,19 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
  * capture, instantiation, update or launch fails. */
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
 
-/* Optional per-kernel timing.  While enabled, every kernel the context
- * enqueues is launched with a start / stop HIP event pair attached to its
- * dispatch (hipExtLaunchKernel), so each interval is that kernel's execution
- * time.  ncodec_timing_read() synchronises the stream, aggregates the
- * intervals per kernel kind (launch count and summed milliseconds), writes at
- * most max_kinds records to out, sets *n_kinds, and clears the log.  Kinds:
- * "embed", "fuse", "dcblock", "down", "prior", "reduce", "up", "recon".
- * Meant for measurement runs; off by default. */
+/* Optional per-kernel timing.  While enabled, the kernels the context
+ * enqueues are launched with HIP events attached to their dispatch
+ * (hipExtLaunchKernel): a start event on the first launch of each run of
+ * consecutive launches of one kind (the DC blocks of a transform form one
+ * run) and a stop event on its last, so each interval is the run's execution
+ * time including the gaps inside it, and the per-launch average is that
+ * interval over the run's launch count.  ncodec_timing_read() synchronises
+ * the stream, aggregates the intervals per kernel kind (launch count and
+ * summed milliseconds), writes at most max_kinds records to out, sets
+ * *n_kinds, and clears the log.  Kinds: "embed", "fuse", "dcblock" (wide
+ * blocks: "dcblock_dw", "dcblock_pw1", "dcblock_pw2"), "down", "prior", "up",
+ * "recon", "zquant", "hyper", "zhat", "yhat", "rans_enc", "rans_dec".  Meant
+ * for measurement runs; off by default. */
 typedef struct {
   char kind[16];
   int32_t launches;

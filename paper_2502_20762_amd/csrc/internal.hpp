@@ -26,7 +26,7 @@ extern thread_local LaunchEvents g_launch_events;
 
 template <typename F, typename... Args>
 inline void launch(F kernel, dim3 grid, dim3 block, hipStream_t st, Args... args) {
-  if (g_launch_events.start)
+  if (g_launch_events.start || g_launch_events.stop)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, st, g_launch_events.start, g_launch_events.stop, 0, args...);
   else
     hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
