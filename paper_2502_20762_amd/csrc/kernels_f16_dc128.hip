@@ -64,15 +64,20 @@ static_assert(band_row_load(BH - 1) == BAND_INSTR - 1, "band geometry");
 // Unit swizzle of band column x: units of neighbouring columns (and of the
 // two lane halves' pixels) spread over all LDS banks.
 __device__ __forceinline__ constexpr int bswz(int x) { return (x >> 1) & 7; }
-// Position of lane slot L (pixel column n = L % 32 = 16 rho + 8 chi + xi,
-// k half L / 32) inside a 1 KiB B fragment.  The depthwise writes one output
-// column x per lane half (x and 15 - x) for 4 k-steps and both k halves at
-// once; this permutation puts those 16 slots in 16 different 4-bank groups.
-// The MFMA reads (lane l reads slot l) use the same map.
+// Position of lane slot L (pixel column n = L % 32 = 16 rho + x, k half
+// kh = L / 32) inside a 1 KiB B fragment.  Two access patterns must both stay
+// free of LDS bank conflicts: the MFMA operand reads and the hidden-layer
+// writes (16 bytes per lane, 16 lanes at a time: position mod 16 must be a
+// bijection of x for fixed rho, kh), and the depthwise's writes (4 bytes per
+// lane; at one output step the lanes write columns x and 15 - x for both k
+// halves into 4 consecutive fragments, so those four positions must fall in
+// different 4-bank groups mod 16, four apart).  With kk = min(x, 15 - x) and
+// side = x > 7: position = 16 (rho + 2 kh) + 4 ((2 (kk / 4) + side + 2 kh) mod 4)
+// + kk mod 4.
 __device__ __forceinline__ constexpr int bslot(int L) {
-  const int rho = (L >> 4) & 1, chi = (L >> 3) & 1, xi = L & 7, kh = L >> 5;
-  const int xp = chi ? 7 - xi : xi;
-  return 16 * (xp >> 1) + 4 * ((chi + 2 * kh) & 3) + 2 * rho + (xp & 1);
+  const int rho = (L >> 4) & 1, x = L & 15, kh = L >> 5;
+  const int kk = x < 8 ? x : 15 - x, side = x > 7 ? 1 : 0;
+  return 16 * (rho + 2 * kh) + 4 * ((2 * (kk >> 2) + side + 2 * kh) & 3) + (kk & 3);
 }
 // a's fragment (pixel group g, k-step s), later the round-1 hidden fragment
 __device__ __forceinline__ constexpr int a_off(int g, int s) { return dcw::OA + (16 * g + s) * dcw::XF; }
