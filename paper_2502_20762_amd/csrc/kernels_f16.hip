@@ -13,8 +13,15 @@
 
 #include <cstring>
 #include <type_traits>
+#include <utility>
 
 namespace nc {
+
+// f(integral_constant<int, T>) for every T of the sequence, in order
+template <typename F, int... T>
+__device__ __forceinline__ void unrolled_steps(F& f, std::integer_sequence<int, T...>) {
+  (f(std::integral_constant<int, T>{}), ...);
+}
 
 // ---------------------------------------------------------------- pointwise
 // out^T[rows n0 .. n0+NT)[128 pixels] = W * act^T (+ bias) for one tile of
@@ -936,6 +943,161 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   }
 }
 
+// ------------------------------------------------- pointwise, 256 rows, one pass
+// The 1/8-scale contractions with N = 256 rows and an NHWC result (the patch
+// embed, K = 192 frame values, and the 2C -> C fuse, K = 512): out^T[256
+// rows][128 pixels] = W act^T + b for one tile of 128 consecutive pixels per
+// workgroup of 8 waves.  Waves 0 .. 3 (one per SIMD) compute: wave w owns rows
+// 64 w .. + 63 (two 32-row tiles) for all 128 pixels (four 32-pixel groups),
+// so each weight fragment it holds feeds four MFMAs; the fragments come
+// straight from global memory (L2) into registers as MFMA A operands, a few
+// k-steps ahead.  Waves 4 .. 7 load: the activation tile (K / 64 slices of 128
+// pixels x 64 contraction indices, 128-byte rows, 16-byte unit v of pixel p at
+// position v ^ ((p / 2) & 7)) arrives by their direct global->LDS loads, at
+// most DEPTH slices in flight, and each slice is released to the compute waves
+// by a barrier once it is in (with every CU requesting its whole tile at once,
+// the first slice would arrive only with the last).  Loads complete in order per wave,
+// so keeping the activation loads (HBM) and the weight loads (L2) in different
+// waves lets the weights stream while the activations are still arriving.  The
+// sums (bias first, fp32) are rounded to fp16 once, parked in LDS and stored as
+// 16-byte vectors: the tile is one contiguous block of 128 x 256 channels.
+template <int LOADER, int K>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pw256_f16(PwArgs a) {
+  constexpr int NK = K / 64;   // activation slices
+  constexpr int NS = K / 16;   // MFMA k-steps
+  constexpr int SLICE = 128 * 128;
+  constexpr int PA = 3, PB = 2;  // prefetch distances (steps) of the A and B windows
+  constexpr int DEPTH = 4;       // activation slices in flight
+  constexpr int SMEM = NK * SLICE > 128 * 512 ? NK * SLICE : 128 * 512;
+  static_assert(K % 64 == 0 && NK >= 2, "K is a multiple of 64, at least 128");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  const int ntile = (a.P + 127) / 128;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= ntile) return;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int myrow = lane & 31;
+
+  floatx16 acc[2][4];  // (row tile c, pixel group g)
+  if (wave >= 4) {
+    // ---- loaders: slice kc is 16 direct loads, instruction i = (wave - 4) + 4 m
+    const int lw = wave - 4;
+    auto load_slice = [&](int kc) __attribute__((always_inline)) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int i = lw + 4 * m;
+        const int S = i * 64 + lane;
+        const int p = S >> 3, v = (S & 7) ^ ((p >> 1) & 7);
+        const int gp = min(tile * 128 + p, a.P - 1);  // pixels past the end reload the last one
+        dma16(pw_act_src<LOADER>(a, gp, kc, v), smem + kc * SLICE + i * 1024);
+      }
+    };
+#pragma unroll
+    for (int kc = 0; kc < DEPTH && kc < NK; ++kc) load_slice(kc);
+    auto release = [&](auto kcc) __attribute__((always_inline)) {
+      constexpr int kc = decltype(kcc)::value;
+      constexpr int later = (kc + DEPTH < NK ? kc + DEPTH : NK) - 1 - kc;  // slices requested after kc
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * later) : "memory");  // slice kc is in
+      lds_barrier();
+      if constexpr (kc + DEPTH < NK) load_slice(kc + DEPTH);
+    };
+    unrolled_steps(release, std::make_integer_sequence<int, NK>{});
+  } else {
+    // ---- compute: rows 64 w + 32 c .., the accumulators start at the bias
+    const half8* wf = (const half8*)a.wfrag + lane;  // fragment (row tile mt, k-step s) at [(mt NS + s) 64]
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const float* b = (const float*)a.bias + 64 * wave + 32 * c + 4 * h;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const floatx4 bv = *(const floatx4*)(b + 8 * q);
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[c][g][4 * q + e] = bv[e];
+      }
+    }
+    auto afrag = [&](int s, int c) __attribute__((always_inline)) { return wf[((size_t)(2 * wave + c) * NS + s) * 64]; };
+    // B fragment of k-step s, group g: pixel 32 g + lane % 32, unit 2 (s % 4) + lane / 32 of slice s / 4
+    auto bfrag = [&](int s, int g) __attribute__((always_inline)) {
+      const int p = 32 * g + myrow, v = 2 * (s & 3) + h;
+      return *(const half8*)(smem + (s >> 2) * SLICE + p * 128 + ((v ^ ((p >> 1) & 7)) << 4));
+    };
+    half8 qa[PA][2], qb[PB][4];
+#pragma unroll
+    for (int s = 0; s < PA; ++s)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) qa[s][c] = afrag(s, c);
+    lds_barrier();  // slice 0
+#pragma unroll
+    for (int s = 0; s < PB; ++s)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) qb[s][g] = bfrag(s, g);
+    // the barrier releasing slice kc + 1 is taken PB steps before slice kc
+    // ends, so the B window runs across the slices
+    auto step = [&](auto sc) __attribute__((always_inline)) {
+      constexpr int s = decltype(sc)::value;
+      if constexpr (s % 4 == 4 - PB && s / 4 + 1 < NK) lds_barrier();
+      half8 A[2], B[4];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        A[c] = qa[s % PA][c];
+        if (s + PA < NS) qa[s % PA][c] = afrag(s + PA, c);
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        B[g] = qb[s % PB][g];
+        if (s + PB < NS) qb[s % PB][g] = bfrag(s + PB, g);
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[c][g] = mfma_f16(A[c], B[g], acc[c][g]);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    static_assert(PB <= 4, "the slice barrier precedes the B reads of the next slice");
+    unrolled_steps(step, std::make_integer_sequence<int, NS>{});
+  }
+  lds_barrier();  // every compute wave is done reading the slices
+  // park: one rounding to fp16, row = tile pixel (512 bytes), 8-byte unit u of
+  // the row at u ^ (row & 15)
+  if (wave < 4) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int p = 32 * g + myrow;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int cc = 64 * wave + 32 * c + 8 * q + 4 * h;
+          half4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = (f16)acc[c][g][4 * q + e];
+          *(half4*)(smem + p * 512 + (((cc >> 2) ^ (p & 15)) << 3)) = o;
+        }
+      }
+  }
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < 128 * 32 / 512; ++i) {
+    const int idx = i * 512 + threadIdx.x;
+    const int px = idx >> 5, k8 = idx & 31;  // tile pixel, 8-channel unit
+    const int gp = tile * 128 + px;
+    if (gp < a.P) {
+      const char* ob = smem + px * 512;
+      // units 2 k8 and 2 k8 + 1 are the aligned pair at 2 k8 ^ (px & 14), swapped when px is odd
+      const half8 pv = *(const half8*)(ob + (((2 * k8) ^ (px & 14)) << 3));
+      half8 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[e] = (px & 1) ? pv[4 + e] : pv[e];
+        o[4 + e] = (px & 1) ? pv[e] : pv[4 + e];
+      }
+      *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + 8 * k8) = o;
+    }
+  }
+}
+
 template <int NT>
 static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t st) {
   dim3 grid(grid_tiles(a.P) * (a.N / NT)), block(512);
@@ -974,6 +1136,13 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   // all N rows in one pass (N = 256: 48 KiB stages, one workgroup per CU) or
   // 128 rows per pass, so each tile is staged once or twice.  The 1/16-scale
   // kernels have 4x fewer tiles and keep 64-row passes to fill the CUs.
+  if (epi == EP_NHWC && a.N == 256 && a.Cdst == 256 && ((loader == LD_FRAME && a.K == 192) ||
+                                                        (loader == LD_NHWC && a.K == 512))) {
+    dim3 grid(grid_tiles(a.P)), block(512);
+    if (loader == LD_FRAME) launch(k_pw256_f16<LD_FRAME, 192>, grid, block, st, a);
+    else launch(k_pw256_f16<LD_NHWC, 512>, grid, block, st, a);
+    return hipGetLastError();
+  }
   if (epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512))) {
     if (a.N == 256) return pw_dispatch<256>(loader, epi, a, st);
     if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
