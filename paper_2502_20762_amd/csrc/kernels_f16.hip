@@ -943,11 +943,13 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
   }
 }
 
-// ------------------------------------------------- pointwise, 256 rows, one pass
-// The 1/8-scale contractions with N = 256 rows and an NHWC result (the patch
-// embed, K = 192 frame values, and the 2C -> C fuse, K = 512): out^T[256
-// rows][128 pixels] = W act^T + b for one tile of 128 consecutive pixels per
-// workgroup of 8 waves.  Waves 0 .. 3 (one per SIMD) compute: wave w owns rows
+// ------------------------------------------------- pointwise, 256-row passes
+// Contractions with 256-row passes and a plain or pixel-shuffled NHWC result
+// (the patch embed, K = 192 frame values, and the 2C -> C fuse, K = 512, one
+// pass each; the upsample, K = C, four passes = the four sub-positions of the
+// shuffle): out^T[256 rows of the pass][128 pixels] = W act^T + b for one tile
+// of 128 consecutive pixels per workgroup of 8 waves, the passes of a tile
+// next to each other on one XCD (they share the tile's activations in L2).  Waves 0 .. 3 (one per SIMD) compute: wave w owns rows
 // 64 w .. + 63 (two 32-row tiles) for all 128 pixels (four 32-pixel groups),
 // so each weight fragment it holds feeds four MFMAs; the fragments come
 // straight from global memory (L2) into registers as MFMA A operands, a few
@@ -960,8 +962,9 @@ __global__ __launch_bounds__(512) void k_dcblock_f16(BlockArgs a) {
 // so keeping the activation loads (HBM) and the weight loads (L2) in different
 // waves lets the weights stream while the activations are still arriving.  The
 // sums (bias first, fp32) are rounded to fp16 once, parked in LDS and stored as
-// 16-byte vectors: the tile is one contiguous block of 128 x 256 channels.
-template <int LOADER, int K>
+// 16-byte vectors (one contiguous block of 128 x 256 channels, or 512 bytes per
+// output pixel of the shuffle).
+template <int LOADER, int K, int EPI>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_pw256_f16(PwArgs a) {
   constexpr int NK = K / 64;   // activation slices
   constexpr int NS = K / 16;   // MFMA k-steps
@@ -971,9 +974,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   constexpr int SMEM = NK * SLICE > 128 * 512 ? NK * SLICE : 128 * 512;
   static_assert(K % 64 == 0 && NK >= 2, "K is a multiple of 64, at least 128");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  const int ntile = (a.P + 127) / 128;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  static_assert(EPI == EP_NHWC || EPI == EP_UP, "plain or shuffled NHWC result");
+  const int ntile = (a.P + 127) / 128, npass = a.N / 256;
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = lin / npass;
   if (tile >= ntile) return;
+  const int n0 = (lin - tile * npass) * 256;  // first row of the pass
+  // the upsample that follows the prior in an encode: workgroup 0 first adds
+  // up the frame's rate partials
+  if constexpr (EPI == EP_UP)
+    if (a.bits_out && blockIdx.x == 0) block_sum_to(a.sum_base, a.n_sum, a.bits_out);
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int myrow = lane & 31;
@@ -1007,7 +1017,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const half8* wf = (const half8*)a.wfrag + lane;  // fragment (row tile mt, k-step s) at [(mt NS + s) 64]
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const float* b = (const float*)a.bias + 64 * wave + 32 * c + 4 * h;
+      const float* b = (const float*)a.bias + n0 + 64 * wave + 32 * c + 4 * h;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const floatx4 bv = *(const floatx4*)(b + 8 * q);
@@ -1017,7 +1027,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           for (int e = 0; e < 4; ++e) acc[c][g][4 * q + e] = bv[e];
       }
     }
-    auto afrag = [&](int s, int c) __attribute__((always_inline)) { return wf[((size_t)(2 * wave + c) * NS + s) * 64]; };
+    auto afrag = [&](int s, int c) __attribute__((always_inline)) {
+      return wf[((size_t)(n0 / 32 + 2 * wave + c) * NS + s) * 64];
+    };
     // B fragment of k-step s, group g: pixel 32 g + lane % 32, unit 2 (s % 4) + lane / 32 of slice s / 4
     auto bfrag = [&](int s, int g) __attribute__((always_inline)) {
       const int p = 32 * g + myrow, v = 2 * (s & 3) + h;
@@ -1093,7 +1105,17 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         o[e] = (px & 1) ? pv[4 + e] : pv[e];
         o[4 + e] = (px & 1) ? pv[e] : pv[4 + e];
       }
-      *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + 8 * k8) = o;
+      size_t off;
+      if constexpr (EPI == EP_NHWC) {
+        off = (size_t)gp * a.Cdst + n0 + 8 * k8;
+      } else {  // rows n = sp C + c: channel c of sub-position sp of the 2 x 2 shuffle
+        const int C = a.Cdst, n = n0 + 8 * k8;
+        const int sp = n / C, c = n - sp * C;
+        const int w16 = a.w8 >> 1;
+        const int Y = gp / w16, X = gp - Y * w16;
+        off = (size_t)((2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1)) * C + c;
+      }
+      *(half8*)((f16*)a.dst + off) = o;
     }
   }
 }
@@ -1136,11 +1158,13 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   // all N rows in one pass (N = 256: 48 KiB stages, one workgroup per CU) or
   // 128 rows per pass, so each tile is staged once or twice.  The 1/16-scale
   // kernels have 4x fewer tiles and keep 64-row passes to fill the CUs.
-  if (epi == EP_NHWC && a.N == 256 && a.Cdst == 256 && ((loader == LD_FRAME && a.K == 192) ||
-                                                        (loader == LD_NHWC && a.K == 512))) {
-    dim3 grid(grid_tiles(a.P)), block(512);
-    if (loader == LD_FRAME) launch(k_pw256_f16<LD_FRAME, 192>, grid, block, st, a);
-    else launch(k_pw256_f16<LD_NHWC, 512>, grid, block, st, a);
+  if ((epi == EP_NHWC && a.N == 256 && a.Cdst == 256 && ((loader == LD_FRAME && a.K == 192) ||
+                                                         (loader == LD_NHWC && a.K == 512))) ||
+      (epi == EP_UP && loader == LD_NHWC && a.K == 256 && a.N % 256 == 0)) {
+    dim3 grid(grid_tiles(a.P) * (a.N / 256)), block(512);
+    if (epi == EP_UP) launch(k_pw256_f16<LD_NHWC, 256, EP_UP>, grid, block, st, a);
+    else if (loader == LD_FRAME) launch(k_pw256_f16<LD_FRAME, 192, EP_NHWC>, grid, block, st, a);
+    else launch(k_pw256_f16<LD_NHWC, 512, EP_NHWC>, grid, block, st, a);
     return hipGetLastError();
   }
   if (epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512))) {
