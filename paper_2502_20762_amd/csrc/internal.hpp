@@ -175,7 +175,7 @@ hipError_t launch_rans_decode(const uint8_t* in, uint64_t in_bytes, const uint8_
 hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_pw_i16(int loader, int epi, const PwArgs& a, hipStream_t st);
 hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t st);
-hipError_t launch_dcblock128_f16(const BlockArgs& a, hipStream_t st);  // C = 256, LeakyReLU form
+hipError_t launch_dcblock128_f16(bool gated, const BlockArgs& a, hipStream_t st);  // C = 256
 hipError_t launch_dcblock_i16(int C, bool gated, const BlockArgs& a, hipStream_t st);
 hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials);
 hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials);

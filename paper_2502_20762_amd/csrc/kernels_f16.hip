@@ -1178,8 +1178,8 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t st) {
-  // C = 256, LeakyReLU form: the 128-pixels-per-wave kernel
-  if (C == 256 && !gated) return launch_dcblock128_f16(a, st);
+  // C = 256: the 128-pixels-per-wave kernel
+  if (C == 256) return launch_dcblock128_f16(gated, a, st);
   dim3 grid(dc_grid(a.h, a.w)), block(512);
   switch (C * 2 + (gated ? 1 : 0)) {
     case 128: launch(k_dcblock_f16<64, false>, grid, block, st, a); break;

@@ -1,4 +1,4 @@
-// fp16 DC block (Supp. B.1, LeakyReLU form) for C = 256 with 128 pixels per
+// fp16 DC block (Supp. B.1, LeakyReLU and gated forms) for C = 256 with 128 pixels per
 // wave: each wave covers the whole 8 x 16 pixel tile of its workgroup, so
 // every weight fragment it loads feeds four MFMAs (the tile's four 32-pixel
 // groups).  The weight fragments are therefore read straight from global
@@ -53,7 +53,6 @@ constexpr int REG = BAND_INSTR * 1024;
 constexpr int OA = 4 * REG;                        // a: [group 4][k-step 16] fragments, later the round-1 hidden layer
 constexpr int OBIAS = OA + 64 * XF;                // pw1 biases (2C fp32), then pw2 biases (C fp32)
 constexpr int SMEM = OBIAS + 3 * C * 4;
-constexpr int NT = 4 * KS;                         // weight-stream steps: pw1 rounds 0, 1, pw2
 static_assert(SMEM <= 160 * 1024, "fits the LDS of a CU");
 static_assert(64 * XF <= OA && TH * TW * C * 2 <= OA, "the round-0 hidden layer and the parked output fit over the bands");
 // direct load holding the last unit of band row y (loads land in order)
@@ -90,8 +89,18 @@ __device__ __forceinline__ void unrolled(F& f, std::integer_sequence<int, T...>)
   (f(std::integral_constant<int, T>{}), ...);
 }
 
+// GATED: the gated form (Supp. B.1, WSiLU and Chunk).  Its weight image pairs
+// the entries: entry 2 p holds the pw1 fragments of h1 rows 32 p .. +31,
+// entry 2 p + 1 those of the matching h2 rows and the pw2 fragments of gated
+// channels 32 p .. +31.  Round r's two chains of wave w are then h1 and h2 of
+// gated pair 4 r + w, and the hand-off writes g = WSiLU(h1) h2 (32 channels,
+// two k-steps) instead of the LeakyReLU of two chunks; pw2 contracts C = 256
+// gated channels (16 k-steps) instead of 2C.
+template <bool GATED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcblock128_f16(BlockArgs a) {
   using namespace dcw;
+  constexpr int KH = GATED ? KS / 2 : KS;  // hidden k-steps per round (the pw2 k-steps of a round)
+  constexpr int NT = 2 * KS + 2 * KH;      // weight-stream steps: pw1 rounds 0, 1, pw2
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   const int tiles_x = (a.w + TW - 1) / TW;
   const int ntile = tiles_x * ((a.h + TH - 1) / TH);
@@ -105,16 +114,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const half8* wimg = (const half8*)a.w1 + lane;  // fragment (chunk j, f) at [(j FR + f) 64]
   const int myslot = bslot(lane) * 16;
 
-  // weight-stream step t, fragment c: pw1 round 0 (t < 16: chunk 2 w + c,
-  // k-step t), round 1 (t < 32: chunk 8 + 2 w + c, k-step t - 16), pw2
-  // (k = t - 32: chunk k / 2, output tile 2 w + c, half k % 2)
+  // weight-stream step t, fragment c: pw1 round 0 (t < 16: entry 2 w + c,
+  // k-step t), round 1 (t < 32: entry 8 + 2 w + c, k-step t - 16), pw2
+  // (k = t - 32: output tile 2 w + c, half k % 2 of the entry holding hidden
+  // chunk k / 2: entry k / 2, or 2 (k / 2) + 1 in the gated form)
   auto afrag = [&](int t, int c) __attribute__((always_inline)) {
     int f;
     if (t < 2 * KS) {
       f = (8 * (t >> 4) + 2 * wave + c) * FR + (t & 15);
     } else {
       const int k = t - 2 * KS;
-      f = (k >> 1) * FR + KS + 1 + 2 * (2 * wave + c) + (k & 1);
+      f = (GATED ? 2 * (k >> 1) + 1 : k >> 1) * FR + KS + 1 + 2 * (2 * wave + c) + (k & 1);
     }
     return wimg[(size_t)f * 64];
   };
@@ -284,12 +294,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   // ---- 2, 3. pw1 (steps 0 .. 31) and pw2 (steps 32 .. 63)
   floatx16 acc[2][4];  // pw1: chunk c, group g; pw2: output tile c, group g
-  // accumulators from the biases in LDS: row0 = the first row of the pair
-  // (pw1: 0 .. 2C - 1, pw2: 2C ..)
-  auto init_acc = [&](int row0) __attribute__((always_inline)) {
+  // accumulators from the biases in LDS: row0[c] = the first row of chain or
+  // tile c (pw1: 0 .. 2C - 1, pw2: 2C ..)
+  auto init_acc = [&](int row00, int row01) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const float* b = (const float*)(smem + OBIAS) + row0 + 32 * c + 4 * h;
+      const float* b = (const float*)(smem + OBIAS) + (c ? row01 : row00) + 4 * h;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const floatx4 bv4 = *(const floatx4*)(b + 8 * q);
@@ -320,6 +330,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           *(half8*)(smem + off(g, 4 * wave + 2 * c + u) + myslot) = gv;
         }
   };
+  // Gated hand-off: WSiLU(h1) = h1 sigmoid(4 h1) rounded to fp16, then
+  // g = WSiLU(h1) h2 rounded to fp16 (h1, h2: the fp32 chains), as pw2 B
+  // fragments: half u of the pair goes to k-step 2 w + u of the round
+  auto gate_write = [&](auto off) __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        half8 gv;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float h1 = acc[0][g][8 * u + e];
+          const f16 ws = (f16)(h1 / (1.f + __expf(-4.f * h1)));
+          gv[e] = (f16)((float)ws * acc[1][g][8 * u + e]);
+        }
+        *(half8*)(smem + off(g, 2 * wave + u) + myslot) = gv;
+      }
+  };
+  auto handoff = [&](auto off) __attribute__((always_inline)) {
+    if constexpr (GATED) gate_write(off);
+    else leaky_write(off);
+  };
+  // pw1 chains of round r: the rows of entries 8 r + 2 w + c
+  auto chain_row = [&](int r, int c) __attribute__((always_inline)) {
+    return GATED ? c * C + 32 * (4 * r + wave) : 32 * (8 * r + 2 * wave + c);
+  };
   // B fragment of step t, group g: a (pw1, k-step t % 16), then the hidden
   // layer (pw2, k-step t - 32: round 0 below 16, round 1 above)
   auto bfrag = [&](int t, int g) __attribute__((always_inline)) {
@@ -328,11 +364,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       off = a_off(g, t & 15);
     } else {
       const int k = t - 2 * KS;
-      off = k < KS ? h0_off(g, k) : a_off(g, k - KS);
+      off = k < KH ? h0_off(g, k) : a_off(g, k - KH);
     }
     return *(const half8*)(smem + off + myslot);
   };
-  init_acc(64 * wave);
+  init_acc(chain_row(0, 0), chain_row(0, 1));
   half8 qb[PB][4];
 #pragma unroll
   for (int s = 0; s < PB; ++s)
@@ -345,16 +381,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if constexpr (t == KS) {
       // round 0 done: its hidden fragments over the bands (no reader before
       // the hand-off barrier), then round 1 from its bias
-      leaky_write(h0_off);
-      init_acc(256 + 64 * wave);
+      handoff(h0_off);
+      init_acc(chain_row(1, 0), chain_row(1, 1));
     }
     if constexpr (t == 2 * KS) {
       // round 1 done: once every wave is past its last read of a (the MFMAs
       // read their operands at issue), its hidden fragments replace a; the
       // pw2 accumulators start from the bias
       lds_barrier();
-      leaky_write(a_off);
-      init_acc(2 * C + 64 * wave);
+      handoff(a_off);
+      init_acc(2 * C + 64 * wave, 2 * C + 64 * wave + 32);
       // the residual enters first, through the identity (the two 32 x 16
       // halves as A, exact products); the sums are rounded to fp16 once
       {
@@ -439,8 +475,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 }
 
-hipError_t launch_dcblock128_f16(const BlockArgs& a, hipStream_t st) {
-  launch(k_dcblock128_f16, dim3(dc_grid(a.h, a.w)), dim3(256), st, a);
+hipError_t launch_dcblock128_f16(bool gated, const BlockArgs& a, hipStream_t st) {
+  if (gated) launch(k_dcblock128_f16<true>, dim3(dc_grid(a.h, a.w)), dim3(256), st, a);
+  else launch(k_dcblock128_f16<false>, dim3(dc_grid(a.h, a.w)), dim3(256), st, a);
   return hipGetLastError();
 }
 

@@ -55,6 +55,13 @@ def test_gated_edge_shapes_int(H, W, C, ne, nd):
     run_int_sequence(H, W, C, ne, nd, frames, "gated edge int", block="gated")
 
 
+def test_gated_c256_ragged_fp16():
+    """C = 256 gated blocks (the 128-pixels-per-wave kernel) over several ragged
+    8 x 16 tiles (34 x 50 pixels at 1/8 scale) and 3 + 3 blocks, two frames."""
+    frames = [synth.random_frame(272, 400, seed=s) for s in (24, 25)]
+    run_fp16_sequence(272, 400, 256, 3, 3, frames, "gated c256 fp16", block="gated")
+
+
 def test_gated_wvga_fp16():
     run_fp16_sequence(480, 832, 128, 6, 6, list(synth.frame_sequence("wvga", 1)), "gated wvga fp16", block="gated")
 
