@@ -106,7 +106,7 @@ def cpu_baseline(pre, weights, strip_rows, path="fp16"):
 
 TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "dcblock_hd1080_hbm_traffic.md")
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2502_20762_amd", "csrc")
-SOURCES = {"k_dcblock128_f16": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
+SOURCES = {"k_dcblock128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
            "k_dcblock_i16<256, false>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
 
 
@@ -481,7 +481,7 @@ def main():
         res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
 
     def summary(path, r, peak_tflops, op_scale, unit):
-        traffic = counted_traffic("k_dcblock128_f16" if path == "fp16" else "k_dcblock_i16<256, false>")
+        traffic = counted_traffic("k_dcblock128_f16<false>" if path == "fp16" else "k_dcblock_i16<256, false>")
         K = args.steps
         fl, by = kinds["dcblock"]
         kd = r["kernels"]["dcblock"]
