@@ -336,7 +336,8 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
 /* Kernel launches one ncodec_encode_frame (decode = 0; one workgroup of the
  * upsample that follows the prior sums the frame's bit total, so d_bits does
  * not change the count) or ncodec_decode_frame (decode = 1) enqueues (three more each with
- * the two-step model),
+ * the two-step model; on the fp16 path the upsample and its fuse conv are one
+ * launch, and so are the patch embed and its fuse conv),
  * counting the feature-extractor and reconstruction-generation blocks
  * (Sec. 3: the number of modules called per frame is one of the costs the
  * design minimises).  0 for a NULL ctx. */

@@ -362,6 +362,8 @@ struct Packer {
 
 struct Layout {
   ConvDev pe, fuse_enc, down, head, up, fuse_dec, rec;
+  // fp16 path: patch embed + fuse and upsample + fuse folded into one conv each
+  ConvDev enc_in, dec_in;
   std::vector<BlockDev> enc, dec, fe, rg;
   size_t sigma_tab = 0;
   size_t sig8 = 0;     // int path, gated block: compact sigmoid table
@@ -498,9 +500,34 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
     return out.data();
   };
   const float* pe_w = take((size_t)C * 192); const float* pe_b = take(C);
-  L.pe = pk.plain(pe_w, pe_b, C, 192);
   const float* fe_w = take((size_t)2 * C * C); const float* fe_b = take(C);
-  L.fuse_enc = pk.plain(fuse_fold(fe_w, ffe), fe_b, C, 2 * C);
+  if (is_int) {
+    L.pe = pk.plain(pe_w, pe_b, C, 192);
+    L.fuse_enc = pk.plain(fuse_fold(fe_w, ffe), fe_b, C, 2 * C);
+  } else {
+    // fp16 path: the patch embed is linear and feeds the fuse conv alone, so
+    // fuse(concat(W_pe u + b_pe, F)) = [W_fe W_pe | W_fc] [u; F] + W_fe b_pe + b_fe
+    // (W_fe, W_fc: the fuse's columns on e and on the context F), composed
+    // in double and rounded to fp16 once
+    const float* fc = fuse_fold(fe_w, ffe);
+    const int K = 192 + C;
+    std::vector<double> acc(192);
+    std::vector<float> m((size_t)C * K), mb(C);
+    for (int n = 0; n < C; ++n) {
+      std::fill(acc.begin(), acc.end(), 0.0);
+      double bb = fe_b[n];
+      for (int j = 0; j < C; ++j) {
+        const double f = fe_w[(size_t)n * 2 * C + j];
+        const float* r = pe_w + (size_t)j * 192;
+        for (int k = 0; k < 192; ++k) acc[k] += f * (double)r[k];
+        bb += f * (double)pe_b[j];
+      }
+      for (int k = 0; k < 192; ++k) m[(size_t)n * K + k] = (float)acc[k];
+      for (int c = 0; c < C; ++c) m[(size_t)n * K + 192 + c] = fc[(size_t)n * 2 * C + C + c];
+      mb[n] = (float)bb;
+    }
+    L.enc_in = pk.plain(m.data(), mb.data(), C, K);
+  }
   for (int k = 0; k < cfg.n_enc_blocks; ++k) L.enc.push_back(pk.block(cur));
   const float* dn_w = take((size_t)4 * C * C); const float* dn_b = take(C);
   if (bank) {  // q_e scales the rows of the downsample (y)
@@ -522,6 +549,35 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
                    [C](int n) { return (n % 64 < 32) ? 32 * (n / 64) + n % 64 : C + 32 * (n / 64) + n % 64 - 32; },
                    [](int k) { return k; });
   const float* up_w = take((size_t)4 * C * C); const float* up_b = take(4 * C);
+  const float* fd_w0 = up_w + (size_t)4 * C * C + 4 * C;  // the fuse conv follows in the list
+  if (!is_int) {
+    // fp16 path: the upsample (then the x2 shuffle) feeds the fuse conv alone,
+    // so at sub-position s of the shuffle the pair is one conv on yhat and F:
+    // [W_fd W_up^(s) diag(q_d) | W_fc] [yhat; F] + W_fd b_up^(s) + b_fd, with
+    // W_up^(s) the upsample rows 4 c + s (channel c of sub-position s); rows
+    // packed s C + n, composed in double and rounded to fp16 once
+    const double* qd = bank ? brow(1) : nullptr;
+    const float* fc = fuse_fold(fd_w0, ffd);
+    const int K = 2 * C;
+    std::vector<double> acc(C);
+    std::vector<float> m((size_t)4 * C * K), mb(4 * C);
+    for (int sp = 0; sp < 4; ++sp)
+      for (int n = 0; n < C; ++n) {
+        std::fill(acc.begin(), acc.end(), 0.0);
+        double bb = fd_w0[(size_t)2 * C * C + n];
+        for (int j = 0; j < C; ++j) {
+          const double f = fd_w0[(size_t)n * 2 * C + j];
+          const float* r = up_w + (size_t)(4 * j + sp) * C;
+          for (int k = 0; k < C; ++k) acc[k] += f * (double)r[k];
+          bb += f * (double)up_b[4 * j + sp];
+        }
+        float* row = m.data() + (size_t)(sp * C + n) * K;
+        for (int k = 0; k < C; ++k) row[k] = (float)(qd ? acc[k] * qd[k] : acc[k]);
+        for (int c = 0; c < C; ++c) row[C + c] = fc[(size_t)n * 2 * C + C + c];
+        mb[sp * C + n] = (float)bb;
+      }
+    L.dec_in = pk.plain(m.data(), mb.data(), 4 * C, K);
+  }
   if (bank) {  // q_d scales the columns of the upsample (its input yhat)
     const double* qd = brow(1);
     fup.assign(up_w, up_w + (size_t)4 * C * C);
@@ -529,10 +585,12 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
       for (int c = 0; c < C; ++c) fup[n * C + c] = fold16(fup[n * C + c], qd[c]);
     up_w = fup.data();
   }
-  // packed row n' = sp * C + c  <-  source row 4c + sp
-  L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });
   const float* fd_w = take((size_t)2 * C * C); const float* fd_b = take(C);
-  L.fuse_dec = pk.plain(fuse_fold(fd_w, ffd), fd_b, C, 2 * C);
+  if (is_int) {
+    // packed row n' = sp * C + c  <-  source row 4c + sp
+    L.up = pk.gemm(up_w, up_b, 4 * C, C, C, [C](int n) { return 4 * (n % C) + n / C; }, [](int k) { return k; });
+    L.fuse_dec = pk.plain(fuse_fold(fd_w, ffd), fd_b, C, 2 * C);
+  }
   for (int k = 0; k < cfg.n_dec_blocks; ++k) L.dec.push_back(pk.block(cur));
   const float* rc_w = take((size_t)192 * C); const float* rc_b = take(192);
   if (bank) {  // q_r scales the columns of the reconstruction (the generated feature)
@@ -899,25 +957,42 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt, double* d_bits = nullptr, in
   const void* f_prev = L.fe.empty() ? ctx->p(L.feat[1 - nxt]) : ctx->p(L.ctxF);  // the temporal context
   void* f_new = ctx->p(L.feat[nxt]);
 
-  PwArgs a = conv_args(ctx, L.up, C, 4 * C, P16);
-  a.src0 = ctx->p(L.yhat[nxt]);
-  a.C0 = C;
-  a.dst = ctx->p(L.ed);
-  a.Cdst = C;
-  a.bits_out = d_bits;
-  a.sum_base = ctx->p<double>(L.partials);
-  a.n_sum = n_parts;
-  NC_HIP(ctx, pw(ctx, "up", LD_NHWC, EP_UP, a), "upsample");
-
   void* z = c.n_dec_blocks == 0 ? f_new : ctx->p(L.zA);
-  a = conv_args(ctx, L.fuse_dec, 2 * C, C, P8);
-  a.src0 = ctx->p(L.ed);
-  a.C0 = C;
-  a.src1 = f_prev;
-  a.C1 = C;
-  a.dst = z;
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_dec");
+  PwArgs a;
+  if (ctx->is_int()) {
+    a = conv_args(ctx, L.up, C, 4 * C, P16);
+    a.src0 = ctx->p(L.yhat[nxt]);
+    a.C0 = C;
+    a.dst = ctx->p(L.ed);
+    a.Cdst = C;
+    a.bits_out = d_bits;
+    a.sum_base = ctx->p<double>(L.partials);
+    a.n_sum = n_parts;
+    NC_HIP(ctx, pw(ctx, "up", LD_NHWC, EP_UP, a), "upsample");
+
+    a = conv_args(ctx, L.fuse_dec, 2 * C, C, P8);
+    a.src0 = ctx->p(L.ed);
+    a.C0 = C;
+    a.src1 = f_prev;
+    a.C1 = C;
+    a.dst = z;
+    a.Cdst = C;
+    NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_dec");
+  } else {
+    // upsample, shuffle and fuse as one conv per sub-position on [yhat; F]
+    // (weights composed at load), written through the x2 shuffle
+    a = conv_args(ctx, L.dec_in, 2 * C, 4 * C, P16);
+    a.src0 = ctx->p(L.yhat[nxt]);
+    a.C0 = C;
+    a.src1 = f_prev;
+    a.C1 = C;
+    a.dst = z;
+    a.Cdst = C;
+    a.bits_out = d_bits;
+    a.sum_base = ctx->p<double>(L.partials);
+    a.n_sum = n_parts;
+    NC_HIP(ctx, pw(ctx, "up_fuse", LD_UP_CTX, EP_UP, a), "upsample + fuse_dec");
+  }
 
   for (int k = 0; k < c.n_dec_blocks; ++k) {
     void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
@@ -1036,21 +1111,28 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   const void* context = nullptr;  // F_{t-1}, also used by the decoder part below
   NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
 
-  PwArgs a = conv_args(ctx, L.pe, 192, C, P8);
-  a.src0 = d_frame;
-  a.dst = ctx->p(L.ed);
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "embed", LD_FRAME, EP_NHWC, a), "patch embed");
-
   void* z = ctx->p(L.zA);
-  a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
-  a.src0 = ctx->p(L.ed);
-  a.C0 = C;
+  PwArgs a;
+  if (ctx->is_int()) {
+    a = conv_args(ctx, L.pe, 192, C, P8);
+    a.src0 = d_frame;
+    a.dst = ctx->p(L.ed);
+    a.Cdst = C;
+    NC_HIP(ctx, pw(ctx, "embed", LD_FRAME, EP_NHWC, a), "patch embed");
+    a = conv_args(ctx, L.fuse_enc, 2 * C, C, P8);
+    a.src0 = ctx->p(L.ed);
+    a.C0 = C;
+  } else {
+    // patch embed and fuse as one conv on [u; F] (weights composed at load)
+    a = conv_args(ctx, L.enc_in, 192 + C, C, P8);
+    a.src0 = d_frame;
+  }
   a.src1 = context;
   a.C1 = C;
   a.dst = z;
   a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "fuse", LD_NHWC, EP_NHWC, a), "fuse_enc");
+  NC_HIP(ctx, pw(ctx, ctx->is_int() ? "fuse" : "embed_fuse", ctx->is_int() ? LD_NHWC : LD_FRAME_CTX, EP_NHWC, a),
+         "fuse_enc");
 
   for (int k = 0; k < c.n_enc_blocks; ++k) {
     void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
@@ -1237,7 +1319,7 @@ hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, con
   hipError_t e = hipSuccess;
   for (const auto& cn : gs.nodes) {
     if (e != hipSuccess) break;
-    if (!decode && !std::strcmp(cn.kind, "embed") && ptr[0] != gs.ptr[0]) {
+    if (!decode && (!std::strcmp(cn.kind, "embed") || !std::strcmp(cn.kind, "embed_fuse")) && ptr[0] != gs.ptr[0]) {
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.src0 = ptr[0]; });
     } else if (!std::strcmp(cn.kind, "prior") && ptr[decode ? 0 : 1] != gs.ptr[decode ? 0 : 1]) {
       int16_t* q = (int16_t*)ptr[decode ? 0 : 1];
@@ -1252,7 +1334,7 @@ hipError_t retarget(ncodec_ctx* ctx, ncodec_ctx::GraphSlot& gs, bool decode, con
       int16_t* qz = (int16_t*)ptr[decode ? 0 : 1] + (size_t)ctx->cfg.channels * P16_of(ctx);
       e = decode ? set_first_ptr_arg(gs.exec, cn.node, qz)
                  : set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.q_out = qz; });
-    } else if (!decode && !std::strcmp(cn.kind, "up") && ptr[2] != gs.ptr[2]) {
+    } else if (!decode && (!std::strcmp(cn.kind, "up") || !std::strcmp(cn.kind, "up_fuse")) && ptr[2] != gs.ptr[2]) {
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { if (v.bits_out) v.bits_out = (double*)ptr[2]; });
     } else if (decode && !std::strcmp(cn.kind, "recon") && ptr[1] != gs.ptr[1]) {
       e = set_struct_arg<PwArgs>(gs.exec, cn.node, [&](PwArgs& v) { v.dst = (void*)ptr[1]; });
@@ -1686,12 +1768,15 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   const ncodec_config& c = ctx->cfg;
   // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
   // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
+  // (the fp16 path runs the upsample and the fuse as one launch, and in an
+  // encode the patch embed and the fuse too)
+  const int fold = c.path == NCODEC_PATH_INT16 ? 0 : 1;
   const int hyper = c.hyperprior ? 3 : 0;
   const int per_block = c.channels > 256 ? 3 : 1;  // a wide block is three launches
-  if (decode) return 4 + hyper + per_block * (c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks);
+  if (decode) return 4 - fold + hyper + per_block * (c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks);
   // feature extractor, embed, fuse, encoder blocks, downsample, prior, upsample (with the bit total), fuse,
   // decoder blocks
-  return 6 + hyper + per_block * (c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks);
+  return 6 - 2 * fold + hyper + per_block * (c.n_fe_blocks + c.n_enc_blocks + c.n_dec_blocks);
 }
 
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {

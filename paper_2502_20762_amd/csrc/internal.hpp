@@ -37,6 +37,13 @@ enum Loader : int {
   LD_NHWC = 0,   // k < C0: src0[p*C0 + k], else src1[p*C1 + k - C0]   (concat on channels)
   LD_FRAME = 1,  // planar 3xHxW frame, pixel-unshuffle x8 on load: k = 64c + 8i + j
   LD_DOWN = 2,   // 2x2 stride-2 gather: k = (2i+j)*Csrc + c from pixel (2Y+i, 2X+j)
+  // k < 192: the frame as LD_FRAME, else src1[p*C1 + k - 192] (patch embed
+  // folded into the encoder's fuse)
+  LD_FRAME_CTX = 3,
+  // 1/16-scale pixel P, pass of sub-position s = n0 / Cdst: k < C0:
+  // src0[P*C0 + k], else src1[child*C1 + k - C0] with child = (2Y + s/2,
+  // 2X + s%2) on the 1/8 grid (upsample folded into the decoder's fuse)
+  LD_UP_CTX = 4,
 };
 // Where a pointwise kernel writes its result.
 enum Epi : int {

@@ -43,17 +43,25 @@ struct PwSmem {
 };
 
 // Global address of 16-byte activation vector v (8 contraction indices
-// starting at 64 kc + 8 v) of output pixel gp.
+// starting at 64 kc + 8 v) of output pixel gp; n0 = the first output row of
+// the workgroup's pass.
 template <int LOADER>
-__device__ __forceinline__ const char* pw_act_src(const PwArgs& a, int gp, int kc, int v) {
+__device__ __forceinline__ const char* pw_act_src(const PwArgs& a, int gp, int kc, int v, int n0) {
   const int k = 64 * kc + 8 * v;
   if constexpr (LOADER == LD_NHWC) {
     if (k < a.C0) return (const char*)((const f16*)a.src0 + (size_t)gp * (a.ld0 ? a.ld0 : a.C0) + k);
     return (const char*)((const f16*)a.src1 + (size_t)gp * a.C1 + (k - a.C0));
-  } else if constexpr (LOADER == LD_FRAME) {
+  } else if constexpr (LOADER == LD_FRAME || LOADER == LD_FRAME_CTX) {
+    if (LOADER == LD_FRAME_CTX && kc >= 3) return (const char*)((const f16*)a.src1 + (size_t)gp * a.C1 + (k - 192));
     // unshuffle x8: k = 64 c + 8 i + j -> colour c = kc, frame row 8 py + i = 8 py + v, columns 8 px .. +7
     const int py = gp / a.w8, px = gp - py * a.w8;
     return (const char*)((const f16*)a.src0 + (size_t)kc * a.H * a.W + (size_t)(8 * py + v) * a.W + 8 * px);
+  } else if constexpr (LOADER == LD_UP_CTX) {
+    if (k < a.C0) return (const char*)((const f16*)a.src0 + (size_t)gp * a.C0 + k);
+    const int sp = n0 / a.Cdst, w16 = a.w8 >> 1;
+    const int Y = gp / w16, X = gp - Y * w16;
+    const int child = (2 * Y + (sp >> 1)) * a.w8 + 2 * X + (sp & 1);
+    return (const char*)((const f16*)a.src1 + (size_t)child * a.C1 + (k - a.C0));
   } else {
     // 2x2 stride 2: k = (2 i + j) Csrc + c from pixel (2 Y + i, 2 X + j)
     const int w16 = a.w8 >> 1;
@@ -74,7 +82,7 @@ __device__ __forceinline__ void pw_issue(const PwArgs& a, int tile, int n0, int 
     const int slot = ins * 64 + lane;
     const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
     const int gp = min(tile * 128 + px, a.P - 1);  // pixels past the end reload the last one
-    dma16(pw_act_src<LOADER>(a, gp, kc, v), stage + ins * 1024);
+    dma16(pw_act_src<LOADER>(a, gp, kc, v, n0), stage + ins * 1024);
   }
   const int ks = a.K / 16;
   const char* w = (const char*)a.wfrag;
@@ -999,7 +1007,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const int S = i * 64 + lane;
         const int p = S >> 3, v = (S & 7) ^ ((p >> 1) & 7);
         const int gp = min(tile * 128 + p, a.P - 1);  // pixels past the end reload the last one
-        dma16(pw_act_src<LOADER>(a, gp, kc, v), smem + kc * SLICE + i * 1024);
+        dma16(pw_act_src<LOADER>(a, gp, kc, v, n0), smem + kc * SLICE + i * 1024);
       }
     };
 #pragma unroll
@@ -1130,9 +1138,11 @@ static hipError_t pw_dispatch(int loader, int epi, const PwArgs& a, hipStream_t 
   }
   NC_PW(LD_NHWC, EP_NHWC)
   NC_PW(LD_FRAME, EP_NHWC)
+  NC_PW(LD_FRAME_CTX, EP_NHWC)
   if constexpr (NT != 256) {
     NC_PW(LD_DOWN, EP_NHWC)
     NC_PW(LD_NHWC, EP_UP)
+    NC_PW(LD_UP_CTX, EP_UP)
     NC_PW(LD_NHWC, EP_REC)
     NC_PW(LD_NHWC, EP_LRELU)
     NC_PW(LD_NHWC, EP_RESID)
@@ -1158,16 +1168,20 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
   // all N rows in one pass (N = 256: 48 KiB stages, one workgroup per CU) or
   // 128 rows per pass, so each tile is staged once or twice.  The 1/16-scale
   // kernels have 4x fewer tiles and keep 64-row passes to fill the CUs.
-  if ((epi == EP_NHWC && a.N == 256 && a.Cdst == 256 && ((loader == LD_FRAME && a.K == 192) ||
-                                                         (loader == LD_NHWC && a.K == 512))) ||
-      (epi == EP_UP && loader == LD_NHWC && a.K == 256 && a.N % 256 == 0)) {
+  if ((epi == EP_NHWC && a.N == 256 && a.Cdst == 256 &&
+       ((loader == LD_FRAME && a.K == 192) || (loader == LD_NHWC && a.K == 512) ||
+        (loader == LD_FRAME_CTX && a.K == 448))) ||
+      (epi == EP_UP && a.N % 256 == 0 &&
+       ((loader == LD_NHWC && a.K == 256) || (loader == LD_UP_CTX && a.K == 512 && a.Cdst == 256)))) {
     dim3 grid(grid_tiles(a.P) * (a.N / 256)), block(512);
-    if (epi == EP_UP) launch(k_pw256_f16<LD_NHWC, 256, EP_UP>, grid, block, st, a);
+    if (epi == EP_UP && loader == LD_UP_CTX) launch(k_pw256_f16<LD_UP_CTX, 512, EP_UP>, grid, block, st, a);
+    else if (epi == EP_UP) launch(k_pw256_f16<LD_NHWC, 256, EP_UP>, grid, block, st, a);
     else if (loader == LD_FRAME) launch(k_pw256_f16<LD_FRAME, 192, EP_NHWC>, grid, block, st, a);
+    else if (loader == LD_FRAME_CTX) launch(k_pw256_f16<LD_FRAME_CTX, 448, EP_NHWC>, grid, block, st, a);
     else launch(k_pw256_f16<LD_NHWC, 512, EP_NHWC>, grid, block, st, a);
     return hipGetLastError();
   }
-  if (epi == EP_NHWC && (loader == LD_FRAME || (loader == LD_NHWC && a.K >= 512))) {
+  if (epi == EP_NHWC && (loader == LD_FRAME || loader == LD_FRAME_CTX || (loader == LD_NHWC && a.K >= 512))) {
     if (a.N == 256) return pw_dispatch<256>(loader, epi, a, st);
     if (a.N % 128 == 0) return pw_dispatch<128>(loader, epi, a, st);
   }

@@ -54,8 +54,12 @@ def check_fp16_encode(p, x, feat_prev, yhat_prev, q_gpu, bits_gpu, feat_new, yha
     assert not mism[sl16].any(), f"{what}: q differs outside the rounding band at {int(mism[sl16].sum())} elements"
     far = np.abs(q - q_ref) > 1
     assert not far[sl16].any(), f"{what}: q off by more than 1 inside the rounding band at {int(far[sl16].sum())} elements"
-    agree = float(np.mean((q == q_ref)[sl16]))
-    assert agree > 0.99, f"{what}: q agreement {agree}"
+    # reading A16 allows a flip only inside the band; as a guard against a
+    # systematic shift, at most 1 % of the symbols may flip (2 where that is
+    # fewer: one latent pixel has only C symbols, a few of them in the band)
+    flips = int(np.count_nonzero((q != q_ref)[sl16]))
+    n = int(np.asarray(q[sl16]).size)
+    assert flips <= max(2, 0.01 * n), f"{what}: {flips} of {n} symbols flipped inside the rounding band"
     yhat_ref = q + mu
     assert_close_fp16(np.asarray(yhat_new)[sl16], yhat_ref[sl16], what + " yhat")
     f_ref = cf.decoder_feature(p, yhat_ref, feat_prev)
