@@ -600,7 +600,16 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
       for (int c = 0; c < C; ++c) frec[(size_t)n * C + c] = fold16(frec[(size_t)n * C + c], qr[c]);
     rc_w = frec.data();
   }
-  L.rec = pk.plain(rc_w, rc_b, 192, C);
+  if (is_int) {
+    L.rec = pk.plain(rc_w, rc_b, 192, C);
+  } else {
+    // 256 rows, 192 .. 255 zero: the 256-row pointwise kernel computes whole
+    // 64-row slices per wave and stores only the 192 frame rows
+    std::vector<float> wpad((size_t)256 * C, 0.f), bpad(256, 0.f);
+    std::copy(rc_w, rc_w + (size_t)192 * C, wpad.begin());
+    std::copy(rc_b, rc_b + 192, bpad.begin());
+    L.rec = pk.plain(wpad.data(), bpad.data(), 256, C);
+  }
   for (int k = 0; k < cfg.n_fe_blocks; ++k) L.fe.push_back(pk.block(cur));
   for (int k = 0; k < cfg.n_rg_blocks; ++k) L.rg.push_back(pk.block(cur));
   if (bank) cur += 4 * nb;

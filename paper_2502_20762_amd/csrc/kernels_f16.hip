@@ -982,8 +982,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   constexpr int SMEM = NK * SLICE > 128 * 512 ? NK * SLICE : 128 * 512;
   static_assert(K % 64 == 0 && NK >= 2, "K is a multiple of 64, at least 128");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  static_assert(EPI == EP_NHWC || EPI == EP_UP, "plain or shuffled NHWC result");
-  const int ntile = (a.P + 127) / 128, npass = a.N / 256;
+  static_assert(EPI == EP_NHWC || EPI == EP_UP || EPI == EP_REC, "plain or shuffled NHWC result, or the frame");
+  // EP_REC: N = 192 rows in one pass; the weight image and the bias are
+  // padded to 256 rows with zeros (wave 3's rows are computed and not stored)
+  const int ntile = (a.P + 127) / 128, npass = (a.N + 255) / 256;
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int tile = lin / npass;
   if (tile >= ntile) return;
@@ -1098,6 +1100,31 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
   }
   lds_barrier();
+  if constexpr (EPI == EP_REC) {
+    // rows 64 c + 8 i + j: a 16-byte store covers the 8 frame pixels j of
+    // (colour c, row i) of one 1/8-scale pixel; consecutive threads walk the
+    // pixels, clamped to [0, 1] (the same as clamping before the rounding)
+#pragma unroll
+    for (int it = 0; it < 128 * 24 / 512; ++it) {
+      const int idx = it * 512 + threadIdx.x;
+      const int nl8 = idx >> 7, px = idx & 127;
+      const int gp = tile * 128 + px;
+      if (gp < a.P) {
+        const half8 pv = *(const half8*)(smem + px * 512 + (((2 * nl8) ^ (px & 14)) << 3));
+        const int c = nl8 >> 3, i = nl8 & 7;
+        const int py = gp / a.w8, pxx = gp - py * a.w8;
+        half8 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const f16 v0 = (px & 1) ? pv[4 + e] : pv[e], v1 = (px & 1) ? pv[e] : pv[4 + e];
+          o[e] = __builtin_fminf16(__builtin_fmaxf16(v0, (f16)0.f), (f16)1.f);
+          o[4 + e] = __builtin_fminf16(__builtin_fmaxf16(v1, (f16)0.f), (f16)1.f);
+        }
+        __builtin_nontemporal_store(o, (half8*)((f16*)a.dst + (size_t)c * a.H * a.W + (size_t)(8 * py + i) * a.W + 8 * pxx));
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 128 * 32 / 512; ++i) {
     const int idx = i * 512 + threadIdx.x;
@@ -1172,9 +1199,11 @@ hipError_t launch_pw_f16(int loader, int epi, const PwArgs& a, hipStream_t st) {
        ((loader == LD_FRAME && a.K == 192) || (loader == LD_NHWC && a.K == 512) ||
         (loader == LD_FRAME_CTX && a.K == 448))) ||
       (epi == EP_UP && a.N % 256 == 0 &&
-       ((loader == LD_NHWC && a.K == 256) || (loader == LD_UP_CTX && a.K == 512 && a.Cdst == 256)))) {
-    dim3 grid(grid_tiles(a.P) * (a.N / 256)), block(512);
-    if (epi == EP_UP && loader == LD_UP_CTX) launch(k_pw256_f16<LD_UP_CTX, 512, EP_UP>, grid, block, st, a);
+       ((loader == LD_NHWC && a.K == 256) || (loader == LD_UP_CTX && a.K == 512 && a.Cdst == 256))) ||
+      (epi == EP_REC && loader == LD_NHWC && a.K == 256 && a.N == 192 && a.C0 == 256 && a.ld0 == 0)) {
+    dim3 grid(grid_tiles(a.P) * ((a.N + 255) / 256)), block(512);
+    if (epi == EP_REC) launch(k_pw256_f16<LD_NHWC, 256, EP_REC>, grid, block, st, a);
+    else if (epi == EP_UP && loader == LD_UP_CTX) launch(k_pw256_f16<LD_UP_CTX, 512, EP_UP>, grid, block, st, a);
     else if (epi == EP_UP) launch(k_pw256_f16<LD_NHWC, 256, EP_UP>, grid, block, st, a);
     else if (loader == LD_FRAME) launch(k_pw256_f16<LD_FRAME, 192, EP_NHWC>, grid, block, st, a);
     else if (loader == LD_FRAME_CTX) launch(k_pw256_f16<LD_FRAME_CTX, 448, EP_NHWC>, grid, block, st, a);
