@@ -29,7 +29,8 @@ __device__ __forceinline__ void unrolled_steps(F& f, std::integer_sequence<int, 
 // +31 and rows (w >> 2) NT/2 .. +NT/2.  K is consumed 64 at a time through three
 // LDS stages (distinct objects, statically indexed), each holding the
 // activation slice (128 pixels x 64 channels, one 128-byte row per pixel,
-// 16-byte vector v of pixel px stored at slot v ^ (px & 7)) and the weight
+// 16-byte vector v of pixel px stored at slot v ^ ((px / 2) & 7), which keeps
+// the 16 lanes of each quarter of a B-fragment read on distinct banks) and the weight
 // fragments of those 64 contraction indices, filled by direct global->LDS
 // loads two stages ahead.  Three stages leave room for two workgroups per CU,
 // so one workgroup's load latency and stores overlap the other's MFMA work.
@@ -80,7 +81,7 @@ __device__ __forceinline__ void pw_issue(const PwArgs& a, int tile, int n0, int 
   for (int i = 0; i < ACT_INSTR / 8; ++i) {
     const int ins = wave + 8 * i;
     const int slot = ins * 64 + lane;
-    const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
+    const int px = slot >> 3, v = (slot & 7) ^ ((px >> 1) & 7);
     const int gp = min(tile * 128 + px, a.P - 1);  // pixels past the end reload the last one
     dma16(pw_act_src<LOADER>(a, gp, kc, v, n0), stage + ins * 1024);
   }
@@ -101,7 +102,7 @@ __device__ __forceinline__ void pw_compute(const char* stage, int pg, int hf, in
   const int pl = pg * 32 + (lane & 31), h = lane >> 5;
   half8 b[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) b[ks] = *(const half8*)(stage + pl * 128 + ((((2 * ks + h) ^ (pl & 7))) << 4));
+  for (int ks = 0; ks < 4; ++ks) b[ks] = *(const half8*)(stage + pl * 128 + ((((2 * ks + h) ^ ((pl >> 1) & 7))) << 4));
   half8 w[RT][4];
 #pragma unroll
   for (int t = 0; t < RT; ++t)

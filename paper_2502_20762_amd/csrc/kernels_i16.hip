@@ -76,7 +76,7 @@ __device__ __forceinline__ void pwi_issue(const PwArgs& a, int tile, int n0, int
   for (int i = 0; i < ACT_INSTR / 8; ++i) {
     const int ins = wave + 8 * i;
     const int slot = ins * 64 + lane;
-    const int px = slot >> 3, v = (slot & 7) ^ (px & 7);
+    const int px = slot >> 3, v = (slot & 7) ^ ((px >> 1) & 7);  // conflict-free B reads (16-lane quarters)
     const int gp = min(tile * 128 + px, a.P - 1);
     dma16(pwi_act_src<LOADER>(a, gp, kc, v), stage + ins * 1024);
   }
@@ -101,16 +101,16 @@ __device__ __forceinline__ void pwi_compute(const char* stage, int pg, int hf, i
     const int v0 = 4 * ks + 2 * h;
     uint32_t d[8];
     if constexpr (LOADER == LD_FRAME) {
-      const half8 x0 = *(const half8*)(stage + pl * 128 + ((v0 ^ (pl & 7)) << 4));
-      const half8 x1 = *(const half8*)(stage + pl * 128 + (((v0 + 1) ^ (pl & 7)) << 4));
+      const half8 x0 = *(const half8*)(stage + pl * 128 + ((v0 ^ ((pl >> 1) & 7)) << 4));
+      const half8 x1 = *(const half8*)(stage + pl * 128 + (((v0 + 1) ^ ((pl >> 1) & 7)) << 4));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         d[e] = pack2(clip16((int)rintf((float)x0[2 * e] * 512.f)), clip16((int)rintf((float)x0[2 * e + 1] * 512.f)));
         d[4 + e] = pack2(clip16((int)rintf((float)x1[2 * e] * 512.f)), clip16((int)rintf((float)x1[2 * e + 1] * 512.f)));
       }
     } else {
-      const intx4 q0 = *(const intx4*)(stage + pl * 128 + ((v0 ^ (pl & 7)) << 4));
-      const intx4 q1 = *(const intx4*)(stage + pl * 128 + (((v0 + 1) ^ (pl & 7)) << 4));
+      const intx4 q0 = *(const intx4*)(stage + pl * 128 + ((v0 ^ ((pl >> 1) & 7)) << 4));
+      const intx4 q1 = *(const intx4*)(stage + pl * 128 + (((v0 + 1) ^ ((pl >> 1) & 7)) << 4));
 #pragma unroll
       for (int e = 0; e < 4; ++e) { d[e] = (uint32_t)q0[e]; d[4 + e] = (uint32_t)q1[e]; }
     }
