@@ -106,7 +106,8 @@ def cpu_baseline(pre, weights, strip_rows, path="fp16"):
 
 TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "dcblock_hd1080_hbm_traffic.md")
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2502_20762_amd", "csrc")
-SOURCES = {"k_dcblock128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
+SOURCES = {"k_dcchain128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
+           "k_dcblock128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
            "k_dcblock_i16<256, false>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
 
 
@@ -299,6 +300,8 @@ def run_path(path, pre, weights, gframes, steps, warmup, torch, Codec):
         "bits_per_frame": float(bits.mean().item()),
         "kernels": {k: {"launches": n, "avg_us": 1e3 * ms / n, "total_ms": ms} for k, (n, ms) in kern.items()},
         "kernels_per_frame": [enc.kernels_per_frame(False), dec.kernels_per_frame(True)],
+        "block_chains": bool(enc.block_chain_status()[0]),
+        "chain_timeouts": enc.block_chain_status()[1] + dec.block_chain_status()[1],
     })
     return r
 
@@ -481,11 +484,21 @@ def main():
         res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
 
     def summary(path, r, peak_tflops, op_scale, unit):
-        traffic = counted_traffic("k_dcblock128_f16<false>" if path == "fp16" else "k_dcblock_i16<256, false>")
+        # the dominant kernel: one DC block per launch, or (fp16 at C = 256)
+        # one chain of a transform's blocks per launch; the timing log counts
+        # blocks either way
+        chained = r["block_chains"]
+        bpl = min(ne, nd, 16) if chained else 1
+        kname = ("k_dcchain128_f16<false>" if chained else "k_dcblock128_f16<false>") if path == "fp16" \
+            else "k_dcblock_i16<256, false>"
+        traffic = counted_traffic(kname)
         K = args.steps
         fl, by = kinds["dcblock"]
+        if chained:  # a chain's algorithmic HBM bytes: its input and its output, once
+            fl, by = bpl * fl, by
         kd = r["kernels"]["dcblock"]
-        achieved = op_scale * fl / (kd["avg_us"] * 1e-6) / 1e12
+        launch_us = kd["avg_us"] * bpl
+        achieved = op_scale * fl / (launch_us * 1e-6) / 1e12
         t_roof = roofline_seconds(kinds, enc_list + dec_list, peak_tflops * 1e12 / op_scale)
         step_ms = (r["enc_ms"] + r["dec_ms"]) / K
         ga = r["graph"]
@@ -498,10 +511,12 @@ def main():
             "decode_fps_median": 1e3 / r["dec_median_ms"],
             "graph_replay": {"value": K / ((ga["enc_ms"] + ga["dec_ms"]) * 1e-3),
                              "encode_fps": K / (ga["enc_ms"] * 1e-3), "decode_fps": K / (ga["dec_ms"] * 1e-3)},
-            "roofline": {"kernel": "dcblock", "bound": "mfma", "achieved": achieved, "peak": peak_tflops,
+            "roofline": {"kernel": kname, "bound": "mfma", "achieved": achieved, "peak": peak_tflops,
                          "unit": unit, "frac": achieved / peak_tflops, "traffic": traffic,
                          "per_launch": {"algorithmic_ops": op_scale * fl, "algorithmic_bytes": by,
-                                        "avg_us": kd["avg_us"], "launches": kd["launches"]}},
+                                        "avg_us": launch_us, "launches": kd["launches"] // bpl,
+                                        "blocks_per_launch": bpl, "per_block_us": kd["avg_us"]}},
+            "chain_timeouts": r["chain_timeouts"],
             "frame_roofline_fps": 1.0 / t_roof,
             "frac_of_frame_roofline": K / ((r["enc_ms"] + r["dec_ms"]) * 1e-3) * t_roof,
             "encode_frac_of_roofline": roofline_seconds(kinds, enc_list, peak_tflops * 1e12 / op_scale)

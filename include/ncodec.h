@@ -337,7 +337,8 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
  * upsample that follows the prior sums the frame's bit total, so d_bits does
  * not change the count) or ncodec_decode_frame (decode = 1) enqueues (three more each with
  * the two-step model; on the fp16 path the upsample and its fuse conv are one
- * launch, and so are the patch embed and its fuse conv),
+ * launch, and so are the patch embed and its fuse conv; a chain of DC blocks
+ * counts as one launch per up to 16 blocks, see ncodec_block_chains),
  * counting the feature-extractor and reconstruction-generation blocks
  * (Sec. 3: the number of modules called per frame is one of the costs the
  * design minimises).  0 for a NULL ctx. */
@@ -355,6 +356,29 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
  * capture, instantiation, update or launch fails. */
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
 
+/* Block chains (Sec. 3: fewer, larger modules per frame; Supp. B.1 blocks run
+ * back to back).  On the fp16 path at C = 256 the consecutive DC blocks of a
+ * transform (the encoder's, the decoder's, the feature extractor's, the
+ * reconstruction generation's; up to 16 per launch) run as one launch in which
+ * every 8 x 16 tile keeps its block output on chip and exchanges only its edge
+ * pixels with the neighbouring tiles through memory.  Used only where every
+ * tile fits the device at once (checked once per context with the occupancy
+ * API; 255 tiles of one workgroup per CU at 1080p); otherwise, and with
+ * enable = 0, one launch per block.  Results are identical either way.  On by
+ * default.  A tile waits at most about 0.1 s for a neighbour (a case that
+ * needs another kernel holding CUs for that long); a wait that gives up
+ * leaves the block outputs wrong and is reported by
+ * ncodec_block_chain_status.  Changing the setting drops captured graphs (the
+ * next graph call captures again).  Errors: EINVAL for a NULL ctx, EHIP. */
+ncodec_status ncodec_block_chains(ncodec_ctx* ctx, int32_t enable);
+
+/* *in_use = 1 if this context's DC blocks run as chains (enabled, fp16,
+ * C = 256 and every tile resident at once), else 0.  Synchronizes the
+ * context's stream and writes to *timeouts 1 if any chain launch of this
+ * context has given up waiting for a neighbouring tile since its creation,
+ * else 0.  Errors: EINVAL for a NULL ctx, in_use or timeouts, EHIP. */
+ncodec_status ncodec_block_chain_status(ncodec_ctx* ctx, int32_t* in_use, int32_t* timeouts);
+
 /* Optional per-kernel timing.  While enabled, the kernels the context
  * enqueues are launched with HIP events attached to their dispatch
  * (hipExtLaunchKernel): a start event on the first launch of each run of
@@ -364,10 +388,12 @@ ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
  * interval over the run's launch count.  ncodec_timing_read() synchronises
  * the stream, aggregates the intervals per kernel kind (launch count and
  * summed milliseconds), writes at most max_kinds records to out, sets
- * *n_kinds, and clears the log.  Kinds: "embed", "fuse", "dcblock" (wide
- * blocks: "dcblock_dw", "dcblock_pw1", "dcblock_pw2"), "down", "prior", "up",
- * "recon", "zquant", "hyper", "zhat", "yhat", "rans_enc", "rans_dec".  Meant
- * for measurement runs; off by default. */
+ * *n_kinds, and clears the log.  Kinds: "embed", "fuse", "embed_fuse",
+ * "dcblock" (wide blocks: "dcblock_dw", "dcblock_pw1", "dcblock_pw2"), "down",
+ * "prior", "up", "up_fuse", "recon", "zquant", "hyper", "zhat", "yhat",
+ * "rans_enc", "rans_dec".  A chain of DC blocks (ncodec_block_chains) counts
+ * as one launch per block, so "dcblock" is always per block.  Meant for
+ * measurement runs; off by default. */
 typedef struct {
   char kind[16];
   int32_t launches;

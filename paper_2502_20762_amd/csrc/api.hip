@@ -374,6 +374,10 @@ struct Layout {
   // state and intermediates (offsets from the workspace base)
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
   size_t dwa = 0, hid = 0;  // wide blocks (C > 256): depthwise output, hidden layer
+  // chains of fp16 C = 256 blocks in one launch: one progress word per tile
+  // (zero at creation; every launch adds the same count to all) and a
+  // timeout flag
+  size_t chain_flags = 0, chain_status = 0;
   // entropy coder: scale indices, symbols, per-stream scratch, lengths,
   // offsets, status words, byte count
   size_t kmap, qtmp, rscratch, rlens, rerrs, rcount;
@@ -708,6 +712,11 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
     L.hid = alloc(2 * fb);
   }
   L.y = alloc(lb);
+  if (!is_int && C == 256) {
+    const size_t tiles = (size_t)((cfg.height / 8 + 7) / 8) * ((cfg.width / 8 + 15) / 16);
+    L.chain_flags = alloc(tiles * 4);
+    L.chain_status = alloc(4);
+  }
   const size_t P32 = P16 / 4;
   // rate partial sums: the prior's (tiles x passes); with the two-step model
   // also the z quantiser's (one per tile) and the second step's
@@ -769,6 +778,10 @@ struct ncodec_ctx {
   };
   bool use_graphs = false;
   GraphSlot graphs[2][2];  // [decode][cur]
+  // consecutive fp16 C = 256 blocks as one chain launch (when every tile fits
+  // the device at once; chain_fit: -1 not yet checked, 0 no, 1 yes)
+  bool chains = true;
+  int chain_fit = -1;
   // Parallel coding (Fig. 6; supplementary "Parallel Coding"): the coded
   // calls run the entropy coder (encode) or the feature extractor (decode) on
   // a second stream of default priority, joined by events before the call's
@@ -803,7 +816,7 @@ ncodec_status hip_fail(ncodec_ctx* ctx, hipError_t e, const char* where) {
 // start / stop event pair (hipExtLaunchKernelGGL), so the recorded interval
 // is that kernel's execution, without the dispatch gap before it.
 template <class F>
-hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch_fn) {
+hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch_fn, int count = 1) {
   if (ctx->capturing) {
     hipError_t e = launch_fn();
     if (e != hipSuccess) return e;
@@ -829,10 +842,10 @@ hipError_t timed(ncodec_ctx* ctx, const char* kind, F&& launch_fn) {
     g_launch_events = {};
     if (t.stop) (void)hipEventDestroy(t.stop);
     t.stop = stop;
-    t.n += 1;
+    t.n += count;
     return e;
   }
-  ncodec_ctx::TimedLaunch t{kind, nullptr, nullptr, 1};
+  ncodec_ctx::TimedLaunch t{kind, nullptr, nullptr, count};
   hipError_t e = hipEventCreate(&t.start);
   if (e == hipSuccess) e = hipEventCreate(&t.stop);
   if (e == hipSuccess) {
@@ -927,18 +940,62 @@ hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* 
   return dcblock(ctx, ba);
 }
 
+// Blocks 0 .. n - 1 of `blocks`, block k from src[k] into dst[k] (src[k + 1]
+// = dst[k]).  On the fp16 path at C = 256 runs of up to kMaxChain blocks go
+// as one chain launch when every tile of the grid fits the device at once;
+// otherwise (and for a run of one) one launch per block.  The timing log
+// counts blocks either way.
+hipError_t run_blocks(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, const std::vector<const void*>& src,
+                      const std::vector<void*>& dst) {
+  const int n = (int)blocks.size();
+  const int C = ctx->cfg.channels;
+  const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
+  const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
+  bool chain = ctx->chains && !ctx->is_int() && C == 256 && n >= 2;
+  if (chain && ctx->chain_fit < 0) ctx->chain_fit = dcchain128_resident(gated) >= dc_grid(h8, w8) ? 1 : 0;
+  chain = chain && ctx->chain_fit == 1;
+  for (int k0 = 0; k0 < n;) {
+    const int m = chain ? std::min(n - k0, kMaxChain) : 1;
+    if (m == 1) {
+      const hipError_t e = run_block(ctx, blocks[k0], src[k0], dst[k0]);
+      if (e != hipSuccess) return e;
+      ++k0;
+      continue;
+    }
+    DcChainArgs ca;
+    std::memset(&ca, 0, sizeof(ca));
+    for (int j = 0; j < m; ++j) {
+      const BlockDev& b = blocks[k0 + j];
+      ca.blk[j] = BlockArgs{ctx->p(b.pw1.w), nullptr, ctx->p(b.pw1.bias), ctx->p(b.pw2.w), nullptr,
+                            ctx->p(b.pw2.bias), ctx->p(b.dww), ctx->p(b.dwb), src[k0 + j], dst[k0 + j],
+                            h8, w8, ctx->p(ctx->L.zpad)};
+    }
+    ca.nb = m;
+    ca.flags = ctx->p<int>(ctx->L.chain_flags);
+    ca.status = ctx->p<int>(ctx->L.chain_status);
+    const hipError_t e = timed(ctx, "dcblock", [&] { return launch_dcchain128_f16(gated, ca, ctx->stream); }, m);
+    if (e != hipSuccess) return e;
+    k0 += m;
+  }
+  return hipSuccess;
+}
+
 // A chain of DC blocks from src, ping-ponging through zA / zB, the last one
 // writing `last`; returns the buffer that holds the result (src if empty).
 // src and last must not be zA or zB.
 hipError_t run_chain(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, const void* src, void* last,
                      const void** result) {
+  std::vector<const void*> srcs;
+  std::vector<void*> dsts;
   const void* z = src;
   for (size_t k = 0; k < blocks.size(); ++k) {
     void* dst = k + 1 == blocks.size() ? last : (z == ctx->p(ctx->L.zA) ? ctx->p(ctx->L.zB) : ctx->p(ctx->L.zA));
-    const hipError_t e = run_block(ctx, blocks[k], z, dst);
-    if (e != hipSuccess) return e;
+    srcs.push_back(z);
+    dsts.push_back(dst);
     z = dst;
   }
+  const hipError_t e = run_blocks(ctx, blocks, srcs, dsts);
+  if (e != hipSuccess) return e;
   *result = z;
   return hipSuccess;
 }
@@ -1003,11 +1060,16 @@ ncodec_status run_decoder(ncodec_ctx* ctx, int nxt, double* d_bits = nullptr, in
     NC_HIP(ctx, pw(ctx, "up_fuse", LD_UP_CTX, EP_UP, a), "upsample + fuse_dec");
   }
 
-  for (int k = 0; k < c.n_dec_blocks; ++k) {
-    void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
-    const BlockDev& b = L.dec[k];
-    NC_HIP(ctx, run_block(ctx, b, z, dst), "decoder block");
-    z = dst;
+  {
+    std::vector<const void*> srcs;
+    std::vector<void*> dsts;
+    for (int k = 0; k < c.n_dec_blocks; ++k) {
+      void* dst = (k == c.n_dec_blocks - 1) ? f_new : (z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA));
+      srcs.push_back(z);
+      dsts.push_back(dst);
+      z = dst;
+    }
+    NC_HIP(ctx, run_blocks(ctx, L.dec, srcs, dsts), "decoder blocks");
   }
   return NCODEC_OK;
 }
@@ -1143,11 +1205,16 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   NC_HIP(ctx, pw(ctx, ctx->is_int() ? "fuse" : "embed_fuse", ctx->is_int() ? LD_NHWC : LD_FRAME_CTX, EP_NHWC, a),
          "fuse_enc");
 
-  for (int k = 0; k < c.n_enc_blocks; ++k) {
-    void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
-    const BlockDev& b = L.enc[k];
-    NC_HIP(ctx, run_block(ctx, b, z, dst), "encoder block");
-    z = dst;
+  {
+    std::vector<const void*> srcs;
+    std::vector<void*> dsts;
+    for (int k = 0; k < c.n_enc_blocks; ++k) {
+      void* dst = z == ctx->p(L.zA) ? ctx->p(L.zB) : ctx->p(L.zA);
+      srcs.push_back(z);
+      dsts.push_back(dst);
+      z = dst;
+    }
+    NC_HIP(ctx, run_blocks(ctx, L.enc, srcs, dsts), "encoder blocks");
   }
 
   a = conv_args(ctx, L.down, 4 * C, C, P16);
@@ -1772,8 +1839,18 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
   return NCODEC_OK;
 }
 
-int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
-  if (!ctx) return 0;
+// Launches of a run of n DC blocks (chains: up to kMaxChain blocks each).
+int block_launches(ncodec_ctx* ctx, int n) {
+  const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
+  if (!ctx->chains || ctx->is_int() || ctx->cfg.channels != 256 || n < 2) return n;
+  if (ctx->chain_fit < 0)
+    ctx->chain_fit = dcchain128_resident(gated) >= dc_grid(ctx->cfg.height / 8, ctx->cfg.width / 8) ? 1 : 0;
+  return ctx->chain_fit == 1 ? (n + kMaxChain - 1) / kMaxChain : n;
+}
+
+int32_t ncodec_kernels_per_frame(const ncodec_ctx* cctx, int32_t decode) {
+  if (!cctx) return 0;
+  ncodec_ctx* ctx = const_cast<ncodec_ctx*>(cctx);  // caches the residency check
   const ncodec_config& c = ctx->cfg;
   // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
   // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
@@ -1782,6 +1859,11 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode) {
   const int fold = c.path == NCODEC_PATH_INT16 ? 0 : 1;
   const int hyper = c.hyperprior ? 3 : 0;
   const int per_block = c.channels > 256 ? 3 : 1;  // a wide block is three launches
+  if (per_block == 1) {  // one launch per block or per chain of blocks
+    const int fe = block_launches(ctx, c.n_fe_blocks), dec = block_launches(ctx, c.n_dec_blocks);
+    if (decode) return 4 - fold + hyper + fe + dec + block_launches(ctx, c.n_rg_blocks);
+    return 6 - 2 * fold + hyper + fe + block_launches(ctx, c.n_enc_blocks) + dec;
+  }
   if (decode) return 4 - fold + hyper + per_block * (c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks);
   // feature extractor, embed, fuse, encoder blocks, downsample, prior, upsample (with the bit total), fuse,
   // decoder blocks
@@ -1792,6 +1874,37 @@ ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable) {
   ncodec_status st = enter(ctx);
   if (st) return st;
   ctx->use_graphs = enable != 0;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_block_chains(ncodec_ctx* ctx, int32_t enable) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (ctx->chains != (enable != 0)) {
+    // captured graphs hold the other launch sequence: capture again on next use
+    NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "block_chains");
+    for (auto& row : ctx->graphs)
+      for (auto& gs : row) {
+        if (gs.exec) (void)hipGraphExecDestroy(gs.exec);
+        if (gs.graph) (void)hipGraphDestroy(gs.graph);
+        gs = ncodec_ctx::GraphSlot{};
+      }
+  }
+  ctx->chains = enable != 0;
+  return NCODEC_OK;
+}
+
+ncodec_status ncodec_block_chain_status(ncodec_ctx* ctx, int32_t* in_use, int32_t* timeouts) {
+  ncodec_status st = enter(ctx);
+  if (st) return st;
+  if (!in_use || !timeouts) return fail(ctx, NCODEC_EINVAL, "in_use and timeouts must not be NULL");
+  *in_use = block_launches(ctx, 2) == 1 ? 1 : 0;
+  *timeouts = 0;
+  if (!ctx->L.chain_status) return NCODEC_OK;
+  int32_t v = 0;
+  NC_HIP(ctx, hipMemcpyAsync(&v, ctx->p(ctx->L.chain_status), 4, hipMemcpyDeviceToHost, ctx->stream), "chain status");
+  NC_HIP(ctx, hipStreamSynchronize(ctx->stream), "chain status");
+  *timeouts = v;
   return NCODEC_OK;
 }
 

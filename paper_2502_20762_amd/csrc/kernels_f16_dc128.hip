@@ -96,23 +96,79 @@ __device__ __forceinline__ void unrolled(F& f, std::integer_sequence<int, T...>)
 // gated pair 4 r + w, and the hand-off writes g = WSiLU(h1) h2 (32 channels,
 // two k-steps) instead of the LeakyReLU of two chunks; pw2 contracts C = 256
 // gated channels (16 k-steps) instead of 2C.
-template <bool GATED>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcblock128_f16(BlockArgs a) {
+//
+// CHAIN: blocks 0 .. nb - 1 of a transform in one launch (blk[b] reads
+// blk[b - 1].dst).  Each tile keeps its block output in LDS, written straight
+// into the next block's band interior, so between blocks only the ring of the
+// band (the neighbours' edge pixels) moves through memory: a block other than
+// the last stores only the tile's 44 edge pixels, then publishes its progress
+// in flags[tile]; the next block waits until every neighbouring tile has
+// published that block, then reads its ring (edge stores, ring loads and the
+// progress words are device-coherent accesses; the stores' acknowledgements
+// are awaited before the word is written).  Every tile of the grid must be
+// resident at once (one workgroup per CU; the host checks the occupancy), and
+// each wait gives up after a bounded time, recording it in *status.  flags
+// hold a running count: every launch adds nb - 1 to each tile's word, so all
+// words are equal between launches and a launch reads its base from its own
+// tile's word.
+
+// 16-byte device-coherent accesses (the sc1 policy of device-scope atomics:
+// past this XCD's L2 to the device's point of coherence), whole 128-byte lines
+// per 8 lanes, without a cache-wide fence (a fence would write back or drop
+// the whole L2, weights included).  The load's result may only be used after
+// wait_coherent() on it.
+__device__ __forceinline__ half8 load_coherent16(const f16* p) {
+  half8 v;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void store_coherent16(f16* p, half8 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
+
+// One block of a tile (FIRST: its band comes whole from a.src; LAST: its
+// output goes whole to a.dst; otherwise the chain's ring and edge exchange).
+template <bool GATED, bool CHAIN, bool FIRST, bool LAST>
+__device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int b, int tile, int tiles_x, int tiles_y,
+                                            int wave0, int base, int* flags, int* status) {
   using namespace dcw;
   constexpr int KH = GATED ? KS / 2 : KS;  // hidden k-steps per round (the pw2 k-steps of a round)
   constexpr int NT = 2 * KS + 2 * KH;      // weight-stream steps: pw1 rounds 0, 1, pw2
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  const int tiles_x = (a.w + TW - 1) / TW;
-  const int ntile = tiles_x * ((a.h + TH - 1) / TH);
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  if (tile >= ntile) return;
-  const int ty0 = (tile / tiles_x) * TH, tx0 = (tile % tiles_x) * TW;
-  const int lane = threadIdx.x & 63, h = lane >> 5;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tyi = tile / tiles_x, txi = tile - tyi * tiles_x;
+  const int ty0 = tyi * TH, tx0 = txi * TW;
+  // the wave index, opaque to the compiler: keeps the weight-stream offsets
+  // (scalar, one per step) from being hoisted out of the chain's block loop,
+  // where they would all stay live at once
+  int wave = wave0;
+  asm volatile("" : "+s"(wave));
+  // the same for the lane index and everything derived from it (the LDS and
+  // global offsets of the unrolled loops)
+  int lane = threadIdx.x & 63;
+  asm volatile("" : "+v"(lane));
+  const int h = lane >> 5;
+  const int myslot = bslot(lane) * 16;
+  constexpr bool first = FIRST, last = LAST;
   const f16* z = (const f16*)a.src;
   const f16* zpad = (const f16*)a.zpad;
   const half8* wimg = (const half8*)a.w1 + lane;  // fragment (chunk j, f) at [(j FR + f) 64]
-  const int myslot = bslot(lane) * 16;
+  if (CHAIN && !first) {
+    // every neighbouring tile has published block b - 1 (its edge pixels are
+    // in a.src): one lane of wave 0 per neighbour polls its word
+    if (wave == 0 && lane < 9 && lane != 4) {
+      const int ny = tyi + lane / 3 - 1, nx = txi + lane % 3 - 1;
+      if (ny >= 0 && ny < tiles_y && nx >= 0 && nx < tiles_x) {
+        const int* f = flags + ny * tiles_x + nx;
+        for (int spin = 0; __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + b; ++spin) {
+          if (spin > (1 << 16)) {  // about 0.1 s (a poll is a memory round trip): give up, record it
+            __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
+    }
+    lds_barrier();
+  }
 
   // weight-stream step t, fragment c: pw1 round 0 (t < 16: entry 2 w + c,
   // k-step t), round 1 (t < 32: entry 8 + 2 w + c, k-step t - 16), pw2
@@ -181,8 +237,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
     // the band's first BAND_FIRST loads now, the rest after the first output row
     constexpr int BAND_FIRST = 14;
+    if (first) {
 #pragma unroll
-    for (int i = 0; i < BAND_FIRST; ++i) band_load(i);
+      for (int i = 0; i < BAND_FIRST; ++i) band_load(i);
+    } else {
+      // the ring (52 pixels: rows -1 and 8, columns -1 and 16 of rows 0 .. 7)
+      // through registers; the interior is this tile's previous output
+      constexpr int RING = 2 * BW + 2 * TH;
+      half8 rv[(RING * 8 + 63) / 64];
+      int ro[(RING * 8 + 63) / 64];
+#pragma unroll
+      for (int i = 0; i < (RING * 8 + 63) / 64; ++i) {
+        const int S = i * 64 + lane, r = S >> 3, u = S & 7;
+        const int by = r < BW ? 0 : r < 2 * BW ? BH - 1 : 1 + (r - 2 * BW) % TH;
+        const int bx = r < BW ? r : r < 2 * BW ? r - BW : (r < 2 * BW + TH ? 0 : BW - 1);
+        const int hy = ty0 - 1 + by, hx = tx0 - 1 + bx;
+        const bool in = S < RING * 8 && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+        // device-coherent loads (they bypass this XCD's L2, which may hold
+        // an older copy of the line): the neighbours wrote these pixels in
+        // this launch
+        rv[i] = load_coherent16(in ? z + (size_t)(hy * a.w + hx) * C + 64 * wave + 8 * u : zpad);
+        ro[i] = S < RING * 8 ? by * BROW + bx * 128 + ((u ^ bswz(bx)) << 4) : -1;
+      }
+      // the loads are opaque to the compiler: wait for them with the values
+      // as operands, so nothing reads them earlier
+      static_assert((RING * 8 + 63) / 64 == 7, "seven ring loads per lane");
+      asm volatile("s_waitcnt vmcnt(0)"
+                   : "+v"(rv[0]), "+v"(rv[1]), "+v"(rv[2]), "+v"(rv[3]), "+v"(rv[4]), "+v"(rv[5]), "+v"(rv[6])
+                   :
+                   : "memory");
+#pragma unroll
+      for (int i = 0; i < (RING * 8 + 63) / 64; ++i)
+        if (ro[i] >= 0) *(half8*)(band + ro[i]) = rv[i];
+    }
     // the lane's band reads: column col(i) of a row, its channel pair's dword
     int va[TW / 2 + 2];
 #pragma unroll
@@ -244,15 +331,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
     // output row r needs band rows .. r + 2: wait until at most
     // (issued - 1 - band_row_load(r + 2)) band loads are outstanding
-#define DW_WAIT(r, issued) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((issued) - 1 - band_row_load((r) + 2)) : "memory")
+#define DW_WAIT(r, issued) \
+  if (first) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((issued) - 1 - band_row_load((r) + 2)) : "memory")
     static_assert(BAND_FIRST > band_row_load(2), "the first output row's band rows are requested first");
     DW_WAIT(0, BAND_FIRST);
     load_row(0);
     load_row(1);
     load_row(2);
     dw_row(0);
+    if (first) {
 #pragma unroll
-    for (int i = BAND_FIRST; i < BAND_INSTR; ++i) band_load(i);
+      for (int i = BAND_FIRST; i < BAND_INSTR; ++i) band_load(i);
+    }
     DW_WAIT(1, BAND_INSTR);
     load_row(3);
     dw_row(1);
@@ -290,6 +380,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           for (int q = 0; q < 2; ++q) res[c][g][q] = *(const half8*)(rb + 2 * g * BROW + ((f ^ (4 * c + 2 * q)) << 4));
     }
   }
+  // the bias loads of wave 0 (the band waits above cover them on a first block)
+  if (!first) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   lds_barrier();  // a complete; every wave holds its residual, the bands are free
 
   // ---- 2, 3. pw1 (steps 0 .. 31) and pw2 (steps 32 .. 63)
@@ -435,50 +527,140 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   };
   unrolled(step, std::make_integer_sequence<int, NT>{});
 
-  // ---- epilogue: one rounding to fp16, parked in LDS from offset 0 (row =
-  // tile pixel, 8-byte unit u of the row at u ^ (row & 15)), stored as
-  // 16-byte vectors
   lds_barrier();  // every wave is done reading the hidden layer
+  if (last) {
+    // ---- epilogue: one rounding to fp16, parked in LDS from offset 0 (row =
+    // tile pixel, 8-byte unit u of the row at u ^ (row & 15)), stored as
+    // 16-byte vectors
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int p = 32 * g + (lane & 31);
+      for (int g = 0; g < 4; ++g) {
+        const int p = 32 * g + (lane & 31);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int cc = 64 * wave + 32 * c + 8 * q + 4 * h;
-        half4 o;
+        for (int q = 0; q < 4; ++q) {
+          const int cc = 64 * wave + 32 * c + 8 * q + 4 * h;
+          half4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (f16)acc[c][g][4 * q + e];
-        *(half4*)(smem + p * 512 + (((cc >> 2) ^ (p & 15)) << 3)) = o;
+          for (int e = 0; e < 4; ++e) o[e] = (f16)acc[c][g][4 * q + e];
+          *(half4*)(smem + p * 512 + (((cc >> 2) ^ (p & 15)) << 3)) = o;
+        }
+      }
+    lds_barrier();
+    f16* dst = (f16*)a.dst;
+#pragma unroll
+    for (int i = 0; i < TH * TW * 32 / 256; ++i) {
+      const int idx = i * 256 + threadIdx.x;
+      const int px = idx >> 5, k8 = idx & 31;  // tile pixel, 8-channel unit
+      const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
+      if (yy < a.h && xx < a.w) {
+        const char* ob = smem + px * 512;
+        // units 2 k8 and 2 k8 + 1 are the aligned pair at 2 k8 ^ (px & 14), swapped when px is odd
+        const half8 pv = *(const half8*)(ob + (((2 * k8) ^ (px & 14)) << 3));
+        half8 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[e] = (px & 1) ? pv[4 + e] : pv[e];
+          o[4 + e] = (px & 1) ? pv[e] : pv[4 + e];
+        }
+        __builtin_nontemporal_store(o, (half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8));
       }
     }
-  lds_barrier();
-  f16* dst = (f16*)a.dst;
+  } else {
+    // ---- a block of a chain: the output (one rounding to fp16; zero outside
+    // the image, the next depthwise's padding) goes into the interior of the
+    // wave's own band: pixel (1 + y, 1 + x), 16-byte unit u = 4 c + q, half h
+    char* const band = smem + wave * REG;
 #pragma unroll
-  for (int i = 0; i < TH * TW * 32 / 256; ++i) {
-    const int idx = i * 256 + threadIdx.x;
-    const int px = idx >> 5, k8 = idx & 31;  // tile pixel, 8-channel unit
-    const int yy = ty0 + (px >> 4), xx = tx0 + (px & 15);
-    if (yy < a.h && xx < a.w) {
-      const char* ob = smem + px * 512;
-      // units 2 k8 and 2 k8 + 1 are the aligned pair at 2 k8 ^ (px & 14), swapped when px is odd
-      const half8 pv = *(const half8*)(ob + (((2 * k8) ^ (px & 14)) << 3));
-      half8 o;
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        o[e] = (px & 1) ? pv[4 + e] : pv[e];
-        o[4 + e] = (px & 1) ? pv[e] : pv[4 + e];
+      for (int g = 0; g < 4; ++g) {
+        const int p = 32 * g + (lane & 31), py = p >> 4, px = p & 15;
+        const bool in = ty0 + py < a.h && tx0 + px < a.w;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          half4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = in ? (f16)acc[c][g][4 * q + e] : (f16)0.f;
+          *(half4*)(band + (1 + py) * BROW + (1 + px) * 128 + (((4 * c + q) ^ bswz(1 + px)) << 4) + 8 * h) = o;
+        }
       }
-      __builtin_nontemporal_store(o, (half8*)(dst + (size_t)(yy * a.w + xx) * C + 8 * k8));
+    // the tile's 44 edge pixels (rows 0 and 7, columns 0 and 15), the wave's
+    // 64 channels, from the band to memory for the neighbours' rings
+    f16* dst = (f16*)a.dst;
+    constexpr int EDGE = 2 * TW + 2 * (TH - 2);
+#pragma unroll
+    for (int i = 0; i < (EDGE * 8 + 63) / 64; ++i) {
+      const int S = i * 64 + lane, e = S >> 3, u = S & 7;
+      const int py = e < TW ? 0 : e < 2 * TW ? TH - 1 : 1 + (e - 2 * TW) % (TH - 2);
+      const int px = e < TW ? e : e < 2 * TW ? e - TW : (e < 2 * TW + TH - 2 ? 0 : TW - 1);
+      const int yy = ty0 + py, xx = tx0 + px;
+      if (S < EDGE * 8 && yy < a.h && xx < a.w) {
+        const half8 v = *(const half8*)(band + (1 + py) * BROW + (1 + px) * 128 + ((u ^ bswz(1 + px)) << 4));
+        store_coherent16(dst + (size_t)(yy * a.w + xx) * C + 64 * wave + 8 * u, v);
+      }
     }
+    // publish: every wave's edge stores are complete at the device's point of
+    // coherence (their acknowledgements counted down) before the tile's word
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    if (threadIdx.x == 0) __hip_atomic_store(flags + tile, base + b + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+}
+
+template <bool GATED, bool CHAIN>
+__device__ __forceinline__ void dc128_body(const BlockArgs* blk, int nb, int* flags, int* status) {
+  using namespace dcw;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  const int tiles_x = (blk[0].w + TW - 1) / TW, tiles_y = (blk[0].h + TH - 1) / TH;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  if (tile >= tiles_x * tiles_y) return;
+  const int wave0 = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if constexpr (!CHAIN) {
+    dc128_block<GATED, false, true, true>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, 0, nullptr, nullptr);
+  } else {
+    // nb >= 2: the first block, the middle ones, the last
+    const int base = __builtin_amdgcn_readfirstlane(__hip_atomic_load(flags + tile, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    dc128_block<GATED, true, true, false>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, base, flags, status);
+    for (int b = 1; b < nb - 1; ++b)
+      dc128_block<GATED, true, false, false>(smem, blk[b], b, tile, tiles_x, tiles_y, wave0, base, flags, status);
+    dc128_block<GATED, true, false, true>(smem, blk[nb - 1], nb - 1, tile, tiles_x, tiles_y, wave0, base, flags, status);
+  }
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcblock128_f16(BlockArgs a) {
+  dc128_body<GATED, false>(&a, 1, nullptr, nullptr);
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcchain128_f16(DcChainArgs ca) {
+  dc128_body<GATED, true>(ca.blk, ca.nb, ca.flags, ca.status);
 }
 
 hipError_t launch_dcblock128_f16(bool gated, const BlockArgs& a, hipStream_t st) {
   if (gated) launch(k_dcblock128_f16<true>, dim3(dc_grid(a.h, a.w)), dim3(256), st, a);
   else launch(k_dcblock128_f16<false>, dim3(dc_grid(a.h, a.w)), dim3(256), st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_dcchain128_f16(bool gated, const DcChainArgs& ca, hipStream_t st) {
+  if (ca.nb < 2 || ca.nb > kMaxChain) return hipErrorInvalidValue;
+  const dim3 grid(dc_grid(ca.blk[0].h, ca.blk[0].w));
+  if (gated) launch(k_dcchain128_f16<true>, grid, dim3(256), st, ca);
+  else launch(k_dcchain128_f16<false>, grid, dim3(256), st, ca);
+  return hipGetLastError();
+}
+
+// Workgroups of the chain kernel that fit the device at once (one per CU
+// with its 160 KiB of LDS); the chain needs every tile resident.
+int dcchain128_resident(bool gated) {
+  int dev = 0, per_cu = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  const hipError_t e = gated ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dcchain128_f16<true>, 256, 0)
+                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dcchain128_f16<false>, 256, 0);
+  return e == hipSuccess ? per_cu * cus : 0;
 }
 
 }  // namespace nc

@@ -83,6 +83,8 @@ _SIGNATURES = {
     "ncodec_kernels_per_frame": (ctypes.c_int32, [_P, ctypes.c_int32]),
     "ncodec_timing_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
     "ncodec_graph_enable": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "ncodec_block_chains": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "ncodec_block_chain_status": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "ncodec_timing_read": (ctypes.c_int, [_P, ctypes.POINTER(ncodec_kernel_timing), ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_int32)]),
     "ncodec_last_error": (ctypes.c_char_p, [_P]),
@@ -231,6 +233,17 @@ def ncodec_timing_enable(ctx, enable: bool) -> None:
 
 def ncodec_graph_enable(ctx, enable: bool) -> None:
     _check(load_library().ncodec_graph_enable(ctx, 1 if enable else 0), ctx)
+
+
+def ncodec_block_chains(ctx, enable: bool) -> None:
+    _check(load_library().ncodec_block_chains(ctx, 1 if enable else 0), ctx)
+
+
+def ncodec_block_chain_status(ctx) -> tuple:
+    """(in_use, timeouts) of the context's block chains."""
+    u, v = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load_library().ncodec_block_chain_status(ctx, ctypes.byref(u), ctypes.byref(v)), ctx)
+    return int(u.value), int(v.value)
 
 
 def ncodec_timing_read(ctx) -> dict:
@@ -404,6 +417,12 @@ class Codec:
 
     def graphs(self, enable: bool):
         ncodec_graph_enable(self.ctx, enable)
+
+    def block_chains(self, enable: bool):
+        ncodec_block_chains(self.ctx, enable)
+
+    def block_chain_status(self) -> tuple:
+        return ncodec_block_chain_status(self.ctx)
 
     def timing_read(self) -> dict:
         return ncodec_timing_read(self.ctx)

@@ -1,0 +1,92 @@
+"""Block chains (the fp16 C = 256 DC blocks of a transform in one launch, tiles
+exchanging only their edge pixels) against one launch per block, through the
+C ABI: both run the same per-block arithmetic, so q, the frame bits, the
+state and the decoded frame must agree bitwise, and no chain wait may time
+out.  Sizes: 1080p with 8 + 8 blocks (the benchmarked transform, 255 tiles),
+a ragged 272 x 400 frame (34 x 50 latent pixels at 1/8: partial tiles on the
+right and bottom), the gated form, chains through the feature extractor and
+reconstruction generation, and graph replay.  The chains themselves are
+checked against the oracle by every fp16 C = 256 parity test, which runs them
+by default."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from paper_2502_20762_amd.ncodec import Codec
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[gpu-chain]", *a, flush=True)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def run(H, W, C, ne, nd, frames, chains, block="lrelu", graphs=False, **mods):
+    flat = synth.make_weights(C, ne, nd, block=block, n_fe=mods.get("n_fe_blocks", 0),
+                              n_rg=mods.get("n_rg_blocks", 0))
+    enc = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block, **mods)
+    dec = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block, **mods)
+    for cdc in (enc, dec):
+        cdc.block_chains(chains)
+        cdc.graphs(graphs)
+    out = []
+    for x in frames:
+        q, bits = enc.encode(torch.from_numpy(x).to(DEV))
+        xh = dec.decode(q)
+        out.append((host(q), float(bits.item()) if hasattr(bits, "item") else bits,
+                    [host(v) for v in enc.get_state()], host(xh)))
+    counts = (enc.kernels_per_frame(False), dec.kernels_per_frame(True))
+    for cdc in (enc, dec):
+        in_use, timeouts = cdc.block_chain_status()
+        assert in_use == (1 if chains else 0), (chains, in_use)
+        assert timeouts == 0, "a chain wait timed out"
+    return out, counts
+
+
+def compare(a, b, what):
+    for k, ((qa, ba, sa, xa), (qb, bb, sb, xb)) in enumerate(zip(a, b)):
+        np.testing.assert_array_equal(qa, qb, err_msg=f"{what} frame {k}: q")
+        assert ba == bb, (what, k, ba, bb)
+        for u, v in zip(sa, sb):
+            np.testing.assert_array_equal(u, v, err_msg=f"{what} frame {k}: state")
+        np.testing.assert_array_equal(xa, xb, err_msg=f"{what} frame {k}: xhat")
+
+
+def test_chain_hd1080_matches_per_block_launches():
+    pre = synth.PRESETS["hd1080"]
+    H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
+    frames = list(synth.frame_sequence(pre, 2))
+    say("1080p, chains on")
+    on, c_on = run(H, W, C, ne, nd, frames, True)
+    say("1080p, chains off")
+    off, c_off = run(H, W, C, ne, nd, frames, False)
+    compare(on, off, "1080p")
+    # one launch per transform's blocks with chains (8 blocks each)
+    assert c_off == (4 + ne + nd, 3 + nd), c_off
+    assert c_on == (4 + 2, 3 + 1), c_on
+
+
+@pytest.mark.parametrize("block", ["lrelu", "gated"])
+def test_chain_ragged_matches_per_block_launches(block):
+    frames = [synth.random_frame(272, 400, seed=s) for s in (30, 31)]
+    say("272x400", block)
+    on, _ = run(272, 400, 256, 3, 3, frames, True, block=block)
+    off, _ = run(272, 400, 256, 3, 3, frames, False, block=block)
+    compare(on, off, f"272x400 {block}")
+
+
+def test_chain_modules_and_graphs_match_per_block_launches():
+    frames = [synth.random_frame(128, 192, seed=s) for s in (32, 33, 34)]
+    mods = dict(n_fe_blocks=2, n_rg_blocks=2)
+    say("128x192 with the modules, graphs")
+    on, _ = run(128, 192, 256, 2, 2, frames, True, graphs=True, **mods)
+    off, _ = run(128, 192, 256, 2, 2, frames, False, graphs=False, **mods)
+    compare(on, off, "128x192 modules")
