@@ -151,25 +151,6 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
   const f16* z = (const f16*)a.src;
   const f16* zpad = (const f16*)a.zpad;
   const half8* wimg = (const half8*)a.w1 + lane;  // fragment (chunk j, f) at [(j FR + f) 64]
-  if (CHAIN && !first) {
-    // every neighbouring tile has published block b - 1 (its edge pixels are
-    // in a.src): one lane of wave 0 per neighbour polls its word
-    if (wave == 0 && lane < 9 && lane != 4) {
-      const int ny = tyi + lane / 3 - 1, nx = txi + lane % 3 - 1;
-      if (ny >= 0 && ny < tiles_y && nx >= 0 && nx < tiles_x) {
-        const int* f = flags + ny * tiles_x + nx;
-        for (int spin = 0; __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + b; ++spin) {
-          if (spin > (1 << 16)) {  // about 0.1 s (a poll is a memory round trip): give up, record it
-            __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-    }
-    lds_barrier();
-  }
-
   // weight-stream step t, fragment c: pw1 round 0 (t < 16: entry 2 w + c,
   // k-step t), round 1 (t < 32: entry 8 + 2 w + c, k-step t - 16), pw2
   // (k = t - 32: output tile 2 w + c, half k % 2 of the entry holding hidden
@@ -240,35 +221,6 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
     if (first) {
 #pragma unroll
       for (int i = 0; i < BAND_FIRST; ++i) band_load(i);
-    } else {
-      // the ring (52 pixels: rows -1 and 8, columns -1 and 16 of rows 0 .. 7)
-      // through registers; the interior is this tile's previous output
-      constexpr int RING = 2 * BW + 2 * TH;
-      half8 rv[(RING * 8 + 63) / 64];
-      int ro[(RING * 8 + 63) / 64];
-#pragma unroll
-      for (int i = 0; i < (RING * 8 + 63) / 64; ++i) {
-        const int S = i * 64 + lane, r = S >> 3, u = S & 7;
-        const int by = r < BW ? 0 : r < 2 * BW ? BH - 1 : 1 + (r - 2 * BW) % TH;
-        const int bx = r < BW ? r : r < 2 * BW ? r - BW : (r < 2 * BW + TH ? 0 : BW - 1);
-        const int hy = ty0 - 1 + by, hx = tx0 - 1 + bx;
-        const bool in = S < RING * 8 && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
-        // device-coherent loads (they bypass this XCD's L2, which may hold
-        // an older copy of the line): the neighbours wrote these pixels in
-        // this launch
-        rv[i] = load_coherent16(in ? z + (size_t)(hy * a.w + hx) * C + 64 * wave + 8 * u : zpad);
-        ro[i] = S < RING * 8 ? by * BROW + bx * 128 + ((u ^ bswz(bx)) << 4) : -1;
-      }
-      // the loads are opaque to the compiler: wait for them with the values
-      // as operands, so nothing reads them earlier
-      static_assert((RING * 8 + 63) / 64 == 7, "seven ring loads per lane");
-      asm volatile("s_waitcnt vmcnt(0)"
-                   : "+v"(rv[0]), "+v"(rv[1]), "+v"(rv[2]), "+v"(rv[3]), "+v"(rv[4]), "+v"(rv[5]), "+v"(rv[6])
-                   :
-                   : "memory");
-#pragma unroll
-      for (int i = 0; i < (RING * 8 + 63) / 64; ++i)
-        if (ro[i] >= 0) *(half8*)(band + ro[i]) = rv[i];
     }
     // the lane's band reads: column col(i) of a row, its channel pair's dword
     int va[TW / 2 + 2];
@@ -312,72 +264,166 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
         P1[y][i] = __builtin_bit_cast(half2, __builtin_amdgcn_perm(vr[i + 1], vr[i], 0x07060302u));
       }
     };
+    // one output (row r, step k) of the channel pair, written into a
+    auto dw_out = [&](int r, int k) __attribute__((always_inline)) {
+      float a0 = bias0, a1 = bias1;
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        a0 = __builtin_amdgcn_fdot2(W0a[ky], P0[r + ky][k], a0, false);
+        a0 = __builtin_amdgcn_fdot2(W0b[ky], P0[r + ky][k + 1], a0, false);
+        a1 = __builtin_amdgcn_fdot2(W1a[ky], P1[r + ky][k], a1, false);
+        a1 = __builtin_amdgcn_fdot2(W1b[ky], P1[r + ky][k + 1], a1, false);
+      }
+      half2 o;
+      o[0] = (f16)a0;
+      o[1] = (f16)a1;
+      *(half2*)(smem + wa[r & 1][k] + 16 * (r >> 1) * XF) = o;
+    };
     auto dw_row = [&](int r) __attribute__((always_inline)) {
 #pragma unroll
-      for (int k = 0; k < TW / 2; ++k) {
-        float a0 = bias0, a1 = bias1;
-#pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-          a0 = __builtin_amdgcn_fdot2(W0a[ky], P0[r + ky][k], a0, false);
-          a0 = __builtin_amdgcn_fdot2(W0b[ky], P0[r + ky][k + 1], a0, false);
-          a1 = __builtin_amdgcn_fdot2(W1a[ky], P1[r + ky][k], a1, false);
-          a1 = __builtin_amdgcn_fdot2(W1b[ky], P1[r + ky][k + 1], a1, false);
-        }
-        half2 o;
-        o[0] = (f16)a0;
-        o[1] = (f16)a1;
-        *(half2*)(smem + wa[r & 1][k] + 16 * (r >> 1) * XF) = o;
-      }
+      for (int k = 0; k < TW / 2; ++k) dw_out(r, k);
     };
-    // output row r needs band rows .. r + 2: wait until at most
-    // (issued - 1 - band_row_load(r + 2)) band loads are outstanding
-#define DW_WAIT(r, issued) \
-  if (first) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((issued) - 1 - band_row_load((r) + 2)) : "memory")
-    static_assert(BAND_FIRST > band_row_load(2), "the first output row's band rows are requested first");
-    DW_WAIT(0, BAND_FIRST);
-    load_row(0);
-    load_row(1);
-    load_row(2);
-    dw_row(0);
-    if (first) {
+    if constexpr (first) {
+      // output row r needs band rows .. r + 2: wait until at most
+      // (issued - 1 - band_row_load(r + 2)) band loads are outstanding
+#define DW_WAIT(r, issued) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((issued) - 1 - band_row_load((r) + 2)) : "memory")
+      static_assert(BAND_FIRST > band_row_load(2), "the first output row's band rows are requested first");
+      DW_WAIT(0, BAND_FIRST);
+      load_row(0);
+      load_row(1);
+      load_row(2);
+      dw_row(0);
 #pragma unroll
       for (int i = BAND_FIRST; i < BAND_INSTR; ++i) band_load(i);
-    }
-    DW_WAIT(1, BAND_INSTR);
-    load_row(3);
-    dw_row(1);
-    DW_WAIT(2, BAND_INSTR);
-    load_row(4);
-    dw_row(2);
-    DW_WAIT(3, BAND_INSTR);
-    load_row(5);
-    dw_row(3);
-    DW_WAIT(4, BAND_INSTR);
-    load_row(6);
-    dw_row(4);
-    DW_WAIT(5, BAND_INSTR);
-    load_row(7);
-    dw_row(5);
-    DW_WAIT(6, BAND_INSTR);
-    load_row(8);
-    dw_row(6);
-    DW_WAIT(7, BAND_INSTR);
-    load_row(9);
-    dw_row(7);
+      DW_WAIT(1, BAND_INSTR);
+      load_row(3);
+      dw_row(1);
+      DW_WAIT(2, BAND_INSTR);
+      load_row(4);
+      dw_row(2);
+      DW_WAIT(3, BAND_INSTR);
+      load_row(5);
+      dw_row(3);
+      DW_WAIT(4, BAND_INSTR);
+      load_row(6);
+      dw_row(4);
+      DW_WAIT(5, BAND_INSTR);
+      load_row(7);
+      dw_row(5);
+      DW_WAIT(6, BAND_INSTR);
+      load_row(8);
+      dw_row(6);
+      DW_WAIT(7, BAND_INSTR);
+      load_row(9);
+      dw_row(7);
 #undef DW_WAIT
-    // the residual of the wave's outputs is its band's interior: (c, g, q),
-    // lane = pixel 32 g + lane % 32 of the tile (band row 1 + 2 g + n / 16,
-    // column 1 + n % 16), unit 4 c + 2 q + lane / 32
-    {
-      const int n = lane & 31, x = 1 + (n & 15);
-      const char* rb = band + (1 + (n >> 4)) * BROW + x * 128;
-      const int f = bswz(x) ^ h;
+      // the residual of the wave's outputs is its band's interior: (c, g, q),
+      // lane = pixel 32 g + lane % 32 of the tile (band row 1 + 2 g + n / 16,
+      // column 1 + n % 16), unit 4 c + 2 q + lane / 32
+      {
+        const int n = lane & 31, x = 1 + (n & 15);
+        const char* rb = band + (1 + (n >> 4)) * BROW + x * 128;
+        const int f = bswz(x) ^ h;
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+          for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int q = 0; q < 2; ++q) res[c][g][q] = *(const half8*)(rb + 2 * g * BROW + ((f ^ (4 * c + 2 * q)) << 4));
+            for (int q = 0; q < 2; ++q) res[c][g][q] = *(const half8*)(rb + 2 * g * BROW + ((f ^ (4 * c + 2 * q)) << 4));
+      }
+    } else {
+      // pass 1, before this block's ring is known: the outputs that read only
+      // the interior (rows 1 .. 6, steps 1 .. 7 of each half row: band
+      // columns 1 .. 16), and the residual
+      auto load_inner = [&](int y) __attribute__((always_inline)) {
+        uint32_t vr[TW / 2 + 2];
+#pragma unroll
+        for (int i = 1; i < TW / 2 + 2; ++i) vr[i] = *(const uint32_t*)(band + y * BROW + va[i]);
+#pragma unroll
+        for (int i = 1; i < TW / 2 + 1; ++i) {
+          P0[y][i] = __builtin_bit_cast(half2, __builtin_amdgcn_perm(vr[i + 1], vr[i], 0x05040100u));
+          P1[y][i] = __builtin_bit_cast(half2, __builtin_amdgcn_perm(vr[i + 1], vr[i], 0x07060302u));
+        }
+      };
+      load_inner(1);
+      load_inner(2);
+#pragma unroll
+      for (int r = 1; r <= TH - 2; ++r) {
+        load_inner(r + 2);
+#pragma unroll
+        for (int k = 1; k < TW / 2; ++k) dw_out(r, k);
+      }
+      // the residual of the wave's outputs is its band's interior: (c, g, q),
+      // lane = pixel 32 g + lane % 32 of the tile (band row 1 + 2 g + n / 16,
+      // column 1 + n % 16), unit 4 c + 2 q + lane / 32
+      {
+        const int n = lane & 31, x = 1 + (n & 15);
+        const char* rb = band + (1 + (n >> 4)) * BROW + x * 128;
+        const int f = bswz(x) ^ h;
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int q = 0; q < 2; ++q) res[c][g][q] = *(const half8*)(rb + 2 * g * BROW + ((f ^ (4 * c + 2 * q)) << 4));
+      }
+      // the ring, once every neighbouring tile has published block b - 1 (its
+      // edge pixels are in a.src): one lane of wave 0 per neighbour polls its
+      // word
+      if (wave == 0 && lane < 9 && lane != 4) {
+        const int ny = tyi + lane / 3 - 1, nx = txi + lane % 3 - 1;
+        if (ny >= 0 && ny < tiles_y && nx >= 0 && nx < tiles_x) {
+          const int* f = flags + ny * tiles_x + nx;
+          for (int spin = 0; __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + b; ++spin) {
+            if (spin > (1 << 16)) {  // about 0.1 s (a poll is a memory round trip): give up, record it
+              __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+      }
+      lds_barrier();
+      // the ring (52 pixels: rows -1 and 8, columns -1 and 16 of rows 0 .. 7)
+      // through registers; the interior is this tile's previous output
+      constexpr int RING = 2 * BW + 2 * TH;
+      half8 rv[(RING * 8 + 63) / 64];
+      int ro[(RING * 8 + 63) / 64];
+#pragma unroll
+      for (int i = 0; i < (RING * 8 + 63) / 64; ++i) {
+        const int S = i * 64 + lane, r = S >> 3, u = S & 7;
+        const int by = r < BW ? 0 : r < 2 * BW ? BH - 1 : 1 + (r - 2 * BW) % TH;
+        const int bx = r < BW ? r : r < 2 * BW ? r - BW : (r < 2 * BW + TH ? 0 : BW - 1);
+        const int hy = ty0 - 1 + by, hx = tx0 - 1 + bx;
+        const bool in = S < RING * 8 && hy >= 0 && hy < a.h && hx >= 0 && hx < a.w;
+        // device-coherent loads (they bypass this XCD's L2, which may hold
+        // an older copy of the line): the neighbours wrote these pixels in
+        // this launch
+        rv[i] = load_coherent16(in ? z + (size_t)(hy * a.w + hx) * C + 64 * wave + 8 * u : zpad);
+        ro[i] = S < RING * 8 ? by * BROW + bx * 128 + ((u ^ bswz(bx)) << 4) : -1;
+      }
+      // the loads are opaque to the compiler: wait for them with the values
+      // as operands, so nothing reads them earlier
+      static_assert((RING * 8 + 63) / 64 == 7, "seven ring loads per lane");
+      asm volatile("s_waitcnt vmcnt(0)"
+                   : "+v"(rv[0]), "+v"(rv[1]), "+v"(rv[2]), "+v"(rv[3]), "+v"(rv[4]), "+v"(rv[5]), "+v"(rv[6])
+                   :
+                   : "memory");
+#pragma unroll
+      for (int i = 0; i < (RING * 8 + 63) / 64; ++i)
+        if (ro[i] >= 0) *(half8*)(band + ro[i]) = rv[i];
+      // pass 2: the outputs that read the ring, in the same order of taps
+      load_row(0);
+      load_row(1);
+      load_row(2);
+      dw_row(0);
+#pragma unroll
+      for (int r = 1; r <= TH - 2; ++r) {
+        load_row(r + 2);
+        dw_out(r, 0);
+      }
+      load_row(TH + 1);
+      dw_row(TH - 1);
     }
   }
   // the bias loads of wave 0 (the band waits above cover them on a first block)
