@@ -617,20 +617,27 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
     // the image, the next depthwise's padding) goes into the interior of the
     // wave's own band: pixel (1 + y, 1 + x), 16-byte unit u = 4 c + q, half h
     char* const band = smem + wave * REG;
+    // a tile that lies wholly inside the image needs no zeroing (uniform)
+    const bool full = ty0 + TH <= a.h && tx0 + TW <= a.w;
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int g = 0; g < 4; ++g) {
+      const int p = 32 * g + (lane & 31), py = p >> 4, px = p & 15;
+      char* const pb = band + (1 + py) * BROW + (1 + px) * 128 + 8 * h;
+      const int sw = bswz(1 + px);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int p = 32 * g + (lane & 31), py = p >> 4, px = p & 15;
-        const bool in = ty0 + py < a.h && tx0 + px < a.w;
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           half4 o;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = in ? (f16)acc[c][g][4 * q + e] : (f16)0.f;
-          *(half4*)(band + (1 + py) * BROW + (1 + px) * 128 + (((4 * c + q) ^ bswz(1 + px)) << 4) + 8 * h) = o;
+          for (int e = 0; e < 4; ++e) o[e] = (f16)acc[c][g][4 * q + e];
+          *(half4*)(pb + (((4 * c + q) ^ sw) << 4)) = o;
         }
+      if (!full && !(ty0 + py < a.h && tx0 + px < a.w)) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) *(half4*)(pb + ((u ^ sw) << 4)) = half4{};
       }
+    }
     // the tile's 44 edge pixels (rows 0 and 7, columns 0 and 15), the wave's
     // 64 channels, from the band to memory for the neighbours' rings
     f16* dst = (f16*)a.dst;
@@ -638,8 +645,11 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
 #pragma unroll
     for (int i = 0; i < (EDGE * 8 + 63) / 64; ++i) {
       const int S = i * 64 + lane, e = S >> 3, u = S & 7;
-      const int py = e < TW ? 0 : e < 2 * TW ? TH - 1 : 1 + (e - 2 * TW) % (TH - 2);
-      const int px = e < TW ? e : e < 2 * TW ? e - TW : (e < 2 * TW + TH - 2 ? 0 : TW - 1);
+      // edge e: row 0 (e < 16), row 7 (e < 32), column 0 of rows 1 .. 6
+      // (e < 38), column 15 of rows 1 .. 6
+      const int e6 = e - 2 * TW, side = e6 >= TH - 2 ? 1 : 0;
+      const int py = e < TW ? 0 : e < 2 * TW ? TH - 1 : 1 + e6 - side * (TH - 2);
+      const int px = e < TW ? e : e < 2 * TW ? e - TW : side * (TW - 1);
       const int yy = ty0 + py, xx = tx0 + px;
       if (S < EDGE * 8 && yy < a.h && xx < a.w) {
         const half8 v = *(const half8*)(band + (1 + py) * BROW + (1 + px) * 128 + ((u ^ bswz(1 + px)) << 4));
