@@ -173,7 +173,8 @@ __device__ __forceinline__ float symbol_bits(float q, float sigma) {
   const float L = 0.5f * (e1 - e2);
   const float b1 = -__log2f(fmaxf(L, 1e-9f));
   const float y = 1.f - e2, d = y - 1.f;  // log1p(-e2) = ln(y) (-e2) / d, or -e2 when y rounds to 1
-  const float l1p = d == 0.f ? -e2 : __logf(y) * (-e2 / d);
+  // (-e2 / d is within an ulp or two of 1: a reciprocal is accurate enough)
+  const float l1p = d == 0.f ? -e2 : __logf(y) * (-e2 * __builtin_amdgcn_rcpf(d));
   const float b0 = fminf(-1.44269504088896341f * l1p, 29.8973529f);  // -log2(1e-9)
   return a == 0.f ? b0 : b1;
 }

@@ -312,14 +312,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NT == 64 ? 
       half8 yv = {};
       if (gp < a.P) yv = *(const half8*)((const f16*)a.y + (size_t)gp * a.Cdst + c);
       half8 yh;
+      float b8 = 0.f;  // the thread's 8 symbols in fp32, then the fixed-order double sums
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float q = rintf((float)yv[e] - mu[e]);
         q = fminf(fmaxf(q, -32768.f), 32767.f);
         qt[(8 * g8 + e) * 128 + px] = (int16_t)q;
         yh[e] = (f16)(q + mu[e]);
-        if (gp < a.P) bsum += (double)symbol_bits(q, softplus_sigma(sg[e]));
+        b8 += symbol_bits(q, softplus_sigma(sg[e]));
       }
+      if (gp < a.P) bsum = (double)b8;
       if (gp < a.P) *(half8*)((f16*)a.dst + (size_t)gp * a.Cdst + c) = yh;
       __shared__ double red[8];
       bsum = wave_sum(bsum);
