@@ -124,6 +124,8 @@ def test_null_context_calls(lib):
     assert lib.ncodec_rans_decode(None, None, 0, None, 1, None, None) == nc.NCODEC_EINVAL
     assert lib.ncodec_encode_frame_coded(None, None, None, None, None, 0, None) == nc.NCODEC_EINVAL
     assert lib.ncodec_decode_frame_coded(None, None, 0, None, None) == nc.NCODEC_EINVAL
+    assert lib.ncodec_block_chains(None, 1) == nc.NCODEC_EINVAL
+    assert lib.ncodec_block_chain_status(None, None, None) == nc.NCODEC_EINVAL
     lib.ncodec_destroy(None)
 
 
