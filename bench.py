@@ -108,7 +108,8 @@ TRAFFIC_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "prof
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2502_20762_amd", "csrc")
 SOURCES = {"k_dcchain128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
            "k_dcblock128_f16<false>": ["kernels_f16_dc128.hip", "common.hpp", "internal.hpp"],
-           "k_dcblock_i16<256, false>": ["kernels_i16.hip", "common.hpp", "internal.hpp"]}
+           "k_dcchain128_i16": ["kernels_i16_dc128.hip", "common.hpp", "internal.hpp"],
+           "k_dcblock128_i16": ["kernels_i16_dc128.hip", "common.hpp", "internal.hpp"]}
 
 
 def counted_traffic(kernel):
@@ -484,13 +485,13 @@ def main():
         res[path] = run_path(path, pre, weights, gframes, args.steps, args.warmup, torch, Codec)
 
     def summary(path, r, peak_tflops, op_scale, unit):
-        # the dominant kernel: one DC block per launch, or (fp16 at C = 256)
-        # one chain of a transform's blocks per launch; the timing log counts
+        # the dominant kernel: one DC block per launch, or (at C = 256) one
+        # chain of a transform's blocks per launch; the timing log counts
         # blocks either way
         chained = r["block_chains"]
         bpl = min(ne, nd, 16) if chained else 1
         kname = ("k_dcchain128_f16<false>" if chained else "k_dcblock128_f16<false>") if path == "fp16" \
-            else "k_dcblock_i16<256, false>"
+            else ("k_dcchain128_i16" if chained else "k_dcblock128_i16")
         traffic = counted_traffic(kname)
         K = args.steps
         fl, by = kinds["dcblock"]

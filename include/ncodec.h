@@ -357,7 +357,8 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* ctx, int32_t decode);
 ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
 
 /* Block chains (Sec. 3: fewer, larger modules per frame; Supp. B.1 blocks run
- * back to back).  On the fp16 path at C = 256 the consecutive DC blocks of a
+ * back to back).  At C = 256 (fp16 path, either block form; int16 path, the
+ * LeakyReLU form) the consecutive DC blocks of a
  * transform (the encoder's, the decoder's, the feature extractor's, the
  * reconstruction generation's; up to 16 per launch) run as one launch in which
  * every 8 x 16 tile keeps its block output on chip and exchanges only its edge

@@ -374,7 +374,7 @@ struct Layout {
   // state and intermediates (offsets from the workspace base)
   size_t feat[2], yhat[2], ed, zA, zB, y, partials, zpad, spare_bits;
   size_t dwa = 0, hid = 0;  // wide blocks (C > 256): depthwise output, hidden layer
-  // chains of fp16 C = 256 blocks in one launch: one progress word per tile
+  // chains of C = 256 blocks in one launch: one progress word per tile
   // (zero at creation; every launch adds the same count to all) and a
   // timeout flag
   size_t chain_flags = 0, chain_status = 0;
@@ -712,7 +712,7 @@ bool build_layout(const ncodec_config& cfg, const float* w, Image& img, Layout& 
     L.hid = alloc(2 * fb);
   }
   L.y = alloc(lb);
-  if (!is_int && C == 256) {
+  if (C == 256) {
     const size_t tiles = (size_t)((cfg.height / 8 + 7) / 8) * ((cfg.width / 8 + 15) / 16);
     L.chain_flags = alloc(tiles * 4);
     L.chain_status = alloc(4);
@@ -778,7 +778,7 @@ struct ncodec_ctx {
   };
   bool use_graphs = false;
   GraphSlot graphs[2][2];  // [decode][cur]
-  // consecutive fp16 C = 256 blocks as one chain launch (when every tile fits
+  // consecutive C = 256 blocks as one chain launch (when every tile fits
   // the device at once; chain_fit: -1 not yet checked, 0 no, 1 yes)
   bool chains = true;
   int chain_fit = -1;
@@ -877,8 +877,9 @@ hipError_t dcblock(ncodec_ctx* ctx, BlockArgs ba) {
   const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
   if (gated && ctx->is_int()) ba.sig8 = ctx->p(ctx->L.sig8);
   return timed(ctx, "dcblock", [&] {
-    return ctx->is_int() ? launch_dcblock_i16(C, gated, ba, ctx->stream)
-                         : launch_dcblock_f16(C, gated, ba, ctx->stream);
+    if (ctx->is_int())
+      return C == 256 && !gated ? launch_dcblock128_i16(ba, ctx->stream) : launch_dcblock_i16(C, gated, ba, ctx->stream);
+    return launch_dcblock_f16(C, gated, ba, ctx->stream);
   });
 }
 
@@ -901,6 +902,19 @@ PwArgs conv_args(const ncodec_ctx* ctx, const ConvDev& c, int K, int N, int P) {
   a.H = ctx->cfg.height;
   a.W = ctx->cfg.width;
   return a;
+}
+
+// Whether runs of DC blocks go as chain launches: C = 256 (fp16 either form,
+// int the LeakyReLU form), enabled, and every tile of the grid resident on the
+// device at once (checked once per context).
+bool chains_usable(ncodec_ctx* ctx) {
+  const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
+  if (!ctx->chains || ctx->cfg.channels != 256 || (ctx->is_int() && gated)) return false;
+  if (ctx->chain_fit < 0) {
+    const int resident = ctx->is_int() ? dcchain128_i16_resident() : dcchain128_resident(gated);
+    ctx->chain_fit = resident >= dc_grid(ctx->cfg.height / 8, ctx->cfg.width / 8) ? 1 : 0;
+  }
+  return ctx->chain_fit == 1;
 }
 
 // One DC block of either form, src -> dst.
@@ -941,19 +955,16 @@ hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* 
 }
 
 // Blocks 0 .. n - 1 of `blocks`, block k from src[k] into dst[k] (src[k + 1]
-// = dst[k]).  On the fp16 path at C = 256 runs of up to kMaxChain blocks go
+// = dst[k]).  At C = 256 (int path: LeakyReLU form) runs of up to kMaxChain blocks go
 // as one chain launch when every tile of the grid fits the device at once;
 // otherwise (and for a run of one) one launch per block.  The timing log
 // counts blocks either way.
 hipError_t run_blocks(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, const std::vector<const void*>& src,
                       const std::vector<void*>& dst) {
   const int n = (int)blocks.size();
-  const int C = ctx->cfg.channels;
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
-  bool chain = ctx->chains && !ctx->is_int() && C == 256 && n >= 2;
-  if (chain && ctx->chain_fit < 0) ctx->chain_fit = dcchain128_resident(gated) >= dc_grid(h8, w8) ? 1 : 0;
-  chain = chain && ctx->chain_fit == 1;
+  const bool chain = n >= 2 && chains_usable(ctx);
   for (int k0 = 0; k0 < n;) {
     const int m = chain ? std::min(n - k0, kMaxChain) : 1;
     if (m == 1) {
@@ -966,14 +977,16 @@ hipError_t run_blocks(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, cons
     std::memset(&ca, 0, sizeof(ca));
     for (int j = 0; j < m; ++j) {
       const BlockDev& b = blocks[k0 + j];
-      ca.blk[j] = BlockArgs{ctx->p(b.pw1.w), nullptr, ctx->p(b.pw1.bias), ctx->p(b.pw2.w), nullptr,
-                            ctx->p(b.pw2.bias), ctx->p(b.dww), ctx->p(b.dwb), src[k0 + j], dst[k0 + j],
+      ca.blk[j] = BlockArgs{ctx->p(b.pw1.w), nullptr, ctx->p(b.pw1.bias), ctx->is_int() ? nullptr : ctx->p(b.pw2.w),
+                            nullptr, ctx->p(b.pw2.bias), ctx->p(b.dww), ctx->p(b.dwb), src[k0 + j], dst[k0 + j],
                             h8, w8, ctx->p(ctx->L.zpad)};
     }
     ca.nb = m;
     ca.flags = ctx->p<int>(ctx->L.chain_flags);
     ca.status = ctx->p<int>(ctx->L.chain_status);
-    const hipError_t e = timed(ctx, "dcblock", [&] { return launch_dcchain128_f16(gated, ca, ctx->stream); }, m);
+    const hipError_t e = timed(ctx, "dcblock", [&] {
+      return ctx->is_int() ? launch_dcchain128_i16(ca, ctx->stream) : launch_dcchain128_f16(gated, ca, ctx->stream);
+    }, m);
     if (e != hipSuccess) return e;
     k0 += m;
   }
@@ -1841,11 +1854,8 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
 
 // Launches of a run of n DC blocks (chains: up to kMaxChain blocks each).
 int block_launches(ncodec_ctx* ctx, int n) {
-  const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
-  if (!ctx->chains || ctx->is_int() || ctx->cfg.channels != 256 || n < 2) return n;
-  if (ctx->chain_fit < 0)
-    ctx->chain_fit = dcchain128_resident(gated) >= dc_grid(ctx->cfg.height / 8, ctx->cfg.width / 8) ? 1 : 0;
-  return ctx->chain_fit == 1 ? (n + kMaxChain - 1) / kMaxChain : n;
+  if (n < 2 || !chains_usable(ctx)) return n;
+  return (n + kMaxChain - 1) / kMaxChain;
 }
 
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* cctx, int32_t decode) {

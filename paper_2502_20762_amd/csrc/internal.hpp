@@ -117,7 +117,7 @@ struct BlockArgs {
   const void* sig8 = nullptr;  // int path, gated form: compact sigmoid table (896 bytes)
 };
 
-// A run of DC blocks in one launch (the C = 256 fp16 chain kernel):
+// A run of DC blocks in one launch (the C = 256 chain kernels):
 // blk[b].src = blk[b - 1].dst; flags: one int per tile, zero at workspace
 // creation and left equal across tiles by every launch; status: set to 1 if a
 // wait for a neighbouring tile timed out.
@@ -197,6 +197,10 @@ hipError_t launch_dcblock_f16(int C, bool gated, const BlockArgs& a, hipStream_t
 hipError_t launch_dcblock128_f16(bool gated, const BlockArgs& a, hipStream_t st);  // C = 256
 hipError_t launch_dcchain128_f16(bool gated, const DcChainArgs& ca, hipStream_t st);  // C = 256, fp16
 int dcchain128_resident(bool gated);
+// int path, LeakyReLU form, C = 256: 128 pixels per wave (one block, or a chain)
+hipError_t launch_dcblock128_i16(const BlockArgs& a, hipStream_t st);
+hipError_t launch_dcchain128_i16(const DcChainArgs& ca, hipStream_t st);
+int dcchain128_i16_resident();
 hipError_t launch_dcblock_i16(int C, bool gated, const BlockArgs& a, hipStream_t st);
 hipError_t launch_prior_f16(const PriorArgs& a, hipStream_t st, int* n_partials);
 hipError_t launch_prior_i16(const PriorArgs& a, hipStream_t st, int* n_partials);

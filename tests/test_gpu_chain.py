@@ -1,13 +1,14 @@
-"""Block chains (the fp16 C = 256 DC blocks of a transform in one launch, tiles
-exchanging only their edge pixels) against one launch per block, through the
-C ABI: both run the same per-block arithmetic, so q, the frame bits, the
-state and the decoded frame must agree bitwise, and no chain wait may time
-out.  Sizes: 1080p with 8 + 8 blocks (the benchmarked transform, 255 tiles),
-a ragged 272 x 400 frame (34 x 50 latent pixels at 1/8: partial tiles on the
-right and bottom), the gated form, chains through the feature extractor and
-reconstruction generation, and graph replay.  The chains themselves are
-checked against the oracle by every fp16 C = 256 parity test, which runs them
-by default."""
+"""Block chains (the C = 256 DC blocks of a transform in one launch, tiles
+exchanging only their edge pixels; fp16 path, and the int16 path's LeakyReLU
+form) against one launch per block, through the C ABI: both run the same
+per-block arithmetic, so q, the frame bits, the state and the decoded frame
+must agree bitwise, and no chain wait may time out.  Sizes: 1080p with 8 + 8
+blocks (the benchmarked transform, 255 tiles), a ragged 272 x 400 frame
+(34 x 50 latent pixels at 1/8: partial tiles on the right and bottom), the
+gated form (fp16), chains through the feature extractor and reconstruction
+generation, and graph replay.  The chains themselves are checked against the
+oracle by every C = 256 parity test of either path, which runs them by
+default."""
 import numpy as np
 import pytest
 import torch
@@ -29,11 +30,11 @@ def host(t):
     return t.cpu().numpy()
 
 
-def run(H, W, C, ne, nd, frames, chains, block="lrelu", graphs=False, **mods):
+def run(H, W, C, ne, nd, frames, chains, block="lrelu", graphs=False, path="fp16", **mods):
     flat = synth.make_weights(C, ne, nd, block=block, n_fe=mods.get("n_fe_blocks", 0),
                               n_rg=mods.get("n_rg_blocks", 0))
-    enc = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block, **mods)
-    dec = Codec(H, W, C, ne, nd, "fp16", flat, device=DEV, block=block, **mods)
+    enc = Codec(H, W, C, ne, nd, path, flat, device=DEV, block=block, **mods)
+    dec = Codec(H, W, C, ne, nd, path, flat, device=DEV, block=block, **mods)
     for cdc in (enc, dec):
         cdc.block_chains(chains)
         cdc.graphs(graphs)
@@ -60,33 +61,46 @@ def compare(a, b, what):
         np.testing.assert_array_equal(xa, xb, err_msg=f"{what} frame {k}: xhat")
 
 
-def test_chain_hd1080_matches_per_block_launches():
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_chain_hd1080_matches_per_block_launches(path):
     pre = synth.PRESETS["hd1080"]
     H, W, C, ne, nd = pre.height, pre.width, pre.channels, pre.n_enc, pre.n_dec
     frames = list(synth.frame_sequence(pre, 2))
-    say("1080p, chains on")
-    on, c_on = run(H, W, C, ne, nd, frames, True)
-    say("1080p, chains off")
-    off, c_off = run(H, W, C, ne, nd, frames, False)
-    compare(on, off, "1080p")
-    # one launch per transform's blocks with chains (8 blocks each)
-    assert c_off == (4 + ne + nd, 3 + nd), c_off
-    assert c_on == (4 + 2, 3 + 1), c_on
+    say("1080p", path, "chains on")
+    on, c_on = run(H, W, C, ne, nd, frames, True, path=path)
+    say("1080p", path, "chains off")
+    off, c_off = run(H, W, C, ne, nd, frames, False, path=path)
+    compare(on, off, f"1080p {path}")
+    # one launch per transform's blocks with chains (8 blocks each); the fp16
+    # path folds the patch embed and the upsample into the fuse convs
+    fold = 1 if path == "fp16" else 0
+    assert c_off == (6 - 2 * fold + ne + nd, 4 - fold + nd), c_off
+    assert c_on == (6 - 2 * fold + 2, 4 - fold + 1), c_on
 
 
-@pytest.mark.parametrize("block", ["lrelu", "gated"])
-def test_chain_ragged_matches_per_block_launches(block):
+@pytest.mark.parametrize("path,block", [("fp16", "lrelu"), ("fp16", "gated"), ("int16", "lrelu")])
+def test_chain_ragged_matches_per_block_launches(path, block):
     frames = [synth.random_frame(272, 400, seed=s) for s in (30, 31)]
-    say("272x400", block)
-    on, _ = run(272, 400, 256, 3, 3, frames, True, block=block)
-    off, _ = run(272, 400, 256, 3, 3, frames, False, block=block)
-    compare(on, off, f"272x400 {block}")
+    say("272x400", path, block)
+    on, _ = run(272, 400, 256, 3, 3, frames, True, block=block, path=path)
+    off, _ = run(272, 400, 256, 3, 3, frames, False, block=block, path=path)
+    compare(on, off, f"272x400 {path} {block}")
 
 
-def test_chain_modules_and_graphs_match_per_block_launches():
+@pytest.mark.parametrize("path", ["fp16", "int16"])
+def test_chain_modules_and_graphs_match_per_block_launches(path):
     frames = [synth.random_frame(128, 192, seed=s) for s in (32, 33, 34)]
     mods = dict(n_fe_blocks=2, n_rg_blocks=2)
-    say("128x192 with the modules, graphs")
-    on, _ = run(128, 192, 256, 2, 2, frames, True, graphs=True, **mods)
-    off, _ = run(128, 192, 256, 2, 2, frames, False, graphs=False, **mods)
-    compare(on, off, "128x192 modules")
+    say("128x192 with the modules, graphs", path)
+    on, _ = run(128, 192, 256, 2, 2, frames, True, graphs=True, path=path, **mods)
+    off, _ = run(128, 192, 256, 2, 2, frames, False, graphs=False, path=path, **mods)
+    compare(on, off, f"128x192 modules {path}")
+
+
+def test_int_gated_runs_without_chains():
+    # the int16 gated block keeps one launch per block: chains report not in use
+    frames = [synth.random_frame(64, 96, seed=35)]
+    flat = synth.make_weights(256, 2, 2, block="gated")
+    c = Codec(64, 96, 256, 2, 2, "int16", flat, device=DEV, block="gated")
+    c.encode(torch.from_numpy(frames[0]).to(DEV))
+    assert c.block_chain_status() == (0, 0)
