@@ -95,6 +95,15 @@ __device__ __forceinline__ int rhe13(int a) {
   const int ac = min(max(a, -(1 << 28)), 1 << 28);
   return (ac + 4095 + ((ac >> 13) & 1)) >> 13;
 }
+// clip(RHE(a / 8192)) to int16 for any int32 a: clamping a to
+// [-2^28, 2^28 - 4097] first gives the saturated value directly (every a above
+// 2^28 - 4097 rounds to at least 32768, every a below -2^28 to at most -32768,
+// and the bounds themselves round to 32767 and -32768).
+__device__ __forceinline__ int rescale13c(int a) {
+  const int ac = min(max(a, -(1 << 28)), (1 << 28) - 4097);
+  return (ac + 4095 + ((ac >> 13) & 1)) >> 13;
+}
+typedef short short2v __attribute__((ext_vector_type(2)));
 // Two int32 values saturated to int16 and packed (first in the low half).
 __device__ __forceinline__ uint32_t pack_sat(int lo, int hi) {
   return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16(lo, hi));
@@ -260,7 +269,6 @@ __device__ __forceinline__ void dci128_block(char* smem, const BlockArgs& a, int
         P1[y][i] = __builtin_amdgcn_perm(vr[i + 1], vr[i], 0x07060302u);
       }
     };
-    typedef short short2v __attribute__((ext_vector_type(2)));
     auto sdot = [](uint32_t w, uint32_t v, int acc) __attribute__((always_inline)) {
       return __builtin_amdgcn_sdot2(__builtin_bit_cast(short2v, w), __builtin_bit_cast(short2v, v), acc, false);
     };
@@ -453,7 +461,7 @@ __device__ __forceinline__ void dci128_block(char* smem, const BlockArgs& a, int
           int v[2];
 #pragma unroll
           for (int u = 0; u < 2; ++u) {
-            const int hv = min(max(rhe13(acc[c][g][2 * e + u]), -32768), 32767);
+            const int hv = rescale13c(acc[c][g][2 * e + u]);
             const int m = 819 * hv;  // |m| < 2^25
             v[u] = max(hv, (m + 4095 + ((m >> 13) & 1)) >> 13);
           }
@@ -544,10 +552,13 @@ __device__ __forceinline__ void dci128_block(char* smem, const BlockArgs& a, int
     intx2 o;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const int r0 = (int)(short)(r[e] & 0xFFFF), r1 = r[e] >> 16;
-      const int v0 = min(max(rhe13(acc[c][g][4 * q + 2 * e]), -32768), 32767);
-      const int v1 = min(max(rhe13(acc[c][g][4 * q + 2 * e + 1]), -32768), 32767);
-      o[e] = (int)pack_sat(r0 + v0, r1 + v1);
+      // saturating packed int16 add of the residual pair and the rescaled pair
+      // (from inline asm: the vector saturating-add builtin was miscompiled
+      // here, adding the first residual word to both pairs)
+      const uint32_t v = pack_sat(rhe13(acc[c][g][4 * q + 2 * e]), rhe13(acc[c][g][4 * q + 2 * e + 1]));
+      int sum;
+      asm("v_pk_add_i16 %0, %1, %2 clamp" : "=v"(sum) : "v"(r[e]), "v"(v));
+      o[e] = sum;
     }
     return o;
   };
