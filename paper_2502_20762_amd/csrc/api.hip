@@ -959,8 +959,13 @@ hipError_t run_block(ncodec_ctx* ctx, const BlockDev& b, const void* src, void* 
 // as one chain launch when every tile of the grid fits the device at once;
 // otherwise (and for a run of one) one launch per block.  The timing log
 // counts blocks either way.
+// With down set (the encoder's blocks, fp16) and the run's last launch a
+// chain, that launch also runs the 2x2 stride-2 downsample on each tile's last
+// block output (into down_y; dst[n - 1] is then not written) and *down_done
+// is set; otherwise the caller runs the downsample.
 hipError_t run_blocks(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, const std::vector<const void*>& src,
-                      const std::vector<void*>& dst) {
+                      const std::vector<void*>& dst, const ConvDev* down = nullptr, void* down_y = nullptr,
+                      bool* down_done = nullptr) {
   const int n = (int)blocks.size();
   const int h8 = ctx->cfg.height / 8, w8 = ctx->cfg.width / 8;
   const bool gated = ctx->cfg.block == NCODEC_BLOCK_GATED;
@@ -984,7 +989,14 @@ hipError_t run_blocks(ncodec_ctx* ctx, const std::vector<BlockDev>& blocks, cons
     ca.nb = m;
     ca.flags = ctx->p<int>(ctx->L.chain_flags);
     ca.status = ctx->p<int>(ctx->L.chain_status);
-    const hipError_t e = timed(ctx, "dcblock", [&] {
+    const bool fuse = down && !ctx->is_int() && k0 + m == n;
+    if (fuse) {
+      ca.down_w = ctx->p(down->w);
+      ca.down_b = ctx->p(down->bias);
+      ca.down_y = down_y;
+      *down_done = true;
+    }
+    const hipError_t e = timed(ctx, fuse ? "dcblock_down" : "dcblock", [&] {
       return ctx->is_int() ? launch_dcchain128_i16(ca, ctx->stream) : launch_dcchain128_f16(gated, ca, ctx->stream);
     }, m);
     if (e != hipSuccess) return e;
@@ -1196,6 +1208,7 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
   NC_HIP(ctx, temporal_context(ctx, &context), "feature extractor");
 
   void* z = ctx->p(L.zA);
+  bool down_done = false;  // the downsample ran inside the encoder's block chain
   PwArgs a;
   if (ctx->is_int()) {
     a = conv_args(ctx, L.pe, 192, C, P8);
@@ -1227,15 +1240,17 @@ ncodec_status enqueue_encode(ncodec_ctx* ctx, const void* d_frame, int16_t* d_q,
       dsts.push_back(dst);
       z = dst;
     }
-    NC_HIP(ctx, run_blocks(ctx, L.enc, srcs, dsts), "encoder blocks");
+    NC_HIP(ctx, run_blocks(ctx, L.enc, srcs, dsts, &L.down, ctx->p(L.y), &down_done), "encoder blocks");
   }
 
-  a = conv_args(ctx, L.down, 4 * C, C, P16);
-  a.src0 = z;
-  a.Csrc = C;
-  a.dst = ctx->p(L.y);
-  a.Cdst = C;
-  NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
+  if (!down_done) {
+    a = conv_args(ctx, L.down, 4 * C, C, P16);
+    a.src0 = z;
+    a.Csrc = C;
+    a.dst = ctx->p(L.y);
+    a.Cdst = C;
+    NC_HIP(ctx, pw(ctx, "down", LD_DOWN, EP_NHWC, a), "downsample");
+  }
 
   double* const parts = ctx->p<double>(L.partials);
   int np_z = 0;
@@ -1858,6 +1873,12 @@ int block_launches(ncodec_ctx* ctx, int n) {
   return (n + kMaxChain - 1) / kMaxChain;
 }
 
+// Whether the encoder's last block launch carries the downsample (fp16: its
+// last run of blocks is a chain of at least two).
+bool down_fused(ncodec_ctx* ctx, int n) {
+  return !ctx->is_int() && n >= 2 && chains_usable(ctx) && n - kMaxChain * ((n - 1) / kMaxChain) >= 2;
+}
+
 int32_t ncodec_kernels_per_frame(const ncodec_ctx* cctx, int32_t decode) {
   if (!cctx) return 0;
   ncodec_ctx* ctx = const_cast<ncodec_ctx*>(cctx);  // caches the residency check
@@ -1865,14 +1886,15 @@ int32_t ncodec_kernels_per_frame(const ncodec_ctx* cctx, int32_t decode) {
   // feature extractor, prior, upsample, fuse, decoder blocks, reconstruction generation, reconstruction
   // (two-step model: z quantiser or z from symbols, hyper-synthesis, second step)
   // (the fp16 path runs the upsample and the fuse as one launch, and in an
-  // encode the patch embed and the fuse too)
+  // encode the patch embed and the fuse too, and the downsample inside the
+  // encoder's block chain)
   const int fold = c.path == NCODEC_PATH_INT16 ? 0 : 1;
   const int hyper = c.hyperprior ? 3 : 0;
   const int per_block = c.channels > 256 ? 3 : 1;  // a wide block is three launches
   if (per_block == 1) {  // one launch per block or per chain of blocks
     const int fe = block_launches(ctx, c.n_fe_blocks), dec = block_launches(ctx, c.n_dec_blocks);
     if (decode) return 4 - fold + hyper + fe + dec + block_launches(ctx, c.n_rg_blocks);
-    return 6 - 2 * fold + hyper + fe + block_launches(ctx, c.n_enc_blocks) + dec;
+    return 6 - 2 * fold + hyper + fe + block_launches(ctx, c.n_enc_blocks) + dec - (down_fused(ctx, c.n_enc_blocks) ? 1 : 0);
   }
   if (decode) return 4 - fold + hyper + per_block * (c.n_fe_blocks + c.n_dec_blocks + c.n_rg_blocks);
   // feature extractor, embed, fuse, encoder blocks, downsample, prior, upsample (with the bit total), fuse,

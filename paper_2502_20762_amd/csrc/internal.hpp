@@ -127,6 +127,13 @@ struct DcChainArgs {
   int nb;
   int* flags;
   int* status;
+  // fp16 chain only: when down_w is set, the last block's output stays in LDS
+  // and feeds the 2x2 stride-2 downsample of the tile instead (down_w: its
+  // weight fragments, K = 4C, N = C; down_b: C fp32 biases; down_y: the 1/16
+  // output, NHWC), the same arithmetic as the downsample launch
+  const void* down_w;
+  const void* down_b;
+  void* down_y;
 };
 
 struct PriorArgs {

@@ -126,11 +126,84 @@ __device__ __forceinline__ void store_coherent16(f16* p, half8 v) {
   asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
 }
 
+// The 2x2 stride-2 downsample of a tile's block output, parked in LDS (row =
+// tile pixel, 8-byte unit u of the row at u ^ (p & 15)): output rows
+// 64 w .. + 63 (tiles c = 0, 1) of the tile's 32 latent pixels (4 x 8 at
+// 1/16), K = 4C with k = (2 i + j) C + c from pixel (2 Y + i, 2 X + j) (Fig. 4's
+// downsampling to 1/16), the k-steps in order from zero, then the fp32 bias
+// and one rounding to fp16: the arithmetic of the downsample launch, so the
+// result is the same bit for bit.
+__device__ __forceinline__ void dc128_down(const char* smem, const DcChainArgs& ca, const BlockArgs& a, int ty0,
+                                           int tx0, int wave, int lane) {
+  using namespace dcw;
+  constexpr int DK = 4 * C / 16;  // 64 k-steps
+  const int h = lane >> 5, n = lane & 31, ly = n >> 3, lx = n & 7;
+  const half8* wimg = (const half8*)ca.down_w + lane;  // fragment (row tile mt, k-step s) at [(mt DK + s) 64]
+  auto afrag = [&](int s, int c) __attribute__((always_inline)) {
+    return wimg[((size_t)(2 * wave + c) * DK + s) * 64];
+  };
+  // B of k-step s: channels 16 (s % 16) + 8 h .. + 7 of tap s / 16 at tile pixel p
+  auto bfrag = [&](int s) __attribute__((always_inline)) {
+    const int tap = s >> 4;
+    const int p = 16 * (2 * ly + (tap >> 1)) + 2 * lx + (tap & 1);
+    const int u = 4 * (s & 15) + 2 * h;
+    const char* pb = smem + p * 512;
+    const half4 lo = *(const half4*)(pb + ((u ^ (p & 15)) << 3));
+    const half4 hi = *(const half4*)(pb + (((u + 1) ^ (p & 15)) << 3));
+    half8 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = lo[e];
+      v[4 + e] = hi[e];
+    }
+    return v;
+  };
+  constexpr int PD = 8;  // prefetch distance (k-steps) of the weight fragments (registers are free here)
+  half8 qa[PD][2];
+#pragma unroll
+  for (int s = 0; s < PD; ++s)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) qa[s][c] = afrag(s, c);
+  floatx16 acc[2] = {floatx16{}, floatx16{}};
+#pragma unroll
+  for (int s = 0; s < DK; ++s) {
+    const half8 B = bfrag(s);
+    half8 A[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      A[c] = qa[s % PD][c];
+      if (s + PD < DK) qa[s % PD][c] = afrag(s + PD, c);
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) acc[c] = mfma_f16(A[c], B, acc[c]);
+  }
+  // latent pixel (Y, X) lies in the image when its top-left child does (the
+  // 1/8 sizes are even)
+  const int Y = (ty0 >> 1) + ly, X = (tx0 >> 1) + lx;
+  if (2 * Y < a.h && 2 * X < a.w) {
+    f16* y = (f16*)ca.down_y + (size_t)(Y * (a.w >> 1) + X) * C;
+    const float* bias = (const float*)ca.down_b;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ch = 64 * wave + 32 * c + 8 * q + 4 * h;
+        const floatx4 bv = *(const floatx4*)(bias + ch);
+        half4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (f16)(acc[c][4 * q + e] + bv[e]);
+        *(half4*)(y + ch) = o;
+      }
+  }
+}
+
 // One block of a tile (FIRST: its band comes whole from a.src; LAST: its
-// output goes whole to a.dst; otherwise the chain's ring and edge exchange).
+// output goes whole to a.dst, or with ca->down_w set through the fused
+// downsample to ca->down_y; otherwise the chain's ring and edge exchange).
 template <bool GATED, bool CHAIN, bool FIRST, bool LAST>
 __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int b, int tile, int tiles_x, int tiles_y,
-                                            int wave0, int base, int* flags, int* status) {
+                                            int wave0, int base, int* flags, int* status,
+                                            const DcChainArgs* ca) {
   using namespace dcw;
   constexpr int KH = GATED ? KS / 2 : KS;  // hidden k-steps per round (the pw2 k-steps of a round)
   constexpr int NT = 2 * KS + 2 * KH;      // weight-stream steps: pw1 rounds 0, 1, pw2
@@ -593,6 +666,12 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
         }
       }
     lds_barrier();
+    if constexpr (CHAIN) {
+      if (ca->down_w) {
+        dc128_down(smem, *ca, a, ty0, tx0, wave, lane);
+        return;
+      }
+    }
     f16* dst = (f16*)a.dst;
 #pragma unroll
     for (int i = 0; i < TH * TW * 32 / 256; ++i) {
@@ -665,7 +744,8 @@ __device__ __forceinline__ void dc128_block(char* smem, const BlockArgs& a, int 
 }
 
 template <bool GATED, bool CHAIN>
-__device__ __forceinline__ void dc128_body(const BlockArgs* blk, int nb, int* flags, int* status) {
+__device__ __forceinline__ void dc128_body(const BlockArgs* blk, int nb, int* flags, int* status,
+                                           const DcChainArgs* ca) {
   using namespace dcw;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   const int tiles_x = (blk[0].w + TW - 1) / TW, tiles_y = (blk[0].h + TH - 1) / TH;
@@ -673,25 +753,26 @@ __device__ __forceinline__ void dc128_body(const BlockArgs* blk, int nb, int* fl
   if (tile >= tiles_x * tiles_y) return;
   const int wave0 = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if constexpr (!CHAIN) {
-    dc128_block<GATED, false, true, true>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, 0, nullptr, nullptr);
+    dc128_block<GATED, false, true, true>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, 0, nullptr, nullptr, nullptr);
   } else {
     // nb >= 2: the first block, the middle ones, the last
     const int base = __builtin_amdgcn_readfirstlane(__hip_atomic_load(flags + tile, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    dc128_block<GATED, true, true, false>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, base, flags, status);
+    dc128_block<GATED, true, true, false>(smem, blk[0], 0, tile, tiles_x, tiles_y, wave0, base, flags, status, ca);
     for (int b = 1; b < nb - 1; ++b)
-      dc128_block<GATED, true, false, false>(smem, blk[b], b, tile, tiles_x, tiles_y, wave0, base, flags, status);
-    dc128_block<GATED, true, false, true>(smem, blk[nb - 1], nb - 1, tile, tiles_x, tiles_y, wave0, base, flags, status);
+      dc128_block<GATED, true, false, false>(smem, blk[b], b, tile, tiles_x, tiles_y, wave0, base, flags, status, ca);
+    dc128_block<GATED, true, false, true>(smem, blk[nb - 1], nb - 1, tile, tiles_x, tiles_y, wave0, base, flags, status,
+                                          ca);
   }
 }
 
 template <bool GATED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcblock128_f16(BlockArgs a) {
-  dc128_body<GATED, false>(&a, 1, nullptr, nullptr);
+  dc128_body<GATED, false>(&a, 1, nullptr, nullptr, nullptr);
 }
 
 template <bool GATED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dcchain128_f16(DcChainArgs ca) {
-  dc128_body<GATED, true>(ca.blk, ca.nb, ca.flags, ca.status);
+  dc128_body<GATED, true>(ca.blk, ca.nb, ca.flags, ca.status, &ca);
 }
 
 hipError_t launch_dcblock128_f16(bool gated, const BlockArgs& a, hipStream_t st) {

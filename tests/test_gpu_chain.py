@@ -6,9 +6,10 @@ must agree bitwise, and no chain wait may time out.  Sizes: 1080p with 8 + 8
 blocks (the benchmarked transform, 255 tiles), a ragged 272 x 400 frame
 (34 x 50 latent pixels at 1/8: partial tiles on the right and bottom), the
 gated form (fp16), chains through the feature extractor and reconstruction
-generation, and graph replay.  The chains themselves are checked against the
-oracle by every C = 256 parity test of either path, which runs them by
-default."""
+generation, and graph replay.  On the fp16 path the encoder's chain also runs
+the downsample (its latent must match the downsample launch's bit for bit).
+The chains themselves are checked against the oracle by every C = 256 parity
+test of either path, which runs them by default."""
 import numpy as np
 import pytest
 import torch
@@ -72,10 +73,11 @@ def test_chain_hd1080_matches_per_block_launches(path):
     off, c_off = run(H, W, C, ne, nd, frames, False, path=path)
     compare(on, off, f"1080p {path}")
     # one launch per transform's blocks with chains (8 blocks each); the fp16
-    # path folds the patch embed and the upsample into the fuse convs
+    # path folds the patch embed and the upsample into the fuse convs, and with
+    # chains runs the downsample inside the encoder's chain
     fold = 1 if path == "fp16" else 0
     assert c_off == (6 - 2 * fold + ne + nd, 4 - fold + nd), c_off
-    assert c_on == (6 - 2 * fold + 2, 4 - fold + 1), c_on
+    assert c_on == (6 - 2 * fold + 2 - fold, 4 - fold + 1), c_on
 
 
 @pytest.mark.parametrize("path,block", [("fp16", "lrelu"), ("fp16", "gated"), ("int16", "lrelu")])
