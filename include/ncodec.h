@@ -338,7 +338,8 @@ ncodec_status ncodec_set_state(ncodec_ctx* ctx, const void* d_feat, const void* 
  * not change the count) or ncodec_decode_frame (decode = 1) enqueues (three more each with
  * the two-step model; on the fp16 path the upsample and its fuse conv are one
  * launch, and so are the patch embed and its fuse conv; a chain of DC blocks
- * counts as one launch per up to 16 blocks, see ncodec_block_chains),
+ * counts as one launch per up to 16 blocks, see ncodec_block_chains, and on
+ * the fp16 path the encoder's last chain also runs the downsample),
  * counting the feature-extractor and reconstruction-generation blocks
  * (Sec. 3: the number of modules called per frame is one of the costs the
  * design minimises).  0 for a NULL ctx. */
@@ -360,7 +361,8 @@ ncodec_status ncodec_graph_enable(ncodec_ctx* ctx, int32_t enable);
  * back to back).  At C = 256 (fp16 path, either block form; int16 path, the
  * LeakyReLU form) the consecutive DC blocks of a
  * transform (the encoder's, the decoder's, the feature extractor's, the
- * reconstruction generation's; up to 16 per launch) run as one launch in which
+ * reconstruction generation's; up to 16 per launch) run as one launch (on the
+ * fp16 path the encoder's together with the downsample) in which
  * every 8 x 16 tile keeps its block output on chip and exchanges only its edge
  * pixels with the neighbouring tiles through memory.  Used only where every
  * tile fits the device at once (checked once per context with the occupancy
@@ -392,8 +394,10 @@ ncodec_status ncodec_block_chain_status(ncodec_ctx* ctx, int32_t* in_use, int32_
  * *n_kinds, and clears the log.  Kinds: "embed", "fuse", "embed_fuse",
  * "dcblock" (wide blocks: "dcblock_dw", "dcblock_pw1", "dcblock_pw2"), "down",
  * "prior", "up", "up_fuse", "recon", "zquant", "hyper", "zhat", "yhat",
- * "rans_enc", "rans_dec".  A chain of DC blocks (ncodec_block_chains) counts
- * as one launch per block, so "dcblock" is always per block.  Meant for
+ * "rans_enc", "rans_dec", "dcblock_down" (the fp16 encoder's chain that also
+ * runs the downsample; it has no "down" launch).  A chain of DC blocks
+ * (ncodec_block_chains) counts as one launch per block, so "dcblock" is
+ * always per block.  Meant for
  * measurement runs; off by default. */
 typedef struct {
   char kind[16];
