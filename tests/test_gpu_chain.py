@@ -106,3 +106,18 @@ def test_int_gated_runs_without_chains():
     c = Codec(64, 96, 256, 2, 2, "int16", flat, device=DEV, block="gated")
     c.encode(torch.from_numpy(frames[0]).to(DEV))
     assert c.block_chain_status() == (0, 0)
+
+
+@pytest.mark.parametrize("ne", [17, 18])
+def test_chain_split_encoder_downsample(ne):
+    # more than 16 encoder blocks: a chain of 16, then the rest; with 17 the
+    # last launch is a single block (the downsample runs as its own launch),
+    # with 18 a chain of two that carries the downsample
+    frames = [synth.random_frame(64, 128, seed=s) for s in (36, 37)]
+    say("64x128 encoder of", ne, "blocks")
+    on, c_on = run(64, 128, 256, ne, 1, frames, True)
+    off, c_off = run(64, 128, 256, ne, 1, frames, False)
+    compare(on, off, f"64x128 ne={ne}")
+    fused = 1 if ne == 18 else 0
+    assert c_off == (4 + ne + 1, 3 + 1), c_off
+    assert c_on == (4 + 2 - fused + 1, 3 + 1), c_on
