@@ -38,7 +38,9 @@ HYPER = dict(hyperprior=True)  # the two-step entropy model: z symbols follow y'
     ("int16", 64, 64, 64, 2, 2, {}), ("fp16", 112, 208, 128, 2, 1, {}), ("int16", 48, 80, 128, 1, 2, {}),
     ("int16", 64, 96, 64, 1, 1, GATED), ("fp16", 64, 96, 64, 1, 1, MODULES),
     ("int16", 48, 80, 128, 1, 1, dict(GATED, **MODULES)), ("int16", 64, 96, 128, 1, 1, HYPER),
-    ("fp16", 64, 96, 128, 1, 1, dict(HYPER, **MODULES))])
+    ("fp16", 64, 96, 128, 1, 1, dict(HYPER, **MODULES)),
+    # C = 256: block chains, the downsample inside the encoder's
+    ("fp16", 112, 208, 256, 2, 2, {})])
 def test_graph_replay_matches_eager(path, H, W, C, ne, nd, extra):
     block = extra.get("block", "lrelu")
     flat = synth.make_weights(C, ne, nd, block=block, n_fe=extra.get("n_fe_blocks", 0),
